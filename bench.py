@@ -1,0 +1,155 @@
+"""Benchmark: batched transformer forward pass of one serverless DL instance on
+one MI355X.
+
+Workload (one "step" = one batch through the whole forward pass):
+BERT-base-shaped post-LN encoder, 12 layers, d_model 768, 12 heads, FFN 3072,
+GELU, per-token 768->2 head, seq 128, batch 32, seeded random-init bf16
+weights, fp32 N(0,1) input embeddings already resident in HBM, full 256-CU
+quota.
+
+Prints one JSON line: inferences/s (one inference = one sequence), the
+forward-level MFMA utilisation, the roofline of the dominant kernel (FFN-up
+GEMM + bias + GELU, timed with HIP events on the instance's stream during the
+timed region) and the fp64 CPU oracle timed on a bounded sample.
+
+  python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense bf16 MFMA
+WORKLOAD = "bert_base_l12_d768_s128"
+
+
+def forward_flops(L, d, F, H, S, n_out, causal=False):
+    """Algorithmic FLOPs of one sequence (multiply-add = 2)."""
+    gemm = 2 * S * d * (3 * d) + 2 * S * d * d + 2 * S * d * F + 2 * S * F * d
+    attn = (2 * (S * (S + 1) // 2) * d * 2) if causal else 4 * S * S * d
+    return L * (gemm + attn) + 2 * S * d * n_out
+
+
+def cpu_baseline(shape, batch_sample: int):
+    """The fp64 oracle on `batch_sample` sequences of the same workload."""
+    from threadpoolctl import threadpool_info
+
+    import workloads as W
+    from oracle import forward as F
+    from oracle import init_spec as I
+
+    w = W.WORKLOADS[WORKLOAD]
+    x = W.make_input(w["input_seed"], batch_sample, w["seq"], shape["d_model"])
+    layers = [I.layer_weights(shape, l) for l in range(shape["n_layers"])]
+    glob = I.global_weights(shape)
+    t0 = time.perf_counter()
+    F.forward_with(x, shape, lambda l: layers[l], glob)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("internal_api") == "openblas"]
+                  or [os.cpu_count() or 1])
+    return {"value": round(batch_sample / dt, 4), "unit": "inferences/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{batch_sample} sequences of the same workload (seq 128), NumPy fp64 forward, "
+                      f"weights pre-generated; {dt:.2f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--batch", type=int, default=32)
+    ap.add_argument("--quota", type=int, default=256)
+    ap.add_argument("--cpu-sample", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (the instances of this workload share one MI355X); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        return 2
+
+    import torch
+
+    import paper_2503_05130_amd as ie
+    import workloads as W
+
+    w = W.WORKLOADS[WORKLOAD]
+    shape = W.model_shape(WORKLOAD)
+    B, S = args.batch, w["seq"]
+    cfg = {k: shape[k] for k in ("n_layers", "d_model", "n_heads", "d_ff", "pre_ln", "causal", "n_out",
+                                 "ln_eps", "w_std", "b_std", "ln_std", "qk_std", "seed")}
+    inst = ie.Instance(device=0, max_batch=B, max_seq=S, **cfg)
+    inst.set_quota(args.quota)
+    x = torch.from_numpy(W.make_input(w["input_seed"], B, S, shape["d_model"])).to("cuda:0")
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        inst.submit(x)
+        inst.wait()
+
+    dominant = ie.K_FFN1
+    inst.time_kernel(dominant, True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        inst.submit(x)
+        inst.wait()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    k_ms, k_launches = inst.kernel_time(dominant)
+    inst.time_kernel(dominant, False)
+
+    out = inst.read_logits()
+    if not np.all(np.isfinite(out)):
+        print("non-finite logits", file=sys.stderr)
+        return 1
+
+    d, F_, L, H = shape["d_model"], shape["d_ff"], shape["n_layers"], shape["n_heads"]
+    flops_seq = forward_flops(L, d, F_, H, S, shape["n_out"])
+    ms_step = elapsed * 1e3 / args.steps
+    value = B * args.steps / elapsed
+    mfma_util = flops_seq * B / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12 * args.quota / 256) * 100
+
+    kernel_flops = 2.0 * (B * S) * d * F_
+    k_avg_s = k_ms * 1e-3 / max(k_launches, 1)
+    achieved = kernel_flops / k_avg_s / 1e12
+    peak = PEAK_BF16_TFLOPS * args.quota / 256
+    roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": round(peak, 1), "unit": "TFLOP/s",
+            "frac": round(achieved / peak, 4), "traffic": None,
+            "kernel": "FFN-up GEMM + bias + GELU", "avg_us": round(k_avg_s * 1e6, 2), "launches": k_launches}
+
+    result = {
+        "metric": "inferences/sec (aggregate, co-located) + MFMA util % at given CU quotas, 1 GPU",
+        "value": round(value, 2),
+        "unit": "inferences/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) fp32 embeddings, seeded random-init bf16 weights)",
+        "config": {"workload": WORKLOAD, "n_layers": L, "d_model": d, "n_heads": H, "d_ff": F_,
+                   "global_batch": B, "seq_len": S, "quota_cus": args.quota, "parallelism": "none (1 instance)"},
+        "mfma_util_pct": round(mfma_util, 2),
+        "roofline": roof,
+    }
+    inst.close()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(shape, args.cpu_sample)
+    print(json.dumps(result))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

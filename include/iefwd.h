@@ -1,0 +1,257 @@
+/*
+ * iefwd.h -- C ABI of libiefwd: the batched transformer forward pass of
+ * co-located serverless DL instances on one MI355X (gfx950), each with a
+ * compute quota expressed as a number of compute units (CUs).
+ *
+ * Problem statement this interface follows (Dilu, ASPLOS '25):
+ *  - every serverless DL instance holds its own model and serves requests in
+ *    batches of at most its inference batch size (Sec. 3.2, "Multi-Factor
+ *    Profiling");
+ *  - each instance has a compute quota that is not an integer number of GPUs
+ *    but a continuous share, scaled up and down at run time (Sec. 3.4,
+ *    "Adaptive 2D Co-Scaling"; Table 1, <request, limit> quotas);
+ *  - a quota change acts between iterations (one batch execution is one
+ *    iteration of an inference instance, Sec. 3.4.1 and Alg. 2);
+ *  - co-located instances are isolated from each other (Sec. 3.4.1, Discussion).
+ * Here the quota is a set of CUs: each instance launches on a HIP stream whose
+ * hardware queue carries a CU mask, and a new mask takes effect at the next
+ * batch boundary.
+ *
+ * Conventions
+ *  - Every function returns an int status (IEFWD_OK = 0, negative = error)
+ *    unless stated otherwise.  No C++ exception crosses the ABI; nothing aborts.
+ *  - On error, iefwd_last_error() returns a message for the calling thread.
+ *  - The caller owns every input/output buffer; an instance owns its weights,
+ *    workspace and streams.  Calls on one instance must be serialised by the
+ *    caller; distinct instances are independent and may be driven from
+ *    different threads.
+ *  - Results are a function of (config, seed, input) only: bit-identical
+ *    across CU quotas, co-location, repeats and batch composition.
+ *  - Device pointers are HIP device addresses on the instance's device.
+ *  - After a HIP runtime error an instance is poisoned: every later call on it
+ *    returns IEFWD_EHIP; destroy and re-create it (weights are a pure function
+ *    of the config, so re-creation restores the same model).
+ */
+#ifndef IEFWD_H
+#define IEFWD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define IEFWD_ABI_VERSION 1u
+
+/* ---- status codes --------------------------------------------------------- */
+#define IEFWD_OK        0
+#define IEFWD_EINVAL   (-1)  /* bad argument: NULL, size out of range, bad shape */
+#define IEFWD_ENODEV   (-2)  /* no usable gfx950 device with that index */
+#define IEFWD_ENOMEM   (-3)  /* device or host allocation failed, or would exceed limits */
+#define IEFWD_EHIP     (-4)  /* HIP runtime error; the instance is poisoned */
+#define IEFWD_ESTATE   (-5)  /* call not valid in the instance's current state */
+#define IEFWD_EVERSION (-6)  /* config.abi_version != IEFWD_ABI_VERSION */
+
+typedef struct iefwd_instance iefwd_instance;   /* opaque, library-owned */
+
+/* ---- model configuration ----------------------------------------------------
+ * One transformer stack.  post-LN (pre_ln = 0): X1 = LN1(X + Attn(X)),
+ * X' = LN2(X1 + FFN(X1)).  pre-LN (pre_ln = 1): X1 = X + Attn(LN1(X)),
+ * X' = X1 + FFN(LN2(X1)), plus a final LN after the last layer.
+ * FFN(Y) = GELU(Y W1 + b1) W2 + b2 with the exact erf GELU.  Attention scores
+ * are Q K^T / sqrt(d_model / n_heads); causal = 1 keeps keys j <= i.
+ * Output: n_out > 0 -> per-token logits X_L Wh + bh, fp32 [batch, seq, n_out];
+ *         n_out = 0 -> final hidden states, fp32 [batch, seq, d_model].
+ * Limits: d_model % 128 == 0, d_model <= 4096, d_model / n_heads in {64, 128},
+ *         d_ff % 64 == 0, n_out <= 16, n_layers >= 1.
+ * Weights are drawn on the host from the seeded init spec: element e of the
+ * tensor with uid 32*layer + slot is sigma * N(0,1) from SplitMix64 +
+ * Box-Muller, rounded fp64 -> fp32 -> bf16 (see iefwd_export_tensor for slots).
+ */
+typedef struct iefwd_config {
+    uint32_t abi_version;   /* must be IEFWD_ABI_VERSION */
+    uint32_t n_layers;
+    uint32_t d_model;
+    uint32_t n_heads;
+    uint32_t d_ff;
+    uint32_t max_batch;     /* workspace is sized for max_batch * max_seq tokens */
+    uint32_t max_seq;
+    uint32_t n_out;         /* head width; 0 = return hidden states */
+    uint32_t pre_ln;        /* 0 = post-LN (BERT-style), 1 = pre-LN + final LN */
+    uint32_t causal;        /* 0 = bidirectional, 1 = causal mask */
+    uint32_t reserved0;     /* must be 0 */
+    float    ln_eps;        /* LayerNorm epsilon (default 1e-5) */
+    float    w_std;         /* std of weight matrices (default 0.02) */
+    float    b_std;         /* std of biases (default 0: biases are zero) */
+    float    ln_std;        /* gamma = 1 + ln_std*n, beta = ln_std*n (default 0) */
+    float    qk_std;        /* std of the Q and K column blocks of Wqkv; 0 = w_std */
+    uint64_t seed;          /* weight seed */
+} iefwd_config;
+
+/* Fills *cfg with the defaults above (abi_version set, all sizes 0). No status. */
+void iefwd_config_init(iefwd_config *cfg);
+
+/* ---- device ------------------------------------------------------------------ */
+
+/* Number of CUs and XCDs of HIP device `device`.  ENODEV if there is no such
+ * device or it is not gfx950. */
+int iefwd_device_info(int device, uint32_t *n_cu, uint32_t *n_xcd);
+
+/* Pure host function: the CU mask the library uses for a quota of `quota` CUs
+ * on a device with n_cu CUs in n_xcd equal XCDs.  Bit i of word i/32 enables
+ * mask bit i (the bit order of hipExtStreamCreateWithCUMask).  The CUs are
+ * spread evenly over the XCDs (XCD x gets quota/n_xcd CUs, the first
+ * quota % n_xcd XCDs one more), so that every XCD's L2 serves an equal share.
+ * n_words must be >= ceil(n_cu / 32); extra words are zeroed.
+ * EINVAL if quota is 0 or > n_cu, n_xcd is 0 or does not divide n_cu. */
+int iefwd_build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t quota,
+                        uint32_t *mask, uint32_t n_words);
+
+/* ---- instance lifecycle -------------------------------------------------------- */
+
+/* Creates an instance on `device`: validates cfg, generates the weights on the
+ * host (multi-threaded), uploads them, allocates the workspace and a stream
+ * masked to all CUs.  On error *out is set to NULL. */
+int iefwd_create(const iefwd_config *cfg, int device, iefwd_instance **out);
+
+/* Waits for in-flight work and frees everything.  NULL is accepted (no-op). */
+int iefwd_destroy(iefwd_instance *inst);
+
+/* ---- quota (compute share) ------------------------------------------------------ */
+
+/* Requests a quota of n_cu CUs (1 .. device CUs), spread evenly over XCDs as by
+ * iefwd_build_cu_mask.  Takes effect at the next iefwd_submit; a batch already
+ * in flight keeps its CUs.  EINVAL if n_cu is out of range. */
+int iefwd_set_quota(iefwd_instance *inst, uint32_t n_cu);
+
+/* Requests an explicit CU mask (n_words 32-bit words, bit order as above);
+ * same timing as iefwd_set_quota.  EINVAL if the mask enables no existing CU. */
+int iefwd_set_cu_mask(iefwd_instance *inst, const uint32_t *mask, uint32_t n_words);
+
+/* Copies the mask of the stream the instance currently launches on (the one
+ * applied at the last submit, or the initial all-CU mask). */
+int iefwd_get_cu_mask(const iefwd_instance *inst, uint32_t *mask, uint32_t n_words);
+
+/* ---- serving ---------------------------------------------------------------------- */
+
+/* Submits one batch: x is fp32 [batch, seq, d_model], row-major.  Asynchronous.
+ * x_is_device = 0: x is host memory, copied before the call returns.
+ * x_is_device = 1: x is device memory that must stay valid and unmodified
+ *                  until iefwd_wait / iefwd_read_logits returns.
+ * 1 <= batch <= max_batch, 1 <= seq <= max_seq.  One batch may be in flight per
+ * instance: submitting while one is in flight returns ESTATE.  A pending quota
+ * change is applied first (the new stream waits for the previous one). */
+int iefwd_submit(iefwd_instance *inst, const float *x, uint32_t batch, uint32_t seq,
+                 int x_is_device);
+
+/* Blocks until the in-flight batch (if any) is complete. */
+int iefwd_wait(iefwd_instance *inst);
+
+/* Waits for the last submitted batch, then copies its output (fp32
+ * [batch, seq, n_out], or [batch, seq, d_model] when n_out = 0) to out.
+ * n_floats must equal that element count exactly (else EINVAL).
+ * ESTATE if nothing was submitted yet. */
+int iefwd_read_logits(iefwd_instance *inst, float *out, size_t n_floats, int out_is_device);
+
+/* Device time of the last completed batch in milliseconds, from HIP events on
+ * the instance's stream (the per-iteration time an elasticity controller
+ * watches, Sec. 3.4.1).  ESTATE if no batch has completed. */
+int iefwd_last_batch_ms(iefwd_instance *inst, float *ms);
+
+/* The hipStream_t the instance currently launches on (for external ordering). */
+int iefwd_get_stream(iefwd_instance *inst, void **hip_stream);
+
+/* ---- per-kernel timing ------------------------------------------------------------- */
+
+/* Kernel classes of the forward pass. */
+#define IEFWD_K_QKV      0u   /* QKV projection GEMM + bias + head scatter */
+#define IEFWD_K_ATTN     1u   /* fused softmax attention */
+#define IEFWD_K_OUTPROJ  2u   /* output projection GEMM + bias + residual */
+#define IEFWD_K_FFN1     3u   /* FFN up GEMM + bias + GELU */
+#define IEFWD_K_FFN2     4u   /* FFN down GEMM + bias + residual */
+#define IEFWD_K_LN       5u   /* LayerNorm kernels (including the fused final LN + head) */
+#define IEFWD_K_COUNT    6u
+
+/* enable != 0: every later launch of class `kind` is bracketed by HIP events on
+ * the instance's stream; iefwd_kernel_time sums the bracketed durations of
+ * completed batches.  enable = 0 stops timing; both calls reset the sums. */
+int iefwd_time_kernel(iefwd_instance *inst, uint32_t kind, int enable);
+int iefwd_kernel_time(iefwd_instance *inst, uint32_t kind, double *total_ms, uint64_t *launches);
+
+/* ---- weights ------------------------------------------------------------------------ */
+
+/* Copies a stored tensor to host memory in its logical layout.
+ * Per-layer slots (layer < n_layers): 0 Wqkv bf16 [d, 3d], 1 bqkv bf16 [3d],
+ * 2 Wo bf16 [d, d], 3 bo bf16 [d], 4 ln1 gamma f32 [d], 5 ln1 beta f32 [d],
+ * 6 W1 bf16 [d, F], 7 b1 bf16 [F], 8 W2 bf16 [F, d], 9 b2 bf16 [d],
+ * 10 ln2 gamma f32 [d], 11 ln2 beta f32 [d].
+ * Global slots (layer == n_layers): 12 final-LN gamma f32 [d], 13 beta f32 [d],
+ * 14 Wh bf16 [d, n_out], 15 bh bf16 [n_out] (only when n_out > 0).
+ * Matrices are [in, out] row-major.  bytes must equal the tensor size. */
+int iefwd_export_tensor(const iefwd_instance *inst, uint32_t layer, uint32_t slot,
+                        void *host_dst, size_t bytes);
+
+/* ---- errors --------------------------------------------------------------------------- */
+
+/* Message for the last failed call on this thread ("" if none).  Valid until
+ * the next iefwd_* call on this thread.  Never NULL. */
+const char *iefwd_last_error(void);
+/* Static name of a status code.  Never NULL. */
+const char *iefwd_status_string(int status);
+
+/* ---- per-kernel entry points (parity tests) ------------------------------------------
+ * Each launches one kernel of the forward pass on `stream` (a hipStream_t, NULL
+ * = the null stream of the current device) and returns without synchronising.
+ * All pointers are device pointers; shapes are validated (EINVAL). */
+
+/* GEMM epilogues */
+#define IEFWD_EPI_BIAS_BF16       0u  /* out bf16 [M, N] = A W^T + b */
+#define IEFWD_EPI_BIAS_GELU_BF16  1u  /* out bf16 [M, N] = GELU(A W^T + b) */
+#define IEFWD_EPI_BIAS_RESID_F32  2u  /* out f32  [M, N] = resid + A W^T + b */
+
+/* out = epilogue(A W^T + b): A bf16 [M, K] row-major (activations), W bf16
+ * [N, K] row-major (the weight stored output-major), bias bf16 [N], resid f32
+ * [M, N] (only for IEFWD_EPI_BIAS_RESID_F32, else may be NULL).  Accumulates
+ * in fp32 with bf16 MFMA.  M >= 0, N % 64 == 0, K % 64 == 0. */
+int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void *bias,
+                    const float *resid, void *out, uint32_t M, uint32_t N, uint32_t K,
+                    void *stream);
+
+/* QKV projection with head scatter: A bf16 [batch*seq, d], W bf16 [3d, d],
+ * bias bf16 [3d].  Writes Q and K as bf16 [batch, heads, seq, dh] and V
+ * transposed as bf16 [batch, heads, dh, seq]. */
+int iefwd_test_gemm_qkv(const void *a, const void *w, const void *bias, void *q, void *k,
+                        void *vt, uint32_t batch, uint32_t seq, uint32_t d_model,
+                        uint32_t n_heads, void *stream);
+
+/* ctx bf16 [batch, seq, heads*dh] = softmax(Q K^T / sqrt(dh) [+ causal]) V per
+ * (batch, head), from Q, K bf16 [batch, heads, seq, dh] and Vt bf16
+ * [batch, heads, dh, seq].  dh in {64, 128}. */
+int iefwd_test_attention(const void *q, const void *k, const void *vt, void *ctx,
+                         uint32_t batch, uint32_t n_heads, uint32_t seq, uint32_t head_dim,
+                         int causal, void *stream);
+
+/* Row LayerNorm of z f32 [rows, d]: out_f32 (may be NULL) and out_bf16 (may be
+ * NULL) get gamma * (z - mean) / sqrt(var + eps) + beta. */
+int iefwd_test_layernorm(const float *z, const float *gamma, const float *beta,
+                         float *out_f32, void *out_bf16, uint32_t rows, uint32_t d,
+                         float eps, void *stream);
+
+/* LayerNorm followed by the per-token head: logits f32 [rows, n_out] =
+ * LN(z) Wh^T + bh with Wh bf16 [n_out, d] (output-major), bh bf16 [n_out]. */
+int iefwd_test_ln_head(const float *z, const float *gamma, const float *beta,
+                       const void *wh, const void *bh, float *logits, uint32_t rows,
+                       uint32_t d, uint32_t n_out, float eps, void *stream);
+
+/* CU residency probe: launches n_groups workgroups of 64 threads on `stream`;
+ * workgroup g writes out[2g] = XCC id, out[2g+1] = the hardware id register
+ * (CU, SIMD, shader-array and shader-engine fields).  out: device uint32
+ * [2 * n_groups]. */
+int iefwd_test_cu_probe(void *stream, uint32_t n_groups, uint32_t *out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IEFWD_H */

@@ -57,6 +57,16 @@ def attention_probs(q: np.ndarray, k: np.ndarray, causal: bool) -> np.ndarray:
     return softmax_rows(a)
 
 
+def linear(y: np.ndarray, w: np.ndarray, b: np.ndarray) -> np.ndarray:
+    """y W + b with W in the logical [in, out] layout."""
+    return y @ w + b
+
+
+def attention_context(q: np.ndarray, k: np.ndarray, v: np.ndarray, causal: bool) -> np.ndarray:
+    """softmax(q k^T / sqrt(dh) [+ causal]) v for [..., S, dh] operands."""
+    return attention_probs(q, k, causal) @ v
+
+
 def self_attention(y: np.ndarray, w: dict, n_heads: int, causal: bool) -> np.ndarray:
     """Attn(Y) for Y of shape [B, S, d]: fused QKV projection, per-head
     softmax attention, heads concatenated, output projection."""

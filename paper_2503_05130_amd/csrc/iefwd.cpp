@@ -1,0 +1,798 @@
+// libiefwd: C ABI, instances and the forward-pass executor.
+//
+// An instance is one serverless DL function instance in the paper's sense
+// (Sec. 3.1 serving plane): its own model weights, its own workspace, and a
+// compute share that the elasticity layer moves between a request and a limit
+// at run time (Sec. 3.2, 3.4).  Each batch execution is one iteration; the
+// share (a CU mask on the instance's stream) changes only between iterations.
+#include "iefwd.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "init_weights.h"
+#include "kernels.h"
+#include "quota.h"
+
+using namespace iefwd;
+
+namespace {
+
+thread_local std::string t_last_error;
+
+struct Error {
+    int status;
+    std::string msg;
+};
+
+[[noreturn]] void fail(int status, const std::string &msg) { throw Error{status, msg}; }
+
+void hip_check(hipError_t e, const char *what) {
+    if (e != hipSuccess) fail(IEFWD_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+template <class F>
+int guarded(F &&f) {
+    t_last_error.clear();
+    try {
+        f();
+        return IEFWD_OK;
+    } catch (const Error &e) {
+        t_last_error = e.msg;
+        return e.status;
+    } catch (const std::bad_alloc &) {
+        t_last_error = "host allocation failed";
+        return IEFWD_ENOMEM;
+    } catch (...) {
+        t_last_error = "unexpected internal error";
+        return IEFWD_EHIP;
+    }
+}
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ------------------------------------------------------------------------------- device
+
+struct DeviceInfo {
+    uint32_t n_cu, n_xcd;
+};
+
+DeviceInfo query_device(int device) {
+    int count = 0;
+    if (hipGetDeviceCount(&count) != hipSuccess || count <= 0) {
+        (void)hipGetLastError();
+        fail(IEFWD_ENODEV, "no HIP device available");
+    }
+    if (device < 0 || device >= count) fail(IEFWD_ENODEV, "device index out of range");
+    hipDeviceProp_t prop;
+    hip_check(hipGetDeviceProperties(&prop, device), "hipGetDeviceProperties");
+    if (std::strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        fail(IEFWD_ENODEV, std::string("device is ") + prop.gcnArchName + ", not gfx950");
+    int xcc = 0;
+    if (hipDeviceGetAttribute(&xcc, hipDeviceAttributeNumberOfXccs, device) != hipSuccess || xcc <= 0) {
+        (void)hipGetLastError();
+        xcc = 8;
+    }
+    return DeviceInfo{(uint32_t)prop.multiProcessorCount, (uint32_t)xcc};
+}
+
+// ------------------------------------------------------------------------------- config
+
+void validate_config(const iefwd_config &c) {
+    if (c.abi_version != IEFWD_ABI_VERSION) fail(IEFWD_EVERSION, "config.abi_version mismatch");
+    auto bad = [](const char *m) { fail(IEFWD_EINVAL, m); };
+    if (c.reserved0 != 0) bad("config.reserved0 must be 0");
+    if (c.n_layers < 1 || c.n_layers > 4096) bad("n_layers must be in [1, 4096]");
+    if (c.d_model < 128 || c.d_model > 4096 || c.d_model % 128 != 0) bad("d_model must be a multiple of 128 in [128, 4096]");
+    if (c.n_heads < 1 || c.d_model % c.n_heads != 0) bad("n_heads must divide d_model");
+    const uint32_t dh = c.d_model / c.n_heads;
+    if (dh != 64 && dh != 128) bad("head dim d_model / n_heads must be 64 or 128");
+    if (c.d_ff < 64 || c.d_ff > 65536 || c.d_ff % 64 != 0) bad("d_ff must be a multiple of 64 in [64, 65536]");
+    if (c.n_out > 16) bad("n_out must be <= 16");
+    if (c.pre_ln > 1 || c.causal > 1) bad("pre_ln and causal must be 0 or 1");
+    if (c.max_batch < 1 || c.max_seq < 1) bad("max_batch and max_seq must be >= 1");
+    if ((uint64_t)c.max_batch * c.n_heads > 65535) bad("max_batch * n_heads must be <= 65535");
+    const uint64_t tmax = (uint64_t)c.max_batch * c.max_seq;
+    // element offsets inside the GEMM are 32-bit: rows * K must stay below 2^31
+    if (tmax * std::max<uint64_t>(c.d_ff, 3ull * c.d_model) >= (1ull << 31)) bad("max_batch * max_seq too large");
+    if (!(c.ln_eps > 0.f) || !std::isfinite(c.ln_eps)) bad("ln_eps must be positive and finite");
+    for (float s : {c.w_std, c.b_std, c.ln_std, c.qk_std})
+        if (!(s >= 0.f) || !std::isfinite(s)) bad("init std values must be finite and >= 0");
+}
+
+// ------------------------------------------------------------------------------- instance
+
+struct LayerWeights {
+    bf16_t *wqkv, *bqkv, *wo, *bo, *w1, *b1, *w2, *b2;   // matrices output-major [out, in]
+    float *g1, *be1, *g2, *be2;
+};
+
+}  // namespace
+
+struct iefwd_instance {
+    iefwd_config cfg{};
+    int device = 0;
+    DeviceInfo dev{};
+    uint32_t head_dim = 0;
+
+    // weights: one device allocation, carved
+    void *wblob = nullptr;
+    std::vector<LayerWeights> layers;
+    float *gf = nullptr, *bef = nullptr;
+    bf16_t *wh = nullptr, *bh = nullptr;
+
+    // workspace: one device allocation, carved (sized for max_batch * max_seq)
+    void *wsblob = nullptr;
+    float *h = nullptr, *z = nullptr, *h1 = nullptr, *out = nullptr, *xstage = nullptr;
+    bf16_t *hb = nullptr, *h1b = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr, *ctx = nullptr,
+           *u = nullptr;
+
+    // quota
+    MaskedStreams streams;
+    hipStream_t stream = nullptr;
+    std::vector<uint32_t> mask, pending_mask;
+    bool pending = false;
+
+    // batch state
+    enum class State { Idle, InFlight, Done } state = State::Idle;
+    uint32_t batch = 0, seq = 0;
+    hipEvent_t ev_start = nullptr, ev_end = nullptr, ev_copy = nullptr;
+    bool poisoned = false;
+    bool have_batch = false;
+
+    // per-kernel timing
+    struct Timing {
+        bool enabled = false;
+        std::vector<std::pair<hipEvent_t, hipEvent_t>> inflight;
+        double total_ms = 0;
+        uint64_t launches = 0;
+    } timing[IEFWD_K_COUNT];
+    std::vector<hipEvent_t> event_pool;
+
+    ~iefwd_instance();
+};
+
+namespace {
+
+void check_alive(const iefwd_instance *inst) {
+    if (!inst) fail(IEFWD_EINVAL, "instance is NULL");
+    if (inst->poisoned) fail(IEFWD_EHIP, "instance is poisoned by an earlier HIP error; destroy it");
+}
+
+// Runs f; a HIP error inside poisons the instance.
+template <class F>
+void on_device(iefwd_instance *inst, F &&f) {
+    try {
+        hip_check(hipSetDevice(inst->device), "hipSetDevice");
+        f();
+    } catch (const Error &e) {
+        if (e.status == IEFWD_EHIP) inst->poisoned = true;
+        throw;
+    }
+}
+
+hipEvent_t take_event(iefwd_instance *inst) {
+    if (!inst->event_pool.empty()) {
+        hipEvent_t e = inst->event_pool.back();
+        inst->event_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e;
+    hip_check(hipEventCreate(&e), "hipEventCreate");
+    return e;
+}
+
+// Launch one kernel of class `kind`, bracketed by events when that class is timed.
+template <class F>
+void launch(iefwd_instance *inst, uint32_t kind, const char *what, F &&f) {
+    auto &t = inst->timing[kind];
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (t.enabled) {
+        e0 = take_event(inst);
+        e1 = take_event(inst);
+        hip_check(hipEventRecord(e0, inst->stream), "hipEventRecord");
+    }
+    hip_check(f(), what);
+    if (t.enabled) {
+        hip_check(hipEventRecord(e1, inst->stream), "hipEventRecord");
+        t.inflight.emplace_back(e0, e1);
+    }
+}
+
+void collect_timings(iefwd_instance *inst) {
+    for (auto &t : inst->timing) {
+        for (auto &pr : t.inflight) {
+            float ms = 0;
+            hip_check(hipEventElapsedTime(&ms, pr.first, pr.second), "hipEventElapsedTime");
+            t.total_ms += ms;
+            t.launches += 1;
+            inst->event_pool.push_back(pr.first);
+            inst->event_pool.push_back(pr.second);
+        }
+        t.inflight.clear();
+    }
+}
+
+// The forward pass of one batch on inst->stream.  x: fp32 [T, d] device.
+void run_forward(iefwd_instance *I, const float *x) {
+    const iefwd_config &c = I->cfg;
+    const int T = (int)(I->batch * I->seq), d = (int)c.d_model, F = (int)c.d_ff;
+    const int H = (int)c.n_heads, dh = (int)I->head_dim, S = (int)I->seq, B = (int)I->batch;
+    const float eps = c.ln_eps;
+    hipStream_t s = I->stream;
+    QkvDst qd{I->q, I->k, I->vt, S, attn_seq_pad(S), H, dh, d};
+
+    auto attention_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid, float *dst) {
+        launch(I, IEFWD_K_QKV, "qkv gemm", [&] {
+            return launch_gemm(Epi::Qkv, y_bf16, w.wqkv, w.bqkv, nullptr, nullptr, T, 3 * d, d, &qd, s);
+        });
+        launch(I, IEFWD_K_ATTN, "attention", [&] {
+            return launch_attention(I->q, I->k, I->vt, I->ctx, B, H, S, dh, c.causal != 0, s);
+        });
+        launch(I, IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
+            return launch_gemm(Epi::BiasResidF32, I->ctx, w.wo, w.bo, resid, dst, T, d, d, nullptr, s);
+        });
+    };
+    auto ffn_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid, float *dst) {
+        launch(I, IEFWD_K_FFN1, "ffn1 gemm", [&] {
+            return launch_gemm(Epi::BiasGeluBf16, y_bf16, w.w1, w.b1, nullptr, I->u, T, F, d, nullptr, s);
+        });
+        launch(I, IEFWD_K_FFN2, "ffn2 gemm", [&] {
+            return launch_gemm(Epi::BiasResidF32, I->u, w.w2, w.b2, resid, dst, T, d, F, nullptr, s);
+        });
+    };
+    auto ln = [&](const float *src, const float *g, const float *b, float *o32, bf16_t *o16) {
+        launch(I, IEFWD_K_LN, "layernorm", [&] { return launch_layernorm(src, g, b, o32, o16, T, d, eps, s); });
+    };
+    auto ln_head = [&](const float *src, const float *g, const float *b) {
+        launch(I, IEFWD_K_LN, "ln+head", [&] {
+            return launch_ln_head(src, g, b, I->wh, I->bh, I->out, T, d, (int)c.n_out, eps, s);
+        });
+    };
+
+    const int L = (int)c.n_layers;
+    if (!c.pre_ln) {
+        // post-LN: X1 = LN1(X + Attn(X)); X' = LN2(X1 + FFN(X1))
+        launch(I, IEFWD_K_LN, "cast", [&] { return launch_cast_bf16(x, I->hb, (size_t)T * d, s); });
+        const float *resid = x;
+        for (int l = 0; l < L; ++l) {
+            const LayerWeights &w = I->layers[l];
+            attention_block(I->hb, w, resid, I->z);
+            ln(I->z, w.g1, w.be1, I->h1, I->h1b);
+            ffn_block(I->h1b, w, I->h1, I->z);
+            if (l + 1 < L) {
+                ln(I->z, w.g2, w.be2, I->h, I->hb);
+                resid = I->h;
+            } else if (c.n_out > 0) {
+                ln_head(I->z, w.g2, w.be2);
+            } else {
+                ln(I->z, w.g2, w.be2, I->out, nullptr);
+            }
+        }
+    } else {
+        // pre-LN: X1 = X + Attn(LN1(X)); X' = X1 + FFN(LN2(X1)); final LN
+        const float *xcur = x;
+        for (int l = 0; l < L; ++l) {
+            const LayerWeights &w = I->layers[l];
+            ln(xcur, w.g1, w.be1, nullptr, I->hb);
+            attention_block(I->hb, w, xcur, I->h1);
+            ln(I->h1, w.g2, w.be2, nullptr, I->hb);
+            ffn_block(I->hb, w, I->h1, I->h);
+            xcur = I->h;
+        }
+        if (c.n_out > 0)
+            ln_head(xcur, I->gf, I->bef);
+        else
+            ln(xcur, I->gf, I->bef, I->out, nullptr);
+    }
+}
+
+size_t out_width(const iefwd_config &c) { return c.n_out > 0 ? c.n_out : c.d_model; }
+
+void upload_weights(iefwd_instance *I) {
+    const iefwd_config &c = I->cfg;
+    const uint32_t d = c.d_model, F = c.d_ff, L = c.n_layers;
+    // sizes (elements)
+    const size_t per_layer_bf16 = (size_t)3 * d * d + 3 * d + (size_t)d * d + d + (size_t)d * F + F + (size_t)F * d + d;
+    const size_t per_layer_f32 = 4 * (size_t)d;
+    size_t bytes = 0;
+    auto reserve = [&](size_t n) { size_t off = bytes; bytes = round_up(bytes + n, 256); return off; };
+    std::vector<size_t> offs;
+    for (uint32_t l = 0; l < L; ++l) {
+        offs.push_back(reserve((size_t)3 * d * d * 2));
+        offs.push_back(reserve((size_t)3 * d * 2));
+        offs.push_back(reserve((size_t)d * d * 2));
+        offs.push_back(reserve((size_t)d * 2));
+        offs.push_back(reserve((size_t)d * F * 2));
+        offs.push_back(reserve((size_t)F * 2));
+        offs.push_back(reserve((size_t)F * d * 2));
+        offs.push_back(reserve((size_t)d * 2));
+        for (int i = 0; i < 4; ++i) offs.push_back(reserve((size_t)d * 4));
+    }
+    const size_t g_off = reserve((size_t)d * 4), b_off = reserve((size_t)d * 4);
+    const size_t wh_off = reserve((size_t)std::max<uint32_t>(c.n_out, 1) * d * 2);
+    const size_t bh_off = reserve((size_t)std::max<uint32_t>(c.n_out, 1) * 2);
+    (void)per_layer_bf16;
+    (void)per_layer_f32;
+
+    if (hipMalloc(&I->wblob, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        I->wblob = nullptr;
+        fail(IEFWD_ENOMEM, "device allocation of weights failed");
+    }
+    char *base = static_cast<char *>(I->wblob);
+
+    std::vector<uint16_t> stage16((size_t)std::max<size_t>((size_t)3 * d * d, (size_t)d * F));
+    std::vector<float> stage32(d);
+    const double ws = c.w_std, bs = c.b_std, ls = c.ln_std, qs = c.qk_std;
+    const uint64_t seed = c.seed;
+    auto put16 = [&](size_t off, size_t n) {
+        hip_check(hipMemcpy(base + off, stage16.data(), n * 2, hipMemcpyHostToDevice), "weight upload");
+    };
+    auto put32 = [&](size_t off, size_t n) {
+        hip_check(hipMemcpy(base + off, stage32.data(), n * 4, hipMemcpyHostToDevice), "weight upload");
+    };
+
+    I->layers.resize(L);
+    size_t oi = 0;
+    for (uint32_t l = 0; l < L; ++l) {
+        LayerWeights &w = I->layers[l];
+        auto at16 = [&](size_t off) { return reinterpret_cast<bf16_t *>(base + off); };
+        auto at32 = [&](size_t off) { return reinterpret_cast<float *>(base + off); };
+        // slot 0: Wqkv [d, 3d]; columns [0, 2d) are the Q and K blocks
+        generate_matrix_transposed(tensor_key(seed, l, 0), d, 3 * d, 2 * d, ws, qs, stage16.data());
+        w.wqkv = at16(offs[oi]); put16(offs[oi++], (size_t)3 * d * d);
+        generate_vector_bf16(tensor_key(seed, l, 1), 3 * d, bs, stage16.data());
+        w.bqkv = at16(offs[oi]); put16(offs[oi++], 3 * d);
+        generate_matrix_transposed(tensor_key(seed, l, 2), d, d, 0, ws, 0.0, stage16.data());
+        w.wo = at16(offs[oi]); put16(offs[oi++], (size_t)d * d);
+        generate_vector_bf16(tensor_key(seed, l, 3), d, bs, stage16.data());
+        w.bo = at16(offs[oi]); put16(offs[oi++], d);
+        generate_matrix_transposed(tensor_key(seed, l, 6), d, F, 0, ws, 0.0, stage16.data());
+        w.w1 = at16(offs[oi]); put16(offs[oi++], (size_t)d * F);
+        generate_vector_bf16(tensor_key(seed, l, 7), F, bs, stage16.data());
+        w.b1 = at16(offs[oi]); put16(offs[oi++], F);
+        generate_matrix_transposed(tensor_key(seed, l, 8), F, d, 0, ws, 0.0, stage16.data());
+        w.w2 = at16(offs[oi]); put16(offs[oi++], (size_t)F * d);
+        generate_vector_bf16(tensor_key(seed, l, 9), d, bs, stage16.data());
+        w.b2 = at16(offs[oi]); put16(offs[oi++], d);
+        generate_vector_f32(tensor_key(seed, l, 4), d, 1.0, ls, stage32.data());
+        w.g1 = at32(offs[oi]); put32(offs[oi++], d);
+        generate_vector_f32(tensor_key(seed, l, 5), d, 0.0, ls, stage32.data());
+        w.be1 = at32(offs[oi]); put32(offs[oi++], d);
+        generate_vector_f32(tensor_key(seed, l, 10), d, 1.0, ls, stage32.data());
+        w.g2 = at32(offs[oi]); put32(offs[oi++], d);
+        generate_vector_f32(tensor_key(seed, l, 11), d, 0.0, ls, stage32.data());
+        w.be2 = at32(offs[oi]); put32(offs[oi++], d);
+    }
+    generate_vector_f32(tensor_key(seed, L, 12), d, 1.0, ls, stage32.data());
+    I->gf = reinterpret_cast<float *>(base + g_off); put32(g_off, d);
+    generate_vector_f32(tensor_key(seed, L, 13), d, 0.0, ls, stage32.data());
+    I->bef = reinterpret_cast<float *>(base + b_off); put32(b_off, d);
+    I->wh = reinterpret_cast<bf16_t *>(base + wh_off);
+    I->bh = reinterpret_cast<bf16_t *>(base + bh_off);
+    if (c.n_out > 0) {
+        generate_matrix_transposed(tensor_key(seed, L, 14), d, c.n_out, 0, ws, 0.0, stage16.data());
+        put16(wh_off, (size_t)c.n_out * d);
+        generate_vector_bf16(tensor_key(seed, L, 15), c.n_out, bs, stage16.data());
+        put16(bh_off, c.n_out);
+    }
+}
+
+void alloc_workspace(iefwd_instance *I) {
+    const iefwd_config &c = I->cfg;
+    const size_t T = (size_t)c.max_batch * c.max_seq, d = c.d_model, F = c.d_ff;
+    const size_t spad = (size_t)attn_seq_pad((int)c.max_seq);
+    size_t bytes = 0;
+    auto reserve = [&](size_t n) { size_t off = bytes; bytes = round_up(bytes + n, 256); return off; };
+    const size_t o_h = reserve(T * d * 4), o_z = reserve(T * d * 4), o_h1 = reserve(T * d * 4);
+    const size_t o_out = reserve(T * out_width(c) * 4), o_x = reserve(T * d * 4);
+    const size_t o_hb = reserve(T * d * 2), o_h1b = reserve(T * d * 2), o_q = reserve(T * d * 2);
+    const size_t o_k = reserve(T * d * 2), o_vt = reserve((size_t)c.max_batch * d * spad * 2);
+    const size_t o_ctx = reserve(T * d * 2), o_u = reserve(T * F * 2);
+    if (hipMalloc(&I->wsblob, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        I->wsblob = nullptr;
+        fail(IEFWD_ENOMEM, "device allocation of the workspace failed");
+    }
+    char *b = static_cast<char *>(I->wsblob);
+    I->h = reinterpret_cast<float *>(b + o_h);
+    I->z = reinterpret_cast<float *>(b + o_z);
+    I->h1 = reinterpret_cast<float *>(b + o_h1);
+    I->out = reinterpret_cast<float *>(b + o_out);
+    I->xstage = reinterpret_cast<float *>(b + o_x);
+    I->hb = reinterpret_cast<bf16_t *>(b + o_hb);
+    I->h1b = reinterpret_cast<bf16_t *>(b + o_h1b);
+    I->q = reinterpret_cast<bf16_t *>(b + o_q);
+    I->k = reinterpret_cast<bf16_t *>(b + o_k);
+    I->vt = reinterpret_cast<bf16_t *>(b + o_vt);
+    I->ctx = reinterpret_cast<bf16_t *>(b + o_ctx);
+    I->u = reinterpret_cast<bf16_t *>(b + o_u);
+}
+
+void apply_pending_quota(iefwd_instance *I) {
+    if (!I->pending) return;
+    hipStream_t next = nullptr;
+    hip_check(I->streams.get(I->pending_mask, I->stream, &next), "hipExtStreamCreateWithCUMask");
+    if (next != I->stream) {
+        // order the new queue after everything the old one was given
+        if (I->have_batch) hip_check(hipStreamWaitEvent(next, I->ev_end, 0), "hipStreamWaitEvent");
+        I->stream = next;
+        I->mask = I->pending_mask;
+    }
+    I->pending = false;
+}
+
+void wait_batch(iefwd_instance *I) {
+    if (I->state != iefwd_instance::State::InFlight) return;
+    hip_check(hipEventSynchronize(I->ev_end), "hipEventSynchronize");
+    collect_timings(I);
+    I->state = iefwd_instance::State::Done;
+}
+
+}  // namespace
+
+iefwd_instance::~iefwd_instance() {
+    if (stream) (void)hipStreamSynchronize(stream);
+    streams.clear();
+    for (auto &t : timing)
+        for (auto &pr : t.inflight) {
+            (void)hipEventDestroy(pr.first);
+            (void)hipEventDestroy(pr.second);
+        }
+    for (hipEvent_t e : event_pool) (void)hipEventDestroy(e);
+    for (hipEvent_t e : {ev_start, ev_end, ev_copy})
+        if (e) (void)hipEventDestroy(e);
+    if (wsblob) (void)hipFree(wsblob);
+    if (wblob) (void)hipFree(wblob);
+}
+
+// =================================================================================== ABI
+
+extern "C" {
+
+void iefwd_config_init(iefwd_config *cfg) {
+    if (!cfg) return;
+    std::memset(cfg, 0, sizeof *cfg);
+    cfg->abi_version = IEFWD_ABI_VERSION;
+    cfg->ln_eps = 1e-5f;
+    cfg->w_std = 0.02f;
+}
+
+int iefwd_device_info(int device, uint32_t *n_cu, uint32_t *n_xcd) {
+    return guarded([&] {
+        if (!n_cu || !n_xcd) fail(IEFWD_EINVAL, "NULL output pointer");
+        const DeviceInfo d = query_device(device);
+        *n_cu = d.n_cu;
+        *n_xcd = d.n_xcd;
+    });
+}
+
+int iefwd_build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t quota, uint32_t *mask, uint32_t n_words) {
+    return guarded([&] {
+        if (!build_cu_mask(n_cu, n_xcd, quota, mask, n_words))
+            fail(IEFWD_EINVAL, "invalid mask request (quota 1..n_cu, n_xcd dividing n_cu, enough words)");
+    });
+}
+
+int iefwd_create(const iefwd_config *cfg, int device, iefwd_instance **out) {
+    if (out) *out = nullptr;
+    iefwd_instance *inst = nullptr;
+    const int st = guarded([&] {
+        if (!cfg || !out) fail(IEFWD_EINVAL, "NULL argument");
+        validate_config(*cfg);
+        const DeviceInfo dev = query_device(device);
+        hip_check(hipSetDevice(device), "hipSetDevice");
+        inst = new iefwd_instance();
+        inst->cfg = *cfg;
+        inst->device = device;
+        inst->dev = dev;
+        inst->head_dim = cfg->d_model / cfg->n_heads;
+        upload_weights(inst);
+        alloc_workspace(inst);
+        hip_check(hipEventCreate(&inst->ev_start), "hipEventCreate");
+        hip_check(hipEventCreate(&inst->ev_end), "hipEventCreate");
+        hip_check(hipEventCreateWithFlags(&inst->ev_copy, hipEventDisableTiming), "hipEventCreate");
+        std::vector<uint32_t> all(mask_words(dev.n_cu));
+        if (!build_cu_mask(dev.n_cu, dev.n_xcd, dev.n_cu, all.data(), (uint32_t)all.size()))
+            fail(IEFWD_ENODEV, "device CU count is not a multiple of its XCD count");
+        hip_check(inst->streams.get(all, nullptr, &inst->stream), "hipExtStreamCreateWithCUMask");
+        inst->mask = all;
+    });
+    if (st != IEFWD_OK) {
+        delete inst;
+        return st;
+    }
+    *out = inst;
+    return IEFWD_OK;
+}
+
+int iefwd_destroy(iefwd_instance *inst) {
+    if (!inst) return IEFWD_OK;
+    return guarded([&] {
+        (void)hipSetDevice(inst->device);
+        delete inst;
+    });
+}
+
+int iefwd_set_quota(iefwd_instance *inst, uint32_t n_cu) {
+    return guarded([&] {
+        check_alive(inst);
+        std::vector<uint32_t> m(mask_words(inst->dev.n_cu));
+        if (!build_cu_mask(inst->dev.n_cu, inst->dev.n_xcd, n_cu, m.data(), (uint32_t)m.size()))
+            fail(IEFWD_EINVAL, "quota must be in [1, device CUs]");
+        inst->pending_mask = m;
+        inst->pending = true;
+    });
+}
+
+int iefwd_set_cu_mask(iefwd_instance *inst, const uint32_t *mask, uint32_t n_words) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!mask || n_words == 0) fail(IEFWD_EINVAL, "NULL or empty mask");
+        std::vector<uint32_t> m(mask_words(inst->dev.n_cu), 0u);
+        for (uint32_t i = 0; i < m.size() && i < n_words; ++i) m[i] = mask[i];
+        const uint32_t tail = inst->dev.n_cu % 32;
+        if (tail) m.back() &= (1u << tail) - 1u;
+        if (mask_popcount(m, inst->dev.n_cu) == 0) fail(IEFWD_EINVAL, "mask enables no CU of this device");
+        inst->pending_mask = m;
+        inst->pending = true;
+    });
+}
+
+int iefwd_get_cu_mask(const iefwd_instance *inst, uint32_t *mask, uint32_t n_words) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!mask || n_words < inst->mask.size()) fail(IEFWD_EINVAL, "mask buffer too small");
+        std::fill(mask, mask + n_words, 0u);
+        std::copy(inst->mask.begin(), inst->mask.end(), mask);
+    });
+}
+
+int iefwd_submit(iefwd_instance *inst, const float *x, uint32_t batch, uint32_t seq, int x_is_device) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!x) fail(IEFWD_EINVAL, "x is NULL");
+        if (batch < 1 || batch > inst->cfg.max_batch) fail(IEFWD_EINVAL, "batch out of range [1, max_batch]");
+        if (seq < 1 || seq > inst->cfg.max_seq) fail(IEFWD_EINVAL, "seq out of range [1, max_seq]");
+        if (inst->state == iefwd_instance::State::InFlight)
+            fail(IEFWD_ESTATE, "a batch is already in flight; call iefwd_wait or iefwd_read_logits first");
+        on_device(inst, [&] {
+            apply_pending_quota(inst);
+            inst->batch = batch;
+            inst->seq = seq;
+            const size_t n = (size_t)batch * seq * inst->cfg.d_model;
+            const float *xin = x;
+            if (!x_is_device) {
+                hip_check(hipMemcpyAsync(inst->xstage, x, n * 4, hipMemcpyHostToDevice, inst->stream), "input copy");
+                hip_check(hipEventRecord(inst->ev_copy, inst->stream), "hipEventRecord");
+                hip_check(hipEventSynchronize(inst->ev_copy), "hipEventSynchronize");
+                xin = inst->xstage;
+            }
+            hip_check(hipEventRecord(inst->ev_start, inst->stream), "hipEventRecord");
+            run_forward(inst, xin);
+            hip_check(hipEventRecord(inst->ev_end, inst->stream), "hipEventRecord");
+            inst->state = iefwd_instance::State::InFlight;
+            inst->have_batch = true;
+        });
+    });
+}
+
+int iefwd_wait(iefwd_instance *inst) {
+    return guarded([&] {
+        check_alive(inst);
+        on_device(inst, [&] { wait_batch(inst); });
+    });
+}
+
+int iefwd_read_logits(iefwd_instance *inst, float *out, size_t n_floats, int out_is_device) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!out) fail(IEFWD_EINVAL, "out is NULL");
+        if (!inst->have_batch) fail(IEFWD_ESTATE, "no batch has been submitted");
+        const size_t want = (size_t)inst->batch * inst->seq * out_width(inst->cfg);
+        if (n_floats != want) fail(IEFWD_EINVAL, "n_floats does not match batch * seq * output width");
+        on_device(inst, [&] {
+            wait_batch(inst);
+            hip_check(hipMemcpyAsync(out, inst->out, want * 4,
+                                     out_is_device ? hipMemcpyDeviceToDevice : hipMemcpyDeviceToHost, inst->stream),
+                      "output copy");
+            hip_check(hipStreamSynchronize(inst->stream), "hipStreamSynchronize");
+        });
+    });
+}
+
+int iefwd_last_batch_ms(iefwd_instance *inst, float *ms) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!ms) fail(IEFWD_EINVAL, "ms is NULL");
+        if (inst->state != iefwd_instance::State::Done) fail(IEFWD_ESTATE, "no completed batch");
+        on_device(inst, [&] { hip_check(hipEventElapsedTime(ms, inst->ev_start, inst->ev_end), "hipEventElapsedTime"); });
+    });
+}
+
+int iefwd_get_stream(iefwd_instance *inst, void **hip_stream) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!hip_stream) fail(IEFWD_EINVAL, "NULL output pointer");
+        *hip_stream = (void *)inst->stream;
+    });
+}
+
+int iefwd_time_kernel(iefwd_instance *inst, uint32_t kind, int enable) {
+    return guarded([&] {
+        check_alive(inst);
+        if (kind >= IEFWD_K_COUNT) fail(IEFWD_EINVAL, "unknown kernel class");
+        if (inst->state == iefwd_instance::State::InFlight) fail(IEFWD_ESTATE, "a batch is in flight");
+        auto &t = inst->timing[kind];
+        t.enabled = enable != 0;
+        t.total_ms = 0;
+        t.launches = 0;
+    });
+}
+
+int iefwd_kernel_time(iefwd_instance *inst, uint32_t kind, double *total_ms, uint64_t *launches) {
+    return guarded([&] {
+        check_alive(inst);
+        if (kind >= IEFWD_K_COUNT) fail(IEFWD_EINVAL, "unknown kernel class");
+        if (!total_ms || !launches) fail(IEFWD_EINVAL, "NULL output pointer");
+        *total_ms = inst->timing[kind].total_ms;
+        *launches = inst->timing[kind].launches;
+    });
+}
+
+int iefwd_export_tensor(const iefwd_instance *cinst, uint32_t layer, uint32_t slot, void *host_dst, size_t bytes) {
+    iefwd_instance *inst = const_cast<iefwd_instance *>(cinst);
+    return guarded([&] {
+        check_alive(inst);
+        if (!host_dst) fail(IEFWD_EINVAL, "host_dst is NULL");
+        const iefwd_config &c = inst->cfg;
+        const size_t d = c.d_model, F = c.d_ff;
+        const void *src = nullptr;
+        size_t rows = 1, cols = 0, esize = 2;   // logical [rows=in, cols=out]
+        bool matrix = false;
+        if (layer < c.n_layers) {
+            const LayerWeights &w = inst->layers[layer];
+            switch (slot) {
+            case 0: src = w.wqkv; rows = d; cols = 3 * d; matrix = true; break;
+            case 1: src = w.bqkv; cols = 3 * d; break;
+            case 2: src = w.wo; rows = d; cols = d; matrix = true; break;
+            case 3: src = w.bo; cols = d; break;
+            case 4: src = w.g1; cols = d; esize = 4; break;
+            case 5: src = w.be1; cols = d; esize = 4; break;
+            case 6: src = w.w1; rows = d; cols = F; matrix = true; break;
+            case 7: src = w.b1; cols = F; break;
+            case 8: src = w.w2; rows = F; cols = d; matrix = true; break;
+            case 9: src = w.b2; cols = d; break;
+            case 10: src = w.g2; cols = d; esize = 4; break;
+            case 11: src = w.be2; cols = d; esize = 4; break;
+            default: fail(IEFWD_EINVAL, "per-layer slot must be 0..11");
+            }
+        } else if (layer == c.n_layers) {
+            switch (slot) {
+            case 12: src = inst->gf; cols = d; esize = 4; break;
+            case 13: src = inst->bef; cols = d; esize = 4; break;
+            case 14: if (!c.n_out) fail(IEFWD_EINVAL, "no head"); src = inst->wh; rows = d; cols = c.n_out; matrix = true; break;
+            case 15: if (!c.n_out) fail(IEFWD_EINVAL, "no head"); src = inst->bh; cols = c.n_out; break;
+            default: fail(IEFWD_EINVAL, "global slot must be 12..15");
+            }
+        } else {
+            fail(IEFWD_EINVAL, "layer out of range");
+        }
+        const size_t n = rows * cols;
+        if (bytes != n * esize) fail(IEFWD_EINVAL, "bytes does not match the tensor size");
+        on_device(inst, [&] {
+            if (!matrix) {
+                hip_check(hipMemcpy(host_dst, src, bytes, hipMemcpyDeviceToHost), "export copy");
+                return;
+            }
+            std::vector<uint16_t> stored(n);   // device layout [cols=out, rows=in]
+            hip_check(hipMemcpy(stored.data(), src, n * 2, hipMemcpyDeviceToHost), "export copy");
+            uint16_t *dst = static_cast<uint16_t *>(host_dst);
+            for (size_t o = 0; o < cols; ++o)
+                for (size_t i = 0; i < rows; ++i) dst[i * cols + o] = stored[o * rows + i];
+        });
+    });
+}
+
+const char *iefwd_last_error(void) { return t_last_error.c_str(); }
+
+const char *iefwd_status_string(int status) {
+    switch (status) {
+    case IEFWD_OK: return "IEFWD_OK";
+    case IEFWD_EINVAL: return "IEFWD_EINVAL";
+    case IEFWD_ENODEV: return "IEFWD_ENODEV";
+    case IEFWD_ENOMEM: return "IEFWD_ENOMEM";
+    case IEFWD_EHIP: return "IEFWD_EHIP";
+    case IEFWD_ESTATE: return "IEFWD_ESTATE";
+    case IEFWD_EVERSION: return "IEFWD_EVERSION";
+    default: return "IEFWD_UNKNOWN";
+    }
+}
+
+// ---------------------------------------------------------------- per-kernel entry points
+
+int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void *bias, const float *resid,
+                    void *out, uint32_t M, uint32_t N, uint32_t K, void *stream) {
+    return guarded([&] {
+        if (epilogue > IEFWD_EPI_BIAS_RESID_F32) fail(IEFWD_EINVAL, "unknown epilogue");
+        if (!a || !w || !bias || !out) fail(IEFWD_EINVAL, "NULL pointer");
+        if (epilogue == IEFWD_EPI_BIAS_RESID_F32 && !resid) fail(IEFWD_EINVAL, "resid is NULL");
+        if (N == 0 || N % 64 || K == 0 || K % 64) fail(IEFWD_EINVAL, "N and K must be positive multiples of 64");
+        if ((uint64_t)M * K >= (1ull << 31) || (uint64_t)N * K >= (1ull << 31)) fail(IEFWD_EINVAL, "too large");
+        hip_check(launch_gemm((Epi)epilogue, (const bf16_t *)a, (const bf16_t *)w, (const bf16_t *)bias, resid,
+                              out, (int)M, (int)N, (int)K, nullptr, (hipStream_t)stream),
+                  "gemm launch");
+    });
+}
+
+int iefwd_test_gemm_qkv(const void *a, const void *w, const void *bias, void *q, void *k, void *vt,
+                        uint32_t batch, uint32_t seq, uint32_t d_model, uint32_t n_heads, void *stream) {
+    return guarded([&] {
+        if (!a || !w || !bias || !q || !k || !vt) fail(IEFWD_EINVAL, "NULL pointer");
+        if (d_model == 0 || d_model % 64 || n_heads == 0 || d_model % n_heads) fail(IEFWD_EINVAL, "bad d_model / n_heads");
+        const uint32_t dh = d_model / n_heads;
+        if (dh % 4) fail(IEFWD_EINVAL, "head dim must be a multiple of 4");
+        if (batch == 0 || seq == 0) fail(IEFWD_EINVAL, "empty batch");
+        const uint64_t M = (uint64_t)batch * seq;
+        if (M * d_model >= (1ull << 31)) fail(IEFWD_EINVAL, "too large");
+        QkvDst qd{(bf16_t *)q, (bf16_t *)k, (bf16_t *)vt, (int)seq, attn_seq_pad((int)seq), (int)n_heads, (int)dh,
+                  (int)d_model};
+        hip_check(launch_gemm(Epi::Qkv, (const bf16_t *)a, (const bf16_t *)w, (const bf16_t *)bias, nullptr, nullptr,
+                              (int)M, (int)(3 * d_model), (int)d_model, &qd, (hipStream_t)stream),
+                  "qkv gemm launch");
+    });
+}
+
+int iefwd_test_attention(const void *q, const void *k, const void *vt, void *ctx, uint32_t batch, uint32_t n_heads,
+                         uint32_t seq, uint32_t head_dim, int causal, void *stream) {
+    return guarded([&] {
+        if (!q || !k || !vt || !ctx) fail(IEFWD_EINVAL, "NULL pointer");
+        if (head_dim != 64 && head_dim != 128) fail(IEFWD_EINVAL, "head_dim must be 64 or 128");
+        if (batch == 0 || n_heads == 0 || seq == 0) fail(IEFWD_EINVAL, "empty shape");
+        if ((uint64_t)batch * n_heads > 65535) fail(IEFWD_EINVAL, "batch * n_heads must be <= 65535");
+        hip_check(launch_attention((const bf16_t *)q, (const bf16_t *)k, (const bf16_t *)vt, (bf16_t *)ctx, (int)batch,
+                                   (int)n_heads, (int)seq, (int)head_dim, causal != 0, (hipStream_t)stream),
+                  "attention launch");
+    });
+}
+
+int iefwd_test_layernorm(const float *z, const float *gamma, const float *beta, float *out_f32, void *out_bf16,
+                         uint32_t rows, uint32_t d, float eps, void *stream) {
+    return guarded([&] {
+        if (!z || !gamma || !beta || (!out_f32 && !out_bf16)) fail(IEFWD_EINVAL, "NULL pointer");
+        if (d < 128 || d > 4096 || d % 128) fail(IEFWD_EINVAL, "d must be a multiple of 128 in [128, 4096]");
+        hip_check(launch_layernorm(z, gamma, beta, out_f32, (bf16_t *)out_bf16, (int)rows, (int)d, eps,
+                                   (hipStream_t)stream),
+                  "layernorm launch");
+    });
+}
+
+int iefwd_test_ln_head(const float *z, const float *gamma, const float *beta, const void *wh, const void *bh,
+                       float *logits, uint32_t rows, uint32_t d, uint32_t n_out, float eps, void *stream) {
+    return guarded([&] {
+        if (!z || !gamma || !beta || !wh || !bh || !logits) fail(IEFWD_EINVAL, "NULL pointer");
+        if (d < 128 || d > 4096 || d % 128) fail(IEFWD_EINVAL, "d must be a multiple of 128 in [128, 4096]");
+        if (n_out < 1 || n_out > 16) fail(IEFWD_EINVAL, "n_out must be in [1, 16]");
+        hip_check(launch_ln_head(z, gamma, beta, (const bf16_t *)wh, (const bf16_t *)bh, logits, (int)rows, (int)d,
+                                 (int)n_out, eps, (hipStream_t)stream),
+                  "ln_head launch");
+    });
+}
+
+int iefwd_test_cu_probe(void *stream, uint32_t n_groups, uint32_t *out) {
+    return guarded([&] {
+        if (!out) fail(IEFWD_EINVAL, "out is NULL");
+        if (n_groups == 0 || n_groups > (1u << 20)) fail(IEFWD_EINVAL, "n_groups must be in [1, 2^20]");
+        hip_check(launch_cu_probe(out, (int)n_groups, (hipStream_t)stream), "probe launch");
+    });
+}
+
+}  // extern "C"

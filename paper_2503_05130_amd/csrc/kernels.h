@@ -1,0 +1,61 @@
+// Launchers of the forward-pass kernels (gfx950).  Host-callable; every
+// launcher validates nothing beyond what its kernel's indexing needs -- shape
+// checks live in the callers (executor and test entry points).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace iefwd {
+
+using bf16_t = uint16_t;   // bf16 storage: the upper half of an fp32 bit pattern
+
+enum class Epi : int {
+    BiasBf16 = 0,       // out bf16 = acc + b
+    BiasGeluBf16 = 1,   // out bf16 = GELU(acc + b)
+    BiasResidF32 = 2,   // out f32  = resid + acc + b
+    Qkv = 3,            // acc + b scattered to Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad]
+};
+
+// Destination of the QKV epilogue.
+struct QkvDst {
+    bf16_t *q, *k, *vt;
+    int seq;       // S
+    int seq_pad;   // row stride of V^T (S rounded up to a multiple of 32)
+    int n_heads;
+    int head_dim;
+    int d_model;
+};
+
+// S rounded up to the attention kernel's key block.
+inline int attn_seq_pad(int seq) { return (seq + 31) / 32 * 32; }
+
+// out = epi(A W^T + b).  A bf16 [M,K], W bf16 [N,K], bias bf16 [N].
+// Requires N % 64 == 0, K % 64 == 0, M >= 1.
+hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
+                       const float *resid, void *out, int M, int N, int K,
+                       const QkvDst *qkv, hipStream_t stream);
+
+// ctx bf16 [B, S, H*dh] from Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad].
+hipError_t launch_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx,
+                            int batch, int n_heads, int seq, int head_dim, bool causal,
+                            hipStream_t stream);
+
+// Row LayerNorm, d % 128 == 0, d <= 4096.  out_f32 / out_bf16 may be null.
+hipError_t launch_layernorm(const float *z, const float *gamma, const float *beta,
+                            float *out_f32, bf16_t *out_bf16, int rows, int d, float eps,
+                            hipStream_t stream);
+
+// LayerNorm + per-token head: logits [rows, n_out] = LN(z) Wh^T + bh, Wh bf16 [n_out, d].
+hipError_t launch_ln_head(const float *z, const float *gamma, const float *beta,
+                          const bf16_t *wh, const bf16_t *bh, float *logits, int rows, int d,
+                          int n_out, float eps, hipStream_t stream);
+
+// bf16 copy of an fp32 array (round to nearest even); n % 4 == 0.
+hipError_t launch_cast_bf16(const float *x, bf16_t *y, size_t n, hipStream_t stream);
+
+// One 64-thread workgroup per entry: out[2g] = XCC id, out[2g+1] = HW_ID register.
+hipError_t launch_cu_probe(uint32_t *out, int n_groups, hipStream_t stream);
+
+}  // namespace iefwd

@@ -1,0 +1,70 @@
+#include "quota.h"
+
+#include <algorithm>
+
+namespace iefwd {
+
+bool build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t q, uint32_t *mask, uint32_t n_words) {
+    if (!mask || n_cu == 0 || n_xcd == 0 || n_cu % n_xcd != 0 || q == 0 || q > n_cu ||
+        n_words < mask_words(n_cu))
+        return false;
+    std::fill(mask, mask + n_words, 0u);
+    const uint32_t per_xcd = n_cu / n_xcd;
+    for (uint32_t x = 0; x < n_xcd; ++x) {
+        const uint32_t take = q / n_xcd + (x < q % n_xcd ? 1u : 0u);
+        for (uint32_t local = 0; local < take && local < per_xcd; ++local) {
+            const uint32_t bit = local * n_xcd + x;
+            mask[bit / 32] |= 1u << (bit % 32);
+        }
+    }
+    return true;
+}
+
+uint32_t mask_popcount(const std::vector<uint32_t> &mask, uint32_t n_cu) {
+    uint32_t n = 0;
+    for (uint32_t b = 0; b < n_cu && b / 32 < mask.size(); ++b) n += (mask[b / 32] >> (b % 32)) & 1u;
+    return n;
+}
+
+MaskedStreams::~MaskedStreams() { clear(); }
+
+void MaskedStreams::clear() {
+    for (Entry &e : entries_) {
+        (void)hipStreamSynchronize(e.stream);
+        (void)hipStreamDestroy(e.stream);
+    }
+    entries_.clear();
+}
+
+hipError_t MaskedStreams::get(const std::vector<uint32_t> &mask, hipStream_t keep, hipStream_t *out) {
+    ++clock_;
+    for (Entry &e : entries_) {
+        if (e.mask == mask) {
+            e.last_use = clock_;
+            *out = e.stream;
+            return hipSuccess;
+        }
+    }
+    if (entries_.size() >= capacity_) {
+        size_t victim = entries_.size();
+        for (size_t i = 0; i < entries_.size(); ++i) {
+            if (entries_[i].stream == keep) continue;
+            if (victim == entries_.size() || entries_[i].last_use < entries_[victim].last_use) victim = i;
+        }
+        if (victim < entries_.size()) {
+            hipError_t err = hipStreamSynchronize(entries_[victim].stream);
+            if (err != hipSuccess) return err;
+            err = hipStreamDestroy(entries_[victim].stream);
+            if (err != hipSuccess) return err;
+            entries_.erase(entries_.begin() + (long)victim);
+        }
+    }
+    hipStream_t s = nullptr;
+    hipError_t err = hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data());
+    if (err != hipSuccess) return err;
+    entries_.push_back(Entry{mask, s, clock_});
+    *out = s;
+    return hipSuccess;
+}
+
+}  // namespace iefwd

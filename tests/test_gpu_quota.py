@@ -1,0 +1,43 @@
+"""Quota layer on the GPU: a CU-masked stream confines an instance's
+workgroups to the CUs of its mask, spread evenly over the XCDs."""
+import collections
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2503_05130_amd as ie
+import workloads as W
+from tests.gpu_util import DEV, instance_config, run_instance
+
+pytestmark = pytest.mark.gpu
+
+
+def observed_cus(stream_handle, n_groups=8192):
+    out = torch.zeros(2 * n_groups, dtype=torch.int32, device=DEV)
+    ie.test_cu_probe(n_groups, out, stream=stream_handle)
+    torch.cuda.synchronize()
+    v = out.cpu().numpy().astype(np.uint32).reshape(-1, 2)
+    xcc = v[:, 0] & 0xF
+    cu = (v[:, 1] >> 8) & 0xFF          # CU, shader-array and shader-engine fields of HW_ID
+    return set(zip(xcc.tolist(), cu.tolist()))
+
+
+def test_device_info():
+    n_cu, n_xcd = ie.device_info(0)
+    print(f"device: {n_cu} CUs, {n_xcd} XCDs", flush=True)
+    assert n_cu == 256 and n_xcd == 8
+
+
+@pytest.mark.parametrize("q", [8, 24, 64, 128, 192, 256])
+def test_masked_stream_residency(q):
+    shape = W.model_shape("encoder_l1_d128_s32_b2")
+    with ie.Instance(**instance_config(shape, 1, 32)) as inst:
+        inst.set_quota(q)
+        run_instance(inst, W.make_input(1, 1, 32, 128))     # applies the mask
+        cus = observed_cus(inst.stream_handle())
+    per_xcc = collections.Counter(x for x, _ in cus)
+    print(f"quota {q}: {len(cus)} CUs seen, per XCC {sorted(per_xcc.items())}", flush=True)
+    assert len(cus) == q
+    assert len(per_xcc) == min(8, q)
+    assert max(per_xcc.values()) - min(per_xcc.values()) <= 1
