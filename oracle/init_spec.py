@@ -20,6 +20,8 @@ that each instance carries its own model weights, Sec. 3.2):
   n = sqrt(-2 ln u1) * cos(2 pi u2)  (Box & Muller 1958), in fp64.
 * weights/biases: sigma*n -> fp32 (RNE) -> bf16 (RNE).  LN gamma = 1 + ln_std*n,
   beta = ln_std*n, kept in fp32.
+* the sigma values are the fp32 numbers a model config carries (its std fields
+  are fp32), widened exactly to fp64: sigma = 0.02 means fl32(0.02).
 """
 from __future__ import annotations
 
@@ -168,10 +170,16 @@ def gen_ln_param(seed: int, layer: int, slot: int, n: int, offset: float, sigma:
 # ----------------------------------------------------------------------------------
 # whole-model weights, one layer at a time (fp64 copies of the bf16/fp32 values)
 # ----------------------------------------------------------------------------------
+def _sigmas(shape: dict):
+    """(w, b, ln, qk) standard deviations as the fp32 values of the config."""
+    f32 = lambda v: float(np.float32(v))
+    return (f32(shape["w_std"]), f32(shape["b_std"]), f32(shape["ln_std"]),
+            f32(shape.get("qk_std", 0.0)))
+
+
 def layer_weights(shape: dict, layer: int) -> dict:
     d, f, seed = shape["d_model"], shape["d_ff"], shape["seed"]
-    ws, bs, ls = shape["w_std"], shape["b_std"], shape["ln_std"]
-    qk = shape.get("qk_std", 0.0)
+    ws, bs, ls, qk = _sigmas(shape)
     S = SLOTS
     return dict(
         wqkv=gen_weight(seed, layer, S["wqkv"], d, 3 * d, ws, qk_cols=2 * d, sigma_qk=qk),
@@ -191,22 +199,22 @@ def layer_weights(shape: dict, layer: int) -> dict:
 
 def global_weights(shape: dict) -> dict:
     d, L, seed = shape["d_model"], shape["n_layers"], shape["seed"]
+    ws, bs, ls, _ = _sigmas(shape)
     out = dict(
-        lnf_g=gen_ln_param(seed, L, SLOTS["lnf_g"], d, 1.0, shape["ln_std"]),
-        lnf_b=gen_ln_param(seed, L, SLOTS["lnf_b"], d, 0.0, shape["ln_std"]),
+        lnf_g=gen_ln_param(seed, L, SLOTS["lnf_g"], d, 1.0, ls),
+        lnf_b=gen_ln_param(seed, L, SLOTS["lnf_b"], d, 0.0, ls),
     )
     n_out = shape["n_out"]
     if n_out > 0:
-        out["wh"] = gen_weight(seed, L, SLOTS["wh"], d, n_out, shape["w_std"])
-        out["bh"] = gen_weight(seed, L, SLOTS["bh"], 1, n_out, shape["b_std"])[0]
+        out["wh"] = gen_weight(seed, L, SLOTS["wh"], d, n_out, ws)
+        out["bh"] = gen_weight(seed, L, SLOTS["bh"], 1, n_out, bs)[0]
     return out
 
 
 def ref_layer_weights(shape: dict, layer: int) -> dict:
     """Same tensors as ``layer_weights`` through the pure-Python path (tiny shapes only)."""
     d, f, seed = shape["d_model"], shape["d_ff"], shape["seed"]
-    ws, bs, ls = shape["w_std"], shape["b_std"], shape["ln_std"]
-    qk = shape.get("qk_std", 0.0)
+    ws, bs, ls, qk = _sigmas(shape)
     S = SLOTS
     return dict(
         wqkv=ref_weight(seed, layer, S["wqkv"], d, 3 * d, ws, qk_cols=2 * d, sigma_qk=qk),
