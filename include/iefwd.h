@@ -220,14 +220,16 @@ int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void 
 
 /* QKV projection with head scatter: A bf16 [batch*seq, d], W bf16 [3d, d],
  * bias bf16 [3d].  Writes Q and K as bf16 [batch, heads, seq, dh] and V
- * transposed as bf16 [batch, heads, dh, seq]. */
+ * transposed as bf16 [batch, heads, dh, seq_pad], seq_pad = seq rounded up to
+ * a multiple of 64 (entries past seq are left untouched). */
 int iefwd_test_gemm_qkv(const void *a, const void *w, const void *bias, void *q, void *k,
                         void *vt, uint32_t batch, uint32_t seq, uint32_t d_model,
                         uint32_t n_heads, void *stream);
 
 /* ctx bf16 [batch, seq, heads*dh] = softmax(Q K^T / sqrt(dh) [+ causal]) V per
  * (batch, head), from Q, K bf16 [batch, heads, seq, dh] and Vt bf16
- * [batch, heads, dh, seq].  dh in {64, 128}. */
+ * [batch, heads, dh, seq_pad] (seq_pad = seq rounded up to a multiple of 64;
+ * the padding may hold any bits).  dh in {64, 128}. */
 int iefwd_test_attention(const void *q, const void *k, const void *vt, void *ctx,
                          uint32_t batch, uint32_t n_heads, uint32_t seq, uint32_t head_dim,
                          int causal, void *stream);

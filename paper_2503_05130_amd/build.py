@@ -52,6 +52,18 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _check_stubs(lib: str) -> None:
+    """Every kernel launched from host code must have its launch stub defined.
+
+    clang's host pass can drop a kernel's stub without a diagnostic when the
+    kernel body holds a device-only construct it cannot check on the host; the
+    library would then fail to load on the GPU machine."""
+    res = subprocess.run(["nm", "-D", "--undefined-only", lib], capture_output=True, text=True, check=True)
+    missing = [line.split()[-1] for line in res.stdout.splitlines() if "__device_stub" in line]
+    if missing:
+        raise RuntimeError(f"undefined kernel launch stubs in {lib}: {missing[:4]}")
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
@@ -61,6 +73,7 @@ def build(verbose: bool = False) -> str:
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    _check_stubs(tmp)
     os.replace(tmp, LIB)
     if verbose:
         print(f"built {LIB}")

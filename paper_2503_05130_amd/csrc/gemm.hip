@@ -4,18 +4,28 @@
 //   A: activations, bf16 [M, K] row-major (tokens x features-in)
 //   W: weights stored output-major, bf16 [N, K] row-major
 //
-// Both operands are K-contiguous, so every MFMA operand fragment is one 16-byte
-// LDS read.  The kernel computes C^T blocks (features x tokens) with
-// v_mfma_f32_16x16x32_bf16: the W fragment is the MFMA "A" operand and the
-// activation fragment the "B" operand, so each lane ends up owning 4
-// consecutive output features of one token and stores them with one vector
-// store.
+// Data movement.  K is walked in 64-wide tiles.  Each tile of A and W is copied
+// from global memory straight into LDS with global_load_lds_dwordx4 (gfx950's
+// 16-byte global->LDS DMA: no VGPR staging), into an S-stage ring, so S-1
+// tiles are in flight while one is consumed.  Each wave copies whole 8-row
+// groups (one 1 KB DMA per group); LDS rows are 128 bytes with the 16-byte
+// chunks XOR-swizzled per row, chosen so that the 16 rows read by one
+// ds_read_b128 fragment load fall in distinct bank groups.  The swizzle is
+// applied on the source side: lane i of a DMA fetches the global chunk that
+// belongs at its fixed LDS slot.  The wave waits for its own DMAs of the tile
+// it is about to read (s_waitcnt vmcnt), then a workgroup barrier makes every
+// wave's copies visible and frees the slot the next DMA will overwrite.
+//
+// Math.  v_mfma_f32_16x16x32_bf16 on C^T blocks (features x tokens): the W
+// fragment is the MFMA "A" operand, the activation fragment the "B" operand,
+// so each lane ends up owning 4 consecutive output features of one token and
+// stores them with one vector store.  4 waves in a 2 x 2 grid over the tile.
 //
 // Determinism and batch invariance: every tile configuration uses the same MFMA
 // instruction and walks K in the same order (64-wide K tiles, two 32-wide MFMA
 // steps each), so out[t, f] depends only on row t of A and row f of W -- never
-// on the tile shape, the grid, the CU mask or the other rows in the batch.
-// No atomics, no split-K.
+// on the tile shape, the ring depth, the grid, the CU mask or the other rows in
+// the batch.  No atomics, no split-K.
 #include "kernels.h"
 
 #include <algorithm>
@@ -25,12 +35,10 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
-constexpr int kBK = 64;               // K tile (bf16 elements) = 128 bytes per row
-constexpr int kLdsStride = kBK + 8;   // 144-byte LDS rows: 16 consecutive rows hit 16
-                                      // distinct 16-byte bank groups for ds_read_b128
+constexpr int kBK = 64;               // K tile (bf16 elements) = one 128-byte LDS row
 constexpr int kThreads = 256;         // 4 waves in a 2 x 2 grid over the tile
 
 struct GemmParams {
@@ -42,6 +50,7 @@ struct GemmParams {
     int M, N, K;
     int tiles_m, tiles_n;
     QkvDst qkv;
+    LnResid ln;
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs.  Renumber them so
@@ -77,54 +86,76 @@ __device__ inline uint32_t pack2(float lo, float hi) {
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
-// GELU with the exact erf form.
-__device__ inline float gelu(float u) { return 0.5f * u * (1.0f + erff(u * 0.7071067811865476f)); }
+// GELU(u) = u/2 (1 + erf(u / sqrt 2)), with erf from Abramowitz & Stegun,
+// Handbook of Mathematical Functions, formula 7.1.26 (|error| <= 1.5e-7 for
+// x >= 0): erfc(x) ~= (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
+// t = 1 / (1 + p x).  Written through erfc so that u < 0 keeps its relative
+// accuracy: GELU(u) = u (1 - erfc(x)/2) for u >= 0 and u erfc(x)/2 for u < 0,
+// x = |u| / sqrt 2.  About 14 VALU operations instead of a full erff.
+__device__ inline float gelu(float u) {
+    const float x = fabsf(u) * 0.7071067811865476f;
+    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
+    float poly = fmaf(1.061405429f, t, -1.453152027f);
+    poly = fmaf(poly, t, 1.421413741f);
+    poly = fmaf(poly, t, -0.284496736f);
+    poly = fmaf(poly, t, 0.254829592f);
+    const float erfc_x = poly * t * __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
+    return u * (u >= 0.f ? fmaf(-0.5f, erfc_x, 1.0f) : 0.5f * erfc_x);
+}
 
-template <int BM, int BN, Epi EPI>
+// 16-byte chunk position of logical chunk 0 in LDS row r (row r holds its
+// chunk c at position c ^ swizzle(r)).  Consecutive rows alternate between the
+// two 128-byte halves of a 256-byte bank line, and within each parity the 8
+// rows of a 16-row fragment get 8 distinct positions.
+__device__ inline int swizzle(int r) { return ((r >> 1) & 7) ^ ((r & 1) << 2); }
+
+// s_waitcnt immediate that waits until at most n vector-memory operations of
+// this wave are outstanding (expcnt and lgkmcnt left unconstrained).
+constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
+template <int BM, int BN, int S, Epi EPI>
 __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
     constexpr int TM = BM / 2, TN = BN / 2;          // per-wave tile (tokens x features)
     constexpr int FM = TM / 16, FN = TN / 16;        // 16x16 MFMA blocks per wave
-    constexpr int A_CH = BM * (kBK / 8) / kThreads;  // 16-byte chunks per thread
-    constexpr int B_CH = BN * (kBK / 8) / kThreads;
-    static_assert(BM * (kBK / 8) % kThreads == 0 && BN * (kBK / 8) % kThreads == 0, "tile");
-    static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tile");
+    constexpr int STAGE = (BM + BN) * kBK;           // bf16 elements per ring slot
+    constexpr int A_PW = BM / 32, W_PW = BN / 32;    // 1 KB DMAs per wave per K tile
+    constexpr int LPW = A_PW + W_PW;
+    static_assert(BM % 32 == 0 && BN % 32 == 0 && TM % 16 == 0 && TN % 16 == 0, "tile");
+    static_assert(S >= 2 && (S - 2) * LPW <= 63, "ring depth");
 
-    __shared__ __attribute__((aligned(16))) bf16_t lds[2 * (BM + BN) * kLdsStride];
+    __shared__ __attribute__((aligned(1024))) bf16_t lds[S * STAGE];
 
     int tm, tn;
     grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
     const int m0 = tm * BM, n0 = tn * BN;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
-    // This thread's global->LDS chunks: rows (tid / 8) + 32 i, 16-byte column
-    // (tid % 8).  Rows past M / N are clamped to the last valid row (their
-    // results are never stored).
-    const int ld_row = tid >> 3, ld_col = (tid & 7) * 8;
-    uint32_t a_off[A_CH], w_off[B_CH];
+    // DMA sources of this lane: DMA i of this wave copies the 8-row group
+    // g = wave + 4 i; lane l fills row 8 g + l / 8 at chunk position l % 8.
+    // Rows past M / N are clamped to the last valid row (never stored).
+    uint32_t a_src[A_PW], w_src[W_PW];
 #pragma unroll
-    for (int i = 0; i < A_CH; ++i)
-        a_off[i] = (uint32_t)min(m0 + ld_row + 32 * i, p.M - 1) * (uint32_t)p.K + ld_col;
+    for (int i = 0; i < A_PW; ++i) {
+        const int r = 8 * (wave + 4 * i) + (lane >> 3);
+        a_src[i] = (uint32_t)min(m0 + r, p.M - 1) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
+    }
 #pragma unroll
-    for (int i = 0; i < B_CH; ++i)
-        w_off[i] = (uint32_t)min(n0 + ld_row + 32 * i, p.N - 1) * (uint32_t)p.K + ld_col;
-    const int st_off = ld_row * kLdsStride + ld_col;
-
-    u32x4 ra[A_CH], rw[B_CH];
-#define IEFWD_GLOAD(k0)                                                                   \
-    do {                                                                                  \
-        _Pragma("unroll") for (int i = 0; i < A_CH; ++i)                                  \
-            ra[i] = *reinterpret_cast<const u32x4 *>(p.a + a_off[i] + (k0));              \
-        _Pragma("unroll") for (int i = 0; i < B_CH; ++i)                                  \
-            rw[i] = *reinterpret_cast<const u32x4 *>(p.w + w_off[i] + (k0));              \
-    } while (0)
-#define IEFWD_LSTORE(buf)                                                                 \
-    do {                                                                                  \
-        bf16_t *base_ = lds + (buf) * (BM + BN) * kLdsStride + st_off;                    \
-        _Pragma("unroll") for (int i = 0; i < A_CH; ++i)                                  \
-            *reinterpret_cast<u32x4 *>(base_ + 32 * i * kLdsStride) = ra[i];              \
-        _Pragma("unroll") for (int i = 0; i < B_CH; ++i)                                  \
-            *reinterpret_cast<u32x4 *>(base_ + (BM + 32 * i) * kLdsStride) = rw[i];       \
+    for (int i = 0; i < W_PW; ++i) {
+        const int r = 8 * (wave + 4 * i) + (lane >> 3);
+        w_src[i] = (uint32_t)min(n0 + r, p.N - 1) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
+    }
+#define IEFWD_ISSUE(kt, slot)                                                                      \
+    do {                                                                                           \
+        const int k0_ = (kt) * kBK;                                                                \
+        bf16_t *ring_ = lds + (slot) * STAGE;                                                      \
+        _Pragma("unroll") for (int i = 0; i < A_PW; ++i)                                           \
+            __builtin_amdgcn_global_load_lds((const void *)(p.a + a_src[i] + k0_),                               \
+                                             (lds_ptr_t)(ring_ + (wave + 4 * i) * 512), 16, 0, 0); \
+        _Pragma("unroll") for (int i = 0; i < W_PW; ++i)                                           \
+            __builtin_amdgcn_global_load_lds((const void *)(p.w + w_src[i] + k0_),                               \
+                                             (lds_ptr_t)(ring_ + BM * kBK + (wave + 4 * i) * 512), \
+                                             16, 0, 0);                                            \
     } while (0)
 
     f32x4 acc[FN][FM];
@@ -133,50 +164,82 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
 #pragma unroll
         for (int i = 0; i < FM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // fragment read offsets: row = lane % 16 of each 16-row block, k = 8 * (lane / 16)
-    const int a_frag = (wm * TM + (lane & 15)) * kLdsStride + (lane >> 4) * 8;
-    const int w_frag = BM * kLdsStride + (wn * TN + (lane & 15)) * kLdsStride + (lane >> 4) * 8;
-
     const int kt_count = p.K / kBK;
-    IEFWD_GLOAD(0);
-    IEFWD_LSTORE(0);
-    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < S - 1; ++s)
+        if (s < kt_count) IEFWD_ISSUE(s, s);
+
+    // fragment rows: lane % 16 of each 16-row block; 16-byte chunk 4 ks + lane / 16
+    const int ra = wm * TM + (lane & 15), rw = wn * TN + (lane & 15);
     for (int kt = 0; kt < kt_count; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < kt_count) IEFWD_GLOAD((kt + 1) * kBK);   // in flight during the MFMAs
-        const bf16_t *base = lds + buf * (BM + BN) * kLdsStride;
+        // this wave's copies of tile kt are done once at most the later tiles'
+        // copies are outstanding; the barrier then publishes every wave's copies
+        // and guarantees the slot reused below is no longer being read
+        if (kt + S - 2 < kt_count)
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm((S - 2) * LPW));
+        else
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");   // keep LDS accesses on their side of the barrier
+        if (kt + S - 1 < kt_count) IEFWD_ISSUE(kt + S - 1, (kt + S - 1) % S);
+        const bf16_t *ring = lds + (kt % S) * STAGE;
 #pragma unroll
         for (int ks = 0; ks < kBK / 32; ++ks) {
+            const int c = ks * 4 + (lane >> 4);
             bf16x8 af[FM], wf[FN];
 #pragma unroll
-            for (int i = 0; i < FM; ++i)
-                af[i] = *reinterpret_cast<const bf16x8 *>(base + a_frag + i * 16 * kLdsStride + ks * 32);
+            for (int i = 0; i < FM; ++i) {
+                const int r = ra + i * 16;
+                af[i] = *reinterpret_cast<const bf16x8 *>(ring + r * kBK + ((c ^ swizzle(r)) * 8));
+            }
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
-                wf[j] = *reinterpret_cast<const bf16x8 *>(base + w_frag + j * 16 * kLdsStride + ks * 32);
+            for (int j = 0; j < FN; ++j) {
+                const int r = rw + j * 16;
+                wf[j] = *reinterpret_cast<const bf16x8 *>(ring + BM * kBK + r * kBK + ((c ^ swizzle(r)) * 8));
+            }
 #pragma unroll
             for (int j = 0; j < FN; ++j)
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
                     acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], af[i], acc[j][i], 0, 0, 0);
         }
-        if (kt + 1 < kt_count) IEFWD_LSTORE(buf ^ 1);
-        __syncthreads();
     }
-#undef IEFWD_GLOAD
-#undef IEFWD_LSTORE
+#undef IEFWD_ISSUE
 
     // Epilogue: lane owns features f..f+3 of token t in every block.
+    int tok[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) tok[i] = m0 + wm * TM + i * 16 + (lane & 15);
+    int tok_b[FM], tok_s[FM];   // (sequence, position) of each token, for the head scatter
+    if constexpr (EPI == Epi::Qkv) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            tok_b[i] = tok[i] / p.qkv.seq;
+            tok_s[i] = tok[i] - tok_b[i] * p.qkv.seq;
+        }
+    }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
         const int f = n0 + wn * TN + j * 16 + (lane >> 4) * 4;
         if (f >= p.N) continue;
         const u32x2 braw = *reinterpret_cast<const u32x2 *>(p.bias + f);
-        const float b0 = __uint_as_float(braw.x << 16), b1 = __uint_as_float(braw.x & 0xffff0000u);
-        const float b2 = __uint_as_float(braw.y << 16), b3 = __uint_as_float(braw.y & 0xffff0000u);
+        const float b0 = __uint_as_float(braw[0] << 16), b1 = __uint_as_float(braw[0] & 0xffff0000u);
+        const float b2 = __uint_as_float(braw[1] << 16), b3 = __uint_as_float(braw[1] & 0xffff0000u);
+        f32x4 ln_g, ln_b;
+        if constexpr (EPI == Epi::BiasLnResidF32) {
+            ln_g = *reinterpret_cast<const f32x4 *>(p.ln.gamma + f);
+            ln_b = *reinterpret_cast<const f32x4 *>(p.ln.beta + f);
+        }
+        int which = 0, head = 0, jj = 0;   // head scatter: Q/K/V block, head, column within head
+        if constexpr (EPI == Epi::Qkv) {
+            which = f / p.qkv.d_model;
+            const int within = f - which * p.qkv.d_model;
+            head = within / p.qkv.head_dim;
+            jj = within - head * p.qkv.head_dim;
+        }
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-            const int t = m0 + wm * TM + i * 16 + (lane & 15);
+            const int t = tok[i];
             if (t >= p.M) continue;
             float v0 = acc[j][i][0] + b0, v1 = acc[j][i][1] + b1;
             float v2 = acc[j][i][2] + b2, v3 = acc[j][i][3] + b3;
@@ -191,18 +254,25 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
                 const f32x4 r = *reinterpret_cast<const f32x4 *>(p.resid + off);
                 *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + off) =
                     f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
+            } else if constexpr (EPI == Epi::BiasLnResidF32) {
+                // residual = LN(z) rebuilt with the LayerNorm kernel's expression
+                const size_t off = (size_t)t * p.N + f;
+                const f32x4 z = *reinterpret_cast<const f32x4 *>(p.ln.z + off);
+                const float mean = p.ln.stats[2 * t], rstd = p.ln.stats[2 * t + 1];
+                f32x4 r;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) r[e] = __builtin_fmaf(ln_g[e], (z[e] - mean) * rstd, ln_b[e]);
+                *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + off) =
+                    f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
             } else {   // Epi::Qkv
                 const QkvDst &d = p.qkv;
-                const int which = f / d.d_model;               // 0 Q, 1 K, 2 V
-                const int within = f - which * d.d_model;
-                const int h = within / d.head_dim, jj = within - h * d.head_dim;
-                const int b = t / d.seq, s = t - b * d.seq;
-                const size_t bh = (size_t)b * d.n_heads + h;
+                const size_t bh = (size_t)tok_b[i] * d.n_heads + head;
+                const int sp = tok_s[i];
                 if (which < 2) {
-                    bf16_t *o = (which == 0 ? d.q : d.k) + (bh * d.seq + s) * d.head_dim + jj;
+                    bf16_t *o = (which == 0 ? d.q : d.k) + (bh * d.seq + sp) * d.head_dim + jj;
                     *reinterpret_cast<u32x2 *>(o) = u32x2{pack2(v0, v1), pack2(v2, v3)};
                 } else {
-                    bf16_t *o = d.vt + (bh * d.head_dim + jj) * d.seq_pad + s;
+                    bf16_t *o = d.vt + (bh * d.head_dim + jj) * d.seq_pad + sp;
                     o[0] = f32_to_bf16(v0);
                     o[d.seq_pad] = f32_to_bf16(v1);
                     o[2 * d.seq_pad] = f32_to_bf16(v2);
@@ -214,37 +284,36 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
 }
 
 struct TileChoice {
-    int bm, bn;
+    int bm, bn, stages;
 };
 
-// Tile shape from (M, N) only -- a fixed cost model of whole-chip rounds of 256
-// workgroups, never the current CU quota.  Smaller tiles pay a per-output
-// overhead factor for their lower operand reuse.
-TileChoice choose_tile(int M, int N) {
-    struct Cand { int bm, bn; double overhead; };
-    static const Cand cands[] = {{128, 128, 1.00}, {128, 96, 1.05}, {128, 64, 1.15}, {64, 64, 1.40}};
-    TileChoice best{128, 128};
-    double best_cost = 1e300;
-    for (const Cand &c : cands) {
-        if (N % c.bn != 0) continue;
-        const long tiles = (long)((M + c.bm - 1) / c.bm) * (N / c.bn);
-        const long rounds = (tiles + 255) / 256;
-        const double cost = (double)rounds * c.bm * c.bn * c.overhead;
-        if (cost < best_cost) { best_cost = cost; best = {c.bm, c.bn}; }
-    }
-    return best;
+// Tile shape and ring depth from (M, N, K) only -- never the current CU quota.
+// Measured on gfx950 at T = 4096 tokens: a 2-slot ring with two workgroups
+// resident per CU beats deeper rings with one, except for long-K narrow-N
+// products (FFN down-projection) where a 4-slot 128 x 96 ring wins.  Small
+// grids fall back to 64 x 64 tiles (up to three workgroups per CU).
+TileChoice choose_tile(int M, int N, int K) {
+    const long tiles_96 = (long)((M + 127) / 128) * (N / 96);
+    const long tiles_128 = (long)((M + 127) / 128) * (N / 128);
+    if (N % 96 == 0 && tiles_96 >= 256) return {128, 96, K >= 2048 ? 4 : 2};
+    if (N % 128 == 0 && tiles_128 >= 256) return {128, 128, 2};
+    if (N % 96 == 0 && tiles_96 >= 128) return {128, 96, 2};
+    return {64, 64, 3};
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int S>
 hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
     p.tiles_m = (p.M + BM - 1) / BM;
     p.tiles_n = p.N / BN;
     const dim3 grid(p.tiles_m * p.tiles_n), block(kThreads);
     switch (epi) {
-    case Epi::BiasBf16: hipLaunchKernelGGL((gemm_kernel<BM, BN, Epi::BiasBf16>), grid, block, 0, s, p); break;
-    case Epi::BiasGeluBf16: hipLaunchKernelGGL((gemm_kernel<BM, BN, Epi::BiasGeluBf16>), grid, block, 0, s, p); break;
-    case Epi::BiasResidF32: hipLaunchKernelGGL((gemm_kernel<BM, BN, Epi::BiasResidF32>), grid, block, 0, s, p); break;
-    case Epi::Qkv: hipLaunchKernelGGL((gemm_kernel<BM, BN, Epi::Qkv>), grid, block, 0, s, p); break;
+    case Epi::BiasBf16: hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::BiasBf16>), grid, block, 0, s, p); break;
+    case Epi::BiasGeluBf16: hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::BiasGeluBf16>), grid, block, 0, s, p); break;
+    case Epi::BiasResidF32: hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::BiasResidF32>), grid, block, 0, s, p); break;
+    case Epi::Qkv: hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::Qkv>), grid, block, 0, s, p); break;
+    case Epi::BiasLnResidF32:
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::BiasLnResidF32>), grid, block, 0, s, p);
+        break;
     }
     return hipGetLastError();
 }
@@ -253,17 +322,18 @@ hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
 
 hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
                        const float *resid, void *out, int M, int N, int K, const QkvDst *qkv,
-                       hipStream_t stream) {
+                       hipStream_t stream, const LnResid *ln) {
     if (M <= 0) return hipSuccess;
     GemmParams p{};
     p.a = a; p.w = w; p.bias = bias; p.resid = resid; p.out = out;
     p.M = M; p.N = N; p.K = K;
     if (qkv) p.qkv = *qkv;
-    const TileChoice t = choose_tile(M, N);
-    if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128>(epi, p, stream);
-    if (t.bm == 128 && t.bn == 96) return launch_tile<128, 96>(epi, p, stream);
-    if (t.bm == 128 && t.bn == 64) return launch_tile<128, 64>(epi, p, stream);
-    return launch_tile<64, 64>(epi, p, stream);
+    if (ln) p.ln = *ln;
+    const TileChoice t = choose_tile(M, N, K);
+    if (t.bm == 128 && t.bn == 96)
+        return t.stages == 4 ? launch_tile<128, 96, 4>(epi, p, stream) : launch_tile<128, 96, 2>(epi, p, stream);
+    if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128, 2>(epi, p, stream);
+    return launch_tile<64, 64, 3>(epi, p, stream);
 }
 
 }  // namespace iefwd

@@ -130,7 +130,8 @@ struct iefwd_instance {
 
     // workspace: one device allocation, carved (sized for max_batch * max_seq)
     void *wsblob = nullptr;
-    float *h = nullptr, *z = nullptr, *h1 = nullptr, *out = nullptr, *xstage = nullptr;
+    float *h = nullptr, *z = nullptr, *z2 = nullptr, *h1 = nullptr, *out = nullptr, *xstage = nullptr;
+    float *stats1 = nullptr, *stats2 = nullptr;   // per-row {mean, rstd} of post-LN LayerNorms
     bf16_t *hb = nullptr, *h1b = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr, *ctx = nullptr,
            *u = nullptr;
 
@@ -229,7 +230,10 @@ void run_forward(iefwd_instance *I, const float *x) {
     hipStream_t s = I->stream;
     QkvDst qd{I->q, I->k, I->vt, S, attn_seq_pad(S), H, dh, d};
 
-    auto attention_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid, float *dst) {
+    // QKV projection, attention and the output projection with its residual:
+    // either a plain fp32 residual or one rebuilt from LayerNorm row statistics.
+    auto attention_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid,
+                               const LnResid *ln_resid, float *dst) {
         launch(I, IEFWD_K_QKV, "qkv gemm", [&] {
             return launch_gemm(Epi::Qkv, y_bf16, w.wqkv, w.bqkv, nullptr, nullptr, T, 3 * d, d, &qd, s);
         });
@@ -237,19 +241,23 @@ void run_forward(iefwd_instance *I, const float *x) {
             return launch_attention(I->q, I->k, I->vt, I->ctx, B, H, S, dh, c.causal != 0, s);
         });
         launch(I, IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
-            return launch_gemm(Epi::BiasResidF32, I->ctx, w.wo, w.bo, resid, dst, T, d, d, nullptr, s);
+            return launch_gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->ctx, w.wo, w.bo, resid, dst,
+                               T, d, d, nullptr, s, ln_resid);
         });
     };
-    auto ffn_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid, float *dst) {
+    auto ffn_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid, const LnResid *ln_resid,
+                         float *dst) {
         launch(I, IEFWD_K_FFN1, "ffn1 gemm", [&] {
             return launch_gemm(Epi::BiasGeluBf16, y_bf16, w.w1, w.b1, nullptr, I->u, T, F, d, nullptr, s);
         });
         launch(I, IEFWD_K_FFN2, "ffn2 gemm", [&] {
-            return launch_gemm(Epi::BiasResidF32, I->u, w.w2, w.b2, resid, dst, T, d, F, nullptr, s);
+            return launch_gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->u, w.w2, w.b2, resid, dst, T,
+                               d, F, nullptr, s, ln_resid);
         });
     };
-    auto ln = [&](const float *src, const float *g, const float *b, float *o32, bf16_t *o16) {
-        launch(I, IEFWD_K_LN, "layernorm", [&] { return launch_layernorm(src, g, b, o32, o16, T, d, eps, s); });
+    auto ln = [&](const float *src, const float *g, const float *b, float *o32, bf16_t *o16, float *stats) {
+        launch(I, IEFWD_K_LN, "layernorm",
+               [&] { return launch_layernorm(src, g, b, o32, o16, T, d, eps, s, stats); });
     };
     auto ln_head = [&](const float *src, const float *g, const float *b) {
         launch(I, IEFWD_K_LN, "ln+head", [&] {
@@ -259,38 +267,44 @@ void run_forward(iefwd_instance *I, const float *x) {
 
     const int L = (int)c.n_layers;
     if (!c.pre_ln) {
-        // post-LN: X1 = LN1(X + Attn(X)); X' = LN2(X1 + FFN(X1))
+        // post-LN: X1 = LN1(X + Attn(X)); X' = LN2(X1 + FFN(X1)).  The LayerNorms
+        // write only the bf16 GEMM operand and {mean, rstd}; the fp32 residual
+        // LN(z) is rebuilt in the epilogue of the GEMM that adds to it.
         launch(I, IEFWD_K_LN, "cast", [&] { return launch_cast_bf16(x, I->hb, (size_t)T * d, s); });
-        const float *resid = x;
         for (int l = 0; l < L; ++l) {
             const LayerWeights &w = I->layers[l];
-            attention_block(I->hb, w, resid, I->z);
-            ln(I->z, w.g1, w.be1, I->h1, I->h1b);
-            ffn_block(I->h1b, w, I->h1, I->z);
-            if (l + 1 < L) {
-                ln(I->z, w.g2, w.be2, I->h, I->hb);
-                resid = I->h;
-            } else if (c.n_out > 0) {
-                ln_head(I->z, w.g2, w.be2);
+            if (l == 0) {
+                attention_block(I->hb, w, x, nullptr, I->z);
             } else {
-                ln(I->z, w.g2, w.be2, I->out, nullptr);
+                const LayerWeights &prev = I->layers[l - 1];
+                const LnResid r2{I->z2, I->stats2, prev.g2, prev.be2};
+                attention_block(I->hb, w, nullptr, &r2, I->z);
             }
+            ln(I->z, w.g1, w.be1, nullptr, I->h1b, I->stats1);
+            const LnResid r1{I->z, I->stats1, w.g1, w.be1};
+            ffn_block(I->h1b, w, nullptr, &r1, I->z2);
+            if (l + 1 < L)
+                ln(I->z2, w.g2, w.be2, nullptr, I->hb, I->stats2);
+            else if (c.n_out > 0)
+                ln_head(I->z2, w.g2, w.be2);
+            else
+                ln(I->z2, w.g2, w.be2, I->out, nullptr, nullptr);
         }
     } else {
         // pre-LN: X1 = X + Attn(LN1(X)); X' = X1 + FFN(LN2(X1)); final LN
         const float *xcur = x;
         for (int l = 0; l < L; ++l) {
             const LayerWeights &w = I->layers[l];
-            ln(xcur, w.g1, w.be1, nullptr, I->hb);
-            attention_block(I->hb, w, xcur, I->h1);
-            ln(I->h1, w.g2, w.be2, nullptr, I->hb);
-            ffn_block(I->hb, w, I->h1, I->h);
+            ln(xcur, w.g1, w.be1, nullptr, I->hb, nullptr);
+            attention_block(I->hb, w, xcur, nullptr, I->h1);
+            ln(I->h1, w.g2, w.be2, nullptr, I->hb, nullptr);
+            ffn_block(I->hb, w, I->h1, nullptr, I->h);
             xcur = I->h;
         }
         if (c.n_out > 0)
             ln_head(xcur, I->gf, I->bef);
         else
-            ln(xcur, I->gf, I->bef, I->out, nullptr);
+            ln(xcur, I->gf, I->bef, I->out, nullptr, nullptr);
     }
 }
 
@@ -393,6 +407,7 @@ void alloc_workspace(iefwd_instance *I) {
     size_t bytes = 0;
     auto reserve = [&](size_t n) { size_t off = bytes; bytes = round_up(bytes + n, 256); return off; };
     const size_t o_h = reserve(T * d * 4), o_z = reserve(T * d * 4), o_h1 = reserve(T * d * 4);
+    const size_t o_z2 = reserve(T * d * 4), o_s1 = reserve(T * 8), o_s2 = reserve(T * 8);
     const size_t o_out = reserve(T * out_width(c) * 4), o_x = reserve(T * d * 4);
     const size_t o_hb = reserve(T * d * 2), o_h1b = reserve(T * d * 2), o_q = reserve(T * d * 2);
     const size_t o_k = reserve(T * d * 2), o_vt = reserve((size_t)c.max_batch * d * spad * 2);
@@ -406,6 +421,9 @@ void alloc_workspace(iefwd_instance *I) {
     I->h = reinterpret_cast<float *>(b + o_h);
     I->z = reinterpret_cast<float *>(b + o_z);
     I->h1 = reinterpret_cast<float *>(b + o_h1);
+    I->z2 = reinterpret_cast<float *>(b + o_z2);
+    I->stats1 = reinterpret_cast<float *>(b + o_s1);
+    I->stats2 = reinterpret_cast<float *>(b + o_s2);
     I->out = reinterpret_cast<float *>(b + o_out);
     I->xstage = reinterpret_cast<float *>(b + o_x);
     I->hb = reinterpret_cast<bf16_t *>(b + o_hb);

@@ -16,36 +16,48 @@ enum class Epi : int {
     BiasGeluBf16 = 1,   // out bf16 = GELU(acc + b)
     BiasResidF32 = 2,   // out f32  = resid + acc + b
     Qkv = 3,            // acc + b scattered to Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad]
+    BiasLnResidF32 = 4, // out f32  = LN(z) + acc + b, LN(z) rebuilt from z and its row stats
+};
+
+// Row statistics a LayerNorm kernel leaves for a later consumer: the residual
+// LN(z)[t, f] = gamma[f] * ((z[t, f] - mean[t]) * rstd[t]) + beta[f] is rebuilt
+// from them with exactly the LayerNorm kernel's arithmetic.
+struct LnResid {
+    const float *z;       // [M, N] fp32 pre-normalisation rows
+    const float *stats;   // [M, 2] fp32 {mean, rstd}
+    const float *gamma;   // [N]
+    const float *beta;    // [N]
 };
 
 // Destination of the QKV epilogue.
 struct QkvDst {
     bf16_t *q, *k, *vt;
     int seq;       // S
-    int seq_pad;   // row stride of V^T (S rounded up to a multiple of 32)
+    int seq_pad;   // row stride of V^T (S rounded up to a multiple of 64)
     int n_heads;
     int head_dim;
     int d_model;
 };
 
-// S rounded up to the attention kernel's key block.
-inline int attn_seq_pad(int seq) { return (seq + 31) / 32 * 32; }
+// S rounded up to the attention kernel's 64-key chunk (the row stride of V^T).
+inline int attn_seq_pad(int seq) { return (seq + 63) / 64 * 64; }
 
 // out = epi(A W^T + b).  A bf16 [M,K], W bf16 [N,K], bias bf16 [N].
 // Requires N % 64 == 0, K % 64 == 0, M >= 1.
 hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
                        const float *resid, void *out, int M, int N, int K,
-                       const QkvDst *qkv, hipStream_t stream);
+                       const QkvDst *qkv, hipStream_t stream, const LnResid *ln = nullptr);
 
 // ctx bf16 [B, S, H*dh] from Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad].
 hipError_t launch_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx,
                             int batch, int n_heads, int seq, int head_dim, bool causal,
                             hipStream_t stream);
 
-// Row LayerNorm, d % 128 == 0, d <= 4096.  out_f32 / out_bf16 may be null.
+// Row LayerNorm, d % 128 == 0, d <= 4096.  out_f32 / out_bf16 / stats may be
+// null; stats receives {mean, rstd} per row.
 hipError_t launch_layernorm(const float *z, const float *gamma, const float *beta,
                             float *out_f32, bf16_t *out_bf16, int rows, int d, float eps,
-                            hipStream_t stream);
+                            hipStream_t stream, float *stats = nullptr);
 
 // LayerNorm + per-token head: logits [rows, n_out] = LN(z) Wh^T + bh, Wh bf16 [n_out, d].
 hipError_t launch_ln_head(const float *z, const float *gamma, const float *beta,

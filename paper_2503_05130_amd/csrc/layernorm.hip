@@ -1,9 +1,9 @@
 // Row LayerNorm kernels (HBM-bound): one wave64 per row, the whole row held in
 // registers, two-pass mean / variance with a fixed xor-butterfly reduction
-// (deterministic), coalesced 8-byte accesses (lane l touches floats 2l, 2l+1 of
-// every 128-float chunk).
+// (deterministic), coalesced 16-byte accesses (8-byte when d is an odd
+// multiple of 128).
 //
-//   layernorm : fp32 [rows, d] -> fp32 and/or bf16 [rows, d]
+//   layernorm : fp32 [rows, d] -> fp32 and/or bf16 [rows, d], optional {mean, rstd}
 //   ln_head   : fp32 [rows, d] -> LN -> per-token head, fp32 logits [rows, n_out]
 //               (the model's last LN fused with its classifier, so the final
 //               hidden states never go back to HBM)
@@ -19,6 +19,10 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kRowsPerBlock = 4;   // 4 waves, one row each
 
+template <int VEC> struct Vec;
+template <> struct Vec<2> { typedef f32x2 f; typedef uint32_t bf; };
+template <> struct Vec<4> { typedef f32x4 f; typedef u32x2 bf; };
+
 __device__ inline float wave_sum(float v) {
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
@@ -30,78 +34,104 @@ __device__ inline uint32_t pack2(float lo, float hi) {
     return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
-// Normalises this lane's NC float2 of the row in place (affine applied).
-template <int NC>
-__device__ inline void normalize_row(f32x2 (&v)[NC], const float *gamma, const float *beta, int lane,
-                                     float eps) {
-    constexpr float inv_d = 1.0f / (float)(NC * 128);
+// One row held by one wave: lane l owns vectors c * 64 + l (VEC floats each).
+// Computes mean and rstd (two-pass, fixed butterfly order) and normalises in
+// place: y = fma(gamma, (z - mean) * rstd, beta) -- the same expression the
+// GEMM epilogue uses when it rebuilds a residual from the row statistics.
+template <int VEC, int NC>
+__device__ inline void normalize_row(typename Vec<VEC>::f (&v)[NC], const float *gamma, const float *beta,
+                                     int lane, float eps, float &mean_out, float &rstd_out) {
+    typedef typename Vec<VEC>::f fv;
+    constexpr float inv_d = 1.0f / (float)(NC * 64 * VEC);
     float s = 0.f;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) s += v[c][0] + v[c][1];
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) s += v[c][e];
     const float mean = wave_sum(s) * inv_d;
     float ss = 0.f;
 #pragma unroll
-    for (int c = 0; c < NC; ++c) {
-        const float a = v[c][0] - mean, b = v[c][1] - mean;
-        ss += a * a + b * b;
-    }
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) {
+            const float a = v[c][e] - mean;
+            ss += a * a;
+        }
     const float rstd = 1.0f / sqrtf(wave_sum(ss) * inv_d + eps);
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
         const int i = c * 64 + lane;
-        const f32x2 g = reinterpret_cast<const f32x2 *>(gamma)[i];
-        const f32x2 b = reinterpret_cast<const f32x2 *>(beta)[i];
-        v[c][0] = g[0] * ((v[c][0] - mean) * rstd) + b[0];
-        v[c][1] = g[1] * ((v[c][1] - mean) * rstd) + b[1];
+        const fv g = reinterpret_cast<const fv *>(gamma)[i];
+        const fv b = reinterpret_cast<const fv *>(beta)[i];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) v[c][e] = __builtin_fmaf(g[e], (v[c][e] - mean) * rstd, b[e]);
     }
+    mean_out = mean;
+    rstd_out = rstd;
 }
 
-template <int NC>
+template <int VEC, int NC>
 __global__ __launch_bounds__(64 * kRowsPerBlock) void layernorm_kernel(
     const float *__restrict__ z, const float *__restrict__ gamma, const float *__restrict__ beta,
-    float *__restrict__ out_f32, bf16_t *__restrict__ out_bf16, int rows, float eps) {
+    float *__restrict__ out_f32, bf16_t *__restrict__ out_bf16, float *__restrict__ stats, int rows,
+    float eps) {
+    typedef typename Vec<VEC>::f fv;
+    typedef typename Vec<VEC>::bf bv;
     const int lane = threadIdx.x & 63;
     const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
     if (row >= rows) return;
-    constexpr int D = NC * 128;
-    const f32x2 *src = reinterpret_cast<const f32x2 *>(z + (size_t)row * D);
-    f32x2 v[NC];
+    constexpr int D = NC * 64 * VEC;
+    const fv *src = reinterpret_cast<const fv *>(z + (size_t)row * D);
+    fv v[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) v[c] = src[c * 64 + lane];
-    normalize_row<NC>(v, gamma, beta, lane, eps);
+    float mean, rstd;
+    normalize_row<VEC, NC>(v, gamma, beta, lane, eps, mean, rstd);
     if (out_f32) {
-        f32x2 *dst = reinterpret_cast<f32x2 *>(out_f32 + (size_t)row * D);
+        fv *dst = reinterpret_cast<fv *>(out_f32 + (size_t)row * D);
 #pragma unroll
         for (int c = 0; c < NC; ++c) dst[c * 64 + lane] = v[c];
     }
     if (out_bf16) {
-        uint32_t *dst = reinterpret_cast<uint32_t *>(out_bf16 + (size_t)row * D);
+        bv *dst = reinterpret_cast<bv *>(out_bf16 + (size_t)row * D);
 #pragma unroll
-        for (int c = 0; c < NC; ++c) dst[c * 64 + lane] = pack2(v[c][0], v[c][1]);
+        for (int c = 0; c < NC; ++c) {
+            if constexpr (VEC == 2) dst[c * 64 + lane] = pack2(v[c][0], v[c][1]);
+            else dst[c * 64 + lane] = u32x2{pack2(v[c][0], v[c][1]), pack2(v[c][2], v[c][3])};
+        }
     }
+    if (stats && lane == 0) reinterpret_cast<f32x2 *>(stats)[row] = f32x2{mean, rstd};
 }
 
-template <int NC>
+template <int VEC, int NC>
 __global__ __launch_bounds__(64 * kRowsPerBlock) void ln_head_kernel(
     const float *__restrict__ z, const float *__restrict__ gamma, const float *__restrict__ beta,
     const bf16_t *__restrict__ wh, const bf16_t *__restrict__ bh, float *__restrict__ logits,
     int rows, int n_out, float eps) {
+    typedef typename Vec<VEC>::f fv;
+    typedef typename Vec<VEC>::bf bv;
     const int lane = threadIdx.x & 63;
     const int row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
     if (row >= rows) return;
-    constexpr int D = NC * 128;
-    const f32x2 *src = reinterpret_cast<const f32x2 *>(z + (size_t)row * D);
-    f32x2 v[NC];
+    constexpr int D = NC * 64 * VEC;
+    const fv *src = reinterpret_cast<const fv *>(z + (size_t)row * D);
+    fv v[NC];
 #pragma unroll
     for (int c = 0; c < NC; ++c) v[c] = src[c * 64 + lane];
-    normalize_row<NC>(v, gamma, beta, lane, eps);
+    float mean, rstd;
+    normalize_row<VEC, NC>(v, gamma, beta, lane, eps, mean, rstd);
     for (int o = 0; o < n_out; ++o) {
-        const uint32_t *wrow = reinterpret_cast<const uint32_t *>(wh + (size_t)o * D);
+        const bv *wrow = reinterpret_cast<const bv *>(wh + (size_t)o * D);
         float part = 0.f;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            const uint32_t w2 = wrow[c * 64 + lane];
-            part += v[c][0] * __uint_as_float(w2 << 16) + v[c][1] * __uint_as_float(w2 & 0xffff0000u);
+            const bv w = wrow[c * 64 + lane];
+            if constexpr (VEC == 2) {
+                part += v[c][0] * __uint_as_float(w << 16) + v[c][1] * __uint_as_float(w & 0xffff0000u);
+            } else {
+                part += v[c][0] * __uint_as_float(w[0] << 16) + v[c][1] * __uint_as_float(w[0] & 0xffff0000u);
+                part += v[c][2] * __uint_as_float(w[1] << 16) + v[c][3] * __uint_as_float(w[1] & 0xffff0000u);
+            }
         }
         const float dot = wave_sum(part);
         if (lane == 0) logits[(size_t)row * n_out + o] = dot + __uint_as_float((uint32_t)bh[o] << 16);
@@ -131,39 +161,40 @@ __global__ __launch_bounds__(64) void cu_probe_kernel(uint32_t *out, int n_group
     out[2 * blockIdx.x + 1] = hw;
 }
 
-template <int NC>
-hipError_t ln_launch(const float *z, const float *g, const float *b, float *o32, bf16_t *o16, int rows,
-                     float eps, hipStream_t s) {
+template <int VEC, int NC>
+hipError_t ln_launch(const float *z, const float *g, const float *b, float *o32, bf16_t *o16, float *stats,
+                     int rows, float eps, hipStream_t s) {
     const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock), block(64 * kRowsPerBlock);
-    hipLaunchKernelGGL(layernorm_kernel<NC>, grid, block, 0, s, z, g, b, o32, o16, rows, eps);
+    hipLaunchKernelGGL((layernorm_kernel<VEC, NC>), grid, block, 0, s, z, g, b, o32, o16, stats, rows, eps);
     return hipGetLastError();
 }
 
-template <int NC>
+template <int VEC, int NC>
 hipError_t ln_head_launch(const float *z, const float *g, const float *b, const bf16_t *wh,
                           const bf16_t *bh, float *logits, int rows, int n_out, float eps, hipStream_t s) {
     const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock), block(64 * kRowsPerBlock);
-    hipLaunchKernelGGL(ln_head_kernel<NC>, grid, block, 0, s, z, g, b, wh, bh, logits, rows, n_out, eps);
+    hipLaunchKernelGGL((ln_head_kernel<VEC, NC>), grid, block, 0, s, z, g, b, wh, bh, logits, rows, n_out, eps);
     return hipGetLastError();
 }
 
-// d / 128 -> template instance (d = 128 .. 4096)
-#define IEFWD_NC_CASES(X) \
-    X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) X(16) \
-    X(17) X(18) X(19) X(20) X(21) X(22) X(23) X(24) X(25) X(26) X(27) X(28) X(29) X(30) X(31) X(32)
+// d = 256 k: 16-byte vectors (k = 1..16); d = 128 (2 k + 1): 8-byte vectors
+#define IEFWD_D_CASES(X) \
+    X(4, 1) X(4, 2) X(4, 3) X(4, 4) X(4, 5) X(4, 6) X(4, 7) X(4, 8) X(4, 9) X(4, 10) X(4, 11) X(4, 12) \
+    X(4, 13) X(4, 14) X(4, 15) X(4, 16) X(2, 1) X(2, 3) X(2, 5) X(2, 7) X(2, 9) X(2, 11) X(2, 13) X(2, 15) \
+    X(2, 17) X(2, 19) X(2, 21) X(2, 23) X(2, 25) X(2, 27) X(2, 29) X(2, 31)
 
 }  // namespace
 
 hipError_t launch_layernorm(const float *z, const float *gamma, const float *beta, float *out_f32,
-                            bf16_t *out_bf16, int rows, int d, float eps, hipStream_t stream) {
+                            bf16_t *out_bf16, int rows, int d, float eps, hipStream_t stream, float *stats) {
     if (rows <= 0) return hipSuccess;
     if (d % 128 != 0) return hipErrorInvalidValue;
-    switch (d / 128) {
-#define X(n) case n: return ln_launch<n>(z, gamma, beta, out_f32, out_bf16, rows, eps, stream);
-        IEFWD_NC_CASES(X)
+    const int vec = d % 256 == 0 ? 4 : 2, nc = d / (64 * vec);
+#define X(V, N) \
+    if (vec == V && nc == N) return ln_launch<V, N>(z, gamma, beta, out_f32, out_bf16, stats, rows, eps, stream);
+    IEFWD_D_CASES(X)
 #undef X
-    default: return hipErrorInvalidValue;
-    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_ln_head(const float *z, const float *gamma, const float *beta, const bf16_t *wh,
@@ -171,12 +202,12 @@ hipError_t launch_ln_head(const float *z, const float *gamma, const float *beta,
                           hipStream_t stream) {
     if (rows <= 0) return hipSuccess;
     if (d % 128 != 0) return hipErrorInvalidValue;
-    switch (d / 128) {
-#define X(n) case n: return ln_head_launch<n>(z, gamma, beta, wh, bh, logits, rows, n_out, eps, stream);
-        IEFWD_NC_CASES(X)
+    const int vec = d % 256 == 0 ? 4 : 2, nc = d / (64 * vec);
+#define X(V, N) \
+    if (vec == V && nc == N) return ln_head_launch<V, N>(z, gamma, beta, wh, bh, logits, rows, n_out, eps, stream);
+    IEFWD_D_CASES(X)
 #undef X
-    default: return hipErrorInvalidValue;
-    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_cast_bf16(const float *x, bf16_t *y, size_t n, hipStream_t stream) {

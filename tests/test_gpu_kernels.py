@@ -91,7 +91,7 @@ def test_qkv_scatter(B, S, d, H):
     dh = d // H
     M = B * S
     a, w, bias, _ = gemm_inputs(M, 3 * d, d, seed=B + S + d)
-    spad = (S + 31) // 32 * 32
+    spad = (S + 63) // 64 * 64
     q = torch.empty((B, H, S, dh), dtype=torch.bfloat16, device=DEV)
     k = torch.empty_like(q)
     vt = torch.zeros((B, H, dh, spad), dtype=torch.bfloat16, device=DEV)
@@ -131,7 +131,7 @@ def attn_inputs(B, H, S, dh, seed, scale=1.0):
 def test_attention(B, H, S, dh, causal, scale):
     print(f"attention B={B} H={H} S={S} dh={dh} causal={causal} scale={scale}", flush=True)
     q, k, v = attn_inputs(B, H, S, dh, seed=S + dh + B, scale=scale)
-    spad = (S + 31) // 32 * 32
+    spad = (S + 63) // 64 * 64
     vt = torch.full((B, H, dh, spad), float("nan"), dtype=torch.bfloat16)   # padding must be ignored
     vt[..., :S] = v.transpose(2, 3)
     ctx = torch.empty((B, S, H * dh), dtype=torch.bfloat16, device=DEV)
@@ -152,9 +152,10 @@ def test_attention_uniform_closed_form():
     B, H, S, dh = 1, 2, 96, 64
     q = torch.zeros((B, H, S, dh), dtype=torch.bfloat16)
     _, _, v = attn_inputs(B, H, S, dh, seed=5)
-    spad = 96
+    spad = 128
     for causal in (False, True):
-        vt = v.transpose(2, 3).contiguous()
+        vt = torch.zeros((B, H, dh, spad), dtype=torch.bfloat16)
+        vt[..., :S] = v.transpose(2, 3)
         ctx = torch.empty((B, S, H * dh), dtype=torch.bfloat16, device=DEV)
         ie.test_attention(to_dev(q), to_dev(q), to_dev(vt), ctx, B, H, S, dh, causal)
         sync()
