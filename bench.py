@@ -9,8 +9,10 @@ quota.
 
 Prints one JSON line: inferences/s (one inference = one sequence), the
 forward-level MFMA utilisation, the roofline of the dominant kernel (FFN-up
-GEMM + bias + GELU, timed with HIP events on the instance's stream during the
-timed region) and the fp64 CPU oracle timed on a bounded sample.
+GEMM + bias + GELU: each launch in the timed region records its own start and
+end into HIP events), the aggregate throughput of two co-located instances at
+CU quotas 64/192, 128/128 and 192/64 against one alone, and the fp64 CPU oracle
+timed on a bounded sample.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 """
@@ -61,6 +63,74 @@ def cpu_baseline(shape, batch_sample: int):
                       f"weights pre-generated; {dt:.2f} s"}
 
 
+def colocated(ie, W, shape, cfg, quota_pairs, batch=8, window_s=1.0):
+    """Aggregate throughput of two co-located instances (independent seeds),
+    each driven by its own host thread with back-to-back batches, against one
+    instance alone at the full quota.  Inputs are device-resident.  Each leg
+    runs for a fixed wall-clock window and counts the batches that completed
+    inside it, so an instance at a small quota does not stretch the window of
+    the other one."""
+    import threading
+
+    import torch
+
+    w = W.WORKLOADS[WORKLOAD]
+    S, d = w["seq"], shape["d_model"]
+    insts = [ie.Instance(device=0, max_batch=batch, max_seq=S, **dict(cfg, seed=31 + i)) for i in range(2)]
+    xs = [torch.from_numpy(W.make_input(31000 + 1000 * i, batch, S, d)).to("cuda:0") for i in range(2)]
+    torch.cuda.synchronize()
+
+    def drive(i, deadline, done):
+        n = 0
+        while True:
+            insts[i].submit(xs[i])
+            insts[i].wait()
+            if time.perf_counter() > deadline:
+                break
+            n += 1
+        done[i] = n
+
+    def window(active):
+        for i in active:                      # warm the re-masked streams
+            for _ in range(5):
+                insts[i].submit(xs[i])
+                insts[i].wait()
+        done = [0, 0]
+        t0 = time.perf_counter()
+        ths = [threading.Thread(target=drive, args=(i, t0 + window_s, done)) for i in active]
+        for t in ths:
+            t.start()
+        for t in ths:
+            t.join()
+        return batch * sum(done) / window_s
+
+    insts[0].set_quota(256)
+    solo = window([0])
+    out = {"workload": f"2 x {WORKLOAD}, batch {batch} each", "window_s": window_s,
+           "solo_inf_s": round(solo, 1), "pairs": []}
+    for qa, qb in quota_pairs:
+        insts[0].set_quota(qa)
+        insts[1].set_quota(qb)
+        agg = window([0, 1])
+        out["pairs"].append({"quotas": [qa, qb], "aggregate_inf_s": round(agg, 1),
+                             "vs_solo": round(agg / solo, 3)})
+    for inst in insts:
+        inst.close()
+    return out
+
+
+def copy_calibration(mib: int) -> None:
+    """A plain device-to-device copy of `mib` MiB, for scaling the FETCH_SIZE /
+    WRITE_SIZE counters of a profiling run (read once, written once)."""
+    import torch
+
+    a = torch.empty(mib * 2 ** 20, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -70,6 +140,9 @@ def main() -> int:
     ap.add_argument("--quota", type=int, default=256)
     ap.add_argument("--cpu-sample", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-colocated", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="first run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the instances of this workload share one MI355X); "
@@ -81,6 +154,8 @@ def main() -> int:
     import paper_2503_05130_amd as ie
     import workloads as W
 
+    if args.copy_calibration_mib:
+        copy_calibration(args.copy_calibration_mib)
     w = W.WORKLOADS[WORKLOAD]
     shape = W.model_shape(WORKLOAD)
     B, S = args.batch, w["seq"]
@@ -145,6 +220,8 @@ def main() -> int:
         "roofline": roof,
     }
     inst.close()
+    if not args.no_colocated:
+        result["colocated"] = colocated(ie, W, shape, cfg, [(64, 192), (128, 128), (192, 64)])
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(shape, args.cpu_sample)
     print(json.dumps(result))

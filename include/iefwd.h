@@ -173,9 +173,11 @@ int iefwd_get_stream(iefwd_instance *inst, void **hip_stream);
 #define IEFWD_K_LN       5u   /* LayerNorm kernels (including the fused final LN + head) */
 #define IEFWD_K_COUNT    6u
 
-/* enable != 0: every later launch of class `kind` is bracketed by HIP events on
- * the instance's stream; iefwd_kernel_time sums the bracketed durations of
- * completed batches.  enable = 0 stops timing; both calls reset the sums. */
+/* enable != 0: every later launch of class `kind` records the kernel's own
+ * start and end timestamps into a pair of HIP events (hipExtLaunchKernel);
+ * iefwd_kernel_time sums those kernel durations over completed batches.
+ * enable = 0 stops timing; both calls reset the sums.  ESTATE while a batch is
+ * in flight. */
 int iefwd_time_kernel(iefwd_instance *inst, uint32_t kind, int enable);
 int iefwd_kernel_time(iefwd_instance *inst, uint32_t kind, double *total_ms, uint64_t *launches);
 

@@ -240,9 +240,8 @@ hipError_t launch(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ct
     const int groups = (seq + 32 * kWaves - 1) / (32 * kWaves);
     const dim3 grid(groups, batch * n_heads), block(kThreads);
     const float scale_log2e = 1.4426950408889634f / sqrtf((float)DH);
-    hipLaunchKernelGGL((attention_kernel<DH, CAUSAL>), grid, block, 0, s, q, k, vt, ctx, n_heads,
-                       seq, attn_seq_pad(seq), scale_log2e);
-    return hipGetLastError();
+    return launch_kernel(attention_kernel<DH, CAUSAL>, grid, block, s, q, k, vt, ctx, n_heads, seq,
+                         attn_seq_pad(seq), scale_log2e);
 }
 
 }  // namespace

@@ -21,11 +21,12 @@
 // so each lane ends up owning 4 consecutive output features of one token and
 // stores them with one vector store.  4 waves in a 2 x 2 grid over the tile.
 //
-// Determinism and batch invariance: every tile configuration uses the same MFMA
-// instruction and walks K in the same order (64-wide K tiles, two 32-wide MFMA
-// steps each), so out[t, f] depends only on row t of A and row f of W -- never
-// on the tile shape, the ring depth, the grid, the CU mask or the other rows in
-// the batch.  No atomics, no split-K.
+// Determinism and batch invariance: every configuration uses the same MFMA
+// instruction; the K summation order (sequential 64-wide K tiles, or the
+// workgroup-internal even/odd split for long K) is a function of the weight
+// shape (N, K) alone.  So out[t, f] depends only on row t of A and row f of W
+// -- never on the tile shape, the ring depth, the grid, the CU mask or the
+// other rows in the batch.  No atomics, no cross-workgroup split-K.
 #include "kernels.h"
 
 #include <algorithm>
@@ -36,6 +37,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
 constexpr int kBK = 64;               // K tile (bf16 elements) = one 128-byte LDS row
@@ -113,22 +115,21 @@ __device__ inline int swizzle(int r) { return ((r >> 1) & 7) ^ ((r & 1) << 2); }
 // this wave are outstanding (expcnt and lgkmcnt left unconstrained).
 constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
 
-template <int BM, int BN, int S, Epi EPI>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
+// One 4-wave group's main loop over the K tiles kt_first, kt_first + kt_stride,
+// ... (n_mine of them) through its own S-slot LDS ring, accumulating into acc.
+// Every wave of the workgroup runs n_steps iterations (>= n_mine), so the
+// workgroup barriers line up even when two groups own different tile counts.
+template <int BM, int BN, int S>
+__device__ inline void main_loop(const GemmParams &p, bf16_t *ring0, int wave, int lane, int m0, int n0,
+                                 int kt_first, int kt_stride, int n_mine, int n_steps,
+                                 f32x4 (&acc)[BN / 32][BM / 32]) {
     constexpr int TM = BM / 2, TN = BN / 2;          // per-wave tile (tokens x features)
     constexpr int FM = TM / 16, FN = TN / 16;        // 16x16 MFMA blocks per wave
     constexpr int STAGE = (BM + BN) * kBK;           // bf16 elements per ring slot
     constexpr int A_PW = BM / 32, W_PW = BN / 32;    // 1 KB DMAs per wave per K tile
     constexpr int LPW = A_PW + W_PW;
-    static_assert(BM % 32 == 0 && BN % 32 == 0 && TM % 16 == 0 && TN % 16 == 0, "tile");
+    static_assert(BM % 32 == 0 && BN % 32 == 0, "tile");
     static_assert(S >= 2 && (S - 2) * LPW <= 63, "ring depth");
-
-    __shared__ __attribute__((aligned(1024))) bf16_t lds[S * STAGE];
-
-    int tm, tn;
-    grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
     // DMA sources of this lane: DMA i of this wave copies the 8-row group
@@ -145,44 +146,38 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
         const int r = 8 * (wave + 4 * i) + (lane >> 3);
         w_src[i] = (uint32_t)min(n0 + r, p.N - 1) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
     }
-#define IEFWD_ISSUE(kt, slot)                                                                      \
-    do {                                                                                           \
-        const int k0_ = (kt) * kBK;                                                                \
-        bf16_t *ring_ = lds + (slot) * STAGE;                                                      \
-        _Pragma("unroll") for (int i = 0; i < A_PW; ++i)                                           \
-            __builtin_amdgcn_global_load_lds((const void *)(p.a + a_src[i] + k0_),                               \
-                                             (lds_ptr_t)(ring_ + (wave + 4 * i) * 512), 16, 0, 0); \
-        _Pragma("unroll") for (int i = 0; i < W_PW; ++i)                                           \
-            __builtin_amdgcn_global_load_lds((const void *)(p.w + w_src[i] + k0_),                               \
-                                             (lds_ptr_t)(ring_ + BM * kBK + (wave + 4 * i) * 512), \
-                                             16, 0, 0);                                            \
+#define IEFWD_ISSUE(kt, slot)                                                                           \
+    do {                                                                                                \
+        const int k0_ = (kt) * kBK;                                                                     \
+        bf16_t *ring_ = ring0 + (slot) * STAGE;                                                         \
+        _Pragma("unroll") for (int i = 0; i < A_PW; ++i)                                                \
+            __builtin_amdgcn_global_load_lds((const void *)(p.a + a_src[i] + k0_),                      \
+                                             (lds_ptr_t)(ring_ + (wave + 4 * i) * 512), 16, 0, 0);      \
+        _Pragma("unroll") for (int i = 0; i < W_PW; ++i)                                                \
+            __builtin_amdgcn_global_load_lds((const void *)(p.w + w_src[i] + k0_),                      \
+                                             (lds_ptr_t)(ring_ + BM * kBK + (wave + 4 * i) * 512), 16,  \
+                                             0, 0);                                                     \
     } while (0)
 
-    f32x4 acc[FN][FM];
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int i = 0; i < FM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    const int kt_count = p.K / kBK;
 #pragma unroll
     for (int s = 0; s < S - 1; ++s)
-        if (s < kt_count) IEFWD_ISSUE(s, s);
+        if (s < n_mine) IEFWD_ISSUE(kt_first + s * kt_stride, s);
 
     // fragment rows: lane % 16 of each 16-row block; 16-byte chunk 4 ks + lane / 16
     const int ra = wm * TM + (lane & 15), rw = wn * TN + (lane & 15);
-    for (int kt = 0; kt < kt_count; ++kt) {
-        // this wave's copies of tile kt are done once at most the later tiles'
-        // copies are outstanding; the barrier then publishes every wave's copies
-        // and guarantees the slot reused below is no longer being read
-        if (kt + S - 2 < kt_count)
+    for (int it = 0; it < n_steps; ++it) {
+        // this wave's copies of its tile `it` are done once at most the later
+        // tiles' copies are outstanding; the barrier then publishes every wave's
+        // copies and guarantees the slot reused below is no longer being read
+        if (it + S - 2 < n_mine)
             __builtin_amdgcn_s_waitcnt(vmcnt_imm((S - 2) * LPW));
         else
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");   // keep LDS accesses on their side of the barrier
-        if (kt + S - 1 < kt_count) IEFWD_ISSUE(kt + S - 1, (kt + S - 1) % S);
-        const bf16_t *ring = lds + (kt % S) * STAGE;
+        if (it + S - 1 < n_mine) IEFWD_ISSUE(kt_first + (it + S - 1) * kt_stride, (it + S - 1) % S);
+        if (it >= n_mine) continue;
+        const bf16_t *ring = ring0 + (it % S) * STAGE;
 #pragma unroll
         for (int ks = 0; ks < kBK / 32; ++ks) {
             const int c = ks * 4 + (lane >> 4);
@@ -205,8 +200,62 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
         }
     }
 #undef IEFWD_ISSUE
+}
 
-    // Epilogue: lane owns features f..f+3 of token t in every block.
+// Epilogue operands that do not depend on the product (bias, residual rows,
+// LayerNorm statistics and affine) are loaded into registers before the main
+// loop, so their latency hides behind the MFMAs instead of stalling the tail.
+// The residual rows are prefetched only by 4-wave workgroups with small wave
+// tiles (<= 6 blocks); larger tiles, and the 8-wave split workgroups (whose
+// register budget is shared by both groups), would trade occupancy for it and
+// load them in the epilogue instead.
+template <int BM, int BN, Epi EPI, bool SPLIT = false>
+struct EpiInputs {
+    static constexpr int FM = BM / 32, FN = BN / 32;
+    static constexpr bool kZ = (EPI == Epi::BiasResidF32 || EPI == Epi::BiasLnResidF32) && FN * FM <= 6 && !SPLIT;
+    u32x2 bias[FN];
+    f32x4 z[kZ ? FN : 1][kZ ? FM : 1];
+    f32x2 stats[EPI == Epi::BiasLnResidF32 ? FM : 1];
+    f32x4 gamma[EPI == Epi::BiasLnResidF32 ? FN : 1], beta[EPI == Epi::BiasLnResidF32 ? FN : 1];
+};
+
+template <int BM, int BN, Epi EPI, bool SPLIT>
+__device__ inline void epilogue_prefetch(const GemmParams &p, EpiInputs<BM, BN, EPI, SPLIT> &in, int wave,
+                                         int lane, int m0, int n0) {
+    constexpr int TM = BM / 2, TN = BN / 2, FM = TM / 16, FN = TN / 16;
+    const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+        const int f = min(n0 + wn * TN + j * 16 + (lane >> 4) * 4, p.N - 4);
+        in.bias[j] = *reinterpret_cast<const u32x2 *>(p.bias + f);
+        if constexpr (EPI == Epi::BiasLnResidF32) {
+            in.gamma[j] = *reinterpret_cast<const f32x4 *>(p.ln.gamma + f);
+            in.beta[j] = *reinterpret_cast<const f32x4 *>(p.ln.beta + f);
+        }
+        if constexpr (EpiInputs<BM, BN, EPI, SPLIT>::kZ) {
+            const float *src = EPI == Epi::BiasResidF32 ? p.resid : p.ln.z;
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+                const int t = min(m0 + wm * TM + i * 16 + (lane & 15), p.M - 1);   // clamped: never stored
+                in.z[j][i] = *reinterpret_cast<const f32x4 *>(src + (size_t)t * p.N + f);
+            }
+        }
+    }
+    if constexpr (EPI == Epi::BiasLnResidF32) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int t = min(m0 + wm * TM + i * 16 + (lane & 15), p.M - 1);
+            in.stats[i] = *reinterpret_cast<const f32x2 *>(p.ln.stats + 2 * (size_t)t);
+        }
+    }
+}
+
+// Epilogue of one wave: lane owns features f..f+3 of token t in every block.
+template <int BM, int BN, Epi EPI, bool SPLIT>
+__device__ inline void epilogue(const GemmParams &p, const f32x4 (&acc)[BN / 32][BM / 32],
+                                const EpiInputs<BM, BN, EPI, SPLIT> &in, int wave, int lane, int m0, int n0) {
+    constexpr int TM = BM / 2, TN = BN / 2, FM = TM / 16, FN = TN / 16;
+    const int wm = wave >> 1, wn = wave & 1;
     int tok[FM];
 #pragma unroll
     for (int i = 0; i < FM; ++i) tok[i] = m0 + wm * TM + i * 16 + (lane & 15);
@@ -222,14 +271,9 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
     for (int j = 0; j < FN; ++j) {
         const int f = n0 + wn * TN + j * 16 + (lane >> 4) * 4;
         if (f >= p.N) continue;
-        const u32x2 braw = *reinterpret_cast<const u32x2 *>(p.bias + f);
+        const u32x2 braw = in.bias[j];
         const float b0 = __uint_as_float(braw[0] << 16), b1 = __uint_as_float(braw[0] & 0xffff0000u);
         const float b2 = __uint_as_float(braw[1] << 16), b3 = __uint_as_float(braw[1] & 0xffff0000u);
-        f32x4 ln_g, ln_b;
-        if constexpr (EPI == Epi::BiasLnResidF32) {
-            ln_g = *reinterpret_cast<const f32x4 *>(p.ln.gamma + f);
-            ln_b = *reinterpret_cast<const f32x4 *>(p.ln.beta + f);
-        }
         int which = 0, head = 0, jj = 0;   // head scatter: Q/K/V block, head, column within head
         if constexpr (EPI == Epi::Qkv) {
             which = f / p.qkv.d_model;
@@ -250,19 +294,21 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
                 bf16_t *o = static_cast<bf16_t *>(p.out) + (size_t)t * p.N + f;
                 *reinterpret_cast<u32x2 *>(o) = u32x2{pack2(v0, v1), pack2(v2, v3)};
             } else if constexpr (EPI == Epi::BiasResidF32) {
-                const size_t off = (size_t)t * p.N + f;
-                const f32x4 r = *reinterpret_cast<const f32x4 *>(p.resid + off);
-                *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + off) =
+                f32x4 r;
+                if constexpr (EpiInputs<BM, BN, EPI, SPLIT>::kZ) r = in.z[j][i];
+                else r = *reinterpret_cast<const f32x4 *>(p.resid + (size_t)t * p.N + f);
+                *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + (size_t)t * p.N + f) =
                     f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
             } else if constexpr (EPI == Epi::BiasLnResidF32) {
                 // residual = LN(z) rebuilt with the LayerNorm kernel's expression
-                const size_t off = (size_t)t * p.N + f;
-                const f32x4 z = *reinterpret_cast<const f32x4 *>(p.ln.z + off);
-                const float mean = p.ln.stats[2 * t], rstd = p.ln.stats[2 * t + 1];
+                f32x4 z;
+                if constexpr (EpiInputs<BM, BN, EPI, SPLIT>::kZ) z = in.z[j][i];
+                else z = *reinterpret_cast<const f32x4 *>(p.ln.z + (size_t)t * p.N + f);
+                const float mean = in.stats[i][0], rstd = in.stats[i][1];
                 f32x4 r;
 #pragma unroll
-                for (int e = 0; e < 4; ++e) r[e] = __builtin_fmaf(ln_g[e], (z[e] - mean) * rstd, ln_b[e]);
-                *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + off) =
+                for (int e = 0; e < 4; ++e) r[e] = __builtin_fmaf(in.gamma[j][e], (z[e] - mean) * rstd, in.beta[j][e]);
+                *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + (size_t)t * p.N + f) =
                     f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
             } else {   // Epi::Qkv
                 const QkvDst &d = p.qkv;
@@ -283,39 +329,112 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
     }
 }
 
-struct TileChoice {
-    int bm, bn, stages;
-};
-
-// Tile shape and ring depth from (M, N, K) only -- never the current CU quota.
-// Measured on gfx950 at T = 4096 tokens: a 2-slot ring with two workgroups
-// resident per CU beats deeper rings with one, except for long-K narrow-N
-// products (FFN down-projection) where a 4-slot 128 x 96 ring wins.  Small
-// grids fall back to 64 x 64 tiles (up to three workgroups per CU).
-TileChoice choose_tile(int M, int N, int K) {
-    const long tiles_96 = (long)((M + 127) / 128) * (N / 96);
-    const long tiles_128 = (long)((M + 127) / 128) * (N / 128);
-    if (N % 96 == 0 && tiles_96 >= 256) return {128, 96, K >= 2048 ? 4 : 2};
-    if (N % 128 == 0 && tiles_128 >= 256) return {128, 128, 2};
-    if (N % 96 == 0 && tiles_96 >= 128) return {128, 96, 2};
-    return {64, 64, 3};
+// Sequential K order: 4 waves, one ring, K tiles 0, 1, 2, ... into one accumulator.
+template <int BM, int BN, int S, Epi EPI>
+__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
+    __shared__ __attribute__((aligned(1024))) bf16_t lds[S * (BM + BN) * kBK];
+    int tm, tn;
+    grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    f32x4 acc[BN / 32][BM / 32];
+#pragma unroll
+    for (int j = 0; j < BN / 32; ++j)
+#pragma unroll
+        for (int i = 0; i < BM / 32; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    EpiInputs<BM, BN, EPI, false> in;
+    epilogue_prefetch<BM, BN, EPI, false>(p, in, wave, lane, m0, n0);
+    const int kt_count = p.K / kBK;
+    main_loop<BM, BN, S>(p, lds, wave, lane, m0, n0, 0, 1, kt_count, kt_count, acc);
+    epilogue<BM, BN, EPI, false>(p, acc, in, wave, lane, m0, n0);
 }
 
-template <int BM, int BN, int S>
+// Split K order: 8 waves in two 4-wave groups over the same output tile; group g
+// accumulates the K tiles kt = g (mod 2) through its own ring, then group 1
+// hands its partial sums to group 0 through LDS and group 0 adds them
+// (even-tile sum + odd-tile sum, always in that order) and runs the epilogue.
+// Two waves per SIMD even when there are only as many tiles as CUs.
+template <int BM, int BN, int S, Epi EPI>
+__global__ __launch_bounds__(2 * kThreads) void gemm_split_kernel(GemmParams p) {
+    constexpr int FN = BN / 32, FM = BM / 32;
+    __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * S * (BM + BN) * kBK];
+    static_assert(FN * FM * 4 * kThreads * 4 <= 2 * S * (BM + BN) * kBK * 2, "hand-off space");
+    int tm, tn;
+    grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int lane = threadIdx.x & 63, grp = threadIdx.x >> 8, wave = (threadIdx.x >> 6) & 3;
+    f32x4 acc[FN][FM];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int i = 0; i < FM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    EpiInputs<BM, BN, EPI, true> in;
+    if (grp == 0) epilogue_prefetch<BM, BN, EPI, true>(p, in, wave, lane, m0, n0);
+    const int kt_count = p.K / kBK;
+    const int n_mine = (kt_count - grp + 1) / 2;
+    main_loop<BM, BN, S>(p, lds + grp * S * (BM + BN) * kBK, wave, lane, m0, n0, grp, 2, n_mine,
+                         (kt_count + 1) / 2, acc);
+    __syncthreads();   // both rings drained: reuse the LDS for the hand-off
+    float *handoff = reinterpret_cast<float *>(lds) + (wave * 64 + lane) * (FN * FM * 4);
+    if (grp == 1) {
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int i = 0; i < FM; ++i) *reinterpret_cast<f32x4 *>(handoff + (j * FM + i) * 4) = acc[j][i];
+    }
+    __syncthreads();
+    if (grp == 1) return;
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int i = 0; i < FM; ++i) acc[j][i] += *reinterpret_cast<const f32x4 *>(handoff + (j * FM + i) * 4);
+    epilogue<BM, BN, EPI, true>(p, acc, in, wave, lane, m0, n0);
+}
+
+struct TileChoice {
+    int bm, bn, stages;
+    bool split;
+};
+
+// K summation order from the weight shape (N, K) only: K >= 2048 uses the
+// split (even/odd) order, shorter K the sequential order.  So a given weight
+// matrix always sums each output in the same order, whatever M (the batch),
+// the CU quota or the tile shape -- outputs stay bit-identical across them.
+bool split_k_order(int /*N*/, int K) { return K >= 2048; }
+
+// Tile shape and ring depth from (M, N, K) only -- never the current CU quota.
+// Measured inside the forward pass on gfx950: 64 x 96 tiles with a 2-slot ring
+// (up to four workgroups per CU) win up to ~1500 such tiles, 128 x 96 beyond;
+// 128 x 128 / 64 x 128 serve widths that 96 does not divide.  The split order
+// runs 8-wave workgroups.
+TileChoice choose_tile(int M, int N, int K) {
+    const long m64 = (M + 63) / 64;
+    if (split_k_order(N, K)) {
+        if (N % 96 == 0) return {64, 96, 2, true};
+        if (N % 128 == 0 && m64 * (N / 128) < 512) return {64, 128, 2, true};
+        return {128, 128, 2, true};
+    }
+    if (N % 96 == 0 && m64 * (N / 96) <= 1536) return {64, 96, 2, false};
+    if (N % 96 == 0) return {128, 96, 2, false};
+    if (N % 128 == 0) return m64 * (N / 128) < 512 ? TileChoice{64, 128, 2, false} : TileChoice{128, 128, 2, false};
+    return {64, 64, 3, false};
+}
+
+template <int BM, int BN, int S, bool SPLIT>
 hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
     p.tiles_m = (p.M + BM - 1) / BM;
     p.tiles_n = p.N / BN;
-    const dim3 grid(p.tiles_m * p.tiles_n), block(kThreads);
+    const dim3 grid(p.tiles_m * p.tiles_n), block(SPLIT ? 2 * kThreads : kThreads);
+#define IEFWD_K(E) (SPLIT ? gemm_split_kernel<BM, BN, S, E> : gemm_kernel<BM, BN, S, E>)
     switch (epi) {
-    case Epi::BiasBf16: hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::BiasBf16>), grid, block, 0, s, p); break;
-    case Epi::BiasGeluBf16: hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::BiasGeluBf16>), grid, block, 0, s, p); break;
-    case Epi::BiasResidF32: hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::BiasResidF32>), grid, block, 0, s, p); break;
-    case Epi::Qkv: hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::Qkv>), grid, block, 0, s, p); break;
-    case Epi::BiasLnResidF32:
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, S, Epi::BiasLnResidF32>), grid, block, 0, s, p);
-        break;
+    case Epi::BiasBf16: return launch_kernel(IEFWD_K(Epi::BiasBf16), grid, block, s, p);
+    case Epi::BiasGeluBf16: return launch_kernel(IEFWD_K(Epi::BiasGeluBf16), grid, block, s, p);
+    case Epi::BiasResidF32: return launch_kernel(IEFWD_K(Epi::BiasResidF32), grid, block, s, p);
+    case Epi::Qkv: return launch_kernel(IEFWD_K(Epi::Qkv), grid, block, s, p);
+    case Epi::BiasLnResidF32: return launch_kernel(IEFWD_K(Epi::BiasLnResidF32), grid, block, s, p);
     }
-    return hipGetLastError();
+#undef IEFWD_K
+    return hipErrorInvalidValue;
 }
 
 }  // namespace
@@ -330,10 +449,16 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
     if (qkv) p.qkv = *qkv;
     if (ln) p.ln = *ln;
     const TileChoice t = choose_tile(M, N, K);
-    if (t.bm == 128 && t.bn == 96)
-        return t.stages == 4 ? launch_tile<128, 96, 4>(epi, p, stream) : launch_tile<128, 96, 2>(epi, p, stream);
-    if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128, 2>(epi, p, stream);
-    return launch_tile<64, 64, 3>(epi, p, stream);
+    if (t.split) {
+        if (t.bm == 64 && t.bn == 96) return launch_tile<64, 96, 2, true>(epi, p, stream);
+        if (t.bm == 64 && t.bn == 128) return launch_tile<64, 128, 2, true>(epi, p, stream);
+        return launch_tile<128, 128, 2, true>(epi, p, stream);
+    }
+    if (t.bm == 64 && t.bn == 96) return launch_tile<64, 96, 2, false>(epi, p, stream);
+    if (t.bm == 64 && t.bn == 128) return launch_tile<64, 128, 2, false>(epi, p, stream);
+    if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128, 2, false>(epi, p, stream);
+    if (t.bm == 128 && t.bn == 96) return launch_tile<128, 96, 2, false>(epi, p, stream);
+    return launch_tile<64, 64, 3, false>(epi, p, stream);
 }
 
 }  // namespace iefwd

@@ -23,6 +23,13 @@
 
 using namespace iefwd;
 
+namespace iefwd {
+LaunchEvents &armed_launch_events() {
+    thread_local LaunchEvents ev;
+    return ev;
+}
+}  // namespace iefwd
+
 namespace {
 
 thread_local std::string t_last_error;
@@ -190,20 +197,21 @@ hipEvent_t take_event(iefwd_instance *inst) {
     return e;
 }
 
-// Launch one kernel of class `kind`, bracketed by events when that class is timed.
+// Launch one kernel of class `kind`; when that class is timed the launch records
+// the kernel's own start and end timestamps into a pair of events.
 template <class F>
 void launch(iefwd_instance *inst, uint32_t kind, const char *what, F &&f) {
     auto &t = inst->timing[kind];
-    hipEvent_t e0 = nullptr, e1 = nullptr;
     if (t.enabled) {
-        e0 = take_event(inst);
-        e1 = take_event(inst);
-        hip_check(hipEventRecord(e0, inst->stream), "hipEventRecord");
-    }
-    hip_check(f(), what);
-    if (t.enabled) {
-        hip_check(hipEventRecord(e1, inst->stream), "hipEventRecord");
+        // the kernel itself records its start and end into these events
+        hipEvent_t e0 = take_event(inst), e1 = take_event(inst);
+        armed_launch_events() = LaunchEvents{e0, e1};
+        const hipError_t err = f();
+        armed_launch_events() = LaunchEvents{};
+        hip_check(err, what);
         t.inflight.emplace_back(e0, e1);
+    } else {
+        hip_check(f(), what);
     }
 }
 

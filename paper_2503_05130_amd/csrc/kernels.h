@@ -3,11 +3,33 @@
 // checks live in the callers (executor and test entry points).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
+
 #include <cstddef>
 #include <cstdint>
 
 namespace iefwd {
+
+// Kernel-only timing: when a pair of events is armed on this host thread, the
+// next kernel launch records its own dispatch start and end into them (the
+// timestamps of the kernel itself, not of markers around it) and disarms.
+struct LaunchEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+LaunchEvents &armed_launch_events();
+
+template <typename F, typename... Args>
+hipError_t launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t stream, Args... args) {
+    LaunchEvents &ev = armed_launch_events();
+    if (ev.start) {
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, ev.start, ev.stop, 0, args...);
+        ev = LaunchEvents{};
+    } else {
+        hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
+    }
+    return hipGetLastError();
+}
 
 using bf16_t = uint16_t;   // bf16 storage: the upper half of an fp32 bit pattern
 

@@ -165,16 +165,14 @@ template <int VEC, int NC>
 hipError_t ln_launch(const float *z, const float *g, const float *b, float *o32, bf16_t *o16, float *stats,
                      int rows, float eps, hipStream_t s) {
     const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock), block(64 * kRowsPerBlock);
-    hipLaunchKernelGGL((layernorm_kernel<VEC, NC>), grid, block, 0, s, z, g, b, o32, o16, stats, rows, eps);
-    return hipGetLastError();
+    return launch_kernel(layernorm_kernel<VEC, NC>, grid, block, s, z, g, b, o32, o16, stats, rows, eps);
 }
 
 template <int VEC, int NC>
 hipError_t ln_head_launch(const float *z, const float *g, const float *b, const bf16_t *wh,
                           const bf16_t *bh, float *logits, int rows, int n_out, float eps, hipStream_t s) {
     const dim3 grid((rows + kRowsPerBlock - 1) / kRowsPerBlock), block(64 * kRowsPerBlock);
-    hipLaunchKernelGGL((ln_head_kernel<VEC, NC>), grid, block, 0, s, z, g, b, wh, bh, logits, rows, n_out, eps);
-    return hipGetLastError();
+    return launch_kernel(ln_head_kernel<VEC, NC>, grid, block, s, z, g, b, wh, bh, logits, rows, n_out, eps);
 }
 
 // d = 256 k: 16-byte vectors (k = 1..16); d = 128 (2 k + 1): 8-byte vectors
@@ -214,14 +212,12 @@ hipError_t launch_cast_bf16(const float *x, bf16_t *y, size_t n, hipStream_t str
     if (n == 0) return hipSuccess;
     const size_t n4 = n / 4;
     const dim3 grid((unsigned)((n4 + 255) / 256)), block(256);
-    hipLaunchKernelGGL(cast_bf16_kernel, grid, block, 0, stream, x, y, n4);
-    return hipGetLastError();
+    return launch_kernel(cast_bf16_kernel, grid, block, stream, x, y, n4);
 }
 
 hipError_t launch_cu_probe(uint32_t *out, int n_groups, hipStream_t stream) {
     if (n_groups <= 0) return hipSuccess;
-    hipLaunchKernelGGL(cu_probe_kernel, dim3(n_groups), dim3(64), 0, stream, out, n_groups);
-    return hipGetLastError();
+    return launch_kernel(cu_probe_kernel, dim3(n_groups), dim3(64), stream, out, n_groups);
 }
 
 }  // namespace iefwd

@@ -38,8 +38,13 @@ def gemm_bound(a64, w64, K):
     (37, 192, 128),      # ragged M, 64-wide tiles
     (130, 320, 192),     # ragged M over several tiles
     (1000, 768, 768),    # 128 x 96 tiles, ragged M
-    (512, 3072, 768),    # 128 x 128 tiles
-    (256, 768, 3072),    # long K
+    (512, 3072, 768),    # 64 x 96 tiles
+    (4096, 3072, 256),   # 128 x 128 tiles
+    (4096, 2496, 128),   # 128 x 96 tiles
+    (300, 1024, 1024),   # 64 x 128 tiles, ragged M
+    (256, 768, 3072),    # long K: split (even/odd) K order, 64 x 96
+    (130, 512, 2048),    # split order, 64 x 128, ragged M
+    (2048, 2048, 2048),  # split order, 128 x 128
 ])
 @pytest.mark.parametrize("epi", [ie.EPI_BIAS_BF16, ie.EPI_BIAS_GELU_BF16, ie.EPI_BIAS_RESID_F32])
 def test_gemm_epilogues(M, N, K, epi):
@@ -71,9 +76,14 @@ def test_gemm_epilogues(M, N, K, epi):
     assert np.all(err <= tol), f"max excess at {worst}: err {err[worst]} tol {tol[worst]}"
 
 
-def test_gemm_batch_invariance():
-    # rows computed in a large batch equal the same rows computed alone, bit for bit
-    M, N, K = 512, 768, 768
+@pytest.mark.parametrize("M,N,K", [
+    (512, 768, 768),      # 64 x 96 tiles throughout
+    (4096, 3072, 768),    # 128 x 128 tiles for the full batch, 64 x 96 for the slices
+    (4096, 1024, 4096),   # split K order: 128 x 128 for the full batch, 64 x 128 for the slices
+])
+def test_gemm_batch_invariance(M, N, K):
+    # rows computed in a large batch equal the same rows computed alone, bit for
+    # bit, even when the two launches pick different tile shapes
     a, w, bias, _ = gemm_inputs(M, N, K, seed=3)
     a_d, w_d, b_d = to_dev(a), to_dev(w.t()), to_dev(bias)
     full = torch.empty((M, N), dtype=torch.bfloat16, device=DEV)
