@@ -12,7 +12,8 @@ forward-level MFMA utilisation, the roofline of the dominant kernel (FFN-up
 GEMM + bias + GELU: each launch in the timed region records its own start and
 end into HIP events), the aggregate throughput of two co-located instances at
 CU quotas 64/192, 128/128 and 192/64 against one alone, and the fp64 CPU oracle
-timed on a bounded sample.
+timed on a bounded sample, and the per-batch cost of re-masking the
+instance's stream between batches.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 """
@@ -31,6 +32,21 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense bf16 MFMA
 WORKLOAD = "bert_base_l12_d768_s128"
+# HBM bytes per launch of the FFN-up kernel (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 KiB,
+# factors from a 256 MiB device copy in the same runs), valid only for the GEMM source
+# they were counted on; any other source reports null.
+FFN1_TRAFFIC = {"source_sha256_16": "ad479054e862fde8", "bytes": (23404.5 * 2.0 + 25036.5 * 1.0) * 1024}
+GEMM_SOURCES = ("paper_2503_05130_amd/csrc/gemm.hip", "paper_2503_05130_amd/csrc/kernels.h")
+
+
+def gemm_source_hash() -> str:
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in GEMM_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
 
 
 def forward_flops(L, d, F, H, S, n_out, causal=False):
@@ -119,6 +135,34 @@ def colocated(ie, W, shape, cfg, quota_pairs, batch=8, window_s=1.0):
     return out
 
 
+def remask_overhead(inst, x, n=40):
+    """Cost of re-masking between batches: mean batch time with the quota
+    alternating 128 <-> 256 on every batch, against the mean of the two fixed
+    quotas.  Each batch is waited for, so the figures are per-batch latencies."""
+    import torch
+
+    def run(quotas):
+        for q in quotas[:4]:
+            inst.set_quota(q)
+            inst.submit(x)
+            inst.wait()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for q in quotas:
+            inst.set_quota(q)
+            inst.submit(x)
+            inst.wait()
+        return (time.perf_counter() - t0) * 1e3 / len(quotas)
+
+    t256 = run([256] * n)
+    t128 = run([128] * n)
+    alt = run([128, 256] * (n // 2))
+    inst.set_quota(256)
+    base = (t128 + t256) / 2
+    return {"ms_fixed_256": round(t256, 4), "ms_fixed_128": round(t128, 4), "ms_alternating": round(alt, 4),
+            "overhead_pct": round((alt - base) / base * 100, 2)}
+
+
 def copy_calibration(mib: int) -> None:
     """A plain device-to-device copy of `mib` MiB, for scaling the FETCH_SIZE /
     WRITE_SIZE counters of a profiling run (read once, written once)."""
@@ -198,7 +242,9 @@ def main() -> int:
     achieved = kernel_flops / k_avg_s / 1e12
     peak = PEAK_BF16_TFLOPS * args.quota / 256
     roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": round(peak, 1), "unit": "TFLOP/s",
-            "frac": round(achieved / peak, 4), "traffic": None,
+            "frac": round(achieved / peak, 4),
+            "traffic": (round(FFN1_TRAFFIC["bytes"]) if gemm_source_hash() == FFN1_TRAFFIC["source_sha256_16"]
+                        else None),
             "kernel": "FFN-up GEMM + bias + GELU", "avg_us": round(k_avg_s * 1e6, 2), "launches": k_launches}
 
     result = {
@@ -219,6 +265,7 @@ def main() -> int:
         "mfma_util_pct": round(mfma_util, 2),
         "roofline": roof,
     }
+    result["remask"] = remask_overhead(inst, x)
     inst.close()
     if not args.no_colocated:
         result["colocated"] = colocated(ie, W, shape, cfg, [(64, 192), (128, 128), (192, 64)])
