@@ -34,9 +34,10 @@ PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense bf16 MFM
 WORKLOAD = "bert_base_l12_d768_s128"
 # HBM bytes per launch of the FFN-up kernel (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 KiB,
 # factors from a 256 MiB device copy in the same runs), valid only for the GEMM source
-# they were counted on; any other source reports null.
+# and build flags they were counted on; any other source reports null.
 FFN1_TRAFFIC = {"source_sha256_16": "ad479054e862fde8", "bytes": (23404.5 * 2.0 + 25036.5 * 1.0) * 1024}
-GEMM_SOURCES = ("paper_2503_05130_amd/csrc/gemm.hip", "paper_2503_05130_amd/csrc/kernels.h")
+GEMM_SOURCES = ("paper_2503_05130_amd/csrc/gemm.hip", "paper_2503_05130_amd/csrc/kernels.h",
+                "paper_2503_05130_amd/build.py")
 
 
 def gemm_source_hash() -> str:

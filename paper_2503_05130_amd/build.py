@@ -29,6 +29,11 @@ COMMON = [
     "-Wno-unused-command-line-argument",
     # no packed-FP32 (v_pk_*_f32) code generation
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in VGPRs: with the default heuristic the register
+    # allocator splits them between AGPRs and VGPRs across the K loop's blocks
+    # and copies every accumulator register with v_accvgpr_read/write on every
+    # K step (48 copies per 24 MFMAs in the 128 x 96 tile)
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 # the init spec rounds every multiply and add separately

@@ -37,11 +37,11 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
 
 constexpr int kBK = 64;               // K tile (bf16 elements) = one 128-byte LDS row
-constexpr int kThreads = 256;         // 4 waves in a 2 x 2 grid over the tile
 
 struct GemmParams {
     const bf16_t *a;
@@ -115,194 +115,211 @@ __device__ inline int swizzle(int r) { return ((r >> 1) & 7) ^ ((r & 1) << 2); }
 // this wave are outstanding (expcnt and lgkmcnt left unconstrained).
 constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
 
-// One 4-wave group's main loop over the K tiles kt_first, kt_first + kt_stride,
+// Tile configuration: BM x BN output tile, WGM x WGN waves, S-slot LDS ring.
+template <int BM_, int BN_, int WGM_, int WGN_, int S_>
+struct Cfg {
+    static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, S = S_;
+    static constexpr int NW = WGM * WGN, NT = 64 * NW;
+    static constexpr int TM = BM / WGM, TN = BN / WGN;         // per-wave tile (tokens x features)
+    static constexpr int FM = TM / 16, FN = TN / 16;           // 16 x 16 MFMA blocks per wave
+    static constexpr int STAGE = (BM + BN) * kBK;              // bf16 elements per ring slot
+    static constexpr int G = (BM + BN) / 8;                    // 1 KB (8-row) DMA groups per slot
+    static constexpr int GPW = (G + NW - 1) / NW, REM = G % NW;  // groups per wave (first REM waves: GPW)
+    static_assert(TM % 16 == 0 && TN % 16 == 0 && BM % 8 == 0 && BN % 8 == 0, "tile");
+    static_assert(S >= 2 && (S - 2) * GPW <= 63, "ring depth");
+};
+
+// One wave group's main loop over the K tiles kt_first, kt_first + kt_stride,
 // ... (n_mine of them) through its own S-slot LDS ring, accumulating into acc.
 // Every wave of the workgroup runs n_steps iterations (>= n_mine), so the
 // workgroup barriers line up even when two groups own different tile counts.
-template <int BM, int BN, int S>
+template <class C>
 __device__ inline void main_loop(const GemmParams &p, bf16_t *ring0, int wave, int lane, int m0, int n0,
                                  int kt_first, int kt_stride, int n_mine, int n_steps,
-                                 f32x4 (&acc)[BN / 32][BM / 32]) {
-    constexpr int TM = BM / 2, TN = BN / 2;          // per-wave tile (tokens x features)
-    constexpr int FM = TM / 16, FN = TN / 16;        // 16x16 MFMA blocks per wave
-    constexpr int STAGE = (BM + BN) * kBK;           // bf16 elements per ring slot
-    constexpr int A_PW = BM / 32, W_PW = BN / 32;    // 1 KB DMAs per wave per K tile
-    constexpr int LPW = A_PW + W_PW;
-    static_assert(BM % 32 == 0 && BN % 32 == 0, "tile");
-    static_assert(S >= 2 && (S - 2) * LPW <= 63, "ring depth");
-    const int wm = wave >> 1, wn = wave & 1;
+                                 f32x4 (&acc)[C::FN][C::FM]) {
+    constexpr int NW = C::NW, GPW = C::GPW, G = C::G;
+    const int wm = wave % C::WGM, wn = wave / C::WGM;
 
     // DMA sources of this lane: DMA i of this wave copies the 8-row group
-    // g = wave + 4 i; lane l fills row 8 g + l / 8 at chunk position l % 8.
-    // Rows past M / N are clamped to the last valid row (never stored).
-    uint32_t a_src[A_PW], w_src[W_PW];
+    // g = wave + NW i (A rows first, then W rows); lane l fills row 8 g + l / 8
+    // of the slot at chunk position l % 8.  Rows past M are clamped to the
+    // last valid row (never stored); N is a multiple of BN.
+    uint32_t src[GPW];
+    const bf16_t *base[GPW];
 #pragma unroll
-    for (int i = 0; i < A_PW; ++i) {
-        const int r = 8 * (wave + 4 * i) + (lane >> 3);
-        a_src[i] = (uint32_t)min(m0 + r, p.M - 1) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
-    }
-#pragma unroll
-    for (int i = 0; i < W_PW; ++i) {
-        const int r = 8 * (wave + 4 * i) + (lane >> 3);
-        w_src[i] = (uint32_t)min(n0 + r, p.N - 1) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
+    for (int i = 0; i < GPW; ++i) {
+        const int g = min(wave + NW * i, G - 1);
+        if (g < C::BM / 8) {
+            const int r = 8 * g + (lane >> 3);
+            src[i] = (uint32_t)min(m0 + r, p.M - 1) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
+            base[i] = p.a;
+        } else {
+            const int r = 8 * (g - C::BM / 8) + (lane >> 3);
+            src[i] = (uint32_t)(n0 + r) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
+            base[i] = p.w;
+        }
     }
 #define IEFWD_ISSUE(kt, slot)                                                                           \
     do {                                                                                                \
         const int k0_ = (kt) * kBK;                                                                     \
-        bf16_t *ring_ = ring0 + (slot) * STAGE;                                                         \
-        _Pragma("unroll") for (int i = 0; i < A_PW; ++i)                                                \
-            __builtin_amdgcn_global_load_lds((const void *)(p.a + a_src[i] + k0_),                      \
-                                             (lds_ptr_t)(ring_ + (wave + 4 * i) * 512), 16, 0, 0);      \
-        _Pragma("unroll") for (int i = 0; i < W_PW; ++i)                                                \
-            __builtin_amdgcn_global_load_lds((const void *)(p.w + w_src[i] + k0_),                      \
-                                             (lds_ptr_t)(ring_ + BM * kBK + (wave + 4 * i) * 512), 16,  \
-                                             0, 0);                                                     \
+        bf16_t *ring_ = ring0 + (slot) * C::STAGE;                                                      \
+        _Pragma("unroll") for (int i = 0; i < GPW; ++i)                                                 \
+            if (wave + NW * i < G)                                                                      \
+                __builtin_amdgcn_global_load_lds((const void *)(base[i] + src[i] + k0_),                \
+                                                 (lds_ptr_t)(ring_ + (wave + NW * i) * 512), 16, 0, 0); \
     } while (0)
 
 #pragma unroll
-    for (int s = 0; s < S - 1; ++s)
+    for (int s = 0; s < C::S - 1; ++s)
         if (s < n_mine) IEFWD_ISSUE(kt_first + s * kt_stride, s);
 
     // fragment rows: lane % 16 of each 16-row block; 16-byte chunk 4 ks + lane / 16
-    const int ra = wm * TM + (lane & 15), rw = wn * TN + (lane & 15);
+    const int ra = wm * C::TM + (lane & 15), rw = wn * C::TN + (lane & 15);
+    const bool full = C::REM == 0 || wave < C::REM;   // this wave issues GPW DMAs per slot, else GPW - 1
     for (int it = 0; it < n_steps; ++it) {
         // this wave's copies of its tile `it` are done once at most the later
         // tiles' copies are outstanding; the barrier then publishes every wave's
         // copies and guarantees the slot reused below is no longer being read
-        if (it + S - 2 < n_mine)
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm((S - 2) * LPW));
-        else
+        if (it + C::S - 2 < n_mine) {
+            if (full) __builtin_amdgcn_s_waitcnt(vmcnt_imm((C::S - 2) * GPW));
+            else __builtin_amdgcn_s_waitcnt(vmcnt_imm((C::S - 2) * (GPW - 1)));
+        } else {
             __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+        }
         __builtin_amdgcn_s_barrier();
         asm volatile("" ::: "memory");   // keep LDS accesses on their side of the barrier
-        if (it + S - 1 < n_mine) IEFWD_ISSUE(kt_first + (it + S - 1) * kt_stride, (it + S - 1) % S);
+        if (it + C::S - 1 < n_mine) IEFWD_ISSUE(kt_first + (it + C::S - 1) * kt_stride, (it + C::S - 1) % C::S);
         if (it >= n_mine) continue;
-        const bf16_t *ring = ring0 + (it % S) * STAGE;
+        const bf16_t *ring = ring0 + (it % C::S) * C::STAGE;
 #pragma unroll
         for (int ks = 0; ks < kBK / 32; ++ks) {
             const int c = ks * 4 + (lane >> 4);
-            bf16x8 af[FM], wf[FN];
+            bf16x8 af[C::FM], wf[C::FN];
 #pragma unroll
-            for (int i = 0; i < FM; ++i) {
+            for (int i = 0; i < C::FM; ++i) {
                 const int r = ra + i * 16;
                 af[i] = *reinterpret_cast<const bf16x8 *>(ring + r * kBK + ((c ^ swizzle(r)) * 8));
             }
 #pragma unroll
-            for (int j = 0; j < FN; ++j) {
+            for (int j = 0; j < C::FN; ++j) {
                 const int r = rw + j * 16;
-                wf[j] = *reinterpret_cast<const bf16x8 *>(ring + BM * kBK + r * kBK + ((c ^ swizzle(r)) * 8));
+                wf[j] = *reinterpret_cast<const bf16x8 *>(ring + C::BM * kBK + r * kBK + ((c ^ swizzle(r)) * 8));
             }
 #pragma unroll
-            for (int j = 0; j < FN; ++j)
+            for (int j = 0; j < C::FN; ++j)
 #pragma unroll
-                for (int i = 0; i < FM; ++i)
+                for (int i = 0; i < C::FM; ++i)
                     acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], af[i], acc[j][i], 0, 0, 0);
         }
     }
 #undef IEFWD_ISSUE
 }
 
+// bf16 outputs (bias, bias + GELU, the QKV scatter) leave through LDS: each wave
+// writes its finished values into an LDS copy of the output tile, then the
+// whole workgroup stores it in 16-byte row segments.  Written straight from
+// the MFMA layout, one store instruction would cover 16 rows x 32 bytes.
+constexpr bool staged(Epi e) { return e == Epi::BiasBf16 || e == Epi::BiasGeluBf16 || e == Epi::Qkv; }
+
 // Epilogue operands that do not depend on the product (bias, residual rows,
 // LayerNorm statistics and affine) are loaded into registers before the main
 // loop, so their latency hides behind the MFMAs instead of stalling the tail.
 // The residual rows are prefetched only by 4-wave workgroups with small wave
-// tiles (<= 6 blocks); larger tiles, and the 8-wave split workgroups (whose
-// register budget is shared by both groups), would trade occupancy for it and
-// load them in the epilogue instead.
-template <int BM, int BN, Epi EPI, bool SPLIT = false>
+// tiles (<= 6 blocks); larger tiles, and the split workgroups (whose register
+// budget is shared by both groups), would trade occupancy for it and load them
+// in the epilogue instead.
+template <class C, Epi EPI, bool SPLIT>
 struct EpiInputs {
-    static constexpr int FM = BM / 32, FN = BN / 32;
-    static constexpr bool kZ = (EPI == Epi::BiasResidF32 || EPI == Epi::BiasLnResidF32) && FN * FM <= 6 && !SPLIT;
+    static constexpr int FM = C::FM, FN = C::FN;
+    static constexpr bool kZ =
+        (EPI == Epi::BiasResidF32 || EPI == Epi::BiasLnResidF32) && FN * FM <= 6 && C::NW == 4 && !SPLIT;
     u32x2 bias[FN];
     f32x4 z[kZ ? FN : 1][kZ ? FM : 1];
     f32x2 stats[EPI == Epi::BiasLnResidF32 ? FM : 1];
     f32x4 gamma[EPI == Epi::BiasLnResidF32 ? FN : 1], beta[EPI == Epi::BiasLnResidF32 ? FN : 1];
 };
 
-template <int BM, int BN, Epi EPI, bool SPLIT>
-__device__ inline void epilogue_prefetch(const GemmParams &p, EpiInputs<BM, BN, EPI, SPLIT> &in, int wave,
-                                         int lane, int m0, int n0) {
-    constexpr int TM = BM / 2, TN = BN / 2, FM = TM / 16, FN = TN / 16;
-    const int wm = wave >> 1, wn = wave & 1;
+template <class C, Epi EPI, bool SPLIT>
+__device__ inline void epilogue_prefetch(const GemmParams &p, EpiInputs<C, EPI, SPLIT> &in, int wave, int lane,
+                                         int m0, int n0) {
+    const int wm = wave % C::WGM, wn = wave / C::WGM;
 #pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int f = min(n0 + wn * TN + j * 16 + (lane >> 4) * 4, p.N - 4);
+    for (int j = 0; j < C::FN; ++j) {
+        const int f = n0 + wn * C::TN + j * 16 + (lane >> 4) * 4;
         in.bias[j] = *reinterpret_cast<const u32x2 *>(p.bias + f);
         if constexpr (EPI == Epi::BiasLnResidF32) {
             in.gamma[j] = *reinterpret_cast<const f32x4 *>(p.ln.gamma + f);
             in.beta[j] = *reinterpret_cast<const f32x4 *>(p.ln.beta + f);
         }
-        if constexpr (EpiInputs<BM, BN, EPI, SPLIT>::kZ) {
+        if constexpr (EpiInputs<C, EPI, SPLIT>::kZ) {
             const float *src = EPI == Epi::BiasResidF32 ? p.resid : p.ln.z;
 #pragma unroll
-            for (int i = 0; i < FM; ++i) {
-                const int t = min(m0 + wm * TM + i * 16 + (lane & 15), p.M - 1);   // clamped: never stored
+            for (int i = 0; i < C::FM; ++i) {
+                const int t = min(m0 + wm * C::TM + i * 16 + (lane & 15), p.M - 1);   // clamped: never stored
                 in.z[j][i] = *reinterpret_cast<const f32x4 *>(src + (size_t)t * p.N + f);
             }
         }
     }
     if constexpr (EPI == Epi::BiasLnResidF32) {
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const int t = min(m0 + wm * TM + i * 16 + (lane & 15), p.M - 1);
+        for (int i = 0; i < C::FM; ++i) {
+            const int t = min(m0 + wm * C::TM + i * 16 + (lane & 15), p.M - 1);
             in.stats[i] = *reinterpret_cast<const f32x2 *>(p.ln.stats + 2 * (size_t)t);
         }
     }
 }
 
-// Epilogue of one wave: lane owns features f..f+3 of token t in every block.
-template <int BM, int BN, Epi EPI, bool SPLIT>
-__device__ inline void epilogue(const GemmParams &p, const f32x4 (&acc)[BN / 32][BM / 32],
-                                const EpiInputs<BM, BN, EPI, SPLIT> &in, int wave, int lane, int m0, int n0) {
-    constexpr int TM = BM / 2, TN = BN / 2, FM = TM / 16, FN = TN / 16;
-    const int wm = wave >> 1, wn = wave & 1;
-    int tok[FM];
+// Row strides (bf16) of the staged output tile: token-major for plain bf16
+// outputs and Q/K, feature-major for V^T.  The 8-element pad keeps rows
+// 16-byte aligned and spreads consecutive rows over the LDS banks.
+template <class C> constexpr int kRowStride = C::BN + 8;
+template <class C> constexpr int kColStride = C::BM + 8;
+
+// Epilogue of one wave.  Lane owns features f..f+3 of token t in every block.
+// fp32 outputs are stored directly (one 16-byte store per block); bf16 outputs
+// go to the LDS tile `ctile` (token-major, or feature-major when `vt_tile`).
+template <class C, Epi EPI, bool SPLIT>
+__device__ inline void epilogue(const GemmParams &p, const f32x4 (&acc)[C::FN][C::FM],
+                                const EpiInputs<C, EPI, SPLIT> &in, int wave, int lane, int m0, int n0,
+                                bf16_t *ctile, bool vt_tile) {
+    const int wm = wave % C::WGM, wn = wave / C::WGM;
 #pragma unroll
-    for (int i = 0; i < FM; ++i) tok[i] = m0 + wm * TM + i * 16 + (lane & 15);
-    int tok_b[FM], tok_s[FM];   // (sequence, position) of each token, for the head scatter
-    if constexpr (EPI == Epi::Qkv) {
-#pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            tok_b[i] = tok[i] / p.qkv.seq;
-            tok_s[i] = tok[i] - tok_b[i] * p.qkv.seq;
-        }
-    }
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
-        const int f = n0 + wn * TN + j * 16 + (lane >> 4) * 4;
-        if (f >= p.N) continue;
+    for (int j = 0; j < C::FN; ++j) {
+        const int fl = wn * C::TN + j * 16 + (lane >> 4) * 4;   // feature within the tile
+        const int f = n0 + fl;
         const u32x2 braw = in.bias[j];
         const float b0 = __uint_as_float(braw[0] << 16), b1 = __uint_as_float(braw[0] & 0xffff0000u);
         const float b2 = __uint_as_float(braw[1] << 16), b3 = __uint_as_float(braw[1] & 0xffff0000u);
-        int which = 0, head = 0, jj = 0;   // head scatter: Q/K/V block, head, column within head
-        if constexpr (EPI == Epi::Qkv) {
-            which = f / p.qkv.d_model;
-            const int within = f - which * p.qkv.d_model;
-            head = within / p.qkv.head_dim;
-            jj = within - head * p.qkv.head_dim;
-        }
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-            const int t = tok[i];
-            if (t >= p.M) continue;
+        for (int i = 0; i < C::FM; ++i) {
+            const int tl = wm * C::TM + i * 16 + (lane & 15);   // token within the tile
+            const int t = m0 + tl;
             float v0 = acc[j][i][0] + b0, v1 = acc[j][i][1] + b1;
             float v2 = acc[j][i][2] + b2, v3 = acc[j][i][3] + b3;
-            if constexpr (EPI == Epi::BiasBf16 || EPI == Epi::BiasGeluBf16) {
+            if constexpr (staged(EPI)) {
                 if constexpr (EPI == Epi::BiasGeluBf16) {
                     v0 = gelu(v0); v1 = gelu(v1); v2 = gelu(v2); v3 = gelu(v3);
                 }
-                bf16_t *o = static_cast<bf16_t *>(p.out) + (size_t)t * p.N + f;
-                *reinterpret_cast<u32x2 *>(o) = u32x2{pack2(v0, v1), pack2(v2, v3)};
+                if (EPI == Epi::Qkv && vt_tile) {
+                    bf16_t *o = ctile + fl * kColStride<C> + tl;
+                    o[0] = f32_to_bf16(v0);
+                    o[kColStride<C>] = f32_to_bf16(v1);
+                    o[2 * kColStride<C>] = f32_to_bf16(v2);
+                    o[3 * kColStride<C>] = f32_to_bf16(v3);
+                } else {
+                    *reinterpret_cast<u32x2 *>(ctile + tl * kRowStride<C> + fl) = u32x2{pack2(v0, v1), pack2(v2, v3)};
+                }
             } else if constexpr (EPI == Epi::BiasResidF32) {
+                if (t >= p.M) continue;
                 f32x4 r;
-                if constexpr (EpiInputs<BM, BN, EPI, SPLIT>::kZ) r = in.z[j][i];
+                if constexpr (EpiInputs<C, EPI, SPLIT>::kZ) r = in.z[j][i];
                 else r = *reinterpret_cast<const f32x4 *>(p.resid + (size_t)t * p.N + f);
                 *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + (size_t)t * p.N + f) =
                     f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
-            } else if constexpr (EPI == Epi::BiasLnResidF32) {
-                // residual = LN(z) rebuilt with the LayerNorm kernel's expression
+            } else {   // Epi::BiasLnResidF32: residual = LN(z) rebuilt with the LayerNorm kernel's expression
+                if (t >= p.M) continue;
                 f32x4 z;
-                if constexpr (EpiInputs<BM, BN, EPI, SPLIT>::kZ) z = in.z[j][i];
+                if constexpr (EpiInputs<C, EPI, SPLIT>::kZ) z = in.z[j][i];
                 else z = *reinterpret_cast<const f32x4 *>(p.ln.z + (size_t)t * p.N + f);
                 const float mean = in.stats[i][0], rstd = in.stats[i][1];
                 f32x4 r;
@@ -310,70 +327,113 @@ __device__ inline void epilogue(const GemmParams &p, const f32x4 (&acc)[BN / 32]
                 for (int e = 0; e < 4; ++e) r[e] = __builtin_fmaf(in.gamma[j][e], (z[e] - mean) * rstd, in.beta[j][e]);
                 *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + (size_t)t * p.N + f) =
                     f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
-            } else {   // Epi::Qkv
-                const QkvDst &d = p.qkv;
-                const size_t bh = (size_t)tok_b[i] * d.n_heads + head;
-                const int sp = tok_s[i];
-                if (which < 2) {
-                    bf16_t *o = (which == 0 ? d.q : d.k) + (bh * d.seq + sp) * d.head_dim + jj;
-                    *reinterpret_cast<u32x2 *>(o) = u32x2{pack2(v0, v1), pack2(v2, v3)};
-                } else {
-                    bf16_t *o = d.vt + (bh * d.head_dim + jj) * d.seq_pad + sp;
-                    o[0] = f32_to_bf16(v0);
-                    o[d.seq_pad] = f32_to_bf16(v1);
-                    o[2 * d.seq_pad] = f32_to_bf16(v2);
-                    o[3 * d.seq_pad] = f32_to_bf16(v3);
-                }
             }
         }
     }
 }
 
-// Sequential K order: 4 waves, one ring, K tiles 0, 1, 2, ... into one accumulator.
-template <int BM, int BN, int S, Epi EPI>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(GemmParams p) {
-    __shared__ __attribute__((aligned(1024))) bf16_t lds[S * (BM + BN) * kBK];
-    int tm, tn;
-    grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    f32x4 acc[BN / 32][BM / 32];
-#pragma unroll
-    for (int j = 0; j < BN / 32; ++j)
-#pragma unroll
-        for (int i = 0; i < BM / 32; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    EpiInputs<BM, BN, EPI, false> in;
-    epilogue_prefetch<BM, BN, EPI, false>(p, in, wave, lane, m0, n0);
-    const int kt_count = p.K / kBK;
-    main_loop<BM, BN, S>(p, lds, wave, lane, m0, n0, 0, 1, kt_count, kt_count, acc);
-    epilogue<BM, BN, EPI, false>(p, acc, in, wave, lane, m0, n0);
+// Store the staged bf16 tile.  Called by all `nt` threads of the workgroup
+// after a barrier that follows every wave's epilogue().
+template <class C, Epi EPI>
+__device__ inline void store_tile(const GemmParams &p, const bf16_t *ctile, bool vt_tile, int tid, int nt, int m0,
+                                  int n0) {
+    if (EPI == Epi::Qkv && vt_tile) {
+        // V^T [B, H, dh, S_pad]: a segment is 8 consecutive tokens of one
+        // (head, column) row, contiguous when S is a multiple of 8
+        const QkvDst &d = p.qkv;
+        constexpr int TG = C::BM / 8;
+        for (int sg = tid; sg < C::BN * TG; sg += nt) {
+            const int fl = sg / TG, t0 = m0 + (sg % TG) * 8;
+            if (t0 >= p.M) continue;
+            const int within = n0 + fl - 2 * d.d_model, head = within / d.head_dim, jj = within - head * d.head_dim;
+            const bf16_t *src = ctile + fl * kColStride<C> + (t0 - m0);
+            if (d.seq % 8 == 0) {
+                const int b = t0 / d.seq, sp = t0 - b * d.seq;
+                bf16_t *o = d.vt + (((size_t)b * d.n_heads + head) * d.head_dim + jj) * d.seq_pad + sp;
+                *reinterpret_cast<u32x4 *>(o) = *reinterpret_cast<const u32x4 *>(src);
+            } else {
+                for (int e = 0; e < 8 && t0 + e < p.M; ++e) {
+                    const int t = t0 + e, b = t / d.seq, sp = t - b * d.seq;
+                    d.vt[(((size_t)b * d.n_heads + head) * d.head_dim + jj) * d.seq_pad + sp] = src[e];
+                }
+            }
+        }
+        return;
+    }
+    constexpr int SEGS = C::BN / 8;   // 16-byte segments per token row
+    for (int sg = tid; sg < C::BM * SEGS; sg += nt) {
+        const int r = sg / SEGS, c = sg - r * SEGS, t = m0 + r;
+        if (t >= p.M) continue;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(ctile + r * kRowStride<C> + c * 8);
+        const int f = n0 + c * 8;
+        bf16_t *o;
+        if constexpr (EPI == Epi::Qkv) {   // Q or K [B, H, S, dh]: 8 columns of one head
+            const QkvDst &d = p.qkv;
+            const int which = f / d.d_model, within = f - which * d.d_model;
+            const int head = within / d.head_dim, jj = within - head * d.head_dim;
+            const int b = t / d.seq, sp = t - b * d.seq;
+            o = (which == 0 ? d.q : d.k) + (((size_t)b * d.n_heads + head) * d.seq + sp) * d.head_dim + jj;
+        } else {
+            o = static_cast<bf16_t *>(p.out) + (size_t)t * p.N + f;
+        }
+        *reinterpret_cast<u32x4 *>(o) = v;
+    }
 }
 
-// Split K order: 8 waves in two 4-wave groups over the same output tile; group g
+// Sequential K order: one wave group, one ring, K tiles 0, 1, 2, ... into one accumulator.
+template <class C, Epi EPI>
+__global__ __launch_bounds__(C::NT) void gemm_kernel(GemmParams p) {
+    __shared__ __attribute__((aligned(1024))) bf16_t lds[C::S * C::STAGE];
+    static_assert(!staged(EPI) || (C::BM * kRowStride<C> <= C::S * C::STAGE &&
+                                   C::BN * kColStride<C> <= C::S * C::STAGE), "staged tile fits in the ring");
+    int tm, tn;
+    grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
+    const int m0 = tm * C::BM, n0 = tn * C::BN;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    f32x4 acc[C::FN][C::FM];
+#pragma unroll
+    for (int j = 0; j < C::FN; ++j)
+#pragma unroll
+        for (int i = 0; i < C::FM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    EpiInputs<C, EPI, false> in;
+    epilogue_prefetch<C, EPI, false>(p, in, wave, lane, m0, n0);
+    const int kt_count = p.K / kBK;
+    main_loop<C>(p, lds, wave, lane, m0, n0, 0, 1, kt_count, kt_count, acc);
+    const bool vt_tile = EPI == Epi::Qkv && n0 >= 2 * p.qkv.d_model;
+    if constexpr (staged(EPI)) __syncthreads();   // every wave is done reading the ring
+    epilogue<C, EPI, false>(p, acc, in, wave, lane, m0, n0, lds, vt_tile);
+    if constexpr (staged(EPI)) {
+        __syncthreads();
+        store_tile<C, EPI>(p, lds, vt_tile, threadIdx.x, C::NT, m0, n0);
+    }
+}
+
+// Split K order: two wave groups over the same output tile; group g
 // accumulates the K tiles kt = g (mod 2) through its own ring, then group 1
 // hands its partial sums to group 0 through LDS and group 0 adds them
 // (even-tile sum + odd-tile sum, always in that order) and runs the epilogue.
-// Two waves per SIMD even when there are only as many tiles as CUs.
-template <int BM, int BN, int S, Epi EPI>
-__global__ __launch_bounds__(2 * kThreads) void gemm_split_kernel(GemmParams p) {
-    constexpr int FN = BN / 32, FM = BM / 32;
-    __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * S * (BM + BN) * kBK];
-    static_assert(FN * FM * 4 * kThreads * 4 <= 2 * S * (BM + BN) * kBK * 2, "hand-off space");
+// Twice the waves per CU for the long K loop.
+template <class C, Epi EPI>
+__global__ __launch_bounds__(2 * C::NT) void gemm_split_kernel(GemmParams p) {
+    constexpr int FN = C::FN, FM = C::FM;
+    __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * C::S * C::STAGE];
+    static_assert(FN * FM * 4 * C::NT * 4 <= 2 * C::S * C::STAGE * 2, "hand-off space");
+    static_assert(!staged(EPI) || (C::BM * kRowStride<C> <= 2 * C::S * C::STAGE &&
+                                   C::BN * kColStride<C> <= 2 * C::S * C::STAGE), "staged tile fits in the rings");
     int tm, tn;
     grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int lane = threadIdx.x & 63, grp = threadIdx.x >> 8, wave = (threadIdx.x >> 6) & 3;
+    const int m0 = tm * C::BM, n0 = tn * C::BN;
+    const int lane = threadIdx.x & 63, grp = threadIdx.x / C::NT, wave = (threadIdx.x >> 6) % C::NW;
     f32x4 acc[FN][FM];
 #pragma unroll
     for (int j = 0; j < FN; ++j)
 #pragma unroll
         for (int i = 0; i < FM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    EpiInputs<BM, BN, EPI, true> in;
-    if (grp == 0) epilogue_prefetch<BM, BN, EPI, true>(p, in, wave, lane, m0, n0);
+    EpiInputs<C, EPI, true> in;
+    if (grp == 0) epilogue_prefetch<C, EPI, true>(p, in, wave, lane, m0, n0);
     const int kt_count = p.K / kBK;
     const int n_mine = (kt_count - grp + 1) / 2;
-    main_loop<BM, BN, S>(p, lds + grp * S * (BM + BN) * kBK, wave, lane, m0, n0, grp, 2, n_mine,
-                         (kt_count + 1) / 2, acc);
+    main_loop<C>(p, lds + grp * C::S * C::STAGE, wave, lane, m0, n0, grp, 2, n_mine, (kt_count + 1) / 2, acc);
     __syncthreads();   // both rings drained: reuse the LDS for the hand-off
     float *handoff = reinterpret_cast<float *>(lds) + (wave * 64 + lane) * (FN * FM * 4);
     if (grp == 1) {
@@ -383,18 +443,38 @@ __global__ __launch_bounds__(2 * kThreads) void gemm_split_kernel(GemmParams p) 
             for (int i = 0; i < FM; ++i) *reinterpret_cast<f32x4 *>(handoff + (j * FM + i) * 4) = acc[j][i];
     }
     __syncthreads();
-    if (grp == 1) return;
+    if (grp == 0) {
 #pragma unroll
-    for (int j = 0; j < FN; ++j)
+        for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int i = 0; i < FM; ++i) acc[j][i] += *reinterpret_cast<const f32x4 *>(handoff + (j * FM + i) * 4);
-    epilogue<BM, BN, EPI, true>(p, acc, in, wave, lane, m0, n0);
+            for (int i = 0; i < FM; ++i) acc[j][i] += *reinterpret_cast<const f32x4 *>(handoff + (j * FM + i) * 4);
+    }
+    const bool vt_tile = EPI == Epi::Qkv && n0 >= 2 * p.qkv.d_model;
+    if constexpr (staged(EPI)) {
+        __syncthreads();   // the hand-off is consumed before the tile overwrites it
+        if (grp == 0) epilogue<C, EPI, true>(p, acc, in, wave, lane, m0, n0, lds, vt_tile);
+        __syncthreads();
+        store_tile<C, EPI>(p, lds, vt_tile, threadIdx.x, 2 * C::NT, m0, n0);
+    } else if (grp == 0) {
+        epilogue<C, EPI, true>(p, acc, in, wave, lane, m0, n0, lds, vt_tile);
+    }
 }
 
-struct TileChoice {
-    int bm, bn, stages;
-    bool split;
-};
+// Tile configurations.  8-wave workgroups for large tiles: two waves per SIMD
+// and a 128-row tile halve the operand bytes each CU pulls through its L1 per
+// MFMA compared with 64-row 4-wave tiles (the per-CU load path, ~62 B/clk,
+// bounds small tiles below the MFMA rate).
+using CfgA = Cfg<128, 192, 2, 4, 2>;   // 8 waves, 64 x 48 per wave
+using CfgD = Cfg<128, 128, 2, 4, 2>;   // 8 waves, 64 x 32
+using CfgB = Cfg<128, 96, 4, 2, 2>;    // 8 waves, 32 x 48
+using CfgC = Cfg<64, 96, 2, 2, 2>;     // 4 waves, 32 x 48
+using CfgE = Cfg<64, 128, 2, 2, 2>;    // 4 waves, 32 x 64
+using CfgF = Cfg<64, 64, 2, 2, 3>;     // 4 waves, 32 x 32
+using SplitC = Cfg<64, 96, 2, 2, 2>;   // split order: two 4-wave groups
+using SplitE = Cfg<64, 128, 2, 2, 2>;
+using SplitD = Cfg<128, 128, 2, 2, 2>;
+
+enum class Tile { A, D, B, C, E, F, SplitC, SplitE, SplitD };
 
 // K summation order from the weight shape (N, K) only: K >= 2048 uses the
 // split (even/odd) order, shorter K the sequential order.  So a given weight
@@ -402,38 +482,51 @@ struct TileChoice {
 // the CU quota or the tile shape -- outputs stay bit-identical across them.
 bool split_k_order(int /*N*/, int K) { return K >= 2048; }
 
-// Tile shape and ring depth from (M, N, K) only -- never the current CU quota.
-// Measured inside the forward pass on gfx950: 64 x 96 tiles with a 2-slot ring
-// (up to four workgroups per CU) win up to ~1500 such tiles, 128 x 96 beyond;
-// 128 x 128 / 64 x 128 serve widths that 96 does not divide.  The split order
-// runs 8-wave workgroups.
-TileChoice choose_tile(int M, int N, int K) {
-    const long m64 = (M + 63) / 64;
+long tiles_of(int M, int N, int bm, int bn) { return (long)((M + bm - 1) / bm) * (N / bn); }
+
+// Tile shape from (M, N, K) only -- never the current CU quota.  The largest
+// tile that still gives at least one workgroup per CU (256 tiles); if none
+// does, the one with the most tiles.  Tile widths divide `align` (d_model for
+// the QKV scatter, so that no tile straddles the Q / K / V boundaries).
+Tile choose_tile(int M, int N, int K, int align) {
     if (split_k_order(N, K)) {
-        if (N % 96 == 0) return {64, 96, 2, true};
-        if (N % 128 == 0 && m64 * (N / 128) < 512) return {64, 128, 2, true};
-        return {128, 128, 2, true};
+        if (align % 96 == 0) return Tile::SplitC;
+        if (align % 128 == 0 && tiles_of(M, N, 64, 128) < 512) return Tile::SplitE;
+        if (align % 128 == 0) return Tile::SplitD;
+        return Tile::F;
     }
-    if (N % 96 == 0 && m64 * (N / 96) <= 1536) return {64, 96, 2, false};
-    if (N % 96 == 0) return {128, 96, 2, false};
-    if (N % 128 == 0) return m64 * (N / 128) < 512 ? TileChoice{64, 128, 2, false} : TileChoice{128, 128, 2, false};
-    return {64, 64, 3, false};
+    struct Cand { Tile t; int bm, bn; } cands[] = {
+        {Tile::A, 128, 192}, {Tile::D, 128, 128}, {Tile::B, 128, 96},
+        {Tile::C, 64, 96}, {Tile::E, 64, 128}, {Tile::F, 64, 64}};
+    Tile best = Tile::F;
+    long best_n = 0;
+    for (const Cand &c : cands) {
+        if (align % c.bn) continue;
+        const long n = tiles_of(M, N, c.bm, c.bn);
+        if (n >= 256) return c.t;
+        if (n > best_n) { best = c.t; best_n = n; }
+    }
+    return best;
 }
 
-template <int BM, int BN, int S, bool SPLIT>
+template <class C, Epi E, bool SPLIT>
+constexpr auto kernel_for() {
+    if constexpr (SPLIT) return gemm_split_kernel<C, E>;
+    else return gemm_kernel<C, E>;
+}
+
+template <class C, bool SPLIT>
 hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
-    p.tiles_m = (p.M + BM - 1) / BM;
-    p.tiles_n = p.N / BN;
-    const dim3 grid(p.tiles_m * p.tiles_n), block(SPLIT ? 2 * kThreads : kThreads);
-#define IEFWD_K(E) (SPLIT ? gemm_split_kernel<BM, BN, S, E> : gemm_kernel<BM, BN, S, E>)
+    p.tiles_m = (p.M + C::BM - 1) / C::BM;
+    p.tiles_n = p.N / C::BN;
+    const dim3 grid(p.tiles_m * p.tiles_n), block(SPLIT ? 2 * C::NT : C::NT);
     switch (epi) {
-    case Epi::BiasBf16: return launch_kernel(IEFWD_K(Epi::BiasBf16), grid, block, s, p);
-    case Epi::BiasGeluBf16: return launch_kernel(IEFWD_K(Epi::BiasGeluBf16), grid, block, s, p);
-    case Epi::BiasResidF32: return launch_kernel(IEFWD_K(Epi::BiasResidF32), grid, block, s, p);
-    case Epi::Qkv: return launch_kernel(IEFWD_K(Epi::Qkv), grid, block, s, p);
-    case Epi::BiasLnResidF32: return launch_kernel(IEFWD_K(Epi::BiasLnResidF32), grid, block, s, p);
+    case Epi::BiasBf16: return launch_kernel(kernel_for<C, Epi::BiasBf16, SPLIT>(), grid, block, s, p);
+    case Epi::BiasGeluBf16: return launch_kernel(kernel_for<C, Epi::BiasGeluBf16, SPLIT>(), grid, block, s, p);
+    case Epi::BiasResidF32: return launch_kernel(kernel_for<C, Epi::BiasResidF32, SPLIT>(), grid, block, s, p);
+    case Epi::Qkv: return launch_kernel(kernel_for<C, Epi::Qkv, SPLIT>(), grid, block, s, p);
+    case Epi::BiasLnResidF32: return launch_kernel(kernel_for<C, Epi::BiasLnResidF32, SPLIT>(), grid, block, s, p);
     }
-#undef IEFWD_K
     return hipErrorInvalidValue;
 }
 
@@ -448,17 +541,20 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
     p.M = M; p.N = N; p.K = K;
     if (qkv) p.qkv = *qkv;
     if (ln) p.ln = *ln;
-    const TileChoice t = choose_tile(M, N, K);
-    if (t.split) {
-        if (t.bm == 64 && t.bn == 96) return launch_tile<64, 96, 2, true>(epi, p, stream);
-        if (t.bm == 64 && t.bn == 128) return launch_tile<64, 128, 2, true>(epi, p, stream);
-        return launch_tile<128, 128, 2, true>(epi, p, stream);
+    // N is a multiple of 64 (checked by the callers); d_model a multiple of 128
+    const int align = epi == Epi::Qkv ? p.qkv.d_model : N;
+    switch (choose_tile(M, N, K, align)) {
+    case Tile::A: return launch_tile<CfgA, false>(epi, p, stream);
+    case Tile::D: return launch_tile<CfgD, false>(epi, p, stream);
+    case Tile::B: return launch_tile<CfgB, false>(epi, p, stream);
+    case Tile::C: return launch_tile<CfgC, false>(epi, p, stream);
+    case Tile::E: return launch_tile<CfgE, false>(epi, p, stream);
+    case Tile::F: return launch_tile<CfgF, false>(epi, p, stream);
+    case Tile::SplitC: return launch_tile<SplitC, true>(epi, p, stream);
+    case Tile::SplitE: return launch_tile<SplitE, true>(epi, p, stream);
+    case Tile::SplitD: return launch_tile<SplitD, true>(epi, p, stream);
     }
-    if (t.bm == 64 && t.bn == 96) return launch_tile<64, 96, 2, false>(epi, p, stream);
-    if (t.bm == 64 && t.bn == 128) return launch_tile<64, 128, 2, false>(epi, p, stream);
-    if (t.bm == 128 && t.bn == 128) return launch_tile<128, 128, 2, false>(epi, p, stream);
-    if (t.bm == 128 && t.bn == 96) return launch_tile<128, 96, 2, false>(epi, p, stream);
-    return launch_tile<64, 64, 3, false>(epi, p, stream);
+    return hipErrorInvalidValue;
 }
 
 }  // namespace iefwd

@@ -35,13 +35,16 @@ def gemm_bound(a64, w64, K):
 @pytest.mark.parametrize("M,N,K", [
     (64, 384, 128),      # one-layer encoder QKV shape
     (1, 64, 64),         # single row
-    (37, 192, 128),      # ragged M, 64-wide tiles
+    (37, 192, 128),      # ragged M, 64 x 64 tiles
     (130, 320, 192),     # ragged M over several tiles
-    (1000, 768, 768),    # 128 x 96 tiles, ragged M
-    (512, 3072, 768),    # 64 x 96 tiles
-    (4096, 3072, 256),   # 128 x 128 tiles
-    (4096, 2496, 128),   # 128 x 96 tiles
-    (300, 1024, 1024),   # 64 x 128 tiles, ragged M
+    (1000, 768, 768),    # 64 x 64 tiles (most tiles), ragged M
+    (512, 3072, 768),    # 64 x 96 tiles, 4 waves
+    (4096, 3072, 256),   # 128 x 192 tiles, 8 waves
+    (4125, 2496, 128),   # 128 x 192 tiles, ragged M
+    (4096, 1024, 256),   # 128 x 128 tiles, 8 waves
+    (4096, 768, 768),    # 128 x 96 tiles, 8 waves
+    (2000, 1024, 512),   # 64 x 128 tiles, ragged M
+    (300, 1024, 1024),   # 64 x 64 tiles, ragged M
     (256, 768, 3072),    # long K: split (even/odd) K order, 64 x 96
     (130, 512, 2048),    # split order, 64 x 128, ragged M
     (2048, 2048, 2048),  # split order, 128 x 128
@@ -77,8 +80,8 @@ def test_gemm_epilogues(M, N, K, epi):
 
 
 @pytest.mark.parametrize("M,N,K", [
-    (512, 768, 768),      # 64 x 96 tiles throughout
-    (4096, 3072, 768),    # 128 x 128 tiles for the full batch, 64 x 96 for the slices
+    (512, 768, 768),      # 64 x 64 tiles throughout
+    (4096, 3072, 768),    # 128 x 192 tiles (8 waves) for the full batch, 64 x 64 / 64 x 96 for the slices
     (4096, 1024, 4096),   # split K order: 128 x 128 for the full batch, 64 x 128 for the slices
 ])
 def test_gemm_batch_invariance(M, N, K):
@@ -95,7 +98,13 @@ def test_gemm_batch_invariance(M, N, K):
         assert torch.equal(part.view(torch.int16), full[lo:hi].view(torch.int16))
 
 
-@pytest.mark.parametrize("B,S,d,H", [(2, 32, 128, 2), (3, 37, 256, 2), (2, 128, 768, 12), (1, 70, 1024, 8)])
+@pytest.mark.parametrize("B,S,d,H", [
+    (2, 32, 128, 2), (3, 37, 256, 2), (2, 128, 768, 12), (1, 70, 1024, 8),
+    (33, 125, 768, 12),   # 128 x 192 tiles, S not a multiple of 8 (V^T element stores), ragged M
+    (32, 128, 768, 12),   # 128 x 192 tiles, V^T 16-byte stores
+    (8, 512, 1024, 16),   # d = 1024: tile widths must divide d (128 x 128)
+    (2, 1024, 2048, 16),  # K = 2048: split K order with the scatter (dh 128)
+])
 def test_qkv_scatter(B, S, d, H):
     print(f"qkv B={B} S={S} d={d} H={H}", flush=True)
     dh = d // H
