@@ -81,9 +81,9 @@ def cpu_baseline(shape, batch_sample: int):
 
 
 def colocated(ie, W, shape, cfg, quota_pairs, batch=8, window_s=1.0):
-    """Aggregate throughput of two co-located instances (independent seeds),
-    each driven by its own host thread with back-to-back batches, against one
-    instance alone at the full quota.  Inputs are device-resident.  Each leg
+    """Aggregate throughput of two co-located instances (independent seeds) on
+    disjoint CU sets, each driven by its own host thread with back-to-back
+    batches, against one instance alone at the full quota.  Inputs are device-resident.  Each leg
     runs for a fixed wall-clock window and counts the batches that completed
     inside it, so an instance at a small quota does not stretch the window of
     the other one."""
@@ -126,8 +126,8 @@ def colocated(ie, W, shape, cfg, quota_pairs, batch=8, window_s=1.0):
     out = {"workload": f"2 x {WORKLOAD}, batch {batch} each", "window_s": window_s,
            "solo_inf_s": round(solo, 1), "pairs": []}
     for qa, qb in quota_pairs:
-        insts[0].set_quota(qa)
-        insts[1].set_quota(qb)
+        insts[0].set_quota(qa, 0)          # disjoint CUs: bits [0, qa) and [qa, qa + qb)
+        insts[1].set_quota(qb, qa)
         agg = window([0, 1])
         out["pairs"].append({"quotas": [qa, qb], "aggregate_inf_s": round(agg, 1),
                              "vs_solo": round(agg / solo, 3)})

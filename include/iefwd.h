@@ -99,13 +99,19 @@ void iefwd_config_init(iefwd_config *cfg);
 int iefwd_device_info(int device, uint32_t *n_cu, uint32_t *n_xcd);
 
 /* Pure host function: the CU mask the library uses for a quota of `quota` CUs
- * on a device with n_cu CUs in n_xcd equal XCDs.  Bit i of word i/32 enables
- * mask bit i (the bit order of hipExtStreamCreateWithCUMask).  The CUs are
- * spread evenly over the XCDs (XCD x gets quota/n_xcd CUs, the first
- * quota % n_xcd XCDs one more), so that every XCD's L2 serves an equal share.
+ * starting at mask bit `first` on a device with n_cu CUs in n_xcd equal XCDs:
+ * bits first, first + 1, ..., first + quota - 1 (mod n_cu).  Bit i of word
+ * i/32 enables mask bit i (the bit order of hipExtStreamCreateWithCUMask),
+ * which drives CU i / n_xcd of XCD i % n_xcd; a run of consecutive bits is
+ * therefore spread evenly over the XCDs (each gets quota/n_xcd CUs or one
+ * more; with first = 0 the first quota % n_xcd XCDs get the extra CU), so
+ * every XCD's L2 serves an equal share.  Co-located instances placed at
+ * first = 0, q0, q0 + q1, ... get disjoint CUs while their quotas sum to at
+ * most n_cu, and overlap cyclically beyond that.
  * n_words must be >= ceil(n_cu / 32); extra words are zeroed.
- * EINVAL if quota is 0 or > n_cu, n_xcd is 0 or does not divide n_cu. */
-int iefwd_build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t quota,
+ * EINVAL if quota is 0 or > n_cu, first >= n_cu, n_xcd is 0 or does not
+ * divide n_cu. */
+int iefwd_build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t quota, uint32_t first,
                         uint32_t *mask, uint32_t n_words);
 
 /* ---- instance lifecycle -------------------------------------------------------- */
@@ -120,9 +126,13 @@ int iefwd_destroy(iefwd_instance *inst);
 
 /* ---- quota (compute share) ------------------------------------------------------ */
 
-/* Requests a quota of n_cu CUs (1 .. device CUs), spread evenly over XCDs as by
- * iefwd_build_cu_mask.  Takes effect at the next iefwd_submit; a batch already
- * in flight keeps its CUs.  EINVAL if n_cu is out of range. */
+/* Requests a quota of n_cu CUs (1 .. device CUs) starting at mask bit `first`
+ * (0 .. device CUs - 1), spread evenly over the XCDs as by iefwd_build_cu_mask.
+ * Takes effect at the next iefwd_submit; a batch already in flight keeps its
+ * CUs.  EINVAL if n_cu or first is out of range. */
+int iefwd_set_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first);
+
+/* iefwd_set_quota_at(inst, n_cu, 0). */
 int iefwd_set_quota(iefwd_instance *inst, uint32_t n_cu);
 
 /* Requests an explicit CU mask (n_words 32-bit words, bit order as above);
@@ -158,6 +168,11 @@ int iefwd_read_logits(iefwd_instance *inst, float *out, size_t n_floats, int out
  * the instance's stream (the per-iteration time an elasticity controller
  * watches, Sec. 3.4.1).  ESTATE if no batch has completed. */
 int iefwd_last_batch_ms(iefwd_instance *inst, float *ms);
+
+/* Number of kernels the instance has launched since it was created (every
+ * kernel of every submitted batch).  An elasticity controller samples it once
+ * per control period to get the instance's kernel rate (Sec. 3.4.1). */
+int iefwd_kernels_launched(const iefwd_instance *inst, uint64_t *count);
 
 /* The hipStream_t the instance currently launches on (for external ordering). */
 int iefwd_get_stream(iefwd_instance *inst, void **hip_stream);
@@ -201,6 +216,76 @@ int iefwd_export_tensor(const iefwd_instance *inst, uint32_t layer, uint32_t slo
 const char *iefwd_last_error(void);
 /* Static name of a status code.  Never NULL. */
 const char *iefwd_status_string(int status);
+
+/* ---- quota controller ------------------------------------------------------------ */
+
+/* The fast scale-up/down control of Sec. 3.4.1 (Alg. 2, IssueToken) with CUs as
+ * tokens.  Pure host code: it neither reads nor changes any instance; the
+ * caller reports each co-located instance's observations once per control
+ * period, calls iefwd_ctl_issue, and applies the returned quota and first
+ * mask bit with iefwd_set_quota_at.  Calls on one controller are serialised
+ * by the caller.
+ *
+ * Per period, for every instance: R_current = kernels launched during the
+ * period (RW keeps the last `window` of them), KLC = duration of its last
+ * completed batch (T_current; T_min = the smallest reported).  SLO-sensitive
+ * instances (evaluated first, in id order), dT = (T_current - T_min) / T_min:
+ *   dT > eta_violation                 -> EMERGENCY,  MaxTokens * limit
+ *   its RW sums to 0                   -> RECOVERY,   MaxTokens * request
+ *   every other instance's RW is 0     -> RECOVERY,   min(R_last * eta_increase, MaxTokens)
+ *   otherwise                          -> CONTENTION, MaxTokens * request
+ * other instances, from the shared state:
+ *   NONE (no SLO-sensitive instance)   -> MaxTokens * limit
+ *   EMERGENCY                          -> min(MaxTokens * request, R_last) / (1 + dT_raiser)
+ *   RECOVERY                           -> min(R_last * eta_increase, MaxTokens * limit)
+ *   CONTENTION                         -> R_last
+ * Only the instance that raised EMERGENCY can change the state.  Tokens become
+ * quotas round(R / granule) * granule clamped to [min_quota, MaxTokens], placed
+ * on consecutive mask bits in id order (first_0 = 0, first_i = first_{i-1} +
+ * quota_{i-1} mod MaxTokens): disjoint CUs while the quotas fit.
+ * Readings where the paper is silent: the eta defaults; dividing by the KLC
+ * ratio 1 + dT rather than dT (dT < 1 would scale up); the SLO scale-up capped
+ * at MaxTokens; T_min over the whole history. */
+typedef struct iefwd_ctl iefwd_ctl;
+
+enum { IEFWD_CTL_NONE = 0, IEFWD_CTL_EMERGENCY = 1, IEFWD_CTL_RECOVERY = 2, IEFWD_CTL_CONTENTION = 3 };
+
+typedef struct {
+    uint32_t abi_version;    /* = IEFWD_ABI_VERSION */
+    uint32_t max_tokens;     /* MaxTokens: CUs that can be issued (the device's CU count); >= 1 */
+    uint32_t window;         /* RW length in control periods; >= 1 */
+    uint32_t granule;        /* quotas are multiples of this many CUs; >= 1 */
+    uint32_t min_quota;      /* smallest quota issued; 1 .. max_tokens */
+    uint32_t reserved0;      /* must be 0 */
+    double eta_violation;    /* relative KLC increase that raises EMERGENCY; >= 0 */
+    double eta_increase;     /* multiplicative scale-up per period; >= 1 */
+} iefwd_ctl_params;
+
+/* Defaults: max_tokens 256, window 4, granule 8, min_quota 8,
+ * eta_violation 0.2, eta_increase 1.25. */
+int iefwd_ctl_params_init(iefwd_ctl_params *p);
+
+/* EINVAL on a field out of range, EVERSION on another ABI version. */
+int iefwd_ctl_create(const iefwd_ctl_params *p, iefwd_ctl **out);
+int iefwd_ctl_destroy(iefwd_ctl *ctl);   /* NULL accepted */
+
+/* Adds an instance with <request, limit> as fractions of MaxTokens
+ * (0 < request <= limit <= 1); *id = 0, 1, ... in order of addition. */
+int iefwd_ctl_add(iefwd_ctl *ctl, double request, double limit, int slo_sensitive, uint32_t *id);
+
+/* Observation of instance `id` for the current period: kernels launched during
+ * it, and the KLC in milliseconds of the last batch it completed in the period
+ * (<= 0 if none).  A later report in the same period replaces the earlier. */
+int iefwd_ctl_report(iefwd_ctl *ctl, uint32_t id, uint64_t kernels, double klc_ms);
+
+/* Ends the period.  Writes, for each of the n instances in id order, the
+ * issued tokens (R_issue), the quota in CUs and the first mask bit of its
+ * placement; any output pointer may be NULL.  EINVAL unless n equals the
+ * number of instances. */
+int iefwd_ctl_issue(iefwd_ctl *ctl, double *tokens, uint32_t *quotas, uint32_t *firsts, uint32_t n);
+
+/* The shared state after the last issue (IEFWD_CTL_*). */
+int iefwd_ctl_state(const iefwd_ctl *ctl, int32_t *state);
 
 /* ---- per-kernel entry points (parity tests) ------------------------------------------
  * Each launches one kernel of the forward pass on `stream` (a hipStream_t, NULL

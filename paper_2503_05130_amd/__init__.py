@@ -32,10 +32,20 @@ _u32, _u64, _i32, _f32, _vp, _sz = (ctypes.c_uint32, ctypes.c_uint64, ctypes.c_i
 SIGNATURES = {
     "iefwd_config_init": (None, [_vp]),
     "iefwd_device_info": (_i32, [_i32, ctypes.POINTER(_u32), ctypes.POINTER(_u32)]),
-    "iefwd_build_cu_mask": (_i32, [_u32, _u32, _u32, ctypes.POINTER(_u32), _u32]),
+    "iefwd_build_cu_mask": (_i32, [_u32, _u32, _u32, _u32, ctypes.POINTER(_u32), _u32]),
     "iefwd_create": (_i32, [_vp, _i32, ctypes.POINTER(_vp)]),
     "iefwd_destroy": (_i32, [_vp]),
     "iefwd_set_quota": (_i32, [_vp, _u32]),
+    "iefwd_set_quota_at": (_i32, [_vp, _u32, _u32]),
+    "iefwd_kernels_launched": (_i32, [_vp, ctypes.POINTER(ctypes.c_uint64)]),
+    "iefwd_ctl_params_init": (_i32, [_vp]),
+    "iefwd_ctl_create": (_i32, [_vp, ctypes.POINTER(_vp)]),
+    "iefwd_ctl_destroy": (_i32, [_vp]),
+    "iefwd_ctl_add": (_i32, [_vp, ctypes.c_double, ctypes.c_double, ctypes.c_int, ctypes.POINTER(_u32)]),
+    "iefwd_ctl_report": (_i32, [_vp, _u32, ctypes.c_uint64, ctypes.c_double]),
+    "iefwd_ctl_issue": (_i32, [_vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_u32), ctypes.POINTER(_u32),
+                                _u32]),
+    "iefwd_ctl_state": (_i32, [_vp, ctypes.POINTER(ctypes.c_int32)]),
     "iefwd_set_cu_mask": (_i32, [_vp, ctypes.POINTER(_u32), _u32]),
     "iefwd_get_cu_mask": (_i32, [_vp, ctypes.POINTER(_u32), _u32]),
     "iefwd_submit": (_i32, [_vp, _vp, _u32, _u32, _i32]),
@@ -131,10 +141,10 @@ def device_info(device: int = 0) -> tuple[int, int]:
     return n_cu.value, n_xcd.value
 
 
-def build_cu_mask(n_cu: int, n_xcd: int, quota: int, n_words: int | None = None) -> list[int]:
+def build_cu_mask(n_cu: int, n_xcd: int, quota: int, first: int = 0, n_words: int | None = None) -> list[int]:
     n_words = n_words if n_words is not None else (n_cu + 31) // 32
     buf = (_u32 * n_words)()
-    _check(lib().iefwd_build_cu_mask(n_cu, n_xcd, quota, buf, n_words), "iefwd_build_cu_mask")
+    _check(lib().iefwd_build_cu_mask(n_cu, n_xcd, quota, first, buf, n_words), "iefwd_build_cu_mask")
     return list(buf)
 
 
@@ -181,8 +191,8 @@ class Instance:
     def __exit__(self, *exc):
         self.close()
 
-    def set_quota(self, n_cu: int) -> None:
-        _check(lib().iefwd_set_quota(self._h, n_cu), "iefwd_set_quota")
+    def set_quota(self, n_cu: int, first: int = 0) -> None:
+        _check(lib().iefwd_set_quota_at(self._h, n_cu, first), "iefwd_set_quota_at")
 
     def set_cu_mask(self, mask) -> None:
         buf = (_u32 * len(mask))(*mask)
@@ -228,6 +238,11 @@ class Instance:
     def last_batch_ms(self) -> float:
         v = _f32()
         _check(lib().iefwd_last_batch_ms(self._h, ctypes.byref(v)), "iefwd_last_batch_ms")
+        return v.value
+
+    def kernels_launched(self) -> int:
+        v = _u64()
+        _check(lib().iefwd_kernels_launched(self._h, ctypes.byref(v)), "iefwd_kernels_launched")
         return v.value
 
     def stream_handle(self) -> int:
@@ -285,3 +300,61 @@ def test_ln_head(z, gamma, beta, wh, bh, logits, rows, d, n_out, eps, stream=Non
 
 def test_cu_probe(n_groups: int, out, stream=None) -> None:
     _check(lib().iefwd_test_cu_probe(_stream(stream), n_groups, _ptr(out)), "iefwd_test_cu_probe")
+
+
+# ------------------------------------------------------------------ quota controller
+CTL_NONE, CTL_EMERGENCY, CTL_RECOVERY, CTL_CONTENTION = 0, 1, 2, 3
+
+
+class CtlParams(ctypes.Structure):
+    _fields_ = [("abi_version", _u32), ("max_tokens", _u32), ("window", _u32), ("granule", _u32),
+                ("min_quota", _u32), ("reserved0", _u32), ("eta_violation", ctypes.c_double),
+                ("eta_increase", ctypes.c_double)]
+
+
+class Controller:
+    """The fast scale-up/down quota controller (iefwd_ctl_*): report each
+    instance's kernels and last batch time once per control period, then
+    issue() returns (tokens, quotas, first mask bits) in id order."""
+
+    def __init__(self, **params):
+        p = CtlParams()
+        _check(lib().iefwd_ctl_params_init(ctypes.byref(p)), "iefwd_ctl_params_init")
+        for k, v in params.items():
+            setattr(p, k, v)
+        h = _vp()
+        _check(lib().iefwd_ctl_create(ctypes.byref(p), ctypes.byref(h)), "iefwd_ctl_create")
+        self._h = h.value
+        self.n = 0
+
+    def add(self, request: float, limit: float, slo_sensitive: bool) -> int:
+        i = _u32()
+        _check(lib().iefwd_ctl_add(self._h, request, limit, 1 if slo_sensitive else 0, ctypes.byref(i)),
+               "iefwd_ctl_add")
+        self.n += 1
+        return i.value
+
+    def report(self, i: int, kernels: int, klc_ms: float) -> None:
+        _check(lib().iefwd_ctl_report(self._h, i, kernels, klc_ms), "iefwd_ctl_report")
+
+    def issue(self) -> tuple[list[float], list[int], list[int]]:
+        t, q, f = (ctypes.c_double * max(self.n, 1))(), (_u32 * max(self.n, 1))(), (_u32 * max(self.n, 1))()
+        _check(lib().iefwd_ctl_issue(self._h, t, q, f, self.n), "iefwd_ctl_issue")
+        return list(t)[:self.n], list(q)[:self.n], list(f)[:self.n]
+
+    def state(self) -> int:
+        v = ctypes.c_int32()
+        _check(lib().iefwd_ctl_state(self._h, ctypes.byref(v)), "iefwd_ctl_state")
+        return v.value
+
+    def close(self) -> None:
+        if getattr(self, "_h", None):
+            lib().iefwd_ctl_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:   # interpreter shutdown
+            pass
+

@@ -22,7 +22,8 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libiefwd.so")
 ARCH = "gfx950"
 
-SOURCES = ["gemm.hip", "attention.hip", "layernorm.hip", "quota.cpp", "init_weights.cpp", "iefwd.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "layernorm.hip", "quota.cpp", "controller.cpp", "init_weights.cpp",
+           "iefwd.cpp"]
 
 COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Werror",

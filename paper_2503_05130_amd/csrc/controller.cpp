@@ -1,0 +1,109 @@
+// Quota controller (Sec. 3.4.1, Alg. 2) on CU quotas; see controller.h.
+#include "controller.h"
+
+#include <algorithm>
+#include <cmath>
+
+namespace iefwd {
+
+uint32_t QuotaController::add(double request, double limit, bool slo_sensitive) {
+    Inst in{};
+    in.request = request;
+    in.limit = limit;
+    in.slo = slo_sensitive;
+    in.r_last = p_.max_tokens * request;
+    insts_.push_back(in);
+    return (uint32_t)insts_.size() - 1;
+}
+
+void QuotaController::report(uint32_t id, uint64_t kernels, double klc_ms) {
+    Inst &in = insts_.at(id);
+    in.r_current = kernels;
+    if (klc_ms > 0) {
+        in.t_current = klc_ms;
+        in.t_min = in.t_min < 0 ? klc_ms : std::min(in.t_min, klc_ms);
+    }
+}
+
+uint64_t QuotaController::window_sum(const Inst &in) {
+    uint64_t s = 0;
+    for (uint64_t v : in.rw) s += v;
+    return s;
+}
+
+double QuotaController::issue_slo(uint32_t i) {
+    Inst &in = insts_[i];
+    in.dt = in.t_min > 0 ? (in.t_current - in.t_min) / in.t_min : 0.0;
+    bool others_idle = true;
+    for (uint32_t j = 0; j < insts_.size(); ++j)
+        if (j != i && window_sum(insts_[j]) != 0) others_idle = false;
+    const double maxt = p_.max_tokens;
+    State st;
+    double r;
+    if (in.dt > p_.eta_violation) {            // protective scale-up
+        st = Emergency;
+        r = maxt * in.limit;
+    } else if (window_sum(in) == 0) {          // idle: back to the request
+        st = Recovery;
+        r = maxt * in.request;
+    } else if (others_idle) {                  // co-located idle: grow
+        st = Recovery;
+        r = std::min(in.r_last * p_.eta_increase, maxt);
+    } else {
+        st = Contention;
+        r = maxt * in.request;
+    }
+    if (state_ != Emergency || owner_ == (int64_t)i) {   // only the raiser may leave EMERGENCY
+        state_ = st;
+        owner_ = st == Emergency ? (int64_t)i : -1;
+        owner_dt_ = st == Emergency ? in.dt : 0.0;
+    }
+    return r;
+}
+
+double QuotaController::issue_other(uint32_t i) const {
+    const Inst &in = insts_[i];
+    const double maxt = p_.max_tokens;
+    switch (state_) {
+    case None: return maxt * in.limit;
+    case Emergency: return std::min(maxt * in.request, in.r_last) / (1.0 + owner_dt_);
+    case Recovery: return std::min(in.r_last * p_.eta_increase, maxt * in.limit);
+    case Contention: break;
+    }
+    return in.r_last;
+}
+
+void QuotaController::issue(std::vector<double> &tokens, std::vector<uint32_t> &quotas,
+                            std::vector<uint32_t> &firsts) {
+    const uint32_t n = (uint32_t)insts_.size();
+    bool any_slo = false;
+    for (Inst &in : insts_) {
+        in.rw.push_back(in.r_current);
+        while (in.rw.size() > p_.window) in.rw.pop_front();
+        any_slo = any_slo || in.slo;
+    }
+    if (!any_slo) {
+        state_ = None;
+        owner_ = -1;
+        owner_dt_ = 0;
+    }
+    tokens.assign(n, 0.0);
+    for (uint32_t i = 0; i < n; ++i)
+        if (insts_[i].slo) tokens[i] = issue_slo(i);
+    for (uint32_t i = 0; i < n; ++i)
+        if (!insts_[i].slo) tokens[i] = issue_other(i);
+    quotas.assign(n, 0);
+    firsts.assign(n, 0);
+    uint32_t first = 0;
+    for (uint32_t i = 0; i < n; ++i) {
+        insts_[i].r_last = tokens[i];
+        insts_[i].r_current = 0;
+        const double units = std::floor(tokens[i] / p_.granule + 0.5);
+        const double q = std::max<double>(p_.min_quota, std::min<double>(p_.max_tokens, units * p_.granule));
+        quotas[i] = (uint32_t)q;
+        firsts[i] = first;
+        first = (first + quotas[i]) % p_.max_tokens;
+    }
+}
+
+}  // namespace iefwd

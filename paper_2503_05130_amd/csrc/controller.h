@@ -1,0 +1,83 @@
+// Quota controller: the paper's fast scale-up/down control (Sec. 3.4.1,
+// Alg. 2) with CUs as tokens.  Pure host code.
+//
+// Every control period each co-located instance reports the kernels it
+// launched during the period and the duration of its last iteration (the
+// kernel launching cycle, KLC: one batch for an inference instance).  issue()
+// then computes each instance's token issue R_issue:
+//   SLO-sensitive instances, from the relative KLC change dT = (T - T_min) / T_min:
+//     dT > eta_violation          -> EMERGENCY,  MaxTokens * limit
+//     no kernels in its window    -> RECOVERY,   MaxTokens * request
+//     no kernels in other windows -> RECOVERY,   min(R_last * eta_increase, MaxTokens)
+//     otherwise                   -> CONTENTION, MaxTokens * request
+//   other instances, from the shared state:
+//     NONE (no SLO-sensitive instance) -> MaxTokens * limit
+//     EMERGENCY  -> min(MaxTokens * request, R_last) / (1 + dT of the instance that raised it)
+//     RECOVERY   -> min(R_last * eta_increase, MaxTokens * limit)
+//     CONTENTION -> R_last
+// Only the instance that raised EMERGENCY can change the state again.  SLO-
+// sensitive instances are evaluated first (they set the state), then the
+// others, each group in id order.
+//
+// Tokens become quotas: round(R / granule) * granule clamped to
+// [min_quota, MaxTokens], placed on consecutive CU-mask bits in id order so
+// that co-located instances share no CU while their quotas fit on the device.
+#pragma once
+
+#include <cstdint>
+#include <deque>
+#include <vector>
+
+namespace iefwd {
+
+class QuotaController {
+public:
+    enum State : int32_t { None = 0, Emergency = 1, Recovery = 2, Contention = 3 };
+
+    struct Params {
+        uint32_t max_tokens = 256;   // MaxTokens: CUs (the device's CU count)
+        uint32_t window = 4;         // RW length in control periods
+        uint32_t granule = 8;        // quota granularity in CUs (one per XCD)
+        uint32_t min_quota = 8;      // smallest quota issued
+        double eta_violation = 0.2;  // relative KLC increase that raises EMERGENCY
+        double eta_increase = 1.25;  // multiplicative scale-up per period
+    };
+
+    explicit QuotaController(const Params &p) : p_(p) {}
+
+    // Adds an instance; returns its id (0, 1, ...).
+    uint32_t add(double request, double limit, bool slo_sensitive);
+    uint32_t size() const { return (uint32_t)insts_.size(); }
+
+    // Observation for the current period: kernels launched during it and the
+    // KLC of the last iteration completed in it (<= 0: none completed).
+    void report(uint32_t id, uint64_t kernels, double klc_ms);
+
+    // Ends the period: R_issue per instance (id order), then quotas and the
+    // first mask bit of each placement.
+    void issue(std::vector<double> &tokens, std::vector<uint32_t> &quotas, std::vector<uint32_t> &firsts);
+
+    State state() const { return state_; }
+
+private:
+    struct Inst {
+        double request, limit;
+        bool slo;
+        std::deque<uint64_t> rw;      // kernels per period, newest last
+        uint64_t r_current = 0;
+        double r_last = 0;
+        double t_current = 0, t_min = -1;   // t_min < 0: no KLC reported yet
+        double dt = 0;
+    };
+    double issue_slo(uint32_t i);
+    double issue_other(uint32_t i) const;
+    static uint64_t window_sum(const Inst &in);
+
+    Params p_;
+    std::vector<Inst> insts_;
+    State state_ = None;
+    int64_t owner_ = -1;   // instance that raised EMERGENCY
+    double owner_dt_ = 0;
+};
+
+}  // namespace iefwd

@@ -17,6 +17,7 @@
 #include <string>
 #include <vector>
 
+#include "controller.h"
 #include "init_weights.h"
 #include "kernels.h"
 #include "quota.h"
@@ -163,6 +164,7 @@ struct iefwd_instance {
         uint64_t launches = 0;
     } timing[IEFWD_K_COUNT];
     std::vector<hipEvent_t> event_pool;
+    uint64_t kernels_launched = 0;   // every kernel this instance has launched
 
     ~iefwd_instance();
 };
@@ -201,6 +203,7 @@ hipEvent_t take_event(iefwd_instance *inst) {
 // the kernel's own start and end timestamps into a pair of events.
 template <class F>
 void launch(iefwd_instance *inst, uint32_t kind, const char *what, F &&f) {
+    inst->kernels_launched += 1;
     auto &t = inst->timing[kind];
     if (t.enabled) {
         // the kernel itself records its start and end into these events
@@ -501,9 +504,10 @@ int iefwd_device_info(int device, uint32_t *n_cu, uint32_t *n_xcd) {
     });
 }
 
-int iefwd_build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t quota, uint32_t *mask, uint32_t n_words) {
+int iefwd_build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t quota, uint32_t first, uint32_t *mask,
+                        uint32_t n_words) {
     return guarded([&] {
-        if (!build_cu_mask(n_cu, n_xcd, quota, mask, n_words))
+        if (!build_cu_mask(n_cu, n_xcd, quota, first, mask, n_words))
             fail(IEFWD_EINVAL, "invalid mask request (quota 1..n_cu, n_xcd dividing n_cu, enough words)");
     });
 }
@@ -527,7 +531,7 @@ int iefwd_create(const iefwd_config *cfg, int device, iefwd_instance **out) {
         hip_check(hipEventCreate(&inst->ev_end), "hipEventCreate");
         hip_check(hipEventCreateWithFlags(&inst->ev_copy, hipEventDisableTiming), "hipEventCreate");
         std::vector<uint32_t> all(mask_words(dev.n_cu));
-        if (!build_cu_mask(dev.n_cu, dev.n_xcd, dev.n_cu, all.data(), (uint32_t)all.size()))
+        if (!build_cu_mask(dev.n_cu, dev.n_xcd, dev.n_cu, 0, all.data(), (uint32_t)all.size()))
             fail(IEFWD_ENODEV, "device CU count is not a multiple of its XCD count");
         hip_check(inst->streams.get(all, nullptr, &inst->stream), "hipExtStreamCreateWithCUMask");
         inst->mask = all;
@@ -548,16 +552,18 @@ int iefwd_destroy(iefwd_instance *inst) {
     });
 }
 
-int iefwd_set_quota(iefwd_instance *inst, uint32_t n_cu) {
+int iefwd_set_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first) {
     return guarded([&] {
         check_alive(inst);
         std::vector<uint32_t> m(mask_words(inst->dev.n_cu));
-        if (!build_cu_mask(inst->dev.n_cu, inst->dev.n_xcd, n_cu, m.data(), (uint32_t)m.size()))
-            fail(IEFWD_EINVAL, "quota must be in [1, device CUs]");
+        if (!build_cu_mask(inst->dev.n_cu, inst->dev.n_xcd, n_cu, first, m.data(), (uint32_t)m.size()))
+            fail(IEFWD_EINVAL, "quota must be in [1, device CUs] and first below the device CUs");
         inst->pending_mask = m;
         inst->pending = true;
     });
 }
+
+int iefwd_set_quota(iefwd_instance *inst, uint32_t n_cu) { return iefwd_set_quota_at(inst, n_cu, 0); }
 
 int iefwd_set_cu_mask(iefwd_instance *inst, const uint32_t *mask, uint32_t n_words) {
     return guarded([&] {
@@ -641,6 +647,14 @@ int iefwd_last_batch_ms(iefwd_instance *inst, float *ms) {
         if (!ms) fail(IEFWD_EINVAL, "ms is NULL");
         if (inst->state != iefwd_instance::State::Done) fail(IEFWD_ESTATE, "no completed batch");
         on_device(inst, [&] { hip_check(hipEventElapsedTime(ms, inst->ev_start, inst->ev_end), "hipEventElapsedTime"); });
+    });
+}
+
+int iefwd_kernels_launched(const iefwd_instance *inst, uint64_t *count) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!count) fail(IEFWD_EINVAL, "count is NULL");
+        *count = inst->kernels_launched;
     });
 }
 
@@ -729,6 +743,92 @@ int iefwd_export_tensor(const iefwd_instance *cinst, uint32_t layer, uint32_t sl
 }
 
 const char *iefwd_last_error(void) { return t_last_error.c_str(); }
+
+// ------------------------------------------------------------------ quota controller
+
+int iefwd_ctl_params_init(iefwd_ctl_params *p) {
+    return guarded([&] {
+        if (!p) fail(IEFWD_EINVAL, "params is NULL");
+        const QuotaController::Params d{};
+        *p = iefwd_ctl_params{};
+        p->abi_version = IEFWD_ABI_VERSION;
+        p->max_tokens = d.max_tokens;
+        p->window = d.window;
+        p->granule = d.granule;
+        p->min_quota = d.min_quota;
+        p->eta_violation = d.eta_violation;
+        p->eta_increase = d.eta_increase;
+    });
+}
+
+int iefwd_ctl_create(const iefwd_ctl_params *p, iefwd_ctl **out) {
+    return guarded([&] {
+        if (!out) fail(IEFWD_EINVAL, "out is NULL");
+        *out = nullptr;
+        if (!p) fail(IEFWD_EINVAL, "params is NULL");
+        if (p->abi_version != IEFWD_ABI_VERSION) fail(IEFWD_EVERSION, "params.abi_version mismatch");
+        if (p->max_tokens == 0 || p->window == 0 || p->granule == 0 || p->min_quota == 0 ||
+            p->min_quota > p->max_tokens || p->reserved0 != 0)
+            fail(IEFWD_EINVAL, "controller sizes out of range");
+        if (!(p->eta_violation >= 0) || !(p->eta_increase >= 1) || !std::isfinite(p->eta_violation) ||
+            !std::isfinite(p->eta_increase))
+            fail(IEFWD_EINVAL, "eta_violation must be >= 0 and eta_increase >= 1");
+        QuotaController::Params q;
+        q.max_tokens = p->max_tokens;
+        q.window = p->window;
+        q.granule = p->granule;
+        q.min_quota = p->min_quota;
+        q.eta_violation = p->eta_violation;
+        q.eta_increase = p->eta_increase;
+        *out = reinterpret_cast<iefwd_ctl *>(new QuotaController(q));
+    });
+}
+
+int iefwd_ctl_destroy(iefwd_ctl *ctl) {
+    return guarded([&] { delete reinterpret_cast<QuotaController *>(ctl); });
+}
+
+int iefwd_ctl_add(iefwd_ctl *ctl, double request, double limit, int slo_sensitive, uint32_t *id) {
+    return guarded([&] {
+        if (!ctl || !id) fail(IEFWD_EINVAL, "NULL argument");
+        if (!(request > 0) || !(limit >= request) || !(limit <= 1))
+            fail(IEFWD_EINVAL, "need 0 < request <= limit <= 1");
+        *id = reinterpret_cast<QuotaController *>(ctl)->add(request, limit, slo_sensitive != 0);
+    });
+}
+
+int iefwd_ctl_report(iefwd_ctl *ctl, uint32_t id, uint64_t kernels, double klc_ms) {
+    return guarded([&] {
+        auto *c = reinterpret_cast<QuotaController *>(ctl);
+        if (!c) fail(IEFWD_EINVAL, "controller is NULL");
+        if (id >= c->size()) fail(IEFWD_EINVAL, "no such instance id");
+        if (!std::isfinite(klc_ms)) fail(IEFWD_EINVAL, "klc_ms is not finite");
+        c->report(id, kernels, klc_ms);
+    });
+}
+
+int iefwd_ctl_issue(iefwd_ctl *ctl, double *tokens, uint32_t *quotas, uint32_t *firsts, uint32_t n) {
+    return guarded([&] {
+        auto *c = reinterpret_cast<QuotaController *>(ctl);
+        if (!c) fail(IEFWD_EINVAL, "controller is NULL");
+        if (n != c->size()) fail(IEFWD_EINVAL, "n must equal the number of instances");
+        std::vector<double> t;
+        std::vector<uint32_t> q, f;
+        c->issue(t, q, f);
+        for (uint32_t i = 0; i < n; ++i) {
+            if (tokens) tokens[i] = t[i];
+            if (quotas) quotas[i] = q[i];
+            if (firsts) firsts[i] = f[i];
+        }
+    });
+}
+
+int iefwd_ctl_state(const iefwd_ctl *ctl, int32_t *state) {
+    return guarded([&] {
+        if (!ctl || !state) fail(IEFWD_EINVAL, "NULL argument");
+        *state = reinterpret_cast<const QuotaController *>(ctl)->state();
+    });
+}
 
 const char *iefwd_status_string(int status) {
     switch (status) {

@@ -4,18 +4,16 @@
 
 namespace iefwd {
 
-bool build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t q, uint32_t *mask, uint32_t n_words) {
-    if (!mask || n_cu == 0 || n_xcd == 0 || n_cu % n_xcd != 0 || q == 0 || q > n_cu ||
+bool build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t q, uint32_t first, uint32_t *mask, uint32_t n_words) {
+    if (!mask || n_cu == 0 || n_xcd == 0 || n_cu % n_xcd != 0 || q == 0 || q > n_cu || first >= n_cu ||
         n_words < mask_words(n_cu))
         return false;
     std::fill(mask, mask + n_words, 0u);
-    const uint32_t per_xcd = n_cu / n_xcd;
-    for (uint32_t x = 0; x < n_xcd; ++x) {
-        const uint32_t take = q / n_xcd + (x < q % n_xcd ? 1u : 0u);
-        for (uint32_t local = 0; local < take && local < per_xcd; ++local) {
-            const uint32_t bit = local * n_xcd + x;
-            mask[bit / 32] |= 1u << (bit % 32);
-        }
+    // mask bit b is CU b / n_xcd of XCD b % n_xcd, so any run of consecutive
+    // bits (cyclically) takes an equal share of every XCD, within one CU
+    for (uint32_t i = 0; i < q; ++i) {
+        const uint32_t bit = (first + i) % n_cu;
+        mask[bit / 32] |= 1u << (bit % 32);
     }
     return true;
 }

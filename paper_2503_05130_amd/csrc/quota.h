@@ -15,11 +15,14 @@
 
 namespace iefwd {
 
-// Mask words for q CUs out of n_cu in n_xcd XCDs.  Mask bit b drives the CU
-// with index b / n_xcd inside XCD b % n_xcd (the driver hands mask bits to the
-// XCDs round-robin); XCD x gets q / n_xcd CUs plus one if x < q % n_xcd.
+// Mask words for q CUs out of n_cu in n_xcd XCDs: mask bits first, first + 1,
+// ..., first + q - 1 (mod n_cu).  Mask bit b drives the CU with index
+// b / n_xcd inside XCD b % n_xcd (the driver hands mask bits to the XCDs
+// round-robin), so every XCD gets q / n_xcd CUs or one more; with first = 0,
+// XCD x gets the extra CU if x < q % n_xcd.  Instances placed at first = 0,
+// q0, q0 + q1, ... get disjoint CUs while the quotas sum to at most n_cu.
 // Returns false if the arguments are out of range.
-bool build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t q, uint32_t *mask, uint32_t n_words);
+bool build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t q, uint32_t first, uint32_t *mask, uint32_t n_words);
 
 inline uint32_t mask_words(uint32_t n_cu) { return (n_cu + 31) / 32; }
 

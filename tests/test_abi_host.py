@@ -116,12 +116,36 @@ def test_mask_nested_and_full():
 def test_mask_extra_words_zeroed_and_errors():
     m = ie.build_cu_mask(256, 8, 16, n_words=10)
     assert m[8:] == [0, 0]
-    for args in [(256, 8, 0), (256, 8, 257), (256, 0, 8), (250, 8, 8)]:
+    for args in [(256, 8, 0), (256, 8, 257), (256, 0, 8), (250, 8, 8), (256, 8, 8, 256)]:
         with pytest.raises(ie.IefwdError) as e:
             ie.build_cu_mask(*args)
         assert e.value.status == ie.EINVAL
     with pytest.raises(ie.IefwdError):
         ie.build_cu_mask(256, 8, 8, n_words=7)
+
+
+@pytest.mark.parametrize("q,first", [(64, 0), (64, 64), (100, 37), (192, 200), (256, 5), (1, 255), (24, 250)])
+def test_mask_placed_balanced(q, first):
+    # a run of q consecutive mask bits starting at `first` (cyclically) is
+    # exactly bits first .. first + q - 1 mod 256, and within one CU per XCD
+    m = ie.build_cu_mask(256, 8, q, first)
+    bits = {b for b in range(256) if (m[b // 32] >> (b % 32)) & 1}
+    assert bits == {(first + i) % 256 for i in range(q)}
+    c = xcd_counts(m, 256, 8)
+    assert max(c) - min(c) <= 1
+
+
+def test_mask_packed_placements_disjoint():
+    # instances packed one after another get disjoint CUs up to 256 CUs in
+    # total and cover the device exactly when the quotas sum to 256
+    for quotas in [(64, 192), (128, 128), (192, 64), (24, 40, 64, 128), (8,) * 32]:
+        first, seen = 0, [0] * 8
+        for q in quotas:
+            m = ie.build_cu_mask(256, 8, q, first)
+            assert all((a & b) == 0 for a, b in zip(seen, m))
+            seen = [a | b for a, b in zip(seen, m)]
+            first = (first + q) % 256
+        assert seen == [0xFFFFFFFF] * 8
 
 
 # ------------------------------------------------------------------------------ create errors
@@ -166,6 +190,7 @@ def test_null_arguments():
     assert L.iefwd_create(None, 0, None) == ie.EINVAL
     assert L.iefwd_destroy(None) == ie.OK
     assert L.iefwd_set_quota(None, 8) == ie.EINVAL
+    assert L.iefwd_set_quota_at(None, 8, 0) == ie.EINVAL
     assert L.iefwd_submit(None, None, 1, 1, 0) == ie.EINVAL
     assert L.iefwd_wait(None) == ie.EINVAL
     assert L.iefwd_read_logits(None, None, 0, 0) == ie.EINVAL

@@ -1,0 +1,203 @@
+"""Quota controller (Sec. 3.4.1, Alg. 2): the oracle pinned to the behaviour
+the paper's text describes, and the library's controller (iefwd_ctl_*)
+compared with the oracle on seeded random observation streams.  Host only."""
+import math
+
+import numpy as np
+import pytest
+
+import paper_2503_05130_amd as ie
+from oracle import controller as O
+
+EMERG, RECOV, CONT, NONE = O.EMERGENCY, O.RECOVERY, O.CONTENTION, O.NONE
+
+
+def periods(ctl, obs):
+    """obs: list of per-period lists of (kernels, klc) per instance -> tokens per period."""
+    out = []
+    for row in obs:
+        for i, (k, t) in enumerate(row):
+            ctl.report(i, k, t)
+        out.append(ctl.issue())
+    return out
+
+
+# ------------------------------------------------------------------ oracle pins (paper text)
+def test_alone_best_effort_gets_its_limit():
+    # without an SLO-sensitive co-located instance the state stays NONE and the
+    # instance runs at its limit, whatever it reports
+    c = O.Controller()
+    c.add(0.25, 0.75, False)
+    for r in periods(c, [[(100, 5.0)], [(0, 0)], [(7, 9.0)]]):
+        assert r == [256 * 0.75]
+        assert c.state == NONE
+
+
+def test_klc_violation_raises_emergency_and_shrinks_colocated():
+    # a significant KLC increase of the SLO instance scales it up to its limit
+    # at once; the co-located instance is scaled down by the KLC change
+    c = O.Controller(eta_violation=0.2)
+    c.add(0.5, 1.0, True)
+    c.add(0.5, 0.75, False)
+    r = periods(c, [[(85, 10.0), (85, 10.0)], [(85, 10.0), (85, 10.0)]])
+    assert c.state == CONT and r[-1][0] == 128.0
+    r_last = r[-1][1]
+    c.report(0, 85, 15.0)            # KLC 10 -> 15 ms: dT = 0.5 > 0.2
+    c.report(1, 85, 10.0)
+    r = c.issue()
+    assert c.state == EMERG
+    assert r[0] == 256.0             # MaxTokens * limit
+    assert r[1] == pytest.approx(min(128.0, r_last) * 10.0 / 15.0)   # scaled by T_min / T_current
+    assert r[1] < r_last
+
+
+def test_small_klc_change_is_contention():
+    c = O.Controller(eta_violation=0.2)
+    c.add(0.5, 1.0, True)
+    c.add(0.5, 1.0, False)
+    periods(c, [[(85, 10.0), (85, 10.0)]])
+    r = periods(c, [[(85, 11.9), (85, 10.0)]] * 3)
+    assert c.state == CONT
+    assert r[-1][0] == 128.0                     # back at the request
+    assert r[-1][1] == r[0][1] == r[1][1]       # CONTENTION keeps R_last
+
+
+def test_only_the_raiser_leaves_emergency():
+    # two SLO instances: A raises EMERGENCY; B's calm reading does not reset it;
+    # once A's KLC recovers, A resets the state
+    c = O.Controller(eta_violation=0.2)
+    c.add(0.25, 1.0, True)
+    c.add(0.25, 1.0, True)
+    periods(c, [[(10, 10.0), (10, 10.0)]])
+    periods(c, [[(10, 20.0), (10, 10.0)]])
+    assert c.state == EMERG and c.owner == 0
+    periods(c, [[(10, 20.0), (10, 10.0)]])
+    assert c.state == EMERG
+    r = periods(c, [[(10, 10.0), (10, 10.0)]])[-1]
+    assert c.state == CONT and c.owner == -1
+    assert r == [64.0, 64.0]
+
+
+def test_idle_slo_instance_scales_down_and_colocated_grows():
+    # no kernels from the SLO instance for a whole window: it drops to its
+    # request, and the co-located instance grows by eta_increase per period up
+    # to its limit
+    c = O.Controller(window=3, eta_increase=1.25)
+    c.add(0.25, 1.0, True)
+    c.add(0.25, 0.5, False)
+    rs = periods(c, [[(0, 0), (50, 10.0)]] * 8)
+    assert all(r[0] == 64.0 for r in rs)
+    assert c.state == RECOV
+    grow = [r[1] for r in rs]
+    expect, v = [], 64.0
+    for _ in rs:
+        v = min(v * 1.25, 128.0)
+        expect.append(v)
+    assert grow == expect
+    assert grow[-1] == 128.0
+
+
+def test_window_remembers_recent_kernels():
+    # one burst keeps an instance active for exactly `window` periods
+    c = O.Controller(window=3)
+    c.add(0.25, 1.0, True)
+    c.add(0.25, 1.0, False)
+    states = []
+    for row in [[(10, 5.0), (10, 5.0)]] + [[(0, 0), (10, 5.0)]] * 4:
+        periods(c, [row])
+        states.append(c.state)
+    assert states == [CONT, CONT, CONT, RECOV, RECOV]
+
+
+def test_idle_colocated_lets_slo_instance_grow_to_the_device():
+    c = O.Controller(eta_increase=1.5)
+    c.add(0.25, 0.5, True)
+    c.add(0.25, 0.5, False)
+    rs = periods(c, [[(20, 5.0), (0, 0)]] * 6)
+    got = [r[0] for r in rs]
+    v, expect = 64.0, []
+    for _ in rs:
+        v = min(v * 1.5, 256.0)                 # not capped at its limit (only at the device)
+        expect.append(v)
+    assert got == expect and got[-1] == 256.0
+
+
+def test_tokens_to_disjoint_placements():
+    c = O.Controller()
+    q, f = c.quotas([63.9, 100.0, 3.0, 43.0])   # 63.9 -> 64, 12.5 granules -> 13, min 8, 5.4 -> 5
+    assert q == [64, 104, 8, 40]
+    assert f == [0, 64, 168, 176]
+    q, f = c.quotas([256.0, 300.0])
+    assert q == [256, 256] and f == [0, 0]      # oversubscribed: overlapping placements
+
+
+# ------------------------------------------------------------------ library vs oracle
+def random_scenario(seed, n_periods=300):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(2, 5))
+    insts = []
+    for _ in range(n):
+        req = float(rng.choice([0.125, 0.25, 0.5]))
+        lim = float(min(1.0, req * rng.choice([1.0, 1.5, 2.0, 4.0])))
+        insts.append((req, lim, bool(rng.random() < 0.5)))
+    obs = []
+    klc = [float(rng.uniform(1, 20)) for _ in range(n)]
+    for _ in range(n_periods):
+        row = []
+        for i in range(n):
+            idle = rng.random() < 0.25
+            k = 0 if idle else int(rng.integers(1, 400))
+            klc[i] = max(0.5, klc[i] * float(rng.choice([0.9, 1.0, 1.05, 1.6])))
+            row.append((k, 0.0 if idle else klc[i]))
+        obs.append(row)
+    return insts, obs
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_library_matches_oracle(seed):
+    insts, obs = random_scenario(seed)
+    params = dict(window=int(1 + seed % 5), eta_violation=[0.1, 0.2, 0.5][seed % 3],
+                  eta_increase=[1.1, 1.25, 2.0][seed % 3])
+    o = O.Controller(**params)
+    lib = ie.Controller(**params)
+    for req, lim, slo in insts:
+        assert o.add(req, lim, slo) == lib.add(req, lim, slo)
+    seen_states = set()
+    for row in obs:
+        for i, (k, t) in enumerate(row):
+            o.report(i, k, t)
+            lib.report(i, k, t)
+        want = o.issue()
+        wq, wf = o.quotas(want)
+        got, gq, gf = lib.issue()
+        assert got == want                        # same fp64 steps: exact
+        assert (gq, gf) == (wq, wf)
+        assert lib.state() == o.state
+        seen_states.add(o.state)
+    lib.close()
+    if any(s for _, _, s in insts) and not all(s for _, _, s in insts):
+        assert len(seen_states) >= 2
+
+
+def test_controller_abi_errors():
+    p = ie.CtlParams()
+    ie.lib().iefwd_ctl_params_init(ie.ctypes.byref(p))
+    h = ie.ctypes.c_void_p()
+    for field, bad, status in [("abi_version", 99, ie.EVERSION), ("window", 0, ie.EINVAL),
+                               ("min_quota", 300, ie.EINVAL), ("eta_increase", 0.5, ie.EINVAL),
+                               ("eta_violation", math.nan, ie.EINVAL), ("reserved0", 1, ie.EINVAL)]:
+        q = ie.CtlParams.from_buffer_copy(p)
+        setattr(q, field, bad)
+        assert ie.lib().iefwd_ctl_create(ie.ctypes.byref(q), ie.ctypes.byref(h)) == status, field
+        assert h.value is None
+    c = ie.Controller()
+    for req, lim in [(0.0, 0.5), (0.5, 0.25), (0.5, 1.5)]:
+        with pytest.raises(ie.IefwdError):
+            c.add(req, lim, True)
+    c.add(0.25, 0.5, True)
+    with pytest.raises(ie.IefwdError):
+        c.report(1, 1, 1.0)                         # no such id
+    t = (ie.ctypes.c_double * 2)()
+    assert ie.lib().iefwd_ctl_issue(c._h, t, None, None, 2) == ie.EINVAL
+    assert ie.lib().iefwd_ctl_destroy(None) == ie.OK
+    c.close()

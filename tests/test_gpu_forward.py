@@ -179,18 +179,19 @@ def test_fresh_instance_read_before_submit():
 
 
 def test_colocated_equals_solo():
-    # two BERT-base-shaped instances (independent seeds) co-located at quotas
-    # 128/128 and 64/192, driven from two host threads: every batch equals the
-    # solo full-quota result bit for bit
+    # two BERT-base-shaped instances (independent seeds) co-located on disjoint
+    # CUs (128/128, 64/192) and on the same CUs (128 each, both at bit 0),
+    # driven from two host threads: every batch equals the solo full-quota
+    # result bit for bit
     n_batches = 12
     shapes = [W.model_shape("bert_base_l12_d768_s128", seed=31), W.model_shape("bert_base_l12_d768_s128", seed=32)]
     xs = [[W.make_input(31000 + 1000 * i + k, 8, 128, 768) for k in range(n_batches)] for i in range(2)]
     insts = [ie.Instance(**instance_config(s, 8, 128)) for s in shapes]
     try:
         solo = [[run_instance(insts[i], xs[i][k]) for k in range(n_batches)] for i in range(2)]
-        for quotas in ((128, 128), (64, 192)):
-            for inst, q in zip(insts, quotas):
-                inst.set_quota(q)
+        for quotas in (((128, 0), (128, 128)), ((64, 0), (192, 64)), ((128, 0), (128, 0))):
+            for inst, (q, first) in zip(insts, quotas):
+                inst.set_quota(q, first)
             results = [[None] * n_batches for _ in range(2)]
             errors = []
 

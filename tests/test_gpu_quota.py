@@ -41,3 +41,20 @@ def test_masked_stream_residency(q):
     assert len(cus) == q
     assert len(per_xcc) == min(8, q)
     assert max(per_xcc.values()) - min(per_xcc.values()) <= 1
+
+
+@pytest.mark.parametrize("q,first", [(64, 64), (128, 128), (24, 250)])
+def test_placed_stream_residency(q, first):
+    # a quota placed at `first` runs on exactly the CUs of its mask: two
+    # placements that do not overlap in the mask see disjoint CU sets
+    shape = W.model_shape("encoder_l1_d128_s32_b2")
+    with ie.Instance(**instance_config(shape, 1, 32)) as a, ie.Instance(**instance_config(shape, 1, 32)) as b:
+        a.set_quota(q, first)
+        b.set_quota(q, (first + q) % 256)
+        x = W.make_input(1, 1, 32, 128)
+        run_instance(a, x)
+        run_instance(b, x)
+        ca, cb = observed_cus(a.stream_handle()), observed_cus(b.stream_handle())
+    print(f"quota {q} at {first}: {len(ca)} and {len(cb)} CUs, overlap {len(ca & cb)}", flush=True)
+    assert len(ca) == q and len(cb) == q
+    assert not (ca & cb)
