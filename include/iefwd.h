@@ -135,6 +135,16 @@ int iefwd_set_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first);
 /* iefwd_set_quota_at(inst, n_cu, 0). */
 int iefwd_set_quota(iefwd_instance *inst, uint32_t n_cu);
 
+/* Creates the CU-masked stream for this quota and placement ahead of time, so
+ * that a later iefwd_set_quota_at with the same arguments switches without
+ * creating a hardware queue at the next submit (creation takes about 5 ms).
+ * Unlike the other calls on an instance, this one may run on another thread
+ * concurrently with them (a controller thread preparing the next quotas while
+ * the serving thread submits).  The instance caches 2 masked streams (the one
+ * in use, never evicted, and one more), since every live masked stream is a
+ * hardware queue.  EINVAL as iefwd_set_quota_at. */
+int iefwd_prepare_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first);
+
 /* Requests an explicit CU mask (n_words 32-bit words, bit order as above);
  * same timing as iefwd_set_quota.  EINVAL if the mask enables no existing CU. */
 int iefwd_set_cu_mask(iefwd_instance *inst, const uint32_t *mask, uint32_t n_words);
@@ -240,9 +250,14 @@ const char *iefwd_status_string(int status);
  *   RECOVERY                           -> min(R_last * eta_increase, MaxTokens * limit)
  *   CONTENTION                         -> R_last
  * Only the instance that raised EMERGENCY can change the state.  Tokens become
- * quotas round(R / granule) * granule clamped to [min_quota, MaxTokens], placed
- * on consecutive mask bits in id order (first_0 = 0, first_i = first_{i-1} +
- * quota_{i-1} mod MaxTokens): disjoint CUs while the quotas fit.
+ * quotas round(R / granule) * granule clamped to [min_quota, MaxTokens] and
+ * fitted so that no two placements share a CU (a shared CU slows both, and an
+ * instance moved onto CUs where another's batch is still in flight waits
+ * behind it): SLO-sensitive quotas are scaled down (granule, >= min_quota)
+ * until every other instance can keep min_quota, the others are scaled into
+ * the CUs that remain.  SLO-sensitive instances take mask bits upward from 0,
+ * the others downward from the top, each group in id order.  Overlap remains
+ * only if the instances outnumber MaxTokens / min_quota.
  * Readings where the paper is silent: the eta defaults; dividing by the KLC
  * ratio 1 + dT rather than dT (dT < 1 would scale up); the SLO scale-up capped
  * at MaxTokens; T_min over the whole history. */

@@ -36,8 +36,15 @@ design notes):
       reported; before any KLC is reported dT = 0.  R_last starts at
       MaxTokens * request.  RW holds the last `window` kernel counts.
   R6  tokens become a CU quota: round(R / granule) * granule, clamped to
-      [min_quota, MaxTokens]; instances are placed on consecutive mask bits in
-      id order (first_0 = 0, first_i = first_{i-1} + quota_{i-1} mod n_cu).
+      [min_quota, MaxTokens].  A CU mask cannot be oversubscribed without the
+      instances slowing each other down (and with a batch in flight on its old
+      mask, an instance moved onto those CUs waits behind it), so placements
+      never overlap: the SLO-sensitive quotas are shrunk until every other
+      instance can keep min_quota, then the others are shrunk into the CUs that
+      remain; shrinking keeps min_quota each and shares the rest in proportion
+      to each quota's excess over min_quota (rounded down to the granule).  SLO-sensitive
+      instances take mask bits upward from 0 (id order), the others downward
+      from the top (id order), so a change of one quota moves one boundary.
 
 Parity unpinned against numbers printed in the paper (it prints no controller
 traces); pinned against the behaviour its text describes (tests).
@@ -145,13 +152,36 @@ class Controller:
             inst.r_current = 0
         return out
 
+    def _fit(self, qs, idx, avail):
+        """Shrink the quotas qs[i], i in idx, to sum to at most avail: each keeps
+        min_quota and the rest of avail is shared in proportion to its excess
+        over min_quota, rounded down to the granule."""
+        want = sum(qs[i] for i in idx)
+        if not idx or want <= avail:
+            return
+        spare = max(avail - len(idx) * self.min_quota, 0)
+        excess = want - len(idx) * self.min_quota
+        for i in idx:
+            extra = ((qs[i] - self.min_quota) * spare // excess) // self.granule * self.granule if excess else 0
+            qs[i] = self.min_quota + extra
+
     def quotas(self, tokens: list[float]) -> tuple[list[int], list[int]]:
         """Tokens -> (CU quota, first mask bit) per instance (reading R6)."""
-        qs, firsts, first = [], [], 0
+        n = len(tokens)
+        qs = []
         for r in tokens:
             q = int(math.floor(r / self.granule + 0.5)) * self.granule
-            q = max(self.min_quota, min(self.n_cu, q))
-            qs.append(q)
-            firsts.append(first)
-            first = (first + q) % self.n_cu
+            qs.append(max(self.min_quota, min(self.n_cu, q)))
+        slo = [i for i in range(n) if self.insts[i].slo]
+        other = [i for i in range(n) if not self.insts[i].slo]
+        self._fit(qs, slo, self.n_cu - len(other) * self.min_quota)
+        self._fit(qs, other, self.n_cu - sum(qs[i] for i in slo))
+        firsts = [0] * n
+        lo, hi = 0, self.n_cu
+        for i in slo:
+            firsts[i] = lo % self.n_cu
+            lo += qs[i]
+        for i in other:
+            hi -= qs[i]
+            firsts[i] = hi % self.n_cu
         return qs, firsts

@@ -37,6 +37,7 @@ SIGNATURES = {
     "iefwd_destroy": (_i32, [_vp]),
     "iefwd_set_quota": (_i32, [_vp, _u32]),
     "iefwd_set_quota_at": (_i32, [_vp, _u32, _u32]),
+    "iefwd_prepare_quota_at": (_i32, [_vp, _u32, _u32]),
     "iefwd_kernels_launched": (_i32, [_vp, ctypes.POINTER(ctypes.c_uint64)]),
     "iefwd_ctl_params_init": (_i32, [_vp]),
     "iefwd_ctl_create": (_i32, [_vp, ctypes.POINTER(_vp)]),
@@ -193,6 +194,11 @@ class Instance:
 
     def set_quota(self, n_cu: int, first: int = 0) -> None:
         _check(lib().iefwd_set_quota_at(self._h, n_cu, first), "iefwd_set_quota_at")
+
+    def prepare_quota(self, n_cu: int, first: int = 0) -> None:
+        """Create the masked stream for (n_cu, first) ahead of time; may be called
+        from another thread while this instance serves."""
+        _check(lib().iefwd_prepare_quota_at(self._h, n_cu, first), "iefwd_prepare_quota_at")
 
     def set_cu_mask(self, mask) -> None:
         buf = (_u32 * len(mask))(*mask)

@@ -92,17 +92,55 @@ void QuotaController::issue(std::vector<double> &tokens, std::vector<uint32_t> &
         if (insts_[i].slo) tokens[i] = issue_slo(i);
     for (uint32_t i = 0; i < n; ++i)
         if (!insts_[i].slo) tokens[i] = issue_other(i);
+    // tokens -> quotas that never share a CU: SLO-sensitive quotas are scaled
+    // so that every other instance keeps min_quota, the others are scaled into
+    // what remains; SLO-sensitive instances are placed upward from mask bit 0,
+    // the others downward from the top
     quotas.assign(n, 0);
     firsts.assign(n, 0);
-    uint32_t first = 0;
     for (uint32_t i = 0; i < n; ++i) {
         insts_[i].r_last = tokens[i];
         insts_[i].r_current = 0;
         const double units = std::floor(tokens[i] / p_.granule + 0.5);
-        const double q = std::max<double>(p_.min_quota, std::min<double>(p_.max_tokens, units * p_.granule));
-        quotas[i] = (uint32_t)q;
-        firsts[i] = first;
-        first = (first + quotas[i]) % p_.max_tokens;
+        quotas[i] = (uint32_t)std::max<double>(p_.min_quota, std::min<double>(p_.max_tokens, units * p_.granule));
+    }
+    // shrink one group to at most `avail` CUs: min_quota each, the rest shared in
+    // proportion to each quota's excess over min_quota (down to the granule)
+    auto fit = [&](bool slo, int64_t avail) {
+        uint64_t want = 0, count = 0;
+        for (uint32_t i = 0; i < n; ++i)
+            if (insts_[i].slo == slo) {
+                want += quotas[i];
+                ++count;
+            }
+        if (count == 0 || (int64_t)want <= avail) return;
+        const int64_t spare_s = avail - (int64_t)(count * p_.min_quota);
+        const uint64_t spare = spare_s > 0 ? (uint64_t)spare_s : 0;
+        const uint64_t excess = want - count * p_.min_quota;
+        for (uint32_t i = 0; i < n; ++i)
+            if (insts_[i].slo == slo) {
+                const uint64_t extra =
+                    excess ? ((quotas[i] - p_.min_quota) * spare / excess) / p_.granule * p_.granule : 0;
+                quotas[i] = p_.min_quota + (uint32_t)extra;
+            }
+    };
+    int64_t n_other = 0, slo_sum = 0;
+    for (uint32_t i = 0; i < n; ++i) n_other += insts_[i].slo ? 0 : 1;
+    fit(true, (int64_t)p_.max_tokens - n_other * (int64_t)p_.min_quota);
+    for (uint32_t i = 0; i < n; ++i) slo_sum += insts_[i].slo ? quotas[i] : 0;
+    fit(false, (int64_t)p_.max_tokens - slo_sum);
+    int64_t lo = 0, hi = p_.max_tokens;
+    for (uint32_t i = 0; i < n; ++i) {
+        if (insts_[i].slo) {
+            firsts[i] = (uint32_t)(lo % p_.max_tokens);
+            lo += quotas[i];
+        }
+    }
+    for (uint32_t i = 0; i < n; ++i) {
+        if (!insts_[i].slo) {
+            hi -= quotas[i];
+            firsts[i] = (uint32_t)(((hi % (int64_t)p_.max_tokens) + p_.max_tokens) % p_.max_tokens);
+        }
     }
 }
 

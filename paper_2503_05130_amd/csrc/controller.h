@@ -20,8 +20,11 @@
 // others, each group in id order.
 //
 // Tokens become quotas: round(R / granule) * granule clamped to
-// [min_quota, MaxTokens], placed on consecutive CU-mask bits in id order so
-// that co-located instances share no CU while their quotas fit on the device.
+// [min_quota, MaxTokens], then fitted so that no two instances share a CU:
+// SLO-sensitive quotas are scaled (granule, >= min_quota) until every other
+// instance can keep min_quota, and the others are scaled into the CUs that
+// remain.  SLO-sensitive instances take mask bits upward from 0 (id order),
+// the others downward from the top (id order).
 #pragma once
 
 #include <cstdint>

@@ -449,7 +449,7 @@ void alloc_workspace(iefwd_instance *I) {
 void apply_pending_quota(iefwd_instance *I) {
     if (!I->pending) return;
     hipStream_t next = nullptr;
-    hip_check(I->streams.get(I->pending_mask, I->stream, &next), "hipExtStreamCreateWithCUMask");
+    hip_check(I->streams.acquire(I->pending_mask, &next), "hipExtStreamCreateWithCUMask");
     if (next != I->stream) {
         // order the new queue after everything the old one was given
         if (I->have_batch) hip_check(hipStreamWaitEvent(next, I->ev_end, 0), "hipStreamWaitEvent");
@@ -533,7 +533,7 @@ int iefwd_create(const iefwd_config *cfg, int device, iefwd_instance **out) {
         std::vector<uint32_t> all(mask_words(dev.n_cu));
         if (!build_cu_mask(dev.n_cu, dev.n_xcd, dev.n_cu, 0, all.data(), (uint32_t)all.size()))
             fail(IEFWD_ENODEV, "device CU count is not a multiple of its XCD count");
-        hip_check(inst->streams.get(all, nullptr, &inst->stream), "hipExtStreamCreateWithCUMask");
+        hip_check(inst->streams.acquire(all, &inst->stream), "hipExtStreamCreateWithCUMask");
         inst->mask = all;
     });
     if (st != IEFWD_OK) {
@@ -564,6 +564,17 @@ int iefwd_set_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first) {
 }
 
 int iefwd_set_quota(iefwd_instance *inst, uint32_t n_cu) { return iefwd_set_quota_at(inst, n_cu, 0); }
+
+int iefwd_prepare_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first) {
+    return guarded([&] {
+        check_alive(inst);
+        std::vector<uint32_t> m(mask_words(inst->dev.n_cu));
+        if (!build_cu_mask(inst->dev.n_cu, inst->dev.n_xcd, n_cu, first, m.data(), (uint32_t)m.size()))
+            fail(IEFWD_EINVAL, "quota must be in [1, device CUs] and first below the device CUs");
+        hip_check(hipSetDevice(inst->device), "hipSetDevice");
+        hip_check(inst->streams.prepare(m), "hipExtStreamCreateWithCUMask");
+    });
+}
 
 int iefwd_set_cu_mask(iefwd_instance *inst, const uint32_t *mask, uint32_t n_words) {
     return guarded([&] {

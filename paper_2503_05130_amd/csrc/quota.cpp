@@ -27,26 +27,39 @@ uint32_t mask_popcount(const std::vector<uint32_t> &mask, uint32_t n_cu) {
 MaskedStreams::~MaskedStreams() { clear(); }
 
 void MaskedStreams::clear() {
+    std::lock_guard<std::mutex> lock(mu_);
     for (Entry &e : entries_) {
         (void)hipStreamSynchronize(e.stream);
         (void)hipStreamDestroy(e.stream);
     }
     entries_.clear();
+    current_ = nullptr;
 }
 
-hipError_t MaskedStreams::get(const std::vector<uint32_t> &mask, hipStream_t keep, hipStream_t *out) {
+hipStream_t MaskedStreams::find_locked(const std::vector<uint32_t> &mask) {
     ++clock_;
     for (Entry &e : entries_) {
         if (e.mask == mask) {
             e.last_use = clock_;
-            *out = e.stream;
-            return hipSuccess;
+            return e.stream;
         }
+    }
+    return nullptr;
+}
+
+// Adds s for mask (or, if another thread added that mask meanwhile, destroys
+// s and returns the cached one), evicting the least recently used stream that
+// is not in use.
+hipError_t MaskedStreams::insert_locked(const std::vector<uint32_t> &mask, hipStream_t s, hipStream_t *out) {
+    if (hipStream_t have = find_locked(mask)) {
+        (void)hipStreamDestroy(s);
+        *out = have;
+        return hipSuccess;
     }
     if (entries_.size() >= capacity_) {
         size_t victim = entries_.size();
         for (size_t i = 0; i < entries_.size(); ++i) {
-            if (entries_[i].stream == keep) continue;
+            if (entries_[i].stream == current_) continue;
             if (victim == entries_.size() || entries_[i].last_use < entries_[victim].last_use) victim = i;
         }
         if (victim < entries_.size()) {
@@ -57,12 +70,44 @@ hipError_t MaskedStreams::get(const std::vector<uint32_t> &mask, hipStream_t kee
             entries_.erase(entries_.begin() + (long)victim);
         }
     }
-    hipStream_t s = nullptr;
-    hipError_t err = hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data());
-    if (err != hipSuccess) return err;
     entries_.push_back(Entry{mask, s, clock_});
     *out = s;
     return hipSuccess;
+}
+
+hipError_t MaskedStreams::get(const std::vector<uint32_t> &mask, hipStream_t *out) {
+    {
+        std::lock_guard<std::mutex> lock(mu_);
+        if ((*out = find_locked(mask))) return hipSuccess;
+    }
+    hipStream_t s = nullptr;   // created without holding the lock
+    hipError_t err = hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data());
+    if (err != hipSuccess) return err;
+    std::lock_guard<std::mutex> lock(mu_);
+    return insert_locked(mask, s, out);
+}
+
+hipError_t MaskedStreams::acquire(const std::vector<uint32_t> &mask, hipStream_t *out) {
+    hipError_t err = get(mask, out);
+    if (err != hipSuccess) return err;
+    std::lock_guard<std::mutex> lock(mu_);
+    // re-check: a concurrent prepare() may have evicted it between get() and here
+    if (hipStream_t have = find_locked(mask)) {
+        *out = have;
+    } else {
+        hipStream_t s = nullptr;
+        err = hipExtStreamCreateWithCUMask(&s, (uint32_t)mask.size(), mask.data());
+        if (err != hipSuccess) return err;
+        err = insert_locked(mask, s, out);
+        if (err != hipSuccess) return err;
+    }
+    current_ = *out;
+    return hipSuccess;
+}
+
+hipError_t MaskedStreams::prepare(const std::vector<uint32_t> &mask) {
+    hipStream_t s = nullptr;
+    return get(mask, &s);
 }
 
 }  // namespace iefwd

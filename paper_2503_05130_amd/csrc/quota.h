@@ -11,6 +11,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
 #include <vector>
 
 namespace iefwd {
@@ -29,18 +30,26 @@ inline uint32_t mask_words(uint32_t n_cu) { return (n_cu + 31) / 32; }
 uint32_t mask_popcount(const std::vector<uint32_t> &mask, uint32_t n_cu);
 
 // Small LRU cache of CU-masked streams for one instance.  Creating a masked
-// stream creates a hardware queue, so it is kept off the batch path once a
-// mask has been seen.  Streams are created at the default priority.
+// stream creates a hardware queue (about 5 ms on MI355X), so it is kept off
+// the batch path: once a mask has been seen, or prepared ahead of time from
+// another thread, switching to it costs one event wait.  The default keeps two
+// (the stream in use and the next one): with several co-located instances,
+// more live queues per instance made batches after a switch stall more often.  Streams are created
+// at the default priority.  Thread-safe: prepare() may run concurrently with
+// acquire(); stream creation happens outside the lock.
 class MaskedStreams {
 public:
-    explicit MaskedStreams(size_t capacity = 4) : capacity_(capacity) {}
+    explicit MaskedStreams(size_t capacity = 2) : capacity_(capacity) {}
     MaskedStreams(const MaskedStreams &) = delete;
     MaskedStreams &operator=(const MaskedStreams &) = delete;
     ~MaskedStreams();
 
-    // Stream with exactly this mask (created on first use).  `keep` is never
-    // evicted (the stream currently in use).
-    hipError_t get(const std::vector<uint32_t> &mask, hipStream_t keep, hipStream_t *out);
+    // The stream with exactly this mask (created if missing); it becomes the
+    // stream in use, which is never evicted until another one is acquired.
+    hipError_t acquire(const std::vector<uint32_t> &mask, hipStream_t *out);
+    // Makes sure a stream with this mask is cached (creating it if missing)
+    // without changing the stream in use.
+    hipError_t prepare(const std::vector<uint32_t> &mask);
     void clear();   // synchronises and destroys every cached stream
 
 private:
@@ -49,9 +58,15 @@ private:
         hipStream_t stream;
         uint64_t last_use;
     };
+    hipStream_t find_locked(const std::vector<uint32_t> &mask);
+    hipError_t insert_locked(const std::vector<uint32_t> &mask, hipStream_t s, hipStream_t *out);
+    hipError_t get(const std::vector<uint32_t> &mask, hipStream_t *out);
+
+    std::mutex mu_;
     std::vector<Entry> entries_;
     size_t capacity_;
     uint64_t clock_ = 0;
+    hipStream_t current_ = nullptr;
 };
 
 }  // namespace iefwd

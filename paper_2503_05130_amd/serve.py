@@ -1,0 +1,258 @@
+"""Co-located serving on one GPU: Poisson request streams into several
+instances, one dispatcher thread per instance, and a quota policy that
+re-masks the instances every control period (the paper's setting of
+Sec. 3.4 and its inference-inference experiments, Sec. 5).
+
+  python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 static proportional shared]
+                                       [--horizon 20] [--warmup 2] [--period-ms 20] [--small]
+
+Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
+batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
+pre-LN decoders (24 x 2048, 16 heads, FFN 8192, S = 1024, batches of up to
+2, 10 requests/s each, best effort).  Every request is one sequence; a
+dispatcher takes up to `max_batch` requests that have arrived, runs them as
+one batch and records each request's latency (completion - arrival).
+
+Policies (each period):
+  shared       every instance on all CUs (no partitioning)
+  static       each instance on its request share, disjoint
+  proportional quota proportional to the queue length (multiples of 32
+               CUs, at least 32), disjoint, all CUs handed out
+  alg2         the fast scale-up/down controller (iefwd_ctl_*, 32-CU
+               granule): kernels launched in the period and the per-batch
+               time go in, quotas and placements come out
+
+A new quota's masked stream is created by the control thread
+(iefwd_prepare_quota_at) before the quota is posted, so a dispatcher only
+switches streams at its next batch boundary.
+
+The KLC an instance reports for a period is the median, over the batches it
+completed in the period, of each batch's device time relative to the fastest
+batch of the same size it has run on the same quota (times 1 ms).  So the
+controller's KLC change measures the slowdown of an iteration of one shape on
+one CU share -- contention -- rather than a change of batch size or of its own
+quota (which the controller itself causes).  This per-<batch, quota> baseline
+is what the paper's profiler supplies (Sec. 3.2).  Inputs are seeded synthetic embeddings already
+in device memory; weights are the library's seeded random init.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import threading
+import time
+
+import numpy as np
+import torch
+
+import paper_2503_05130_amd as ie
+
+BERT = dict(n_layers=12, d_model=768, n_heads=12, d_ff=3072, pre_ln=0, causal=0, n_out=2)
+DECODER = dict(n_layers=24, d_model=2048, n_heads=16, d_ff=8192, pre_ln=1, causal=1, n_out=2)
+SMALL = dict(n_layers=2, d_model=256, n_heads=4, d_ff=1024, pre_ln=0, causal=0, n_out=2)
+
+
+def default_mix(small: bool = False):
+    """(name, shape, seq, max_batch, rate/s, request, limit, slo_sensitive, weight seed)."""
+    if small:
+        return [("enc_a", SMALL, 64, 4, 200.0, 0.25, 0.5, True, 51),
+                ("enc_b", SMALL, 64, 4, 200.0, 0.25, 0.5, True, 52),
+                ("dec_a", dict(SMALL, pre_ln=1, causal=1), 256, 2, 20.0, 0.25, 0.5, False, 53),
+                ("dec_b", dict(SMALL, pre_ln=1, causal=1), 256, 2, 20.0, 0.25, 0.5, False, 54)]
+    return [("bert_a", BERT, 128, 4, 200.0, 0.25, 0.5, True, 51),
+            ("bert_b", BERT, 128, 4, 200.0, 0.25, 0.5, True, 52),
+            ("dec_a", DECODER, 1024, 2, 10.0, 0.25, 0.5, False, 53),
+            ("dec_b", DECODER, 1024, 2, 10.0, 0.25, 0.5, False, 54)]
+
+
+class Served:
+    """One instance with its request stream, pool of inputs and statistics."""
+
+    def __init__(self, idx, name, shape, seq, max_batch, rate, request, limit, slo, seed, pool=16):
+        self.idx, self.name, self.seq, self.max_batch, self.rate = idx, name, seq, max_batch, rate
+        self.request, self.limit, self.slo = request, limit, slo
+        self.inst = ie.Instance(device=0, max_batch=max_batch, max_seq=seq, seed=seed, **shape)
+        rng = np.random.default_rng(5000 + idx)
+        d = shape["d_model"]
+        self.pool = torch.from_numpy(rng.standard_normal((pool, seq, d), dtype=np.float32)).to("cuda:0")
+        self.lock = threading.Lock()
+
+    def reset(self, horizon):
+        """Fresh request stream (the same for every policy) and statistics."""
+        arr = np.random.default_rng(5100 + self.idx)
+        gaps = arr.exponential(1.0 / self.rate, size=int(self.rate * horizon * 2) + 16)
+        t = np.cumsum(gaps)
+        self.arrivals = t[t < horizon]
+        self.latency = np.full(len(self.arrivals), np.nan)
+        self.next = 0                       # first request not yet dispatched
+        self.best_ms = {}                   # fastest batch time per (batch size, quota)
+        self.kernels = self.inst.kernels_launched()   # read by the control thread
+        self.ratios = []                    # batch time / best, batches of the current period
+        self.pending = None                 # (quota, first) posted by the control thread
+        self.inst.set_quota(ie.device_info(0)[0], 0)
+        self.applied = (ie.device_info(0)[0], 0)
+        self.batches = 0
+        self.changes = 0                    # quota switches applied
+        self.klc_log = []                   # KLC ratios reported to the controller
+        self.plans = set()                  # distinct (quota, first) applied
+
+    def queue_len(self, now):
+        return int(np.searchsorted(self.arrivals, now, side="right")) - self.next
+
+    def run(self, t0, horizon, stop):
+        slot = 0
+        while not stop.is_set():
+            now = time.perf_counter() - t0
+            if self.next >= len(self.arrivals) or now > horizon + 5.0:
+                return
+            if self.arrivals[self.next] > now:
+                time.sleep(min(self.arrivals[self.next] - now, 0.002))
+                continue
+            k = min(self.max_batch, self.queue_len(now))
+            with self.lock:
+                pend, self.pending = self.pending, None
+            if pend is not None and pend != self.applied:
+                self.inst.set_quota(*pend)
+                self.applied = pend
+                self.changes += 1
+                self.plans.add(pend)
+            x = self.pool[slot:slot + k]
+            slot = (slot + k) % (len(self.pool) - self.max_batch + 1)
+            self.inst.submit(x)
+            self.inst.wait()
+            done = time.perf_counter() - t0
+            self.latency[self.next:self.next + k] = done - self.arrivals[self.next:self.next + k]
+            self.next += k
+            self.batches += 1
+            ms = self.inst.last_batch_ms()
+            key = (k, self.applied[0] if self.applied else 0)
+            best = min(self.best_ms.get(key, ms), ms)
+            self.best_ms[key] = best
+            with self.lock:
+                self.kernels = self.inst.kernels_launched()
+                self.ratios.append(ms / best)
+
+    def stats(self, warmup):
+        keep = (self.arrivals >= warmup) & np.isfinite(self.latency)
+        lat = self.latency[keep] * 1e3
+        return {"name": self.name, "requests": int(keep.sum()), "dropped": int(np.isnan(self.latency).sum()),
+                "p50_ms": round(float(np.percentile(lat, 50)), 3) if len(lat) else None,
+                "p99_ms": round(float(np.percentile(lat, 99)), 3) if len(lat) else None,
+                "batches": self.batches, "quota_changes": self.changes, "distinct_placements": len(self.plans),
+                "klc_ratio_p50_p90": ([round(float(np.percentile(self.klc_log, p)), 3) for p in (50, 90)]
+                                      if self.klc_log else None)}
+
+
+GRANULE = 32   # quota granularity of the dynamic policies: 4 CUs per XCD, few distinct masks
+
+
+def control_loop(policy, served, t0, horizon, period, stop, history):
+    n_cu = ie.device_info(0)[0]
+    ctl = None
+    if policy == "alg2":
+        ctl = ie.Controller(max_tokens=n_cu, granule=GRANULE, min_quota=GRANULE)
+        for s in served:
+            ctl.add(s.request, s.limit, s.slo)
+    last_k = [s.kernels for s in served]
+    posted = [None] * len(served)
+    while not stop.is_set():
+        now = time.perf_counter() - t0
+        if now > horizon:
+            return
+        if policy == "shared":
+            plan = [(n_cu, 0)] * len(served)
+        elif policy == "static":
+            plan, first = [], 0
+            for s in served:
+                q = max(8, int(round(s.request * n_cu / 8)) * 8)
+                plan.append((q, first))
+                first = (first + q) % n_cu
+        elif policy == "proportional":
+            ql = np.array([max(s.queue_len(now), 0) for s in served], dtype=np.float64)
+            share = np.full(len(served), 1.0 / len(served)) if ql.sum() == 0 else ql / ql.sum()
+            qs = np.maximum(GRANULE, np.floor(share * n_cu / GRANULE) * GRANULE).astype(int)
+            while qs.sum() > n_cu:
+                qs[int(np.argmax(qs))] -= GRANULE
+            qs[int(np.argmax(share))] += n_cu - qs.sum()
+            plan, first = [], 0
+            for q in qs:
+                plan.append((int(q), first))
+                first = (first + int(q)) % n_cu
+        else:
+            for i, s in enumerate(served):
+                with s.lock:
+                    k, ratios = s.kernels, s.ratios
+                    s.ratios = []
+                klc = float(np.median(ratios)) if ratios else 0.0
+                if klc > 0:
+                    s.klc_log.append(klc)
+                ctl.report(i, k - last_k[i], klc)
+                last_k[i] = k
+            _, qs, firsts = ctl.issue()
+            plan = list(zip(qs, firsts))
+        for i, (s, p) in enumerate(zip(served, plan)):
+            if p != posted[i]:
+                s.inst.prepare_quota(*p)       # hardware queue created here, not on the batch path
+                posted[i] = p
+            with s.lock:
+                s.pending = p
+        history.append((round(now, 3), [p[0] for p in plan], ctl.state() if ctl else -1))
+        time.sleep(period)
+
+
+def run_policy(policy, served, horizon, warmup, period):
+    for s in served:
+        s.reset(horizon)
+        s.inst.submit(s.pool[:1])              # warm the instance and its full-device stream
+        s.inst.wait()
+    torch.cuda.synchronize()
+    stop, history = threading.Event(), []
+    t0 = time.perf_counter()
+    threads = [threading.Thread(target=s.run, args=(t0, horizon, stop)) for s in served]
+    ctl = threading.Thread(target=control_loop, args=(policy, served, t0, horizon, period, stop, history))
+    for t in threads + [ctl]:
+        t.start()
+    for t in threads:
+        t.join()
+    stop.set()
+    ctl.join()
+    qs = np.array([h[1] for h in history]) if history else np.zeros((0, len(served)))
+    states = [h[2] for h in history]
+    return {"policy": policy, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
+            "instances": [s.stats(warmup) for s in served],
+            "mean_quota": [round(float(v), 1) for v in qs.mean(0)] if len(qs) else None,
+            "periods": len(history),
+            "state_counts": {str(k): states.count(k) for k in sorted(set(states))}}
+
+
+def build_mix(mix):
+    return [Served(i, *m) for i, m in enumerate(mix)]
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--policy", nargs="+", default=["shared", "static", "proportional", "alg2"])
+    ap.add_argument("--horizon", type=float, default=20.0)
+    ap.add_argument("--warmup", type=float, default=2.0)
+    ap.add_argument("--period-ms", type=float, default=20.0)
+    ap.add_argument("--small", action="store_true", help="small models (quick functional run)")
+    args = ap.parse_args()
+    t = time.perf_counter()
+    served = build_mix(default_mix(args.small))
+    print(json.dumps({"setup_s": round(time.perf_counter() - t, 1),
+                      "mix": [(s.name, s.seq, s.max_batch, s.rate, s.request, s.limit, s.slo) for s in served]}),
+          flush=True)
+    try:
+        for pol in args.policy:
+            name, _, per = pol.partition("@")          # "alg2@100": policy with its own period in ms
+            period = float(per) if per else args.period_ms
+            res = run_policy(name, served, args.horizon, args.warmup, period / 1e3)
+            print(json.dumps(res), flush=True)
+    finally:
+        for s in served:
+            s.inst.close()
+    return 0
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())

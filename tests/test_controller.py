@@ -124,11 +124,50 @@ def test_idle_colocated_lets_slo_instance_grow_to_the_device():
 
 def test_tokens_to_disjoint_placements():
     c = O.Controller()
+    for _ in range(4):
+        c.add(0.25, 0.5, False)
     q, f = c.quotas([63.9, 100.0, 3.0, 43.0])   # 63.9 -> 64, 12.5 granules -> 13, min 8, 5.4 -> 5
     assert q == [64, 104, 8, 40]
-    assert f == [0, 64, 168, 176]
-    q, f = c.quotas([256.0, 300.0])
-    assert q == [256, 256] and f == [0, 0]      # oversubscribed: overlapping placements
+    assert f == [192, 88, 80, 40]                 # best effort: downward from the top, id order
+
+
+def cu_sets(q, f):
+    return [set((fi + k) % 256 for k in range(qi)) for qi, fi in zip(q, f)]
+
+
+def test_oversubscribed_placements_never_share_a_cu():
+    # SLO-sensitive instances upward from bit 0; best-effort instances scaled
+    # into the CUs left free, downward from the top
+    c = O.Controller()
+    c.add(0.25, 1.0, True)
+    c.add(0.25, 0.5, False)
+    c.add(0.25, 0.5, True)
+    c.add(0.25, 0.5, False)
+    q, f = c.quotas([128.0, 128.0, 64.0, 64.0])
+    assert q == [128, 40, 64, 16]                  # 8 each + (120, 56) * 48 // 176 = (32, 15) -> 32, 8
+    assert f == [0, 216, 128, 200]
+    sets = cu_sets(q, f)
+    assert all(not (sets[a] & sets[b]) for a in range(4) for b in range(a + 1, 4))
+    # SLO tokens alone exceed the device: they give way so each best-effort
+    # instance keeps min_quota, still without sharing
+    q, f = c.quotas([256.0, 128.0, 200.0, 64.0])
+    assert q[0] + q[2] <= 256 - 2 * 8 and min(q[1], q[3]) >= 8
+    assert sum(q) <= 256
+    sets = cu_sets(q, f)
+    assert all(not (sets[a] & sets[b]) for a in range(4) for b in range(a + 1, 4))
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_random_placements_never_share_a_cu(seed):
+    rng = np.random.default_rng(seed)
+    c = O.Controller(granule=int(rng.choice([8, 32])), min_quota=32)
+    n = int(rng.integers(1, 8))
+    for _ in range(n):
+        c.add(0.25, 1.0, bool(rng.random() < 0.5))
+    q, f = c.quotas([float(v) for v in rng.uniform(0, 300, n)])
+    assert all(32 <= x <= 256 for x in q)
+    sets = cu_sets(q, f)
+    assert all(not (sets[a] & sets[b]) for a in range(n) for b in range(a + 1, n))
 
 
 # ------------------------------------------------------------------ library vs oracle

@@ -58,3 +58,38 @@ def test_placed_stream_residency(q, first):
     print(f"quota {q} at {first}: {len(ca)} and {len(cb)} CUs, overlap {len(ca & cb)}", flush=True)
     assert len(ca) == q and len(cb) == q
     assert not (ca & cb)
+
+
+def test_prepare_from_another_thread():
+    # a controller thread prepares masked streams while the instance serves;
+    # switching to a prepared quota is then cheap and lands on the right CUs
+    import threading
+    import time
+    shape = W.model_shape("encoder_l1_d128_s32_b2")
+    x = W.make_input(1, 1, 32, 128)
+    with ie.Instance(**instance_config(shape, 1, 32)) as inst:
+        run_instance(inst, x)
+        plans = [(32 * (i + 1), (32 * i) % 256) for i in range(6)]
+        errors = []
+
+        def prep():
+            try:
+                for q, f in plans:
+                    inst.prepare_quota(q, f)
+            except Exception as e:        # surfaced below
+                errors.append(e)
+
+        t = threading.Thread(target=prep)
+        t.start()
+        for _ in range(20):
+            run_instance(inst, x)
+        t.join(timeout=60)
+        assert not errors, errors
+        for q, f in plans[-4:]:
+            inst.set_quota(q, f)
+            t0 = time.perf_counter()
+            run_instance(inst, x)
+            ms = (time.perf_counter() - t0) * 1e3
+            cus = observed_cus(inst.stream_handle())
+            print(f"prepared quota {q} at {f}: first batch {ms:.2f} ms, {len(cus)} CUs", flush=True)
+            assert len(cus) == q

@@ -1,0 +1,32 @@
+"""Co-located serving with a quota policy per control period (small models,
+short horizon): every request is served under each policy and the controller
+re-masks the instances."""
+import numpy as np
+import pytest
+
+from paper_2503_05130_amd import serve
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def served():
+    s = serve.build_mix(serve.default_mix(small=True))
+    yield s
+    for x in s:
+        x.inst.close()
+
+
+@pytest.mark.parametrize("policy", ["shared", "static", "proportional", "alg2"])
+def test_policy_serves_every_request(served, policy):
+    print(f"serve policy={policy}", flush=True)
+    res = serve.run_policy(policy, served, horizon=1.5, warmup=0.2, period=0.01)
+    print(res, flush=True)
+    for st in res["instances"]:
+        assert st["dropped"] == 0, st
+        assert st["requests"] > 0 and st["p99_ms"] is not None and st["p99_ms"] >= st["p50_ms"] > 0
+    assert res["periods"] > 10
+    q = np.array(res["mean_quota"])
+    assert np.all((q >= 8) & (q <= 256))
+    if policy == "alg2":
+        assert sum(res["state_counts"].values()) == res["periods"]
