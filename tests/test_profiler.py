@@ -1,0 +1,87 @@
+"""HGSS inference profiling (Sec. 3.2): the search on synthetic latency
+surfaces, pinned to the example path the paper prints, against a traversal."""
+import math
+
+import pytest
+
+from paper_2503_05130_amd import profiler as P
+
+
+def test_smr_to_cus():
+    assert [P.smr_to_cus(s) for s in (10, 20, 30, 40, 50, 100)] == [24, 48, 80, 104, 128, 256]
+    assert all(P.smr_to_cus(s) % 8 == 0 for s in range(1, 101))
+    assert P.smr_to_cus(0.1) == 8
+
+
+def test_paper_example_path():
+    # the paper's GPT2-large example (100 ms SLO): <1,10>, <2,20>, <4,30> meet
+    # the SLO, <8,40> violates it and the search stops there
+    def measure(ibs, smr):
+        return 60.0 if ibs >= 8 else 20.0 * ibs / (smr / 10.0)
+    r = P.hgss(measure, slo_ms=100.0)
+    assert r["path"] == [(1, 10.0), (2, 20.0), (4, 30.0), (8, 40.0)]
+    assert r["trials"] == 4
+    # TE = IBS / (t * SMR): 1/(0.02*10) = 5, 2/(0.02*20) = 5, 4/(0.02667*30) = 5  -> ties: first max
+    tes = [P.throughput_efficacy(b, measure(b, s), s) for b, s in r["path"][:3]]
+    assert tes == pytest.approx([5.0, 5.0, 5.0])
+    assert r["request_smr"] == 10.0 and r["limit_smr"] == 20.0
+
+
+def test_request_is_max_te_and_limit_doubles():
+    # batching helps sublinearly, SMR with diminishing returns
+    def measure(ibs, smr):
+        return 2.0 + 3.0 * ibs ** 0.6 * (100.0 / smr) ** 0.5
+    r = P.hgss(measure, slo_ms=100.0, max_ibs=256)
+    feas = [(b, s) for b, s in r["path"] if measure(b, s) <= 50.0]
+    best = max(feas, key=lambda c: c[0] / (measure(*c) * 1e-3 * c[1]))
+    assert (r["ibs"], r["request_smr"]) == best
+    assert r["limit_smr"] == min(100.0, 2 * best[1])
+
+
+def test_heavy_model_climbs_smr_first():
+    # nothing fits at 10% for one sequence: SMR rises at IBS 1 until it does
+    def measure(ibs, smr):
+        return 800.0 * ibs / smr
+    r = P.hgss(measure, slo_ms=100.0)
+    assert r["path"][:3] == [(1, 10.0), (1, 20.0), (2, 30.0)]
+    assert measure(*r["path"][0]) > 50.0 and measure(*r["path"][1]) <= 50.0
+
+
+def test_never_feasible_ends_at_full_device():
+    r = P.hgss(lambda b, s: 1e6, slo_ms=100.0)
+    assert r["path"][-1] == (1, 100.0) and r.get("best") is None and r["trials"] == 10
+
+
+def convex(ibs, smr):
+    # batch time grows with IBS, falls with SM rate with diminishing returns
+    return 1.5 + 0.25 * ibs * (100.0 / smr) ** 0.35 + 0.02 * ibs ** 1.3
+
+
+def test_walks_against_traversal():
+    ibs_list = [1 << k for k in range(9)]
+    smr_list = [10.0 * k for k in range(1, 11)]
+    t = P.traversal(convex, 100.0, ibs_list, smr_list)
+    d = P.hgss(convex, 100.0, max_ibs=256)
+    f = P.hgss(convex, 100.0, max_ibs=256, walk="frontier")
+    assert t["trials"] == 90
+    assert d["trials"] <= 10 and f["trials"] <= len(ibs_list) + len(smr_list)
+    # the frontier walk reaches the traversal's optimum (it lies on the
+    # smallest-feasible-SMR frontier); the printed diagonal cannot reach it
+    assert f["best"]["te"] == pytest.approx(t["best"]["te"])
+    assert (f["ibs"], f["request_smr"]) == (t["ibs"], t["request_smr"])
+    assert d["best"]["te"] < t["best"]["te"]
+
+
+def test_frontier_visits_smallest_feasible_smr_per_ibs():
+    f = P.hgss(convex, 100.0, max_ibs=256, walk="frontier")
+    seen = {}
+    for b, s in f["path"]:
+        if convex(b, s) <= 50.0:
+            seen.setdefault(b, s)
+    for b, s in seen.items():
+        assert s == 10.0 or convex(b, s - 10.0) > 50.0
+
+
+def test_unknown_walk_rejected():
+    with pytest.raises(ValueError):
+        P.hgss(convex, 100.0, walk="spiral")
