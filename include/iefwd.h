@@ -80,7 +80,8 @@ typedef struct iefwd_config {
     uint32_t n_out;         /* head width; 0 = return hidden states */
     uint32_t pre_ln;        /* 0 = post-LN (BERT-style), 1 = pre-LN + final LN */
     uint32_t causal;        /* 0 = bidirectional, 1 = causal mask */
-    uint32_t reserved0;     /* must be 0 */
+    uint32_t kv_cache;      /* 1 = keep every layer's K and V for iefwd_decode (needs pre_ln = causal
+                               = 1 and max_seq <= 8192); 0 = prefill only (default) */
     float    ln_eps;        /* LayerNorm epsilon (default 1e-5) */
     float    w_std;         /* std of weight matrices (default 0.02) */
     float    b_std;         /* std of biases (default 0: biases are zero) */
@@ -164,6 +165,18 @@ int iefwd_get_cu_mask(const iefwd_instance *inst, uint32_t *mask, uint32_t n_wor
  * change is applied first (the new stream waits for the previous one). */
 int iefwd_submit(iefwd_instance *inst, const float *x, uint32_t batch, uint32_t seq,
                  int x_is_device);
+
+/* Decode step (instances created with kv_cache = 1): one new token per
+ * sequence at position `pos`.  x is fp32 [batch, d_model], the embeddings of
+ * the new tokens (host or device, as for iefwd_submit).  Every layer appends
+ * the tokens' K and V to its cache at `pos` and attends to positions
+ * 0 .. pos; the output (iefwd_read_logits) is fp32 [batch, 1, n_out or
+ * d_model].  The cache holds what the last iefwd_submit (the prompt,
+ * positions 0 .. seq - 1) and the decode steps since wrote: 1 <= batch <=
+ * the prompt's batch, pos <= the cached length (pos < length rewrites from
+ * there on) and pos < max_seq; otherwise EINVAL, or ESTATE without a prompt
+ * or a KV cache.  Asynchronous; one batch in flight per instance. */
+int iefwd_decode(iefwd_instance *inst, const float *x, uint32_t batch, uint32_t pos, int x_is_device);
 
 /* Blocks until the in-flight batch (if any) is complete. */
 int iefwd_wait(iefwd_instance *inst);
@@ -347,6 +360,15 @@ int iefwd_test_layernorm(const float *z, const float *gamma, const float *beta,
 int iefwd_test_ln_head(const float *z, const float *gamma, const float *beta,
                        const void *wh, const void *bh, float *logits, uint32_t rows,
                        uint32_t d, uint32_t n_out, float eps, void *stream);
+
+/* Decode attention: one query per (batch, head), q bf16 [batch, heads, dh],
+ * against keys 0 .. n_keys - 1 of K bf16 [batch, heads, k_rows, dh] and
+ * V^T bf16 [batch, heads, dh, vt_stride] (columns >= n_keys may hold any
+ * bits); ctx bf16 [batch, heads * dh].  dh in {64, 128}, 1 <= n_keys <= 8192,
+ * k_rows >= n_keys, vt_stride >= n_keys and a multiple of 64. */
+int iefwd_test_decode_attention(const void *q, const void *k, const void *vt, void *ctx, uint32_t batch,
+                                uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
+                                uint32_t vt_stride, void *stream);
 
 /* CU residency probe: launches n_groups workgroups of 64 threads on `stream`;
  * workgroup g writes out[2g] = XCC id, out[2g+1] = the hardware id register

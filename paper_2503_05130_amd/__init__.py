@@ -37,6 +37,7 @@ SIGNATURES = {
     "iefwd_destroy": (_i32, [_vp]),
     "iefwd_set_quota": (_i32, [_vp, _u32]),
     "iefwd_set_quota_at": (_i32, [_vp, _u32, _u32]),
+    "iefwd_decode": (_i32, [_vp, _vp, _u32, _u32, _i32]),
     "iefwd_prepare_quota_at": (_i32, [_vp, _u32, _u32]),
     "iefwd_kernels_launched": (_i32, [_vp, ctypes.POINTER(ctypes.c_uint64)]),
     "iefwd_ctl_params_init": (_i32, [_vp]),
@@ -65,6 +66,7 @@ SIGNATURES = {
     "iefwd_test_layernorm": (_i32, [_vp, _vp, _vp, _vp, _vp, _u32, _u32, _f32, _vp]),
     "iefwd_test_ln_head": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _f32, _vp]),
     "iefwd_test_cu_probe": (_i32, [_vp, _u32, _vp]),
+    "iefwd_test_decode_attention": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _u32, _u32, _vp]),
 }
 
 
@@ -73,7 +75,7 @@ class Config(ctypes.Structure):
     _fields_ = [
         ("abi_version", _u32), ("n_layers", _u32), ("d_model", _u32), ("n_heads", _u32),
         ("d_ff", _u32), ("max_batch", _u32), ("max_seq", _u32), ("n_out", _u32),
-        ("pre_ln", _u32), ("causal", _u32), ("reserved0", _u32),
+        ("pre_ln", _u32), ("causal", _u32), ("kv_cache", _u32),
         ("ln_eps", _f32), ("w_std", _f32), ("b_std", _f32), ("ln_std", _f32), ("qk_std", _f32),
         ("seed", _u64),
     ]
@@ -227,6 +229,23 @@ class Instance:
         _check(lib().iefwd_submit(self._h, _ptr(x), b, s, is_dev), "iefwd_submit")
         self._last_shape = (b, s)
 
+    def decode(self, x, pos: int) -> None:
+        """One decode step (kv_cache instances): x fp32 [batch, d_model] -- the new
+        tokens' embeddings -- appended at position `pos`."""
+        if isinstance(x, torch.Tensor):
+            if x.dtype != torch.float32 or not x.is_contiguous():
+                raise ValueError("x must be a contiguous float32 tensor")
+            is_dev = 1 if x.is_cuda else 0
+        else:
+            x = np.ascontiguousarray(x, dtype=np.float32)
+            is_dev = 0
+        b = x.shape[0]
+        if int(np.prod(x.shape)) != b * self.cfg.d_model:
+            raise ValueError("x does not have batch * d_model elements")
+        self._x_keep = x
+        _check(lib().iefwd_decode(self._h, _ptr(x), b, pos, is_dev), "iefwd_decode")
+        self._last_shape = (b, 1)
+
     def wait(self) -> None:
         _check(lib().iefwd_wait(self._h), "iefwd_wait")
 
@@ -302,6 +321,12 @@ def test_layernorm(z, gamma, beta, out_f32, out_bf16, rows, d, eps, stream=None)
 def test_ln_head(z, gamma, beta, wh, bh, logits, rows, d, n_out, eps, stream=None) -> None:
     _check(lib().iefwd_test_ln_head(_ptr(z), _ptr(gamma), _ptr(beta), _ptr(wh), _ptr(bh), _ptr(logits), rows,
                                     d, n_out, eps, _stream(stream)), "iefwd_test_ln_head")
+
+
+def test_decode_attention(q, k, vt, ctx, batch, n_heads, n_keys, head_dim, k_rows, vt_stride, stream=None) -> None:
+    _check(lib().iefwd_test_decode_attention(_ptr(q), _ptr(k), _ptr(vt), _ptr(ctx), batch, n_heads, n_keys,
+                                             head_dim, k_rows, vt_stride, _stream(stream)),
+           "iefwd_test_decode_attention")
 
 
 def test_cu_probe(n_groups: int, out, stream=None) -> None:

@@ -52,7 +52,7 @@ __device__ inline bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, 
 template <int DH, bool CAUSAL>
 __global__ __launch_bounds__(kThreads) void attention_kernel(
     const bf16_t *__restrict__ Q, const bf16_t *__restrict__ K, const bf16_t *__restrict__ Vt,
-    bf16_t *__restrict__ ctx, int n_heads, int seq, int seq_pad, float scale_log2e) {
+    bf16_t *__restrict__ ctx, int n_heads, int seq, int k_rows, int seq_pad, float scale_log2e) {
     constexpr int KS = DH / 16;              // 16-wide k steps of the QK^T product
     constexpr int DB = DH / 32;              // 32-row dh blocks of the context accumulator
     constexpr int K_STRIDE = DH + 8;         // K chunk row (bf16): 16 consecutive rows in distinct banks
@@ -72,7 +72,7 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(
     const int q0 = qg0 + wave * 32;                      // this wave's first query
     const int bh = blockIdx.y;
     const bf16_t *Qh = Q + (size_t)bh * seq * DH;
-    const bf16_t *Kh = K + (size_t)bh * seq * DH;
+    const bf16_t *Kh = K + (size_t)bh * k_rows * DH;
     const bf16_t *Vh = Vt + (size_t)bh * DH * seq_pad;
 
     const int query = q0 + col;
@@ -236,26 +236,29 @@ __global__ __launch_bounds__(kThreads) void attention_kernel(
 
 template <int DH, bool CAUSAL>
 hipError_t launch(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx, int batch,
-                  int n_heads, int seq, hipStream_t s) {
+                  int n_heads, int seq, int k_rows, int vt_stride, hipStream_t s) {
     const int groups = (seq + 32 * kWaves - 1) / (32 * kWaves);
     const dim3 grid(groups, batch * n_heads), block(kThreads);
     const float scale_log2e = 1.4426950408889634f / sqrtf((float)DH);
-    return launch_kernel(attention_kernel<DH, CAUSAL>, grid, block, s, q, k, vt, ctx, n_heads, seq,
-                         attn_seq_pad(seq), scale_log2e);
+    return launch_kernel(attention_kernel<DH, CAUSAL>, grid, block, s, q, k, vt, ctx, n_heads, seq, k_rows,
+                         vt_stride, scale_log2e);
 }
 
 }  // namespace
 
 hipError_t launch_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx,
                             int batch, int n_heads, int seq, int head_dim, bool causal,
-                            hipStream_t stream) {
+                            hipStream_t stream, int k_rows, int vt_stride) {
     if (batch <= 0 || seq <= 0) return hipSuccess;
+    if (k_rows <= 0) k_rows = seq;
+    if (vt_stride <= 0) vt_stride = attn_seq_pad(seq);
+    if (k_rows < seq || vt_stride < attn_seq_pad(seq) || vt_stride % 64 != 0) return hipErrorInvalidValue;
     if (head_dim == 64)
-        return causal ? launch<64, true>(q, k, vt, ctx, batch, n_heads, seq, stream)
-                      : launch<64, false>(q, k, vt, ctx, batch, n_heads, seq, stream);
+        return causal ? launch<64, true>(q, k, vt, ctx, batch, n_heads, seq, k_rows, vt_stride, stream)
+                      : launch<64, false>(q, k, vt, ctx, batch, n_heads, seq, k_rows, vt_stride, stream);
     if (head_dim == 128)
-        return causal ? launch<128, true>(q, k, vt, ctx, batch, n_heads, seq, stream)
-                      : launch<128, false>(q, k, vt, ctx, batch, n_heads, seq, stream);
+        return causal ? launch<128, true>(q, k, vt, ctx, batch, n_heads, seq, k_rows, vt_stride, stream)
+                      : launch<128, false>(q, k, vt, ctx, batch, n_heads, seq, k_rows, vt_stride, stream);
     return hipErrorInvalidValue;
 }
 

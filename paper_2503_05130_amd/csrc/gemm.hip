@@ -338,8 +338,8 @@ template <class C, Epi EPI>
 __device__ inline void store_tile(const GemmParams &p, const bf16_t *ctile, bool vt_tile, int tid, int nt, int m0,
                                   int n0) {
     if (EPI == Epi::Qkv && vt_tile) {
-        // V^T [B, H, dh, S_pad]: a segment is 8 consecutive tokens of one
-        // (head, column) row, contiguous when S is a multiple of 8
+        // V^T [B, H, dh, vt_stride]: a segment is 8 consecutive tokens of one
+        // (head, column) row, contiguous when seq and pos0 are multiples of 8
         const QkvDst &d = p.qkv;
         constexpr int TG = C::BM / 8;
         for (int sg = tid; sg < C::BN * TG; sg += nt) {
@@ -347,14 +347,14 @@ __device__ inline void store_tile(const GemmParams &p, const bf16_t *ctile, bool
             if (t0 >= p.M) continue;
             const int within = n0 + fl - 2 * d.d_model, head = within / d.head_dim, jj = within - head * d.head_dim;
             const bf16_t *src = ctile + fl * kColStride<C> + (t0 - m0);
-            if (d.seq % 8 == 0) {
-                const int b = t0 / d.seq, sp = t0 - b * d.seq;
-                bf16_t *o = d.vt + (((size_t)b * d.n_heads + head) * d.head_dim + jj) * d.seq_pad + sp;
+            if (d.seq % 8 == 0 && d.pos0 % 8 == 0) {
+                const int b = t0 / d.seq, sp = d.pos0 + t0 - b * d.seq;
+                bf16_t *o = d.vt + (((size_t)b * d.n_heads + head) * d.head_dim + jj) * d.vt_stride + sp;
                 *reinterpret_cast<u32x4 *>(o) = *reinterpret_cast<const u32x4 *>(src);
             } else {
                 for (int e = 0; e < 8 && t0 + e < p.M; ++e) {
-                    const int t = t0 + e, b = t / d.seq, sp = t - b * d.seq;
-                    d.vt[(((size_t)b * d.n_heads + head) * d.head_dim + jj) * d.seq_pad + sp] = src[e];
+                    const int t = t0 + e, b = t / d.seq, sp = d.pos0 + t - b * d.seq;
+                    d.vt[(((size_t)b * d.n_heads + head) * d.head_dim + jj) * d.vt_stride + sp] = src[e];
                 }
             }
         }
@@ -372,7 +372,8 @@ __device__ inline void store_tile(const GemmParams &p, const bf16_t *ctile, bool
             const int which = f / d.d_model, within = f - which * d.d_model;
             const int head = within / d.head_dim, jj = within - head * d.head_dim;
             const int b = t / d.seq, sp = t - b * d.seq;
-            o = (which == 0 ? d.q : d.k) + (((size_t)b * d.n_heads + head) * d.seq + sp) * d.head_dim + jj;
+            o = which == 0 ? d.q + (((size_t)b * d.n_heads + head) * d.seq + sp) * d.head_dim + jj
+                           : d.k + (((size_t)b * d.n_heads + head) * d.k_rows + d.pos0 + sp) * d.head_dim + jj;
         } else {
             o = static_cast<bf16_t *>(p.out) + (size_t)t * p.N + f;
         }

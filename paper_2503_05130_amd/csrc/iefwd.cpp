@@ -96,7 +96,9 @@ DeviceInfo query_device(int device) {
 void validate_config(const iefwd_config &c) {
     if (c.abi_version != IEFWD_ABI_VERSION) fail(IEFWD_EVERSION, "config.abi_version mismatch");
     auto bad = [](const char *m) { fail(IEFWD_EINVAL, m); };
-    if (c.reserved0 != 0) bad("config.reserved0 must be 0");
+    if (c.kv_cache > 1) bad("kv_cache must be 0 or 1");
+    if (c.kv_cache && !(c.pre_ln && c.causal)) bad("kv_cache (decode) needs pre_ln = 1 and causal = 1");
+    if (c.kv_cache && c.max_seq > 8192) bad("kv_cache needs max_seq <= 8192");
     if (c.n_layers < 1 || c.n_layers > 4096) bad("n_layers must be in [1, 4096]");
     if (c.d_model < 128 || c.d_model > 4096 || c.d_model % 128 != 0) bad("d_model must be a multiple of 128 in [128, 4096]");
     if (c.n_heads < 1 || c.d_model % c.n_heads != 0) bad("n_heads must divide d_model");
@@ -140,6 +142,11 @@ struct iefwd_instance {
     void *wsblob = nullptr;
     float *h = nullptr, *z = nullptr, *z2 = nullptr, *h1 = nullptr, *out = nullptr, *xstage = nullptr;
     float *stats1 = nullptr, *stats2 = nullptr;   // per-row {mean, rstd} of post-LN LayerNorms
+    // KV cache (kv_cache = 1): per layer K [max_batch, H, max_seq, dh] and
+    // V^T [max_batch, H, dh, max_seq rounded up to 64]
+    void *kvblob = nullptr;
+    std::vector<bf16_t *> kcache, vtcache;
+    uint32_t kv_len = 0, kv_batch = 0;            // positions and sequences the cache holds
     bf16_t *hb = nullptr, *h1b = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr, *ctx = nullptr,
            *u = nullptr;
 
@@ -233,23 +240,39 @@ void collect_timings(iefwd_instance *inst) {
 }
 
 // The forward pass of one batch on inst->stream.  x: fp32 [T, d] device.
-void run_forward(iefwd_instance *I, const float *x) {
+// decode_pos >= 0: one new token per sequence (I->seq == 1) at that position:
+// its K and V are appended to the KV cache and it attends to positions
+// 0 .. decode_pos.
+void run_forward(iefwd_instance *I, const float *x, int decode_pos = -1) {
     const iefwd_config &c = I->cfg;
     const int T = (int)(I->batch * I->seq), d = (int)c.d_model, F = (int)c.d_ff;
     const int H = (int)c.n_heads, dh = (int)I->head_dim, S = (int)I->seq, B = (int)I->batch;
     const float eps = c.ln_eps;
     hipStream_t s = I->stream;
-    QkvDst qd{I->q, I->k, I->vt, S, attn_seq_pad(S), H, dh, d};
+    // K and V go to the layer's KV cache when the instance keeps one (for
+    // iefwd_decode), else to the per-batch buffers
+    const int kv_rows = (int)c.max_seq, kv_stride = attn_seq_pad((int)c.max_seq);
+    const bool decode = decode_pos >= 0;
+    auto qkv_dst = [&](int l) {
+        return c.kv_cache ? QkvDst{I->q, I->kcache[l], I->vtcache[l], S, decode ? decode_pos : 0, kv_rows,
+                                   kv_stride, H, dh, d}
+                          : QkvDst{I->q, I->k, I->vt, S, 0, S, attn_seq_pad(S), H, dh, d};
+    };
 
     // QKV projection, attention and the output projection with its residual:
     // either a plain fp32 residual or one rebuilt from LayerNorm row statistics.
-    auto attention_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid,
+    auto attention_block = [&](int l, const bf16_t *y_bf16, const LayerWeights &w, const float *resid,
                                const LnResid *ln_resid, float *dst) {
+        const QkvDst qd = qkv_dst(l);
         launch(I, IEFWD_K_QKV, "qkv gemm", [&] {
             return launch_gemm(Epi::Qkv, y_bf16, w.wqkv, w.bqkv, nullptr, nullptr, T, 3 * d, d, &qd, s);
         });
         launch(I, IEFWD_K_ATTN, "attention", [&] {
-            return launch_attention(I->q, I->k, I->vt, I->ctx, B, H, S, dh, c.causal != 0, s);
+            if (decode)
+                return launch_decode_attention(I->q, qd.k, qd.vt, I->ctx, B, H, decode_pos + 1, dh, qd.k_rows,
+                                               qd.vt_stride, s);
+            return launch_attention(I->q, qd.k, qd.vt, I->ctx, B, H, S, dh, c.causal != 0, s, qd.k_rows,
+                                    qd.vt_stride);
         });
         launch(I, IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
             return launch_gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->ctx, w.wo, w.bo, resid, dst,
@@ -285,11 +308,11 @@ void run_forward(iefwd_instance *I, const float *x) {
         for (int l = 0; l < L; ++l) {
             const LayerWeights &w = I->layers[l];
             if (l == 0) {
-                attention_block(I->hb, w, x, nullptr, I->z);
+                attention_block(l, I->hb, w, x, nullptr, I->z);
             } else {
                 const LayerWeights &prev = I->layers[l - 1];
                 const LnResid r2{I->z2, I->stats2, prev.g2, prev.be2};
-                attention_block(I->hb, w, nullptr, &r2, I->z);
+                attention_block(l, I->hb, w, nullptr, &r2, I->z);
             }
             ln(I->z, w.g1, w.be1, nullptr, I->h1b, I->stats1);
             const LnResid r1{I->z, I->stats1, w.g1, w.be1};
@@ -307,7 +330,7 @@ void run_forward(iefwd_instance *I, const float *x) {
         for (int l = 0; l < L; ++l) {
             const LayerWeights &w = I->layers[l];
             ln(xcur, w.g1, w.be1, nullptr, I->hb, nullptr);
-            attention_block(I->hb, w, xcur, nullptr, I->h1);
+            attention_block(l, I->hb, w, xcur, nullptr, I->h1);
             ln(I->h1, w.g2, w.be2, nullptr, I->hb, nullptr);
             ffn_block(I->hb, w, I->h1, nullptr, I->h);
             xcur = I->h;
@@ -444,6 +467,21 @@ void alloc_workspace(iefwd_instance *I) {
     I->vt = reinterpret_cast<bf16_t *>(b + o_vt);
     I->ctx = reinterpret_cast<bf16_t *>(b + o_ctx);
     I->u = reinterpret_cast<bf16_t *>(b + o_u);
+
+    if (c.kv_cache) {
+        const size_t kbytes = round_up((size_t)c.max_batch * d * c.max_seq * 2, 256);
+        const size_t vbytes = round_up((size_t)c.max_batch * d * spad * 2, 256);
+        if (hipMalloc(&I->kvblob, (kbytes + vbytes) * c.n_layers) != hipSuccess) {
+            (void)hipGetLastError();
+            I->kvblob = nullptr;
+            fail(IEFWD_ENOMEM, "device allocation of the KV cache failed");
+        }
+        char *kv = static_cast<char *>(I->kvblob);
+        for (uint32_t l = 0; l < c.n_layers; ++l) {
+            I->kcache.push_back(reinterpret_cast<bf16_t *>(kv + l * (kbytes + vbytes)));
+            I->vtcache.push_back(reinterpret_cast<bf16_t *>(kv + l * (kbytes + vbytes) + kbytes));
+        }
+    }
 }
 
 void apply_pending_quota(iefwd_instance *I) {
@@ -480,6 +518,7 @@ iefwd_instance::~iefwd_instance() {
     for (hipEvent_t e : {ev_start, ev_end, ev_copy})
         if (e) (void)hipEventDestroy(e);
     if (wsblob) (void)hipFree(wsblob);
+    if (kvblob) (void)hipFree(kvblob);
     if (wblob) (void)hipFree(wblob);
 }
 
@@ -624,6 +663,42 @@ int iefwd_submit(iefwd_instance *inst, const float *x, uint32_t batch, uint32_t 
             hip_check(hipEventRecord(inst->ev_end, inst->stream), "hipEventRecord");
             inst->state = iefwd_instance::State::InFlight;
             inst->have_batch = true;
+            inst->kv_len = inst->cfg.kv_cache ? seq : 0;
+            inst->kv_batch = inst->cfg.kv_cache ? batch : 0;
+        });
+    });
+}
+
+int iefwd_decode(iefwd_instance *inst, const float *x, uint32_t batch, uint32_t pos, int x_is_device) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!x) fail(IEFWD_EINVAL, "x is NULL");
+        if (!inst->cfg.kv_cache) fail(IEFWD_ESTATE, "the instance keeps no KV cache (config.kv_cache = 0)");
+        if (inst->state == iefwd_instance::State::InFlight)
+            fail(IEFWD_ESTATE, "a batch is already in flight; call iefwd_wait or iefwd_read_logits first");
+        if (inst->kv_len == 0) fail(IEFWD_ESTATE, "no prompt in the KV cache: call iefwd_submit first");
+        if (batch < 1 || batch > inst->kv_batch) fail(IEFWD_EINVAL, "batch out of range [1, sequences in the cache]");
+        if (pos > inst->kv_len || pos >= inst->cfg.max_seq)
+            fail(IEFWD_EINVAL, "pos must be <= the cached length and < max_seq");
+        on_device(inst, [&] {
+            apply_pending_quota(inst);
+            inst->batch = batch;
+            inst->seq = 1;
+            const size_t n = (size_t)batch * inst->cfg.d_model;
+            const float *xin = x;
+            if (!x_is_device) {
+                hip_check(hipMemcpyAsync(inst->xstage, x, n * 4, hipMemcpyHostToDevice, inst->stream), "input copy");
+                hip_check(hipEventRecord(inst->ev_copy, inst->stream), "hipEventRecord");
+                hip_check(hipEventSynchronize(inst->ev_copy), "hipEventSynchronize");
+                xin = inst->xstage;
+            }
+            hip_check(hipEventRecord(inst->ev_start, inst->stream), "hipEventRecord");
+            run_forward(inst, xin, (int)pos);
+            hip_check(hipEventRecord(inst->ev_end, inst->stream), "hipEventRecord");
+            inst->state = iefwd_instance::State::InFlight;
+            inst->have_batch = true;
+            inst->kv_len = pos + 1;
+            inst->kv_batch = batch;
         });
     });
 }
@@ -876,12 +951,12 @@ int iefwd_test_gemm_qkv(const void *a, const void *w, const void *bias, void *q,
         if (!a || !w || !bias || !q || !k || !vt) fail(IEFWD_EINVAL, "NULL pointer");
         if (d_model == 0 || d_model % 64 || n_heads == 0 || d_model % n_heads) fail(IEFWD_EINVAL, "bad d_model / n_heads");
         const uint32_t dh = d_model / n_heads;
-        if (dh % 4) fail(IEFWD_EINVAL, "head dim must be a multiple of 4");
+        if (dh % 8) fail(IEFWD_EINVAL, "head dim must be a multiple of 8");
         if (batch == 0 || seq == 0) fail(IEFWD_EINVAL, "empty batch");
         const uint64_t M = (uint64_t)batch * seq;
         if (M * d_model >= (1ull << 31)) fail(IEFWD_EINVAL, "too large");
-        QkvDst qd{(bf16_t *)q, (bf16_t *)k, (bf16_t *)vt, (int)seq, attn_seq_pad((int)seq), (int)n_heads, (int)dh,
-                  (int)d_model};
+        QkvDst qd{(bf16_t *)q, (bf16_t *)k, (bf16_t *)vt, (int)seq, 0, (int)seq, attn_seq_pad((int)seq),
+                  (int)n_heads, (int)dh, (int)d_model};
         hip_check(launch_gemm(Epi::Qkv, (const bf16_t *)a, (const bf16_t *)w, (const bf16_t *)bias, nullptr, nullptr,
                               (int)M, (int)(3 * d_model), (int)d_model, &qd, (hipStream_t)stream),
                   "qkv gemm launch");
@@ -921,6 +996,22 @@ int iefwd_test_ln_head(const float *z, const float *gamma, const float *beta, co
         hip_check(launch_ln_head(z, gamma, beta, (const bf16_t *)wh, (const bf16_t *)bh, logits, (int)rows, (int)d,
                                  (int)n_out, eps, (hipStream_t)stream),
                   "ln_head launch");
+    });
+}
+
+int iefwd_test_decode_attention(const void *q, const void *k, const void *vt, void *ctx, uint32_t batch,
+                                uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
+                                uint32_t vt_stride, void *stream) {
+    return guarded([&] {
+        if (!q || !k || !vt || !ctx) fail(IEFWD_EINVAL, "NULL pointer");
+        if (batch == 0 || n_heads == 0 || (uint64_t)batch * n_heads > 65535) fail(IEFWD_EINVAL, "bad batch / heads");
+        if (head_dim != 64 && head_dim != 128) fail(IEFWD_EINVAL, "head_dim must be 64 or 128");
+        if (n_keys == 0 || n_keys > 8192 || k_rows < n_keys || vt_stride < n_keys || vt_stride % 64)
+            fail(IEFWD_EINVAL, "need 1 <= n_keys <= 8192, k_rows >= n_keys, vt_stride >= n_keys and % 64 == 0");
+        hip_check(launch_decode_attention((const bf16_t *)q, (const bf16_t *)k, (const bf16_t *)vt, (bf16_t *)ctx,
+                                          (int)batch, (int)n_heads, (int)n_keys, (int)head_dim, (int)k_rows,
+                                          (int)vt_stride, (hipStream_t)stream),
+                  "decode attention launch");
     });
 }
 

@@ -52,10 +52,18 @@ struct LnResid {
 };
 
 // Destination of the QKV epilogue.
+// Where the QKV epilogue puts each token's Q, K and V.  Token t of a launch is
+// position pos0 + t % seq of sequence t / seq.  Q goes to the per-launch
+// buffer [B, H, seq, dh]; K and V^T go to buffers that may be a KV cache:
+// K [B, H, k_rows, dh] at row pos0 + t % seq, V^T [B, H, dh, vt_stride] at
+// column pos0 + t % seq.  A prefill without a cache has pos0 = 0,
+// k_rows = seq, vt_stride = S rounded up to a multiple of 64.
 struct QkvDst {
     bf16_t *q, *k, *vt;
-    int seq;       // S
-    int seq_pad;   // row stride of V^T (S rounded up to a multiple of 64)
+    int seq;        // tokens per sequence in this launch
+    int pos0;       // position of the launch's first token of each sequence
+    int k_rows;     // rows of K per (batch, head)
+    int vt_stride;  // row stride of V^T (a multiple of 64)
     int n_heads;
     int head_dim;
     int d_model;
@@ -71,9 +79,18 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
                        const QkvDst *qkv, hipStream_t stream, const LnResid *ln = nullptr);
 
 // ctx bf16 [B, S, H*dh] from Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad].
+// k_rows: rows of K per (batch, head) (0: seq); vt_stride: row stride of V^T
+// (0: seq rounded up to 64), so that K and V^T may live in a longer KV cache.
 hipError_t launch_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx,
                             int batch, int n_heads, int seq, int head_dim, bool causal,
-                            hipStream_t stream);
+                            hipStream_t stream, int k_rows = 0, int vt_stride = 0);
+
+// Attention of one new query per (batch, head) over keys 0 .. n_keys - 1 of a
+// KV cache: q bf16 [B, H, dh], K [B, H, k_rows, dh], V^T [B, H, dh, vt_stride];
+// ctx bf16 [B, H * dh].  fp32 scores, softmax and sums.  n_keys <= 8192.
+hipError_t launch_decode_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx,
+                                   int batch, int n_heads, int n_keys, int head_dim, int k_rows,
+                                   int vt_stride, hipStream_t stream);
 
 // Row LayerNorm, d % 128 == 0, d <= 4096.  out_f32 / out_bf16 / stats may be
 // null; stats receives {mean, rstd} per row.

@@ -164,7 +164,9 @@ BASE = dict(n_layers=1, d_model=128, n_heads=2, d_ff=512, max_batch=2, max_seq=3
     (dict(n_layers=0), ie.EINVAL),
     (dict(ln_eps=0.0), ie.EINVAL),
     (dict(w_std=-1.0), ie.EINVAL),
-    (dict(reserved0=1), ie.EINVAL),
+    (dict(kv_cache=2), ie.EINVAL),
+    (dict(kv_cache=1, pre_ln=0), ie.EINVAL),          # decode needs a causal pre-LN stack
+    (dict(kv_cache=1, pre_ln=1, causal=0), ie.EINVAL),
     (dict(max_batch=1 << 16, max_seq=1 << 14), ie.EINVAL),
 ])
 def test_create_rejects_bad_config(bad, status):
@@ -191,6 +193,7 @@ def test_null_arguments():
     assert L.iefwd_destroy(None) == ie.OK
     assert L.iefwd_set_quota(None, 8) == ie.EINVAL
     assert L.iefwd_set_quota_at(None, 8, 0) == ie.EINVAL
+    assert L.iefwd_decode(None, None, 1, 0, 1) == ie.EINVAL
     assert L.iefwd_prepare_quota_at(None, 8, 0) == ie.EINVAL
     assert L.iefwd_submit(None, None, 1, 1, 0) == ie.EINVAL
     assert L.iefwd_wait(None) == ie.EINVAL
@@ -208,6 +211,10 @@ def test_kernel_entry_points_validate_shapes():
     assert L.iefwd_test_gemm(2, p, p, p, None, p, 4, 64, 64, None) == ie.EINVAL   # resid missing
     assert L.iefwd_test_attention(p, p, p, p, 1, 1, 8, 32, 0, None) == ie.EINVAL  # head dim
     assert L.iefwd_test_attention(p, p, p, p, 0, 1, 8, 64, 0, None) == ie.EINVAL  # empty
+    assert L.iefwd_test_decode_attention(p, p, p, p, 1, 1, 8, 32, 8, 64, None) == ie.EINVAL    # head dim
+    assert L.iefwd_test_decode_attention(p, p, p, p, 1, 1, 9000, 64, 9000, 9024, None) == ie.EINVAL  # > 8192 keys
+    assert L.iefwd_test_decode_attention(p, p, p, p, 1, 1, 65, 64, 64, 128, None) == ie.EINVAL  # k_rows < keys
+    assert L.iefwd_test_decode_attention(p, p, p, p, 1, 1, 8, 64, 8, 100, None) == ie.EINVAL   # stride % 64
     assert L.iefwd_test_layernorm(p, p, p, p, None, 4, 100, 1e-5, None) == ie.EINVAL
     assert L.iefwd_test_ln_head(p, p, p, p, p, p, 4, 128, 0, 1e-5, None) == ie.EINVAL
     assert L.iefwd_test_cu_probe(None, 0, p) == ie.EINVAL

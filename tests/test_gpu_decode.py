@@ -1,0 +1,129 @@
+"""Decode phase on the GPU: attention of one new query per (batch, head)
+against a KV cache, and whole decode steps against the fp64 oracle.  A causal
+model's output at position t depends only on tokens 0 .. t, so the oracle runs
+the prompt plus the decoded tokens as one sequence and its output at the new
+position is the reference for the step."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2503_05130_amd as ie
+import workloads as W
+from oracle import forward as F
+from tests.gpu_util import DEV, bf16_round, compare, f64, instance_config, sync, to_dev
+
+pytestmark = pytest.mark.gpu
+
+UBF = 2.0 ** -8
+U32 = 2.0 ** -24
+MAX_ABS, REL_L2 = 2e-2, 1e-2
+NAN_BF16 = 0x7FC0
+
+
+def check(got, ref, what=""):
+    ma, rl = compare(got, ref)
+    print(f"  {what}: max_abs={ma:.3e} rel_l2={rl:.3e}", flush=True)
+    assert np.all(np.isfinite(got))
+    assert ma <= MAX_ABS and rl <= REL_L2, (what, ma, rl)
+
+
+@pytest.mark.parametrize("B,H,n_keys,dh,k_rows,vt_stride", [
+    (1, 1, 1, 64, 1, 64),
+    (2, 3, 7, 64, 16, 64),
+    (3, 2, 513, 64, 600, 640),
+    (2, 16, 1025, 128, 1100, 1152),
+    (1, 4, 8192, 128, 8192, 8192),
+])
+def test_decode_attention_kernel(B, H, n_keys, dh, k_rows, vt_stride):
+    print(f"decode attention B={B} H={H} keys={n_keys} dh={dh}", flush=True)
+    rng = np.random.default_rng(n_keys + dh)
+    q = bf16_round(rng.standard_normal((B, H, dh)))
+    k = bf16_round(rng.standard_normal((B, H, k_rows, dh)))
+    vt = bf16_round(rng.standard_normal((B, H, dh, vt_stride)))
+    # cache positions past n_keys hold arbitrary bits: make them NaN
+    k.view(torch.int16)[:, :, n_keys:, :] = NAN_BF16
+    vt.view(torch.int16)[:, :, :, n_keys:] = NAN_BF16
+    ctx = torch.empty((B, H * dh), dtype=torch.bfloat16, device=DEV)
+    ie.test_decode_attention(to_dev(q), to_dev(k), to_dev(vt), ctx, B, H, n_keys, dh, k_rows, vt_stride)
+    sync()
+    q64, k64, v64 = f64(q), f64(k)[:, :, :n_keys], f64(vt)[..., :n_keys]
+    s = np.einsum("bhd,bhjd->bhj", q64, k64) / np.sqrt(dh)
+    p = F.softmax_rows(s)
+    ref = np.einsum("bhj,bhdj->bhd", p, v64).reshape(B, H * dh)
+    # fp32 dot products and sums over n_keys terms, then one bf16 rounding
+    bound = (dh + 8) * U32 * np.einsum("bhj,bhdj->bhd", p, np.abs(v64)).reshape(B, H * dh) * 4 \
+        + (n_keys + 8) * U32 * np.abs(v64).max() + 1e-6
+    got = f64(ctx)
+    assert np.all(np.isfinite(got))
+    err = np.abs(got - ref)
+    tol = 1.01 * UBF * np.abs(ref) + bound
+    worst = np.unravel_index(np.argmax(err - tol), err.shape)
+    assert np.all(err <= tol), (worst, err[worst], tol[worst])
+
+
+DECODERS = [
+    # shape overrides (pre-LN causal), prompt batch, prompt length, decode steps
+    (dict(W.STRESS_INIT, n_layers=2, d_model=256, n_heads=4, d_ff=1024, pre_ln=1, causal=1, n_out=2), 3, 37, 4),
+    (dict(W.STRESS_INIT, n_layers=2, d_model=256, n_heads=2, d_ff=640, pre_ln=1, causal=1, n_out=0), 2, 64, 3),
+    (dict(n_layers=3, d_model=128, n_heads=2, d_ff=512, pre_ln=1, causal=1, n_out=3), 1, 1, 5),
+]
+
+
+@pytest.mark.parametrize("over,B,P,G", DECODERS)
+def test_decode_steps_match_oracle(over, B, P, G):
+    shape = W.model_shape("encoder_l1_d128_s32_b2", **over)
+    d = shape["d_model"]
+    print(f"decode {over} B={B} prompt={P} steps={G}", flush=True)
+    x = W.make_input(7000 + P, B, P + G, d)
+    with ie.Instance(**instance_config(shape, B, P + G + 3), kv_cache=1) as inst:
+        inst.submit(torch.from_numpy(x[:, :P].copy()).to(DEV))
+        check(inst.read_logits(), F.forward(x[:, :P], shape), "prompt")
+        first = None
+        for g in range(G):
+            xt = torch.from_numpy(np.ascontiguousarray(x[:, P + g])).to(DEV)
+            inst.decode(xt, P + g)
+            got = inst.read_logits()
+            assert got.shape == (B, 1, shape["n_out"] or d)
+            check(got[:, 0], F.forward(x[:, :P + g + 1], shape)[:, P + g], f"step {g}")
+            if g == 0:
+                first = got.copy()
+        # rewinding to the first decoded position rewrites the same K and V: same result, bit for bit
+        inst.decode(np.ascontiguousarray(x[:, P]), P)      # host input this time
+        again = inst.read_logits()
+        assert np.array_equal(again.view(np.uint32), first.view(np.uint32))
+
+
+def test_full_size_decoder_decode():
+    name = "decoder_l24_d2048_s1024"
+    shape = W.model_shape(name)
+    B, P, G = 2, 30, 2
+    print(f"decode {name} B={B} prompt={P} steps={G}", flush=True)
+    x = W.make_input(W.WORKLOADS[name]["input_seed"], B, P + G, shape["d_model"])
+    with ie.Instance(**instance_config(shape, B, 1024), kv_cache=1) as inst:
+        inst.submit(torch.from_numpy(x[:, :P].copy()).to(DEV))
+        inst.wait()
+        for g in range(G):
+            inst.decode(torch.from_numpy(np.ascontiguousarray(x[:, P + g])).to(DEV), P + g)
+            got = inst.read_logits()
+            check(got[:, 0], F.forward(x[:, :P + g + 1], shape)[:, P + g], f"step {g}")
+
+
+def test_decode_state_errors():
+    shape = W.model_shape("encoder_l1_d128_s32_b2", pre_ln=1, causal=1, n_out=2)
+    x = W.make_input(1, 2, 8, 128)
+    with ie.Instance(**instance_config(shape, 2, 16)) as plain:
+        with pytest.raises(ie.IefwdError) as e:
+            plain.decode(x[:, 0], 0)                        # no KV cache
+        assert e.value.status == ie.ESTATE
+    with ie.Instance(**instance_config(shape, 2, 16), kv_cache=1) as inst:
+        with pytest.raises(ie.IefwdError) as e:
+            inst.decode(x[:, 0], 0)                         # no prompt yet
+        assert e.value.status == ie.ESTATE
+        inst.submit(x[:, :5].copy())
+        inst.wait()
+        for bad_pos, bad_x in ((6, x[:, 5]), (16, x[:, 5]), (5, np.zeros((3, 128), np.float32))):
+            with pytest.raises(ie.IefwdError) as e:
+                inst.decode(np.ascontiguousarray(bad_x), bad_pos)   # past the cache, past max_seq, batch > prompt's
+            assert e.value.status == ie.EINVAL
+        inst.decode(np.ascontiguousarray(x[:1, 5]), 5)          # fewer sequences than the prompt: fine
+        assert inst.read_logits().shape == (1, 1, 2)
