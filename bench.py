@@ -8,7 +8,7 @@ weights, fp32 N(0,1) input embeddings already resident in HBM, full 256-CU
 quota.
 
 Prints one JSON line: inferences/s (one inference = one sequence), the
-forward-level MFMA utilisation, the roofline of the dominant kernel (FFN-up
+forward-level MFMA utilisation, the roofline of the dominant kernel (FFN-down
 GEMM + bias + LayerNorm residual: each launch in the timed region records its own
 start and end into HIP events), the aggregate throughput of two co-located instances at
 CU quotas 64/192, 128/128 and 192/64 against one alone, and the fp64 CPU oracle
@@ -16,6 +16,7 @@ timed on a bounded sample, and the per-batch cost of re-masking the
 instance's stream between batches.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-colocated] [--no-remask]
+                  [--decode | --decode-only]
 """
 from __future__ import annotations
 
@@ -164,6 +165,55 @@ def remask_overhead(inst, x, n=40):
             "overhead_pct": round((alt - base) / base * 100, 2)}
 
 
+def decode_leg(ie, W, batch=2, prompt=512, steps=64):
+    """Decode phase of the d = 2048 causal decoder (24 layers, 16 heads, FFN
+    8192): a prompt of `prompt` tokens per sequence, then `steps` decode steps
+    of one token per sequence (fresh synthetic embeddings each step).  Time per
+    output token (TPOT) is the mean device time of a step; the roofline counts
+    the bytes a step must read (every weight once, the KV cache up to the
+    position) against 8 TB/s."""
+    import torch
+
+    name = "decoder_l24_d2048_s1024"
+    shape = W.model_shape(name)
+    d, L, F_, H = shape["d_model"], shape["n_layers"], shape["d_ff"], shape["n_heads"]
+    cfg = {k: shape[k] for k in ("n_layers", "d_model", "n_heads", "d_ff", "pre_ln", "causal", "n_out",
+                                 "ln_eps", "w_std", "b_std", "ln_std", "qk_std", "seed")}
+    inst = ie.Instance(device=0, max_batch=batch, max_seq=prompt + steps, kv_cache=1, **cfg)
+    rng = np.random.default_rng(9100)
+    xp = torch.from_numpy(rng.standard_normal((batch, prompt, d), dtype=np.float32)).to("cuda:0")
+    xs = torch.from_numpy(rng.standard_normal((steps, batch, d), dtype=np.float32)).to("cuda:0")
+    kinds = {"qkv": ie.K_QKV, "attn": ie.K_ATTN, "out": ie.K_OUTPROJ, "ffn1": ie.K_FFN1, "ffn2": ie.K_FFN2,
+             "ln": ie.K_LN}
+    ms = []
+    for rep in range(3):                      # warm-up, TPOT, per-kernel-class times
+        inst.submit(xp)
+        inst.wait()
+        if rep == 2:
+            for k in kinds.values():
+                inst.time_kernel(k, True)
+        for g in range(steps):
+            inst.decode(xs[g], prompt + g)
+            inst.wait()
+            if rep == 1:
+                ms.append(inst.last_batch_ms())
+    per = {}
+    for nm, k in kinds.items():
+        t, n = inst.kernel_time(k)
+        inst.time_kernel(k, False)
+        per[nm] = round(t * 1e3 / steps, 2)        # us per step
+    inst.close()
+    tpot = float(np.mean(ms))
+    wbytes = L * 2 * (3 * d * d + d * d + 2 * d * F_) + L * 2 * 4 * (2 * d) + 2 * 4 * d
+    kvbytes = sum(L * batch * 2 * (prompt + g + 1) * d * 2 for g in range(steps)) / steps
+    gbs = (wbytes + kvbytes) / (tpot * 1e-3) / 1e9
+    return {"workload": f"{name} decode, batch {batch}, prompt {prompt}, {steps} steps", "tpot_ms": round(tpot, 4),
+            "tokens_per_s": round(batch / (tpot * 1e-3), 1),
+            "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": 8000.0, "unit": "GB/s",
+                         "frac": round(gbs / 8000.0, 4), "bytes_per_step": round(wbytes + kvbytes)},
+            "us_per_step": per}
+
+
 def copy_calibration(mib: int) -> None:
     """A plain device-to-device copy of `mib` MiB, for scaling the FETCH_SIZE /
     WRITE_SIZE counters of a profiling run (read once, written once)."""
@@ -187,6 +237,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-colocated", action="store_true")
     ap.add_argument("--no-remask", action="store_true")
+    ap.add_argument("--decode", action="store_true", help="also time the decode phase of the d=2048 decoder")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="time only the decode phase (a profiling aid: prints {\"decode\": ...})")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -202,6 +255,9 @@ def main() -> int:
 
     if args.copy_calibration_mib:
         copy_calibration(args.copy_calibration_mib)
+    if args.decode_only:
+        print(json.dumps({"decode": decode_leg(ie, W)}))
+        return 0
     w = W.WORKLOADS[WORKLOAD]
     shape = W.model_shape(WORKLOAD)
     B, S = args.batch, w["seq"]
@@ -272,6 +328,8 @@ def main() -> int:
     inst.close()
     if not args.no_colocated:
         result["colocated"] = colocated(ie, W, shape, cfg, [(64, 192), (128, 128), (192, 64)])
+    if args.decode:
+        result["decode"] = decode_leg(ie, W)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(shape, args.cpu_sample)
     print(json.dumps(result))

@@ -333,6 +333,19 @@ int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void 
                     const float *resid, void *out, uint32_t M, uint32_t N, uint32_t K,
                     void *stream);
 
+/* The decode-step product for M <= 16 activation rows: the same operands and
+ * epilogues as iefwd_test_gemm, N % 16 == 0, K % 32 == 0.  Its K summation
+ * order differs from iefwd_test_gemm's (bound by reading W once, not by the
+ * matrix cores).  ln_z non-NULL: the activations are LayerNorm(z) instead of a
+ * (a is then ignored): z f32 [M, K], ln_gamma / ln_beta f32 [K], row
+ * statistics in fp32, the normalised rows rounded to bf16; needs M * K <=
+ * 16384 (EINVAL otherwise).  This is how a pre-LN block's LayerNorm is fused
+ * into its QKV and FFN-up products during decode. */
+int iefwd_test_gemm_skinny(uint32_t epilogue, const void *a, const void *w, const void *bias,
+                           const float *resid, void *out, uint32_t M, uint32_t N, uint32_t K,
+                           const float *ln_z, const float *ln_gamma, const float *ln_beta, float ln_eps,
+                           void *stream);
+
 /* QKV projection with head scatter: A bf16 [batch*seq, d], W bf16 [3d, d],
  * bias bf16 [3d].  Writes Q and K as bf16 [batch, heads, seq, dh] and V
  * transposed as bf16 [batch, heads, dh, seq_pad], seq_pad = seq rounded up to
@@ -365,7 +378,10 @@ int iefwd_test_ln_head(const float *z, const float *gamma, const float *beta,
  * against keys 0 .. n_keys - 1 of K bf16 [batch, heads, k_rows, dh] and
  * V^T bf16 [batch, heads, dh, vt_stride] (columns >= n_keys may hold any
  * bits); ctx bf16 [batch, heads * dh].  dh in {64, 128}, 1 <= n_keys <= 8192,
- * k_rows >= n_keys, vt_stride >= n_keys and a multiple of 64. */
+ * k_rows >= n_keys, vt_stride >= n_keys and a multiple of 64,
+ * batch * heads <= 65535.  The keys are split into chunks (64 keys up to 2048,
+ * else 256) whose partial results a second kernel combines; the call
+ * allocates that scratch and returns after the stream has drained. */
 int iefwd_test_decode_attention(const void *q, const void *k, const void *vt, void *ctx, uint32_t batch,
                                 uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
                                 uint32_t vt_stride, void *stream);

@@ -61,6 +61,7 @@ SIGNATURES = {
     "iefwd_last_error": (ctypes.c_char_p, []),
     "iefwd_status_string": (ctypes.c_char_p, [_i32]),
     "iefwd_test_gemm": (_i32, [_u32, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp]),
+    "iefwd_test_gemm_skinny": (_i32, [_u32, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp, _vp, _vp, _f32, _vp]),
     "iefwd_test_gemm_qkv": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _vp]),
     "iefwd_test_attention": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _i32, _vp]),
     "iefwd_test_layernorm": (_i32, [_vp, _vp, _vp, _vp, _vp, _u32, _u32, _f32, _vp]),
@@ -301,6 +302,13 @@ class Instance:
 def test_gemm(epilogue, a, w, bias, resid, out, M, N, K, stream=None) -> None:
     _check(lib().iefwd_test_gemm(epilogue, _ptr(a), _ptr(w), _ptr(bias), _ptr(resid), _ptr(out), M, N, K,
                                  _stream(stream)), "iefwd_test_gemm")
+
+
+def test_gemm_skinny(epilogue, a, w, bias, resid, out, M, N, K, ln=None, stream=None) -> None:
+    """ln: None, or (z, gamma, beta, eps) to take the activations as LayerNorm(z)."""
+    z, g, b, eps = ln if ln is not None else (None, None, None, 0.0)
+    _check(lib().iefwd_test_gemm_skinny(epilogue, _ptr(a), _ptr(w), _ptr(bias), _ptr(resid), _ptr(out), M, N, K,
+                                        _ptr(z), _ptr(g), _ptr(b), eps, _stream(stream)), "iefwd_test_gemm_skinny")
 
 
 def test_gemm_qkv(a, w, bias, q, k, vt, batch, seq, d_model, n_heads, stream=None) -> None:

@@ -53,6 +53,7 @@ struct GemmParams {
     int tiles_m, tiles_n;
     QkvDst qkv;
     LnResid ln;
+    LnIn lnin;
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs.  Renumber them so
@@ -86,6 +87,12 @@ __device__ inline bf16_t f32_to_bf16(float f) {
 
 __device__ inline uint32_t pack2(float lo, float hi) {
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+    return v;
 }
 
 // GELU(u) = u/2 (1 + erf(u / sqrt 2)), with erf from Abramowitz & Stegun,
@@ -531,6 +538,170 @@ hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
     return hipErrorInvalidValue;
 }
 
+// ---------------------------------------------------------------- skinny GEMM (decode)
+//
+// M <= 16 token rows (one decode step of a batch): the product is bound by
+// reading W once, so what matters is how many weight bytes are in flight on
+// how many CUs.  A workgroup of 8 waves owns 16 / G output features and the
+// whole of K, cut into G equal K-groups that one MFMA works on side by side:
+// operand row (g, f) holds feature f's weights of K-group g, operand column
+// (g, t) token t's activations of K-group g, and the diagonal blocks of the
+// 16 x 16 product (row group == column group) are the per-group partial sums,
+// added over g at the end (the off-diagonal blocks are discarded).  G = 1, 2
+// or 4 (up to 16 / G tokens) is picked so that N / (16 / G) gives about 512
+// workgroups.  The waves split the K steps (wave w takes w, w + 8, ...); each
+// lane loads its weight and activation fragments straight into registers (16
+// bytes each; token columns past M repeat the last row and are never stored),
+// 8 K steps deep.  The waves' partial sums are added in wave order through
+// LDS, then the K-groups in group order through lane shuffles: the summation
+// order depends on N, K and G only.
+//
+// LNA: the activations are LayerNorm(z) of fp32 rows z (a pre-LN block's
+// input), normalised by the workgroup itself into LDS as bf16 -- row
+// statistics two-pass with a fixed butterfly, one wave per row, then
+// y = fma(gamma, (z - mean) * rstd, beta) -- while the first weight
+// fragments are already in flight.  Needs M * K <= kSkinnyLnElems.
+constexpr int kSkinnyWaves = 8, kSkinnyUnroll = 8;
+constexpr int kSkinnyLnElems = 16384;
+constexpr int kSkinnyTargetGroups = 512;
+
+// One wave per row; three passes over the row (the second and third hit the
+// cache): sum -> mean, squared deviations -> rstd, normalise -> LDS.
+__device__ inline void skinny_ln_prologue(const GemmParams &p, bf16_t *a_lds, int lane, int wave) {
+    const int nv = p.K / 4;                   // f32x4 vectors per row; lane owns c * 64 + lane
+    const float inv_k = 1.0f / (float)p.K;
+    const f32x4 *g4 = reinterpret_cast<const f32x4 *>(p.lnin.gamma);
+    const f32x4 *b4 = reinterpret_cast<const f32x4 *>(p.lnin.beta);
+    for (int r = wave; r < p.M; r += kSkinnyWaves) {
+        const f32x4 *zr = reinterpret_cast<const f32x4 *>(p.lnin.z + (size_t)r * p.K);
+        float s = 0.f;
+#pragma unroll 4
+        for (int i = lane; i < nv; i += 64) {
+            const f32x4 v = zr[i];
+            s += v[0] + v[1] + v[2] + v[3];
+        }
+        const float mean = wave_sum(s) * inv_k;
+        float ss = 0.f;
+#pragma unroll 4
+        for (int i = lane; i < nv; i += 64) {
+            const f32x4 v = zr[i];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float d = v[e] - mean;
+                ss += d * d;
+            }
+        }
+        const float rstd = 1.0f / sqrtf(wave_sum(ss) * inv_k + p.lnin.eps);
+#pragma unroll 4
+        for (int i = lane; i < nv; i += 64) {
+            const f32x4 v = zr[i], g = g4[i], b = b4[i];
+            float y[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) y[e] = __builtin_fmaf(g[e], (v[e] - mean) * rstd, b[e]);
+            *reinterpret_cast<u32x2 *>(a_lds + (size_t)r * p.K + 4 * i) = u32x2{pack2(y[0], y[1]), pack2(y[2], y[3])};
+        }
+    }
+}
+
+template <Epi EPI, int G, bool LNA>
+__global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p) {
+    constexpr int NW = kSkinnyWaves;
+    constexpr int FPW = 16 / G, TPW = 16 / G;      // features and token columns per K-group
+    constexpr int kPartBytes = (NW - 1) * 64 * 16;
+    constexpr int kLdsBytes = LNA && kSkinnyLnElems * 2 > kPartBytes ? kSkinnyLnElems * 2 : kPartBytes;
+    __shared__ __attribute__((aligned(16))) char lds[kLdsBytes];
+    f32x4 (*part)[64] = reinterpret_cast<f32x4 (*)[64]>(lds);
+    bf16_t *a_lds = reinterpret_cast<bf16_t *>(lds);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int n0 = blockIdx.x * FPW;
+    const int row = lane & 15, chunk = lane >> 4;               // operand row / column, 8-element K chunk
+    const int kg = p.K / G;                                     // K-group length
+    const int grp = row / FPW;                                  // K-group of this lane's row and column
+    const int wf_row = n0 + row % FPW, a_row = min(row % TPW, p.M - 1);
+    const bf16_t *wrow = p.w + (size_t)wf_row * p.K + grp * kg + chunk * 8;
+    const bf16_t *arow = (LNA ? a_lds : p.a) + (size_t)a_row * p.K + grp * kg + chunk * 8;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    const int steps = kg / 32;
+    bf16x8 wf[kSkinnyUnroll], af[kSkinnyUnroll];
+    // Fragments past the wave's last K step are not loaded but zero-filled, and
+    // every MFMA runs: a skipped step adds exactly zero.  (A conditional MFMA
+    // may be issued with the wave's EXEC mask empty, which does not stop it
+    // from reading its operand registers.)
+    const bf16x8 zero = {};
+    auto load_w = [&](int s0) {
+#pragma unroll
+        for (int u = 0; u < kSkinnyUnroll; ++u)
+            wf[u] = s0 + u * NW < steps ? *reinterpret_cast<const bf16x8 *>(wrow + (s0 + u * NW) * 32) : zero;
+    };
+    load_w(wave);                                              // first weights in flight ...
+    if constexpr (LNA) {
+        skinny_ln_prologue(p, a_lds, lane, wave);              // ... while the activations are normalised
+        __syncthreads();
+    }
+    for (int s0 = wave; s0 < steps; s0 += NW * kSkinnyUnroll) {
+#pragma unroll
+        for (int u = 0; u < kSkinnyUnroll; ++u)
+            af[u] = s0 + u * NW < steps ? *reinterpret_cast<const bf16x8 *>(arow + (s0 + u * NW) * 32) : zero;
+#pragma unroll
+        for (int u = 0; u < kSkinnyUnroll; ++u) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[u], af[u], acc, 0, 0, 0);
+        if (s0 + NW * kSkinnyUnroll < steps) load_w(s0 + NW * kSkinnyUnroll);
+    }
+    if constexpr (LNA) __syncthreads();                        // the partials reuse the activations' LDS
+    if (wave > 0) part[wave - 1][lane] = acc;
+    __syncthreads();
+    if (wave > 0) return;
+#pragma unroll
+    for (int w = 0; w < NW - 1; ++w) acc += part[w][lane];
+    // lane l holds product rows 4 (l / 16) + e, column l % 16.  Output lane
+    // (fq, t) gathers features 4 fq .. 4 fq + 3 of token t from the diagonal
+    // block of every K-group: row g FPW + 4 fq + e, column g TPW + t.
+    const int fq = lane / TPW, t = lane % TPW;
+    if constexpr (G > 1) {
+        f32x4 sum = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const int src = (16 * (g * FPW / 4 + fq) + g * TPW + t) & 63;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) sum[e] += __shfl(acc[e], src);
+        }
+        acc = sum;
+    }
+    if (lane >= (FPW / 4) * TPW || t >= p.M) return;
+    const int f = n0 + 4 * fq;
+    // this lane: features f .. f + 3 of token t
+    const u32x2 braw = *reinterpret_cast<const u32x2 *>(p.bias + f);
+    float v0 = acc[0] + __uint_as_float(braw[0] << 16), v1 = acc[1] + __uint_as_float(braw[0] & 0xffff0000u);
+    float v2 = acc[2] + __uint_as_float(braw[1] << 16), v3 = acc[3] + __uint_as_float(braw[1] & 0xffff0000u);
+    if constexpr (EPI == Epi::BiasBf16 || EPI == Epi::BiasGeluBf16) {
+        if constexpr (EPI == Epi::BiasGeluBf16) {
+            v0 = gelu(v0); v1 = gelu(v1); v2 = gelu(v2); v3 = gelu(v3);
+        }
+        *reinterpret_cast<u32x2 *>(static_cast<bf16_t *>(p.out) + (size_t)t * p.N + f) =
+            u32x2{pack2(v0, v1), pack2(v2, v3)};
+    } else if constexpr (EPI == Epi::BiasResidF32) {
+        const f32x4 r = *reinterpret_cast<const f32x4 *>(p.resid + (size_t)t * p.N + f);
+        *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + (size_t)t * p.N + f) =
+            f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
+    } else if constexpr (EPI == Epi::Qkv) {
+        const QkvDst &d = p.qkv;
+        const int which = f / d.d_model, within = f - which * d.d_model;
+        const int head = within / d.head_dim, jj = within - head * d.head_dim;
+        const int b = t / d.seq, sp = t - b * d.seq;
+        const size_t bh = (size_t)b * d.n_heads + head;
+        if (which < 2) {
+            bf16_t *o = which == 0 ? d.q + (bh * d.seq + sp) * d.head_dim + jj
+                                   : d.k + (bh * d.k_rows + d.pos0 + sp) * d.head_dim + jj;
+            *reinterpret_cast<u32x2 *>(o) = u32x2{pack2(v0, v1), pack2(v2, v3)};
+        } else {
+            bf16_t *o = d.vt + (bh * d.head_dim + jj) * d.vt_stride + d.pos0 + sp;
+            o[0] = f32_to_bf16(v0);
+            o[d.vt_stride] = f32_to_bf16(v1);
+            o[2 * (size_t)d.vt_stride] = f32_to_bf16(v2);
+            o[3 * (size_t)d.vt_stride] = f32_to_bf16(v3);
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
@@ -556,6 +727,55 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
     case Tile::SplitD: return launch_tile<SplitD, true>(epi, p, stream);
     }
     return hipErrorInvalidValue;
+}
+
+namespace {
+
+template <int G, bool LNA>
+hipError_t launch_skinny(Epi epi, const GemmParams &p, hipStream_t stream) {
+    const dim3 grid(p.N / (16 / G)), block(64 * kSkinnyWaves);
+    switch (epi) {
+    case Epi::BiasBf16: return launch_kernel(skinny_kernel<Epi::BiasBf16, G, LNA>, grid, block, stream, p);
+    case Epi::BiasGeluBf16: return launch_kernel(skinny_kernel<Epi::BiasGeluBf16, G, LNA>, grid, block, stream, p);
+    case Epi::BiasResidF32: return launch_kernel(skinny_kernel<Epi::BiasResidF32, G, LNA>, grid, block, stream, p);
+    case Epi::Qkv: return launch_kernel(skinny_kernel<Epi::Qkv, G, LNA>, grid, block, stream, p);
+    case Epi::BiasLnResidF32: break;
+    }
+    return hipErrorInvalidValue;
+}
+
+template <bool LNA>
+hipError_t launch_skinny_g(Epi epi, const GemmParams &p, hipStream_t stream) {
+    switch (skinny_groups(p.M, p.N, p.K)) {
+    case 1: return launch_skinny<1, LNA>(epi, p, stream);
+    case 2: return launch_skinny<2, LNA>(epi, p, stream);
+    case 4: return launch_skinny<4, LNA>(epi, p, stream);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+int skinny_groups(int M, int N, int K) {
+    int g = 1;
+    while (g < 4 && N / (16 / g) < kSkinnyTargetGroups && M <= 16 / (2 * g) && K % (32 * 2 * g) == 0) g *= 2;
+    return g;
+}
+
+bool skinny_ln_fits(int M, int K) { return M >= 1 && M <= 16 && K % 32 == 0 && M * K <= kSkinnyLnElems; }
+
+hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias, const float *resid,
+                              void *out, int M, int N, int K, const QkvDst *qkv, hipStream_t stream,
+                              const LnIn *ln_in) {
+    if (M <= 0) return hipSuccess;
+    if (M > 16 || N % 16 || K % 32 || epi == Epi::BiasLnResidF32) return hipErrorInvalidValue;
+    if (ln_in && !skinny_ln_fits(M, K)) return hipErrorInvalidValue;
+    GemmParams p{};
+    p.a = a; p.w = w; p.bias = bias; p.resid = resid; p.out = out;
+    p.M = M; p.N = N; p.K = K;
+    if (qkv) p.qkv = *qkv;
+    if (ln_in) p.lnin = *ln_in;
+    return ln_in ? launch_skinny_g<true>(epi, p, stream) : launch_skinny_g<false>(epi, p, stream);
 }
 
 }  // namespace iefwd

@@ -29,6 +29,10 @@ LaunchEvents &armed_launch_events() {
     thread_local LaunchEvents ev;
     return ev;
 }
+uint64_t &launch_count() {
+    thread_local uint64_t n = 0;
+    return n;
+}
 }  // namespace iefwd
 
 namespace {
@@ -147,6 +151,7 @@ struct iefwd_instance {
     void *kvblob = nullptr;
     std::vector<bf16_t *> kcache, vtcache;
     uint32_t kv_len = 0, kv_batch = 0;            // positions and sequences the cache holds
+    float *dec_partials = nullptr;                // decode attention: per-chunk partial results
     bf16_t *hb = nullptr, *h1b = nullptr, *q = nullptr, *k = nullptr, *vt = nullptr, *ctx = nullptr,
            *u = nullptr;
 
@@ -210,18 +215,21 @@ hipEvent_t take_event(iefwd_instance *inst) {
 // the kernel's own start and end timestamps into a pair of events.
 template <class F>
 void launch(iefwd_instance *inst, uint32_t kind, const char *what, F &&f) {
-    inst->kernels_launched += 1;
+    const uint64_t before = launch_count();
     auto &t = inst->timing[kind];
     if (t.enabled) {
-        // the kernel itself records its start and end into these events
+        // the operation's first kernel records its start, its last kernel its end
         hipEvent_t e0 = take_event(inst), e1 = take_event(inst);
         armed_launch_events() = LaunchEvents{e0, e1};
         const hipError_t err = f();
         armed_launch_events() = LaunchEvents{};
+        inst->kernels_launched += launch_count() - before;
         hip_check(err, what);
         t.inflight.emplace_back(e0, e1);
     } else {
-        hip_check(f(), what);
+        const hipError_t err = f();
+        inst->kernels_launched += launch_count() - before;
+        hip_check(err, what);
     }
 }
 
@@ -261,32 +269,43 @@ void run_forward(iefwd_instance *I, const float *x, int decode_pos = -1) {
 
     // QKV projection, attention and the output projection with its residual:
     // either a plain fp32 residual or one rebuilt from LayerNorm row statistics.
+    // decode steps of up to 16 sequences use the skinny GEMM (bound by reading
+    // the weights once); everything else the tiled GEMM
+    // the skinny GEMM can also normalise its activations itself (a pre-LN
+    // block's LayerNorm fused into the product that consumes it)
+    const bool skinny = decode && T <= 16;
+    const bool fuse_ln = skinny && c.pre_ln && skinny_ln_fits(T, d);
+    auto gemm = [&](Epi epi, const bf16_t *a, const bf16_t *wt, const bf16_t *bias, const float *resid, void *out,
+                    int N, int K, const QkvDst *qkv, const LnResid *ln_resid, const LnIn *ln_in = nullptr) {
+        if (skinny && !ln_resid) return launch_gemm_skinny(epi, a, wt, bias, resid, out, T, N, K, qkv, s, ln_in);
+        return launch_gemm(epi, a, wt, bias, resid, out, T, N, K, qkv, s, ln_resid);
+    };
     auto attention_block = [&](int l, const bf16_t *y_bf16, const LayerWeights &w, const float *resid,
-                               const LnResid *ln_resid, float *dst) {
+                               const LnResid *ln_resid, float *dst, const LnIn *ln_in = nullptr) {
         const QkvDst qd = qkv_dst(l);
         launch(I, IEFWD_K_QKV, "qkv gemm", [&] {
-            return launch_gemm(Epi::Qkv, y_bf16, w.wqkv, w.bqkv, nullptr, nullptr, T, 3 * d, d, &qd, s);
+            return gemm(Epi::Qkv, y_bf16, w.wqkv, w.bqkv, nullptr, nullptr, 3 * d, d, &qd, nullptr, ln_in);
         });
         launch(I, IEFWD_K_ATTN, "attention", [&] {
             if (decode)
                 return launch_decode_attention(I->q, qd.k, qd.vt, I->ctx, B, H, decode_pos + 1, dh, qd.k_rows,
-                                               qd.vt_stride, s);
+                                               qd.vt_stride, I->dec_partials, s);
             return launch_attention(I->q, qd.k, qd.vt, I->ctx, B, H, S, dh, c.causal != 0, s, qd.k_rows,
                                     qd.vt_stride);
         });
         launch(I, IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
-            return launch_gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->ctx, w.wo, w.bo, resid, dst,
-                               T, d, d, nullptr, s, ln_resid);
+            return gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->ctx, w.wo, w.bo, resid, dst, d, d,
+                        nullptr, ln_resid);
         });
     };
     auto ffn_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid, const LnResid *ln_resid,
-                         float *dst) {
+                         float *dst, const LnIn *ln_in = nullptr) {
         launch(I, IEFWD_K_FFN1, "ffn1 gemm", [&] {
-            return launch_gemm(Epi::BiasGeluBf16, y_bf16, w.w1, w.b1, nullptr, I->u, T, F, d, nullptr, s);
+            return gemm(Epi::BiasGeluBf16, y_bf16, w.w1, w.b1, nullptr, I->u, F, d, nullptr, nullptr, ln_in);
         });
         launch(I, IEFWD_K_FFN2, "ffn2 gemm", [&] {
-            return launch_gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->u, w.w2, w.b2, resid, dst, T,
-                               d, F, nullptr, s, ln_resid);
+            return gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->u, w.w2, w.b2, resid, dst, d, F,
+                        nullptr, ln_resid);
         });
     };
     auto ln = [&](const float *src, const float *g, const float *b, float *o32, bf16_t *o16, float *stats) {
@@ -329,10 +348,16 @@ void run_forward(iefwd_instance *I, const float *x, int decode_pos = -1) {
         const float *xcur = x;
         for (int l = 0; l < L; ++l) {
             const LayerWeights &w = I->layers[l];
-            ln(xcur, w.g1, w.be1, nullptr, I->hb, nullptr);
-            attention_block(l, I->hb, w, xcur, nullptr, I->h1);
-            ln(I->h1, w.g2, w.be2, nullptr, I->hb, nullptr);
-            ffn_block(I->hb, w, I->h1, nullptr, I->h);
+            if (fuse_ln) {
+                const LnIn ln1{xcur, w.g1, w.be1, eps}, ln2{I->h1, w.g2, w.be2, eps};
+                attention_block(l, nullptr, w, xcur, nullptr, I->h1, &ln1);
+                ffn_block(nullptr, w, I->h1, nullptr, I->h, &ln2);
+            } else {
+                ln(xcur, w.g1, w.be1, nullptr, I->hb, nullptr);
+                attention_block(l, I->hb, w, xcur, nullptr, I->h1);
+                ln(I->h1, w.g2, w.be2, nullptr, I->hb, nullptr);
+                ffn_block(I->hb, w, I->h1, nullptr, I->h);
+            }
             xcur = I->h;
         }
         if (c.n_out > 0)
@@ -471,7 +496,9 @@ void alloc_workspace(iefwd_instance *I) {
     if (c.kv_cache) {
         const size_t kbytes = round_up((size_t)c.max_batch * d * c.max_seq * 2, 256);
         const size_t vbytes = round_up((size_t)c.max_batch * d * spad * 2, 256);
-        if (hipMalloc(&I->kvblob, (kbytes + vbytes) * c.n_layers) != hipSuccess) {
+        const size_t bh = (size_t)c.max_batch * c.n_heads;
+        const size_t pbytes = round_up(bh * kDecodeMaxChunks * (I->head_dim + 2) * 4, 256);
+        if (hipMalloc(&I->kvblob, (kbytes + vbytes) * c.n_layers + pbytes) != hipSuccess) {
             (void)hipGetLastError();
             I->kvblob = nullptr;
             fail(IEFWD_ENOMEM, "device allocation of the KV cache failed");
@@ -481,6 +508,7 @@ void alloc_workspace(iefwd_instance *I) {
             I->kcache.push_back(reinterpret_cast<bf16_t *>(kv + l * (kbytes + vbytes)));
             I->vtcache.push_back(reinterpret_cast<bf16_t *>(kv + l * (kbytes + vbytes) + kbytes));
         }
+        I->dec_partials = reinterpret_cast<float *>(kv + c.n_layers * (kbytes + vbytes));
     }
 }
 
@@ -945,6 +973,30 @@ int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void 
     });
 }
 
+int iefwd_test_gemm_skinny(uint32_t epilogue, const void *a, const void *w, const void *bias, const float *resid,
+                           void *out, uint32_t M, uint32_t N, uint32_t K, const float *ln_z, const float *ln_gamma,
+                           const float *ln_beta, float ln_eps, void *stream) {
+    return guarded([&] {
+        if (epilogue > IEFWD_EPI_BIAS_RESID_F32) fail(IEFWD_EINVAL, "unknown epilogue");
+        if (!w || !bias || !out) fail(IEFWD_EINVAL, "NULL pointer");
+        if (epilogue == IEFWD_EPI_BIAS_RESID_F32 && !resid) fail(IEFWD_EINVAL, "resid is NULL");
+        if (M == 0 || M > 16) fail(IEFWD_EINVAL, "M must be in [1, 16]");
+        if (N == 0 || N % 16 || K == 0 || K % 32) fail(IEFWD_EINVAL, "N must be a positive multiple of 16, K of 32");
+        if ((uint64_t)N * K >= (1ull << 31)) fail(IEFWD_EINVAL, "too large");
+        LnIn lnin{ln_z, ln_gamma, ln_beta, ln_eps};
+        if (ln_z) {
+            if (!ln_gamma || !ln_beta) fail(IEFWD_EINVAL, "NULL LayerNorm parameters");
+            if (!skinny_ln_fits((int)M, (int)K)) fail(IEFWD_EINVAL, "M * K too large for the LayerNorm prologue");
+        } else if (!a) {
+            fail(IEFWD_EINVAL, "a is NULL");
+        }
+        hip_check(launch_gemm_skinny((Epi)epilogue, (const bf16_t *)a, (const bf16_t *)w, (const bf16_t *)bias, resid,
+                                     out, (int)M, (int)N, (int)K, nullptr, (hipStream_t)stream,
+                                     ln_z ? &lnin : nullptr),
+                  "skinny gemm launch");
+    });
+}
+
 int iefwd_test_gemm_qkv(const void *a, const void *w, const void *bias, void *q, void *k, void *vt,
                         uint32_t batch, uint32_t seq, uint32_t d_model, uint32_t n_heads, void *stream) {
     return guarded([&] {
@@ -1008,10 +1060,20 @@ int iefwd_test_decode_attention(const void *q, const void *k, const void *vt, vo
         if (head_dim != 64 && head_dim != 128) fail(IEFWD_EINVAL, "head_dim must be 64 or 128");
         if (n_keys == 0 || n_keys > 8192 || k_rows < n_keys || vt_stride < n_keys || vt_stride % 64)
             fail(IEFWD_EINVAL, "need 1 <= n_keys <= 8192, k_rows >= n_keys, vt_stride >= n_keys and % 64 == 0");
+        // scratch for this call only: allocated, released after the stream drains
+        const size_t bh = (size_t)batch * n_heads;
+        const size_t pbytes = round_up(bh * kDecodeMaxChunks * (head_dim + 2) * 4, 256);
+        void *scratch = nullptr;
+        hip_check(hipMalloc(&scratch, pbytes), "hipMalloc");
+        struct Release {
+            void *p;
+            ~Release() { (void)hipFree(p); }
+        } release{scratch};
         hip_check(launch_decode_attention((const bf16_t *)q, (const bf16_t *)k, (const bf16_t *)vt, (bf16_t *)ctx,
                                           (int)batch, (int)n_heads, (int)n_keys, (int)head_dim, (int)k_rows,
-                                          (int)vt_stride, (hipStream_t)stream),
+                                          (int)vt_stride, static_cast<float *>(scratch), (hipStream_t)stream),
                   "decode attention launch");
+        hip_check(hipStreamSynchronize((hipStream_t)stream), "hipStreamSynchronize");
     });
 }
 

@@ -17,17 +17,23 @@ namespace iefwd {
 struct LaunchEvents {
     hipEvent_t start = nullptr, stop = nullptr;
 };
+// Events armed by the caller for the next launches on this thread: the first
+// kernel records `start` as it begins, and every kernel records `stop` as it
+// ends, so for an operation of several kernels the pair spans all of them.
 LaunchEvents &armed_launch_events();
+// Kernels launched by this thread so far.
+uint64_t &launch_count();
 
 template <typename F, typename... Args>
 hipError_t launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t stream, Args... args) {
     LaunchEvents &ev = armed_launch_events();
-    if (ev.start) {
+    if (ev.stop) {
         hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, ev.start, ev.stop, 0, args...);
-        ev = LaunchEvents{};
+        ev.start = nullptr;
     } else {
         hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
     }
+    ++launch_count();
     return hipGetLastError();
 }
 
@@ -78,6 +84,27 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
                        const float *resid, void *out, int M, int N, int K,
                        const QkvDst *qkv, hipStream_t stream, const LnResid *ln = nullptr);
 
+// Activations given as LayerNorm(z): z fp32 [M, K] rows, gamma / beta fp32 [K].
+struct LnIn {
+    const float *z;
+    const float *gamma;
+    const float *beta;
+    float eps;
+};
+
+// The same product for M <= 16 rows (a decode step), bound by reading W once:
+// N % 16 == 0, K % 32 == 0; every epilogue but BiasLnResidF32.  Its K
+// summation order differs from launch_gemm's (the two agree within rounding).
+// With ln_in the activations are LayerNorm(z), normalised in the kernel (then
+// `a` is unused); that needs skinny_ln_fits(M, K).
+hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
+                              const float *resid, void *out, int M, int N, int K, const QkvDst *qkv,
+                              hipStream_t stream, const LnIn *ln_in = nullptr);
+bool skinny_ln_fits(int M, int K);
+// K-groups per MFMA the skinny product uses for this shape (1, 2 or 4); its
+// summation order depends on N, K and this number.
+int skinny_groups(int M, int N, int K);
+
 // ctx bf16 [B, S, H*dh] from Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad].
 // k_rows: rows of K per (batch, head) (0: seq); vt_stride: row stride of V^T
 // (0: seq rounded up to 64), so that K and V^T may live in a longer KV cache.
@@ -88,9 +115,15 @@ hipError_t launch_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, 
 // Attention of one new query per (batch, head) over keys 0 .. n_keys - 1 of a
 // KV cache: q bf16 [B, H, dh], K [B, H, k_rows, dh], V^T [B, H, dh, vt_stride];
 // ctx bf16 [B, H * dh].  fp32 scores, softmax and sums.  n_keys <= 8192.
+// The keys are split into decode_attention_chunks(n_keys) <= kDecodeMaxChunks
+// chunks, one workgroup each; with more than one chunk a second kernel
+// combines them.  partials: at least B * H * kDecodeMaxChunks * (dh + 2)
+// floats of scratch; launches sharing it must not overlap.
+constexpr int kDecodeMaxChunks = 32;
+int decode_attention_chunks(int n_keys);
 hipError_t launch_decode_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx,
                                    int batch, int n_heads, int n_keys, int head_dim, int k_rows,
-                                   int vt_stride, hipStream_t stream);
+                                   int vt_stride, float *partials, hipStream_t stream);
 
 // Row LayerNorm, d % 128 == 0, d <= 4096.  out_f32 / out_bf16 / stats may be
 // null; stats receives {mean, rstd} per row.

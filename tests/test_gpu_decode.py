@@ -31,7 +31,10 @@ def check(got, ref, what=""):
     (1, 1, 1, 64, 1, 64),
     (2, 3, 7, 64, 16, 64),
     (3, 2, 513, 64, 600, 640),
+    (1, 1, 64, 128, 64, 64),                # one full chunk of 64
     (2, 16, 1025, 128, 1100, 1152),
+    (1, 2, 2048, 64, 2048, 2048),           # 32 chunks of 64: the most chunks
+    (2, 2, 2049, 64, 2100, 2112),           # first length split into chunks of 256
     (1, 4, 8192, 128, 8192, 8192),
 ])
 def test_decode_attention_kernel(B, H, n_keys, dh, k_rows, vt_stride):
@@ -66,6 +69,8 @@ DECODERS = [
     (dict(W.STRESS_INIT, n_layers=2, d_model=256, n_heads=4, d_ff=1024, pre_ln=1, causal=1, n_out=2), 3, 37, 4),
     (dict(W.STRESS_INIT, n_layers=2, d_model=256, n_heads=2, d_ff=640, pre_ln=1, causal=1, n_out=0), 2, 64, 3),
     (dict(n_layers=3, d_model=128, n_heads=2, d_ff=512, pre_ln=1, causal=1, n_out=3), 1, 1, 5),
+    # decode steps across the 2048 -> 2049 key boundary where the key chunking changes
+    (dict(n_layers=1, d_model=128, n_heads=1, d_ff=256, pre_ln=1, causal=1, n_out=2), 2, 2046, 4),
 ]
 
 
@@ -127,3 +132,86 @@ def test_decode_state_errors():
             assert e.value.status == ie.EINVAL
         inst.decode(np.ascontiguousarray(x[:1, 5]), 5)          # fewer sequences than the prompt: fine
         assert inst.read_logits().shape == (1, 1, 2)
+
+
+SKINNY = [
+    # M, N, K, epilogue, LayerNorm activations; K-groups per MFMA in the comments where more than one
+    (1, 16, 32, ie.EPI_BIAS_BF16, False),           # one workgroup, one K step
+    (16, 768, 96, ie.EPI_BIAS_GELU_BF16, False),    # fewer K steps than waves
+    (2, 6144, 2048, ie.EPI_BIAS_BF16, False),       # decoder QKV width: 2 K-groups
+    (3, 2048, 8192, ie.EPI_BIAS_RESID_F32, False),  # FFN-down: 4 K-groups
+    (7, 128, 4096, ie.EPI_BIAS_GELU_BF16, False),
+    (5, 4096, 1056, ie.EPI_BIAS_RESID_F32, False),  # K not a multiple of 64
+    (8, 1024, 2048, ie.EPI_BIAS_BF16, False),       # two K-groups, 8 tokens (their limit)
+    (4, 2048, 2048, ie.EPI_BIAS_RESID_F32, False),  # four K-groups, 4 tokens (their limit)
+    (2, 6144, 2048, ie.EPI_BIAS_BF16, True),
+    (16, 1024, 1024, ie.EPI_BIAS_GELU_BF16, True),  # M * K at the prologue's limit
+    (4, 512, 4096, ie.EPI_BIAS_RESID_F32, True),    # the longest row; 4 K-groups
+    (3, 2304, 768, ie.EPI_BIAS_GELU_BF16, True),    # 4 K-groups
+    (1, 64, 96, ie.EPI_BIAS_BF16, True),            # a row shorter than 64 lanes x 4
+]
+
+
+@pytest.mark.parametrize("M,N,K,epi,ln", SKINNY)
+def test_gemm_skinny(M, N, K, epi, ln):
+    """The decode-step product (optionally with its LayerNorm prologue) against
+    the oracle's linear layer, LayerNorm and GELU in fp64."""
+    print(f"skinny gemm M={M} N={N} K={K} epi={epi} ln={ln}", flush=True)
+    rng = np.random.default_rng(M * 1000 + N + K + epi + (7 if ln else 0))
+    w = bf16_round(rng.standard_normal((K, N)) * 0.05)                  # [in, out]
+    bias = bf16_round(rng.standard_normal(N) * 0.1)
+    resid = rng.standard_normal((M, N)).astype(np.float32)
+    w64, b64 = f64(w), f64(bias)
+    out = torch.empty((M, N), dtype=torch.float32 if epi == ie.EPI_BIAS_RESID_F32 else torch.bfloat16, device=DEV)
+    r_d = torch.from_numpy(resid).to(DEV) if epi == ie.EPI_BIAS_RESID_F32 else None
+    if ln:
+        z = (rng.standard_normal((M, K)) * 2.0 + 0.5).astype(np.float32)
+        g = (1.0 + 0.1 * rng.standard_normal(K)).astype(np.float32)
+        be = (0.1 * rng.standard_normal(K)).astype(np.float32)
+        eps = 1e-5
+        ie.test_gemm_skinny(epi, None, to_dev(w.t()), to_dev(bias), r_d, out, M, N, K,
+                            ln=(torch.from_numpy(z).to(DEV), torch.from_numpy(g).to(DEV),
+                                torch.from_numpy(be).to(DEV), eps))
+        z64 = z.astype(np.float64)
+        a64 = F.layer_norm(z64, g.astype(np.float64), be.astype(np.float64), eps)
+        mean = z64.mean(axis=1, keepdims=True)
+        rstd = 1.0 / np.sqrt(z64.var(axis=1, keepdims=True) + eps)
+        # fp32 statistics (K-term sums) and the bf16 rounding of the normalised rows
+        t = np.abs(g.astype(np.float64)) * rstd * (np.abs(z64 - mean) + np.abs(z64).mean(axis=1, keepdims=True))
+        da = 1.01 * UBF * np.abs(a64) + (K + 16) * U32 * t
+    else:
+        a = bf16_round(rng.standard_normal((M, K)))
+        ie.test_gemm_skinny(epi, to_dev(a), to_dev(w.t()), to_dev(bias), r_d, out, M, N, K)
+        a64 = f64(a)
+        da = np.zeros_like(a64)
+    sync()
+    pre = F.linear(a64, w64, b64)
+    bound = (K + 16) * U32 * ((np.abs(a64) + da) @ np.abs(w64)) + da @ np.abs(w64) + 1e-7
+    got = f64(out)
+    if epi == ie.EPI_BIAS_BF16:
+        ref, tol = pre, bound + 1.01 * UBF * (np.abs(pre) + bound)
+    elif epi == ie.EPI_BIAS_GELU_BF16:
+        ref = F.gelu(pre)
+        tol = 1.13 * bound + 1.01 * UBF * (np.abs(ref) + 1.13 * bound) + 1e-6 * np.abs(pre) + 1e-7
+    else:
+        ref = pre + resid.astype(np.float64)
+        tol = bound + 2 * U32 * (np.abs(ref) + np.abs(resid)) + 1e-7
+    err = np.abs(got - ref)
+    assert np.all(np.isfinite(got))
+    worst = np.unravel_index(np.argmax(err - tol), err.shape)
+    assert np.all(err <= tol), f"max excess at {worst}: err {err[worst]} tol {tol[worst]}"
+
+
+def test_gemm_skinny_rejects():
+    w = torch.zeros((64, 64), dtype=torch.bfloat16, device=DEV)
+    b = torch.zeros(64, dtype=torch.bfloat16, device=DEV)
+    a = torch.zeros((17, 64), dtype=torch.bfloat16, device=DEV)
+    out = torch.zeros((17, 64), dtype=torch.bfloat16, device=DEV)
+    z = torch.zeros((16, 2048), dtype=torch.float32, device=DEV)
+    for args, kw in (((a, w, b, None, out, 17, 64, 64), {}),            # M > 16
+                     ((a, w, b, None, out, 2, 40, 64), {}),             # N % 16
+                     ((a, w, b, None, out, 2, 64, 48), {}),             # K % 32
+                     ((None, w, b, None, out, 16, 64, 2048), {"ln": (z, z[0], z[0], 1e-5)})):  # M * K > 16384
+        with pytest.raises(ie.IefwdError) as e:
+            ie.test_gemm_skinny(ie.EPI_BIAS_BF16, *args, **kw)
+        assert e.value.status == ie.EINVAL
