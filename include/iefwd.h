@@ -338,8 +338,8 @@ int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void 
  * order differs from iefwd_test_gemm's (bound by reading W once, not by the
  * matrix cores).  ln_z non-NULL: the activations are LayerNorm(z) instead of a
  * (a is then ignored): z f32 [M, K], ln_gamma / ln_beta f32 [K], row
- * statistics in fp32, the normalised rows rounded to bf16; needs M * K <=
- * 16384 (EINVAL otherwise).  This is how a pre-LN block's LayerNorm is fused
+ * statistics in fp32, the normalised rows rounded to bf16; needs K <= 4096
+ * and M * K <= 16384 (EINVAL otherwise).  This is how a pre-LN block's LayerNorm is fused
  * into its QKV and FFN-up products during decode. */
 int iefwd_test_gemm_skinny(uint32_t epilogue, const void *a, const void *w, const void *bias,
                            const float *resid, void *out, uint32_t M, uint32_t N, uint32_t K,

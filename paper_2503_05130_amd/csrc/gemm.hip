@@ -548,70 +548,123 @@ hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
 // (g, t) token t's activations of K-group g, and the diagonal blocks of the
 // 16 x 16 product (row group == column group) are the per-group partial sums,
 // added over g at the end (the off-diagonal blocks are discarded).  G = 1, 2
-// or 4 (up to 16 / G tokens) is picked so that N / (16 / G) gives about 512
-// workgroups.  The waves split the K steps (wave w takes w, w + 8, ...); each
-// lane loads its weight and activation fragments straight into registers (16
-// bytes each; token columns past M repeat the last row and are never stored),
-// 8 K steps deep.  The waves' partial sums are added in wave order through
+// or 4 (up to 16 / G tokens) is the largest whose N / (16 / G) workgroups all
+// fit the chip at once.  The waves split the K steps (wave w takes w, w + 8,
+// ...); each lane loads its weight and activation fragments straight into
+// registers (16 bytes each; token columns past M repeat the last row and are
+// never stored), 8 K steps deep.  The waves' partial sums are added in wave order through
 // LDS, then the K-groups in group order through lane shuffles: the summation
-// order depends on N, K and G only.
+// order depends on K and G only.
 //
-// LNA: the activations are LayerNorm(z) of fp32 rows z (a pre-LN block's
-// input), normalised by the workgroup itself into LDS as bf16 -- row
-// statistics two-pass with a fixed butterfly, one wave per row, then
-// y = fma(gamma, (z - mean) * rstd, beta) -- while the first weight
-// fragments are already in flight.  Needs M * K <= kSkinnyLnElems.
+// With a LayerNorm prologue the activations are LayerNorm(z) of fp32 rows z
+// (a pre-LN block's input), normalised by the workgroup itself into LDS as
+// bf16 while the first weight fragments are already in flight.  Needs
+// M * K <= kSkinnyLnElems and K <= 4096.
 constexpr int kSkinnyWaves = 8, kSkinnyUnroll = 8;
 constexpr int kSkinnyLnElems = 16384;
-constexpr int kSkinnyTargetGroups = 512;
+constexpr int kSkinnyCus = 256;              // MI355X compute units
 
-// One wave per row; three passes over the row (the second and third hit the
-// cache): sum -> mean, squared deviations -> rstd, normalise -> LDS.
-__device__ inline void skinny_ln_prologue(const GemmParams &p, bf16_t *a_lds, int lane, int wave) {
-    const int nv = p.K / 4;                   // f32x4 vectors per row; lane owns c * 64 + lane
-    const float inv_k = 1.0f / (float)p.K;
-    const f32x4 *g4 = reinterpret_cast<const f32x4 *>(p.lnin.gamma);
-    const f32x4 *b4 = reinterpret_cast<const f32x4 *>(p.lnin.beta);
-    for (int r = wave; r < p.M; r += kSkinnyWaves) {
+// One wave per row (rows w and w + 8 for wave w), the row held in registers
+// (lane l owns the f32x4 vectors l + 64 c).  load() issues the first row and
+// this thread's share of gamma and beta -- before the weight fragments, so
+// that they are not queued behind them; finish() stages gamma and beta in LDS,
+// takes mean and rstd two-pass over the registers with a fixed butterfly and
+// writes y = fma(gamma, (z - mean) * rstd, beta), rounded to bf16, into the
+// activation tile.  NVL = K / 256 rounded up to 8 or 16 (K <= 4096).
+// finish() contains one barrier, reached by every wave.
+template <int NVL>
+struct SkinnyLn {
+    static constexpr int GBV = NVL * 64 / (64 * kSkinnyWaves);   // gamma / beta vectors per thread
+    f32x4 v[NVL];
+    f32x4 g[GBV], b[GBV];
+
+    // Unconditional loads (indices clamped into the row; the extra vectors are
+    // never used), so that the wait for them does not wait for the weights.
+    __device__ void load_row(const GemmParams &p, int r, int lane) {
         const f32x4 *zr = reinterpret_cast<const f32x4 *>(p.lnin.z + (size_t)r * p.K);
-        float s = 0.f;
-#pragma unroll 4
-        for (int i = lane; i < nv; i += 64) {
-            const f32x4 v = zr[i];
-            s += v[0] + v[1] + v[2] + v[3];
-        }
-        const float mean = wave_sum(s) * inv_k;
-        float ss = 0.f;
-#pragma unroll 4
-        for (int i = lane; i < nv; i += 64) {
-            const f32x4 v = zr[i];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const float d = v[e] - mean;
-                ss += d * d;
+        for (int c = 0; c < NVL; ++c) v[c] = zr[min(c * 64 + lane, p.K / 4 - 1)];
+    }
+
+    __device__ void load(const GemmParams &p, int tid, int lane, int wave) {
+#pragma unroll
+        for (int j = 0; j < GBV; ++j) {
+            const int i = min(tid + j * 64 * kSkinnyWaves, p.K / 4 - 1);
+            g[j] = reinterpret_cast<const f32x4 *>(p.lnin.gamma)[i];
+            b[j] = reinterpret_cast<const f32x4 *>(p.lnin.beta)[i];
+        }
+        load_row(p, min(wave, p.M - 1), lane);
+    }
+
+    __device__ void finish(const GemmParams &p, bf16_t *a_lds, float *gb_lds, int tid, int lane, int wave) {
+        const int nv = p.K / 4;
+        const float inv_k = 1.0f / (float)p.K;
+        f32x4 *g_l = reinterpret_cast<f32x4 *>(gb_lds), *b_l = g_l + nv;
+#pragma unroll
+        for (int j = 0; j < GBV; ++j) {
+            const int i = tid + j * 64 * kSkinnyWaves;
+            if (i < nv) {
+                g_l[i] = g[j];
+                b_l[i] = b[j];
             }
         }
-        const float rstd = 1.0f / sqrtf(wave_sum(ss) * inv_k + p.lnin.eps);
-#pragma unroll 4
-        for (int i = lane; i < nv; i += 64) {
-            const f32x4 v = zr[i], g = g4[i], b = b4[i];
-            float y[4];
+        float mean = 0.f, rstd = 0.f;
+        auto stats = [&] {
+            float sum = 0.f;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) y[e] = __builtin_fmaf(g[e], (v[e] - mean) * rstd, b[e]);
-            *reinterpret_cast<u32x2 *>(a_lds + (size_t)r * p.K + 4 * i) = u32x2{pack2(y[0], y[1]), pack2(y[2], y[3])};
+            for (int c = 0; c < NVL; ++c)
+                if (c * 64 + lane < nv) sum += v[c][0] + v[c][1] + v[c][2] + v[c][3];
+            mean = wave_sum(sum) * inv_k;
+            float ss = 0.f;
+#pragma unroll
+            for (int c = 0; c < NVL; ++c)
+                if (c * 64 + lane < nv)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float d = v[c][e] - mean;
+                        ss += d * d;
+                    }
+            rstd = 1.0f / sqrtf(wave_sum(ss) * inv_k + p.lnin.eps);
+        };
+        auto emit = [&](int r) {
+#pragma unroll
+            for (int c = 0; c < NVL; ++c) {
+                const int i = c * 64 + lane;
+                if (i < nv) {
+                    const f32x4 gg = g_l[i], bb = b_l[i];
+                    float y[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) y[e] = __builtin_fmaf(gg[e], (v[c][e] - mean) * rstd, bb[e]);
+                    *reinterpret_cast<u32x2 *>(a_lds + (size_t)r * p.K + 4 * i) =
+                        u32x2{pack2(y[0], y[1]), pack2(y[2], y[3])};
+                }
+            }
+        };
+        if (wave < p.M) stats();
+        __syncthreads();                      // gamma and beta staged
+        if (wave < p.M) emit(wave);
+        if (wave + kSkinnyWaves < p.M) {
+            load_row(p, wave + kSkinnyWaves, lane);
+            stats();
+            emit(wave + kSkinnyWaves);
         }
     }
-}
+};
 
-template <Epi EPI, int G, bool LNA>
+// NVL: 0 = activations from a; 8 or 16 = LayerNorm prologue for K <= 2048 / 4096
+template <Epi EPI, int G, int NVL>
 __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p) {
+    constexpr bool LNA = NVL > 0;
     constexpr int NW = kSkinnyWaves;
     constexpr int FPW = 16 / G, TPW = 16 / G;      // features and token columns per K-group
     constexpr int kPartBytes = (NW - 1) * 64 * 16;
-    constexpr int kLdsBytes = LNA && kSkinnyLnElems * 2 > kPartBytes ? kSkinnyLnElems * 2 : kPartBytes;
+    // LayerNorm: the bf16 activation tile, then gamma and beta (fp32, K each)
+    constexpr int kLnBytes = kSkinnyLnElems * 2 + 2 * NVL * 256 * 4;
+    constexpr int kLdsBytes = LNA && kLnBytes > kPartBytes ? kLnBytes : kPartBytes;
     __shared__ __attribute__((aligned(16))) char lds[kLdsBytes];
     f32x4 (*part)[64] = reinterpret_cast<f32x4 (*)[64]>(lds);
     bf16_t *a_lds = reinterpret_cast<bf16_t *>(lds);
+    float *gb_lds = reinterpret_cast<float *>(lds + kSkinnyLnElems * 2);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int n0 = blockIdx.x * FPW;
     const int row = lane & 15, chunk = lane >> 4;               // operand row / column, 8-element K chunk
@@ -633,10 +686,26 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
         for (int u = 0; u < kSkinnyUnroll; ++u)
             wf[u] = s0 + u * NW < steps ? *reinterpret_cast<const bf16x8 *>(wrow + (s0 + u * NW) * 32) : zero;
     };
-    load_w(wave);                                              // first weights in flight ...
+    // the same with every load issued (clamped to the last step, then zeroed):
+    // lets the LayerNorm prologue wait for its own loads alone
+    auto load_w_all = [&](int s0) {
+#pragma unroll
+        for (int u = 0; u < kSkinnyUnroll; ++u) {
+            const bf16x8 x = *reinterpret_cast<const bf16x8 *>(wrow + min(s0 + u * NW, steps - 1) * 32);
+            wf[u] = s0 + u * NW < steps ? x : zero;
+        }
+    };
     if constexpr (LNA) {
-        skinny_ln_prologue(p, a_lds, lane, wave);              // ... while the activations are normalised
+        // the LayerNorm inputs first, then the weights; the activations are
+        // normalised while the weights stream in
+        SkinnyLn<NVL> ln;
+        ln.load(p, threadIdx.x, lane, wave);
+        __builtin_amdgcn_sched_barrier(0);     // keep these loads ahead of the weights' (in-order returns)
+        load_w_all(wave);
+        ln.finish(p, a_lds, gb_lds, threadIdx.x, lane, wave);
         __syncthreads();
+    } else {
+        load_w(wave);
     }
     for (int s0 = wave; s0 < steps; s0 += NW * kSkinnyUnroll) {
 #pragma unroll
@@ -731,38 +800,44 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
 
 namespace {
 
-template <int G, bool LNA>
+template <int G, int NVL>
 hipError_t launch_skinny(Epi epi, const GemmParams &p, hipStream_t stream) {
     const dim3 grid(p.N / (16 / G)), block(64 * kSkinnyWaves);
     switch (epi) {
-    case Epi::BiasBf16: return launch_kernel(skinny_kernel<Epi::BiasBf16, G, LNA>, grid, block, stream, p);
-    case Epi::BiasGeluBf16: return launch_kernel(skinny_kernel<Epi::BiasGeluBf16, G, LNA>, grid, block, stream, p);
-    case Epi::BiasResidF32: return launch_kernel(skinny_kernel<Epi::BiasResidF32, G, LNA>, grid, block, stream, p);
-    case Epi::Qkv: return launch_kernel(skinny_kernel<Epi::Qkv, G, LNA>, grid, block, stream, p);
+    case Epi::BiasBf16: return launch_kernel(skinny_kernel<Epi::BiasBf16, G, NVL>, grid, block, stream, p);
+    case Epi::BiasGeluBf16: return launch_kernel(skinny_kernel<Epi::BiasGeluBf16, G, NVL>, grid, block, stream, p);
+    case Epi::BiasResidF32: return launch_kernel(skinny_kernel<Epi::BiasResidF32, G, NVL>, grid, block, stream, p);
+    case Epi::Qkv: return launch_kernel(skinny_kernel<Epi::Qkv, G, NVL>, grid, block, stream, p);
     case Epi::BiasLnResidF32: break;
     }
     return hipErrorInvalidValue;
 }
 
-template <bool LNA>
+template <int NVL>
 hipError_t launch_skinny_g(Epi epi, const GemmParams &p, hipStream_t stream) {
-    switch (skinny_groups(p.M, p.N, p.K)) {
-    case 1: return launch_skinny<1, LNA>(epi, p, stream);
-    case 2: return launch_skinny<2, LNA>(epi, p, stream);
-    case 4: return launch_skinny<4, LNA>(epi, p, stream);
+    switch (skinny_groups(p.M, p.N, p.K, NVL > 0)) {
+    case 1: return launch_skinny<1, NVL>(epi, p, stream);
+    case 2: return launch_skinny<2, NVL>(epi, p, stream);
+    case 4: return launch_skinny<4, NVL>(epi, p, stream);
     }
     return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-int skinny_groups(int M, int N, int K) {
+int skinny_groups(int M, int N, int K, bool ln) {
+    // more K-groups while the workgroups still fit the CUs in one round (3 per
+    // CU, 2 with the LayerNorm prologue's registers and LDS), so that no
+    // workgroup starts streaming its weights only after another has finished
+    const int limit = (ln ? 2 : 3) * kSkinnyCus;
     int g = 1;
-    while (g < 4 && N / (16 / g) < kSkinnyTargetGroups && M <= 16 / (2 * g) && K % (32 * 2 * g) == 0) g *= 2;
+    while (g < 4 && N / (16 / (2 * g)) <= limit && M <= 16 / (2 * g) && K % (32 * 2 * g) == 0) g *= 2;
     return g;
 }
 
-bool skinny_ln_fits(int M, int K) { return M >= 1 && M <= 16 && K % 32 == 0 && M * K <= kSkinnyLnElems; }
+bool skinny_ln_fits(int M, int K) {
+    return M >= 1 && M <= 16 && K % 32 == 0 && K <= 4096 && M * K <= kSkinnyLnElems;
+}
 
 hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias, const float *resid,
                               void *out, int M, int N, int K, const QkvDst *qkv, hipStream_t stream,
@@ -775,7 +850,8 @@ hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const b
     p.M = M; p.N = N; p.K = K;
     if (qkv) p.qkv = *qkv;
     if (ln_in) p.lnin = *ln_in;
-    return ln_in ? launch_skinny_g<true>(epi, p, stream) : launch_skinny_g<false>(epi, p, stream);
+    if (!ln_in) return launch_skinny_g<0>(epi, p, stream);
+    return K <= 2048 ? launch_skinny_g<8>(epi, p, stream) : launch_skinny_g<16>(epi, p, stream);
 }
 
 }  // namespace iefwd

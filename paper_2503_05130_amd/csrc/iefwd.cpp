@@ -986,7 +986,7 @@ int iefwd_test_gemm_skinny(uint32_t epilogue, const void *a, const void *w, cons
         LnIn lnin{ln_z, ln_gamma, ln_beta, ln_eps};
         if (ln_z) {
             if (!ln_gamma || !ln_beta) fail(IEFWD_EINVAL, "NULL LayerNorm parameters");
-            if (!skinny_ln_fits((int)M, (int)K)) fail(IEFWD_EINVAL, "M * K too large for the LayerNorm prologue");
+            if (!skinny_ln_fits((int)M, (int)K)) fail(IEFWD_EINVAL, "the LayerNorm prologue needs K <= 4096 and M * K <= 16384");
         } else if (!a) {
             fail(IEFWD_EINVAL, "a is NULL");
         }

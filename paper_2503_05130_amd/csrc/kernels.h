@@ -101,9 +101,10 @@ hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const b
                               const float *resid, void *out, int M, int N, int K, const QkvDst *qkv,
                               hipStream_t stream, const LnIn *ln_in = nullptr);
 bool skinny_ln_fits(int M, int K);
-// K-groups per MFMA the skinny product uses for this shape (1, 2 or 4); its
-// summation order depends on N, K and this number.
-int skinny_groups(int M, int N, int K);
+// K-groups per MFMA the skinny product uses for this shape (1, 2 or 4), with
+// or without the LayerNorm prologue; its summation order depends on K and
+// this number.
+int skinny_groups(int M, int N, int K, bool ln);
 
 // ctx bf16 [B, S, H*dh] from Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad].
 // k_rows: rows of K per (batch, head) (0: seq); vt_stride: row stride of V^T

@@ -147,7 +147,7 @@ SKINNY = [
     (2, 6144, 2048, ie.EPI_BIAS_BF16, True),
     (16, 1024, 1024, ie.EPI_BIAS_GELU_BF16, True),  # M * K at the prologue's limit
     (4, 512, 4096, ie.EPI_BIAS_RESID_F32, True),    # the longest row; 4 K-groups
-    (3, 2304, 768, ie.EPI_BIAS_GELU_BF16, True),    # 4 K-groups
+    (3, 2304, 768, ie.EPI_BIAS_GELU_BF16, True),    # 2 K-groups (4 would not fit in one round)
     (1, 64, 96, ie.EPI_BIAS_BF16, True),            # a row shorter than 64 lanes x 4
 ]
 
