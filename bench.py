@@ -12,11 +12,13 @@ forward-level MFMA utilisation, the roofline of the dominant kernel (FFN-down
 GEMM + bias + LayerNorm residual: each launch in the timed region records its own
 start and end into HIP events), the aggregate throughput of two co-located instances at
 CU quotas 64/192, 128/128 and 192/64 against one alone, and the fp64 CPU oracle
-timed on a bounded sample, and the per-batch cost of re-masking the
-instance's stream between batches.
+timed on a bounded sample, the per-batch cost of re-masking the
+instance's stream between batches, throughput and MFMA utilisation at CU
+quotas (BERT-base batch 32; the RoBERTa-large-sized causal decoder at batch 8,
+S 512), and the four GEMM classes against hipBLASLt on the same shapes.
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-colocated] [--no-remask]
-                  [--decode | --decode-only]
+                  [--no-quota-sweep] [--no-gemm-reference] [--decode | --decode-only]
 """
 from __future__ import annotations
 
@@ -36,7 +38,7 @@ WORKLOAD = "bert_base_l12_d768_s128"
 # HBM bytes per launch of the FFN-down kernel (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 KiB,
 # factors from a 256 MiB device copy in the same runs), valid only for the GEMM source
 # and build flags they were counted on; any other source reports null.
-FFN2_TRAFFIC = {"source_sha256_16": "8e81d4d7d8f890a5", "bytes": (36999.1 * 2.0 + 14367.8 * 1.0) * 1024}
+FFN2_TRAFFIC = {"source_sha256_16": "44063643aeb1d6c0", "bytes": (36983.3 * 2.0 + 14573.1 * 1.0) * 1024}
 GEMM_SOURCES = ("paper_2503_05130_amd/csrc/gemm.hip", "paper_2503_05130_amd/csrc/kernels.h",
                 "paper_2503_05130_amd/build.py")
 
@@ -214,6 +216,93 @@ def decode_leg(ie, W, batch=2, prompt=512, steps=64):
             "us_per_step": per}
 
 
+def quota_sweep(ie, W, inst, x, B, S, shape):
+    """Throughput and forward-level MFMA utilisation at CU quotas: the BERT-base
+    batch at 64 / 128 / 192 / 256 CUs, and the RoBERTa-large-sized causal
+    decoder (24 layers, d 1024, S 512, batch 8) at 64 / 128 / 256 CUs.  Device
+    time per batch from the instance's own events; utilisation against the
+    quota's share of the bf16 peak."""
+    def run(instance, xin, quotas, flops_batch, batch, n_warm, n_time):
+        out = []
+        for q in quotas:
+            instance.set_quota(q)
+            for _ in range(n_warm):
+                instance.submit(xin)
+                instance.wait()
+            ms = []
+            for _ in range(n_time):
+                instance.submit(xin)
+                instance.wait()
+                ms.append(instance.last_batch_ms())
+            t = float(np.median(ms))
+            out.append({"quota_cus": q, "ms_per_batch": round(t, 4), "inferences_s": round(batch / (t * 1e-3), 1),
+                        "mfma_util_pct": round(flops_batch / (t * 1e-3) / (PEAK_BF16_TFLOPS * 1e12 * q / 256) * 100, 2)})
+        instance.set_quota(256)
+        return out
+
+    d, F_, L, H = shape["d_model"], shape["d_ff"], shape["n_layers"], shape["n_heads"]
+    res = {"bert": {"workload": f"{WORKLOAD}, batch {B}",
+                    "points": run(inst, x, (64, 128, 192, 256), forward_flops(L, d, F_, H, S, shape["n_out"]) * B, B,
+                                  3, 10)}}
+    import torch
+
+    name = "decoder_l24_d1024_s512"
+    ds = W.model_shape(name)
+    wd = W.WORKLOADS[name]
+    cfg = {k: ds[k] for k in ("n_layers", "d_model", "n_heads", "d_ff", "pre_ln", "causal", "n_out", "ln_eps",
+                              "w_std", "b_std", "ln_std", "qk_std", "seed")}
+    dec = ie.Instance(device=0, max_batch=wd["batch"], max_seq=wd["seq"], **cfg)
+    xd = torch.from_numpy(W.make_input(wd["input_seed"], wd["batch"], wd["seq"], ds["d_model"])).to("cuda:0")
+    fl = forward_flops(ds["n_layers"], ds["d_model"], ds["d_ff"], ds["n_heads"], wd["seq"], ds["n_out"], causal=True)
+    res["decoder"] = {"workload": f"{name}, batch {wd['batch']}",
+                      "points": run(dec, xd, (64, 128, 256), fl * wd["batch"], wd["batch"], 2, 5),
+                      "paper_context": "RoBERTa-large inference iteration 25 ms solo, 50 ms under SM contention, "
+                                       "NVIDIA A100-40GB, batch / sequence / precision not stated (Sec. 3.4.1)"}
+    dec.close()
+    return res
+
+
+def gemm_reference(ie, inst, x, B, S, shape, reps=20):
+    """The forward's four GEMM classes against torch.matmul (hipBLASLt) on the
+    same shapes with plain bf16 outputs: the library reference for what these
+    small products reach on this chip.  Ours include their fused epilogues
+    (head scatter, residual, GELU, LayerNorm residual rebuild and fp32 out)."""
+    import torch
+
+    kinds = {"qkv": ie.K_QKV, "out_proj": ie.K_OUTPROJ, "ffn_up": ie.K_FFN1, "ffn_down": ie.K_FFN2}
+    for k in kinds.values():
+        inst.time_kernel(k, True)
+    for _ in range(reps):
+        inst.submit(x)
+        inst.wait()
+    ours = {}
+    for nm, k in kinds.items():
+        t, n = inst.kernel_time(k)
+        inst.time_kernel(k, False)
+        ours[nm] = t * 1e3 / max(n, 1)
+    T, d, F_ = B * S, shape["d_model"], shape["d_ff"]
+    shapes = {"qkv": (T, 3 * d, d), "out_proj": (T, d, d), "ffn_up": (T, F_, d), "ffn_down": (T, d, F_)}
+    out = {}
+    for nm, (M, N, K) in shapes.items():
+        a = torch.randn(M, K, device="cuda:0", dtype=torch.bfloat16)
+        w = torch.randn(N, K, device="cuda:0", dtype=torch.bfloat16)
+        c = torch.empty(M, N, device="cuda:0", dtype=torch.bfloat16)
+        for _ in range(5):
+            torch.matmul(a, w.t(), out=c)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            torch.matmul(a, w.t(), out=c)
+        e1.record()
+        torch.cuda.synchronize()
+        lib_us = e0.elapsed_time(e1) * 1e3 / reps
+        fl = 2.0 * M * N * K
+        out[nm] = {"mnk": [M, N, K], "ours_us": round(ours[nm], 2), "hipblaslt_us": round(lib_us, 2),
+                   "ours_tflops": round(fl / ours[nm] / 1e6, 1), "hipblaslt_tflops": round(fl / lib_us / 1e6, 1)}
+    return out
+
+
 def copy_calibration(mib: int) -> None:
     """A plain device-to-device copy of `mib` MiB, for scaling the FETCH_SIZE /
     WRITE_SIZE counters of a profiling run (read once, written once)."""
@@ -237,6 +326,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-colocated", action="store_true")
     ap.add_argument("--no-remask", action="store_true")
+    ap.add_argument("--no-quota-sweep", action="store_true")
+    ap.add_argument("--no-gemm-reference", action="store_true")
     ap.add_argument("--decode", action="store_true", help="also time the decode phase of the d=2048 decoder")
     ap.add_argument("--decode-only", action="store_true",
                     help="time only the decode phase (a profiling aid: prints {\"decode\": ...})")
@@ -325,6 +416,10 @@ def main() -> int:
     }
     if not args.no_remask:
         result["remask"] = remask_overhead(inst, x)
+    if not args.no_quota_sweep:
+        result["quota_sweep"] = quota_sweep(ie, W, inst, x, B, S, shape)
+    if not args.no_gemm_reference:
+        result["gemm_reference"] = gemm_reference(ie, inst, x, B, S, shape)
     inst.close()
     if not args.no_colocated:
         result["colocated"] = colocated(ie, W, shape, cfg, [(64, 192), (128, 128), (192, 64)])
