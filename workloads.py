@@ -65,3 +65,9 @@ def tiny_shape(pre_ln: int, causal: int, n_out: int = 0, seed: int = 7, **kw) ->
                  seed=seed)
     shape.update(kw)
     return shape
+
+
+def make_labels(seed: int, batch: int, seq: int, n_classes: int) -> np.ndarray:
+    """int32 [batch, seq] uniform class labels in [0, n_classes)."""
+    rng = np.random.default_rng(seed)
+    return rng.integers(0, n_classes, size=(batch, seq), dtype=np.int32)
