@@ -209,7 +209,10 @@ int iefwd_get_stream(iefwd_instance *inst, void **hip_stream);
 #define IEFWD_K_FFN1     3u   /* FFN up GEMM + bias + GELU */
 #define IEFWD_K_FFN2     4u   /* FFN down GEMM + bias + residual */
 #define IEFWD_K_LN       5u   /* LayerNorm kernels (including the fused final LN + head) */
-#define IEFWD_K_COUNT    6u
+#define IEFWD_K_BWD_GEMM 6u   /* training: the backward pass's GEMMs (input and weight gradients) */
+#define IEFWD_K_BWD      7u   /* training: the other backward kernels (LayerNorm, attention, sums, transposes) */
+#define IEFWD_K_OPTIM    8u   /* training: the AdamW update and the transposed weight copies */
+#define IEFWD_K_COUNT    9u
 
 /* enable != 0: every later launch of class `kind` records the kernel's own
  * start and end timestamps into a pair of HIP events (hipExtLaunchKernel);
@@ -218,6 +221,68 @@ int iefwd_get_stream(iefwd_instance *inst, void **hip_stream);
  * in flight. */
 int iefwd_time_kernel(iefwd_instance *inst, uint32_t kind, int enable);
 int iefwd_kernel_time(iefwd_instance *inst, uint32_t kind, double *total_ms, uint64_t *launches);
+
+/* ---- training (an SLO-insensitive training function, Sec. 3.4.1 and 5.2) ----------------
+ * A training instance runs whole training steps of a post-LN encoder on the
+ * same quota machinery as an inference instance: iefwd_set_quota* apply at
+ * the next step, iefwd_last_batch_ms is the last step's device time and
+ * iefwd_kernels_launched counts its kernels.  One step: forward (saving the
+ * activations the backward needs), loss = mean over the B*S tokens of the
+ * softmax cross-entropy of the token's n_out logits against its label,
+ * backward of every parameter, one AdamW update (decoupled weight decay on the
+ * weight matrices only, bias-corrected moments), all on the GPU.  The
+ * optimiser keeps fp32 master weights and moments; the forward reads their
+ * bf16 (matrices, biases) or fp32 (LayerNorm) copies.  Deterministic: a step's
+ * results are a function of the config, the parameters, the inputs and the
+ * step count, independent of the quota. */
+typedef struct iefwd_train_params {
+    uint32_t abi_version;   /* must be IEFWD_ABI_VERSION */
+    uint32_t reserved0;
+    float    lr;            /* learning rate (default 1e-4) */
+    float    beta1, beta2;  /* moment decay rates (0.9, 0.999) */
+    float    eps;           /* denominator offset (1e-8) */
+    float    weight_decay;  /* decoupled weight decay of the weight matrices (0.01) */
+    float    reserved1;
+} iefwd_train_params;
+
+/* Fills *tp with the defaults above. No status. */
+void iefwd_train_params_init(iefwd_train_params *tp);
+
+/* Creates a training instance: as iefwd_create (same weights for the same
+ * config), plus the optimiser state (4 fp32 copies of the parameters) and the
+ * activations of max_batch * max_seq tokens per layer.  Needs pre_ln = 0,
+ * kv_cache = 0, 1 <= n_out <= 16 (classes), head dim 64 and max_seq <= 128;
+ * EINVAL otherwise, EVERSION for a wrong tp->abi_version. */
+int iefwd_train_create(const iefwd_config *cfg, const iefwd_train_params *tp, int device, iefwd_instance **out);
+
+/* One training step, asynchronous like iefwd_submit: x fp32 [batch, seq,
+ * d_model] and labels int32 [batch, seq] (class indices in [0, n_out); a
+ * label outside that range counts as no class), both on the host (copied
+ * before return) or both on the device (valid until the step completes).
+ * batch * seq must be a multiple of 64.  ESTATE on an inference instance or
+ * with a step or batch in flight.  After the step, iefwd_read_logits returns
+ * the step's logits (computed before its update). */
+int iefwd_train_step(iefwd_instance *inst, const float *x, const int32_t *labels, uint32_t batch, uint32_t seq,
+                     int inputs_are_device);
+
+/* Waits for the step in flight and writes its loss (before the update).
+ * ESTATE if no step has run. */
+int iefwd_train_loss(iefwd_instance *inst, float *loss);
+
+/* Number of completed optimiser steps. */
+int iefwd_train_steps(const iefwd_instance *inst, uint64_t *steps);
+
+#define IEFWD_TRAIN_MASTER   0u   /* fp32 master weights */
+#define IEFWD_TRAIN_GRAD     1u   /* gradients of the last step */
+#define IEFWD_TRAIN_MOMENT1  2u   /* AdamW first moments */
+#define IEFWD_TRAIN_MOMENT2  3u   /* AdamW second moments */
+
+/* Copies one tensor of the optimiser state as fp32 in the logical layout of
+ * iefwd_export_tensor (matrices [in, out]); slots as there (per layer 0..11;
+ * layer = n_layers: 14 Wh, 15 bh).  n_floats must equal the tensor's size.
+ * Waits for the step in flight. */
+int iefwd_train_export(iefwd_instance *inst, uint32_t layer, uint32_t slot, uint32_t what, float *host_dst,
+                       size_t n_floats);
 
 /* ---- weights ------------------------------------------------------------------------ */
 

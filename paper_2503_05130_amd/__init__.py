@@ -22,7 +22,8 @@ LIB_PATH = os.path.join(_HERE, "libiefwd.so")
 
 ABI_VERSION = 1
 OK, EINVAL, ENODEV, ENOMEM, EHIP, ESTATE, EVERSION = 0, -1, -2, -3, -4, -5, -6
-K_QKV, K_ATTN, K_OUTPROJ, K_FFN1, K_FFN2, K_LN = range(6)
+K_QKV, K_ATTN, K_OUTPROJ, K_FFN1, K_FFN2, K_LN, K_BWD_GEMM, K_BWD, K_OPTIM = range(9)
+TRAIN_MASTER, TRAIN_GRAD, TRAIN_MOMENT1, TRAIN_MOMENT2 = range(4)
 EPI_BIAS_BF16, EPI_BIAS_GELU_BF16, EPI_BIAS_RESID_F32 = 0, 1, 2
 
 _u32, _u64, _i32, _f32, _vp, _sz = (ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int, ctypes.c_float,
@@ -58,6 +59,12 @@ SIGNATURES = {
     "iefwd_time_kernel": (_i32, [_vp, _u32, _i32]),
     "iefwd_kernel_time": (_i32, [_vp, _u32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_u64)]),
     "iefwd_export_tensor": (_i32, [_vp, _u32, _u32, _vp, _sz]),
+    "iefwd_train_params_init": (None, [_vp]),
+    "iefwd_train_create": (_i32, [_vp, _vp, _i32, ctypes.POINTER(_vp)]),
+    "iefwd_train_step": (_i32, [_vp, _vp, _vp, _u32, _u32, _i32]),
+    "iefwd_train_loss": (_i32, [_vp, ctypes.POINTER(_f32)]),
+    "iefwd_train_steps": (_i32, [_vp, ctypes.POINTER(_u64)]),
+    "iefwd_train_export": (_i32, [_vp, _u32, _u32, _u32, _vp, _sz]),
     "iefwd_last_error": (ctypes.c_char_p, []),
     "iefwd_status_string": (ctypes.c_char_p, [_i32]),
     "iefwd_test_gemm": (_i32, [_u32, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp]),
@@ -343,6 +350,73 @@ def test_cu_probe(n_groups: int, out, stream=None) -> None:
 
 # ------------------------------------------------------------------ quota controller
 CTL_NONE, CTL_EMERGENCY, CTL_RECOVERY, CTL_CONTENTION = 0, 1, 2, 3
+
+
+class TrainParams(ctypes.Structure):
+    """Mirror of ``iefwd_train_params``."""
+    _fields_ = [("abi_version", _u32), ("reserved0", _u32), ("lr", _f32), ("beta1", _f32), ("beta2", _f32),
+                ("eps", _f32), ("weight_decay", _f32), ("reserved1", _f32)]
+
+
+def train_params(**kw) -> TrainParams:
+    tp = TrainParams()
+    lib().iefwd_train_params_init(ctypes.byref(tp))
+    for k, v in kw.items():
+        if k not in ("lr", "beta1", "beta2", "eps", "weight_decay"):
+            raise ValueError(f"unknown training parameter {k}")
+        setattr(tp, k, v)
+    return tp
+
+
+class Trainer(Instance):
+    """A training instance (post-LN encoder, softmax cross-entropy, AdamW): the
+    same quota calls as an inference instance, plus whole training steps."""
+
+    def __init__(self, device: int = 0, train: dict | None = None, **config):
+        self._h = None
+        self.cfg = make_config(**config)
+        self.tp = train_params(**(train or {}))
+        h = _vp()
+        _check(lib().iefwd_train_create(ctypes.byref(self.cfg), ctypes.byref(self.tp), device, ctypes.byref(h)),
+               "iefwd_train_create")
+        self._h = h
+        self.device = device
+
+    def step(self, x, labels) -> None:
+        """One asynchronous training step.  x fp32 [B, S, d], labels int32 [B, S]:
+        both CUDA tensors (kept alive until the step completes) or both host arrays."""
+        if isinstance(x, torch.Tensor) and x.is_cuda:
+            if not (isinstance(labels, torch.Tensor) and labels.is_cuda):
+                raise ValueError("x and labels must both be on the device or both on the host")
+            if x.dtype != torch.float32 or not x.is_contiguous():
+                raise ValueError("x must be a contiguous float32 tensor")
+            if labels.dtype != torch.int32 or not labels.is_contiguous():
+                raise ValueError("labels must be a contiguous int32 tensor")
+            is_dev = 1
+        else:
+            x = np.ascontiguousarray(x.cpu().numpy() if isinstance(x, torch.Tensor) else x, dtype=np.float32)
+            labels = np.ascontiguousarray(labels.cpu().numpy() if isinstance(labels, torch.Tensor) else labels,
+                                          dtype=np.int32)
+            is_dev = 0
+        b, s_ = x.shape[0], x.shape[1]
+        _check(lib().iefwd_train_step(self._h, _ptr(x), _ptr(labels), b, s_, is_dev), "iefwd_train_step")
+        self._last_shape = (b, s_)
+        self._keep = (x, labels)
+
+    def loss(self) -> float:
+        v = _f32()
+        _check(lib().iefwd_train_loss(self._h, ctypes.byref(v)), "iefwd_train_loss")
+        return float(v.value)
+
+    def steps(self) -> int:
+        v = _u64()
+        _check(lib().iefwd_train_steps(self._h, ctypes.byref(v)), "iefwd_train_steps")
+        return int(v.value)
+
+    def export(self, layer: int, slot: int, what: int, shape) -> np.ndarray:
+        out = np.empty(shape, dtype=np.float32)
+        _check(lib().iefwd_train_export(self._h, layer, slot, what, out.ctypes.data, out.size), "iefwd_train_export")
+        return out
 
 
 class CtlParams(ctypes.Structure):

@@ -22,7 +22,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libiefwd.so")
 ARCH = "gfx950"
 
-SOURCES = ["gemm.hip", "attention.hip", "decode.hip", "layernorm.hip", "quota.cpp", "controller.cpp", "init_weights.cpp",
+SOURCES = ["gemm.hip", "attention.hip", "decode.hip", "layernorm.hip", "train.hip", "quota.cpp", "controller.cpp", "init_weights.cpp",
            "iefwd.cpp"]
 
 COMMON = [

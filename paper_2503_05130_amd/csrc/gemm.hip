@@ -27,6 +27,7 @@
 // shape (N, K) alone.  So out[t, f] depends only on row t of A and row f of W
 // -- never on the tile shape, the ring depth, the grid, the CU mask or the
 // other rows in the batch.  No atomics, no cross-workgroup split-K.
+#include "gelu.h"
 #include "kernels.h"
 
 #include <algorithm>
@@ -54,6 +55,7 @@ struct GemmParams {
     QkvDst qkv;
     LnResid ln;
     LnIn lnin;
+    const bf16_t *aux;   // Epi::GeluBwdBf16: the GELU's input [M, N]
 };
 
 // Workgroups are dispatched round-robin over the 8 XCDs.  Renumber them so
@@ -93,23 +95,6 @@ __device__ inline float wave_sum(float v) {
 #pragma unroll
     for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
     return v;
-}
-
-// GELU(u) = u/2 (1 + erf(u / sqrt 2)), with erf from Abramowitz & Stegun,
-// Handbook of Mathematical Functions, formula 7.1.26 (|error| <= 1.5e-7 for
-// x >= 0): erfc(x) ~= (a1 t + a2 t^2 + a3 t^3 + a4 t^4 + a5 t^5) exp(-x^2),
-// t = 1 / (1 + p x).  Written through erfc so that u < 0 keeps its relative
-// accuracy: GELU(u) = u (1 - erfc(x)/2) for u >= 0 and u erfc(x)/2 for u < 0,
-// x = |u| / sqrt 2.  About 14 VALU operations instead of a full erff.
-__device__ inline float gelu(float u) {
-    const float x = fabsf(u) * 0.7071067811865476f;
-    const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, x, 1.0f));
-    float poly = fmaf(1.061405429f, t, -1.453152027f);
-    poly = fmaf(poly, t, 1.421413741f);
-    poly = fmaf(poly, t, -0.284496736f);
-    poly = fmaf(poly, t, 0.254829592f);
-    const float erfc_x = poly * t * __builtin_amdgcn_exp2f(-x * x * 1.4426950408889634f);
-    return u * (u >= 0.f ? fmaf(-0.5f, erfc_x, 1.0f) : 0.5f * erfc_x);
 }
 
 // 16-byte chunk position of logical chunk 0 in LDS row r (row r holds its
@@ -226,7 +211,10 @@ __device__ inline void main_loop(const GemmParams &p, bf16_t *ring0, int wave, i
 // writes its finished values into an LDS copy of the output tile, then the
 // whole workgroup stores it in 16-byte row segments.  Written straight from
 // the MFMA layout, one store instruction would cover 16 rows x 32 bytes.
-constexpr bool staged(Epi e) { return e == Epi::BiasBf16 || e == Epi::BiasGeluBf16 || e == Epi::Qkv; }
+constexpr bool staged(Epi e) {
+    return e == Epi::BiasBf16 || e == Epi::BiasGeluBf16 || e == Epi::Qkv || e == Epi::GeluBwdBf16;
+}
+constexpr bool has_bias(Epi e) { return e != Epi::F32 && e != Epi::GeluBwdBf16; }
 
 // Epilogue operands that do not depend on the product (bias, residual rows,
 // LayerNorm statistics and affine) are loaded into registers before the main
@@ -253,7 +241,8 @@ __device__ inline void epilogue_prefetch(const GemmParams &p, EpiInputs<C, EPI, 
 #pragma unroll
     for (int j = 0; j < C::FN; ++j) {
         const int f = n0 + wn * C::TN + j * 16 + (lane >> 4) * 4;
-        in.bias[j] = *reinterpret_cast<const u32x2 *>(p.bias + f);
+        if constexpr (has_bias(EPI)) in.bias[j] = *reinterpret_cast<const u32x2 *>(p.bias + f);
+        else in.bias[j] = u32x2{0u, 0u};
         if constexpr (EPI == Epi::BiasLnResidF32) {
             in.gamma[j] = *reinterpret_cast<const f32x4 *>(p.ln.gamma + f);
             in.beta[j] = *reinterpret_cast<const f32x4 *>(p.ln.beta + f);
@@ -307,6 +296,13 @@ __device__ inline void epilogue(const GemmParams &p, const f32x4 (&acc)[C::FN][C
                 if constexpr (EPI == Epi::BiasGeluBf16) {
                     v0 = gelu(v0); v1 = gelu(v1); v2 = gelu(v2); v3 = gelu(v3);
                 }
+                if constexpr (EPI == Epi::GeluBwdBf16) {   // rows past M read row M - 1: never stored
+                    const u32x2 g = *reinterpret_cast<const u32x2 *>(p.aux + (size_t)min(t, p.M - 1) * p.N + f);
+                    v0 *= gelu_grad(__uint_as_float(g[0] << 16));
+                    v1 *= gelu_grad(__uint_as_float(g[0] & 0xffff0000u));
+                    v2 *= gelu_grad(__uint_as_float(g[1] << 16));
+                    v3 *= gelu_grad(__uint_as_float(g[1] & 0xffff0000u));
+                }
                 if (EPI == Epi::Qkv && vt_tile) {
                     bf16_t *o = ctile + fl * kColStride<C> + tl;
                     o[0] = f32_to_bf16(v0);
@@ -316,6 +312,9 @@ __device__ inline void epilogue(const GemmParams &p, const f32x4 (&acc)[C::FN][C
                 } else {
                     *reinterpret_cast<u32x2 *>(ctile + tl * kRowStride<C> + fl) = u32x2{pack2(v0, v1), pack2(v2, v3)};
                 }
+            } else if constexpr (EPI == Epi::F32) {
+                if (t >= p.M) continue;
+                *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + (size_t)t * p.N + f) = f32x4{v0, v1, v2, v3};
             } else if constexpr (EPI == Epi::BiasResidF32) {
                 if (t >= p.M) continue;
                 f32x4 r;
@@ -534,6 +533,8 @@ hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
     case Epi::BiasResidF32: return launch_kernel(kernel_for<C, Epi::BiasResidF32, SPLIT>(), grid, block, s, p);
     case Epi::Qkv: return launch_kernel(kernel_for<C, Epi::Qkv, SPLIT>(), grid, block, s, p);
     case Epi::BiasLnResidF32: return launch_kernel(kernel_for<C, Epi::BiasLnResidF32, SPLIT>(), grid, block, s, p);
+    case Epi::F32: return launch_kernel(kernel_for<C, Epi::F32, SPLIT>(), grid, block, s, p);
+    case Epi::GeluBwdBf16: return launch_kernel(kernel_for<C, Epi::GeluBwdBf16, SPLIT>(), grid, block, s, p);
     }
     return hipErrorInvalidValue;
 }
@@ -775,10 +776,11 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
 
 hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
                        const float *resid, void *out, int M, int N, int K, const QkvDst *qkv,
-                       hipStream_t stream, const LnResid *ln) {
+                       hipStream_t stream, const LnResid *ln, const bf16_t *aux) {
     if (M <= 0) return hipSuccess;
+    if (epi == Epi::GeluBwdBf16 && !aux) return hipErrorInvalidValue;
     GemmParams p{};
-    p.a = a; p.w = w; p.bias = bias; p.resid = resid; p.out = out;
+    p.a = a; p.w = w; p.bias = bias; p.resid = resid; p.out = out; p.aux = aux;
     p.M = M; p.N = N; p.K = K;
     if (qkv) p.qkv = *qkv;
     if (ln) p.ln = *ln;
@@ -808,7 +810,9 @@ hipError_t launch_skinny(Epi epi, const GemmParams &p, hipStream_t stream) {
     case Epi::BiasGeluBf16: return launch_kernel(skinny_kernel<Epi::BiasGeluBf16, G, NVL>, grid, block, stream, p);
     case Epi::BiasResidF32: return launch_kernel(skinny_kernel<Epi::BiasResidF32, G, NVL>, grid, block, stream, p);
     case Epi::Qkv: return launch_kernel(skinny_kernel<Epi::Qkv, G, NVL>, grid, block, stream, p);
-    case Epi::BiasLnResidF32: break;
+    case Epi::BiasLnResidF32:
+    case Epi::F32:
+    case Epi::GeluBwdBf16: break;
     }
     return hipErrorInvalidValue;
 }
@@ -843,7 +847,8 @@ hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const b
                               void *out, int M, int N, int K, const QkvDst *qkv, hipStream_t stream,
                               const LnIn *ln_in) {
     if (M <= 0) return hipSuccess;
-    if (M > 16 || N % 16 || K % 32 || epi == Epi::BiasLnResidF32) return hipErrorInvalidValue;
+    if (M > 16 || N % 16 || K % 32 || epi == Epi::BiasLnResidF32 || epi == Epi::F32 || epi == Epi::GeluBwdBf16)
+        return hipErrorInvalidValue;
     if (ln_in && !skinny_ln_fits(M, K)) return hipErrorInvalidValue;
     GemmParams p{};
     p.a = a; p.w = w; p.bias = bias; p.resid = resid; p.out = out;

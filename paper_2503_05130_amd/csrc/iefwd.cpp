@@ -10,6 +10,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
+#include <memory>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -128,6 +130,49 @@ struct LayerWeights {
     float *g1, *be1, *g2, *be2;
 };
 
+// Training state of an instance created with iefwd_train_create: the flat
+// fp32 optimiser state (master weights, gradients, two moments, one segment
+// per parameter tensor), transposed bf16 weights for the input-gradient
+// products, the activations the forward saves per layer, and the backward's
+// scratch.  One device allocation, carved.
+struct TrainState {
+    iefwd_train_params hp{};
+    uint64_t steps = 0;
+    void *blob = nullptr;
+    float *loss_host = nullptr;                   // pinned: the last step's summed token losses
+    // optimiser state, segments in (layer, slot) order then the head
+    float *master = nullptr, *grad = nullptr, *mom1 = nullptr, *mom2 = nullptr;
+    size_t n_params = 0;                          // padded element count
+    std::vector<std::array<size_t, 12>> off;      // per layer: element offset of each slot
+    size_t off_wh = 0, off_bh = 0;
+    std::vector<AdamSegment> segs;
+    AdamSegment *segs_d = nullptr;
+    uint32_t *blk_seg_d = nullptr;
+    int n_blocks = 0;
+    // W^T [in, out] bf16 of the four matrices per layer
+    struct Transposed {
+        bf16_t *wqkv, *wo, *w1, *w2;
+    };
+    std::vector<Transposed> wt;
+    // saved activations per layer (T = max_batch * max_seq rows)
+    struct Saved {
+        bf16_t *hb, *q, *k, *vt, *ctx, *h1b, *v, *u;
+        float *z1, *st1, *z2, *st2;
+    };
+    std::vector<Saved> saved;
+    // backward scratch
+    float *dxa = nullptr, *dxb = nullptr, *dz = nullptr, *xl = nullptr, *loss_t = nullptr, *dlogits = nullptr;
+    float *part = nullptr, *part2 = nullptr, *loss_sum = nullptr;
+    bf16_t *dzb = nullptr, *dvb = nullptr, *dctx = nullptr, *dqkv = nullptr, *ta = nullptr, *tb = nullptr;
+    bf16_t *zero_bias = nullptr;
+    int32_t *labels = nullptr;
+
+    ~TrainState() {
+        if (blob) (void)hipFree(blob);
+        if (loss_host) (void)hipHostFree(loss_host);
+    }
+};
+
 }  // namespace
 
 struct iefwd_instance {
@@ -177,6 +222,8 @@ struct iefwd_instance {
     } timing[IEFWD_K_COUNT];
     std::vector<hipEvent_t> event_pool;
     uint64_t kernels_launched = 0;   // every kernel this instance has launched
+
+    std::unique_ptr<TrainState> train;   // iefwd_train_create only
 
     ~iefwd_instance();
 };
@@ -532,6 +579,314 @@ void wait_batch(iefwd_instance *I) {
     I->state = iefwd_instance::State::Done;
 }
 
+// ----------------------------------------------------------------------------- training
+
+void validate_train(const iefwd_config &c, const iefwd_train_params &p) {
+    if (p.abi_version != IEFWD_ABI_VERSION) fail(IEFWD_EVERSION, "train params abi_version mismatch");
+    auto bad = [](const char *m) { fail(IEFWD_EINVAL, m); };
+    if (c.pre_ln) bad("training covers post-LN stacks (pre_ln = 0)");
+    if (c.kv_cache) bad("a training instance keeps no KV cache");
+    if (c.n_out < 1) bad("training needs a head: n_out classes in [1, 16]");
+    if (c.d_model / c.n_heads != 64) bad("training needs head dim 64");
+    if (c.max_seq > 128) bad("training needs max_seq <= 128");
+    if (!(p.lr >= 0.f) || !std::isfinite(p.lr)) bad("lr must be finite and >= 0");
+    if (!(p.beta1 >= 0.f && p.beta1 < 1.f) || !(p.beta2 >= 0.f && p.beta2 < 1.f)) bad("betas must be in [0, 1)");
+    if (!(p.eps > 0.f) || !std::isfinite(p.eps)) bad("eps must be positive and finite");
+    if (!(p.weight_decay >= 0.f) || !std::isfinite(p.weight_decay)) bad("weight_decay must be finite and >= 0");
+}
+
+// Allocates the training state and initialises the fp32 master weights from
+// the instance's stored bf16 / fp32 weights, the moments to zero and W^T.
+void train_alloc(iefwd_instance *I, const iefwd_train_params &hp) {
+    const iefwd_config &c = I->cfg;
+    auto ts = std::make_unique<TrainState>();
+    TrainState &t = *ts;
+    t.hp = hp;
+    const size_t L = c.n_layers, d = c.d_model, F = c.d_ff, T = (size_t)c.max_batch * c.max_seq;
+    const size_t no = c.n_out, spad = (size_t)attn_seq_pad((int)c.max_seq);
+
+    // parameter segments, each padded to the AdamW block
+    const size_t blk = (size_t)adamw_block();
+    const size_t counts[12] = {3 * d * d, 3 * d, d * d, d, d, d, F * d, F, d * F, d, d, d};
+    size_t n = 0;
+    t.off.resize(L);
+    for (size_t l = 0; l < L; ++l)
+        for (int k = 0; k < 12; ++k) {
+            t.off[l][k] = n;
+            n += round_up(counts[k], blk);
+        }
+    t.off_wh = n;
+    n += round_up(no * d, blk);
+    t.off_bh = n;
+    n += round_up(no, blk);
+    t.n_params = n;
+
+    // one allocation
+    size_t bytes = 0;
+    auto reserve = [&](size_t b) { size_t o = bytes; bytes = round_up(bytes + b, 256); return o; };
+    const size_t o_master = reserve(n * 4), o_grad = reserve(n * 4), o_m = reserve(n * 4), o_v = reserve(n * 4);
+    const size_t n_seg = 12 * L + 2;
+    const size_t o_segs = reserve(n_seg * sizeof(AdamSegment)), o_blk = reserve(n / blk * 4);
+    std::vector<std::array<size_t, 4>> o_wt(L);
+    for (size_t l = 0; l < L; ++l)
+        o_wt[l] = {reserve(3 * d * d * 2), reserve(d * d * 2), reserve(d * F * 2), reserve(F * d * 2)};
+    struct SavedOff { size_t hb, q, k, vt, ctx, h1b, v, u, z1, st1, z2, st2; };
+    std::vector<SavedOff> o_sv(L);
+    for (size_t l = 0; l < L; ++l)
+        o_sv[l] = {reserve(T * d * 2), reserve(T * d * 2), reserve(T * d * 2), reserve(c.max_batch * d * spad * 2),
+                   reserve(T * d * 2), reserve(T * d * 2), reserve(T * F * 2), reserve(T * F * 2),
+                   reserve(T * d * 4), reserve(T * 8), reserve(T * d * 4), reserve(T * 8)};
+    const size_t wide = std::max(F, 3 * d), parts = (size_t)colsum_partials((int)T);
+    const size_t o_dxa = reserve(T * d * 4), o_dxb = reserve(T * d * 4), o_dz = reserve(T * d * 4);
+    const size_t o_xl = reserve(T * d * 4), o_loss = reserve(T * 4), o_dl = reserve(T * no * 4);
+    const size_t o_part = reserve(parts * std::max(wide, no * d) * 4), o_part2 = reserve(parts * std::max(wide, no * d) * 4);
+    const size_t o_lsum = reserve(parts * 4 + 4);
+    const size_t o_dzb = reserve(T * d * 2), o_dvb = reserve(T * F * 2), o_dctx = reserve(T * d * 2);
+    const size_t o_dqkv = reserve(T * 3 * d * 2), o_ta = reserve(wide * T * 2), o_tb = reserve(wide * T * 2);
+    const size_t o_zero = reserve(wide * 2), o_lab = reserve(T * 4);
+    if (hipMalloc(&t.blob, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        t.blob = nullptr;
+        fail(IEFWD_ENOMEM, "device allocation of the training state failed");
+    }
+    if (hipHostMalloc(reinterpret_cast<void **>(&t.loss_host), 4) != hipSuccess) {
+        (void)hipGetLastError();
+        t.loss_host = nullptr;
+        fail(IEFWD_ENOMEM, "pinned host allocation failed");
+    }
+    char *b = static_cast<char *>(t.blob);
+    auto f32 = [&](size_t o) { return reinterpret_cast<float *>(b + o); };
+    auto b16 = [&](size_t o) { return reinterpret_cast<bf16_t *>(b + o); };
+    t.master = f32(o_master);
+    t.grad = f32(o_grad);
+    t.mom1 = f32(o_m);
+    t.mom2 = f32(o_v);
+    t.segs_d = reinterpret_cast<AdamSegment *>(b + o_segs);
+    t.blk_seg_d = reinterpret_cast<uint32_t *>(b + o_blk);
+    for (size_t l = 0; l < L; ++l) {
+        t.wt.push_back({b16(o_wt[l][0]), b16(o_wt[l][1]), b16(o_wt[l][2]), b16(o_wt[l][3])});
+        const SavedOff &o = o_sv[l];
+        t.saved.push_back({b16(o.hb), b16(o.q), b16(o.k), b16(o.vt), b16(o.ctx), b16(o.h1b), b16(o.v), b16(o.u),
+                           f32(o.z1), f32(o.st1), f32(o.z2), f32(o.st2)});
+    }
+    t.dxa = f32(o_dxa); t.dxb = f32(o_dxb); t.dz = f32(o_dz); t.xl = f32(o_xl); t.loss_t = f32(o_loss);
+    t.dlogits = f32(o_dl); t.part = f32(o_part); t.part2 = f32(o_part2); t.loss_sum = f32(o_lsum);
+    t.dzb = b16(o_dzb); t.dvb = b16(o_dvb); t.dctx = b16(o_dctx); t.dqkv = b16(o_dqkv); t.ta = b16(o_ta);
+    t.tb = b16(o_tb); t.zero_bias = b16(o_zero);
+    t.labels = reinterpret_cast<int32_t *>(b + o_lab);
+
+    // segments: where each tensor's updated value goes (the forward's copy)
+    for (size_t l = 0; l < L; ++l) {
+        const LayerWeights &w = I->layers[l];
+        void *outs[12] = {w.wqkv, w.bqkv, w.wo, w.bo, w.g1, w.be1, w.w1, w.b1, w.w2, w.b2, w.g2, w.be2};
+        for (int k = 0; k < 12; ++k) {
+            const bool is_f32 = k == 4 || k == 5 || k == 10 || k == 11;
+            const bool decay = k == 0 || k == 2 || k == 6 || k == 8;
+            t.segs.push_back({t.off[l][k], counts[k], outs[k], is_f32 ? 0 : 1, decay ? 1 : 0});
+        }
+    }
+    t.segs.push_back({t.off_wh, no * d, I->wh, 1, 1});
+    t.segs.push_back({t.off_bh, no, I->bh, 1, 0});
+    std::vector<uint32_t> blk_seg(n / blk);
+    for (size_t si = 0; si < t.segs.size(); ++si) {
+        const size_t b0 = t.segs[si].offset / blk, b1 = (t.segs[si].offset + t.segs[si].count + blk - 1) / blk;
+        for (size_t bb = b0; bb < b1; ++bb) blk_seg[bb] = (uint32_t)si;
+    }
+    t.n_blocks = (int)blk_seg.size();
+    hipStream_t s = I->stream;
+    hip_check(hipMemcpyAsync(t.segs_d, t.segs.data(), t.segs.size() * sizeof(AdamSegment), hipMemcpyHostToDevice, s),
+              "segment upload");
+    hip_check(hipMemcpyAsync(t.blk_seg_d, blk_seg.data(), blk_seg.size() * 4, hipMemcpyHostToDevice, s),
+              "segment upload");
+    hip_check(hipMemsetAsync(t.master, 0, n * 4, s), "hipMemsetAsync");
+    hip_check(hipMemsetAsync(t.grad, 0, n * 4, s), "hipMemsetAsync");
+    hip_check(hipMemsetAsync(t.mom1, 0, n * 4, s), "hipMemsetAsync");
+    hip_check(hipMemsetAsync(t.mom2, 0, n * 4, s), "hipMemsetAsync");
+    hip_check(hipMemsetAsync(t.zero_bias, 0, wide * 2, s), "hipMemsetAsync");
+    for (const AdamSegment &sg : t.segs) {
+        if (sg.out_bf16)
+            hip_check(launch_bf16_to_f32(static_cast<const bf16_t *>(sg.out), t.master + sg.offset, sg.count, s),
+                      "master init");
+        else
+            hip_check(hipMemcpyAsync(t.master + sg.offset, sg.out, sg.count * 4, hipMemcpyDeviceToDevice, s),
+                      "master init");
+    }
+    for (size_t l = 0; l < L; ++l) {
+        const LayerWeights &w = I->layers[l];
+        hip_check(launch_transpose_bf16(w.wqkv, t.wt[l].wqkv, (int)(3 * d), (int)d, s), "transpose");
+        hip_check(launch_transpose_bf16(w.wo, t.wt[l].wo, (int)d, (int)d, s), "transpose");
+        hip_check(launch_transpose_bf16(w.w1, t.wt[l].w1, (int)F, (int)d, s), "transpose");
+        hip_check(launch_transpose_bf16(w.w2, t.wt[l].w2, (int)d, (int)F, s), "transpose");
+    }
+    hip_check(hipStreamSynchronize(s), "hipStreamSynchronize");
+    I->train = std::move(ts);
+}
+
+// One training step on I->stream: forward with saved activations, loss, backward,
+// AdamW, then W^T refreshed.  x fp32 [B*S, d] and labels int32 [B*S] on the device.
+void train_run(iefwd_instance *I, const float *x) {
+    TrainState &t = *I->train;
+    const iefwd_config &c = I->cfg;
+    const int B = (int)I->batch, S = (int)I->seq, T = B * S, d = (int)c.d_model, F = (int)c.d_ff;
+    const int H = (int)c.n_heads, dh = (int)I->head_dim, L = (int)c.n_layers, no = (int)c.n_out;
+    const int spad = attn_seq_pad(S);
+    const float eps = c.ln_eps;
+    const bool causal = c.causal != 0;
+    hipStream_t s = I->stream;
+    auto fwd = [&](uint32_t kind, const char *what, auto &&f) { launch(I, kind, what, f); };
+    auto bwd_gemm = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD_GEMM, what, f); };
+    auto bwd = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD, what, f); };
+    // column sums of a [rows, n] matrix into dst [n], two fixed-order stages
+    auto colsum = [&](const void *src, bool is_bf16, int rows, int n, float *dst) {
+        const int parts = colsum_partials(rows);
+        bwd("column sums", [&] { return launch_colsum(src, is_bf16, t.part2, rows, n, 64, s); });
+        bwd("column sums", [&] { return launch_colsum(t.part2, false, dst, parts, n, parts, s); });
+    };
+
+    // ---- forward, saving what the backward needs
+    for (int l = 0; l < L; ++l) {
+        const LayerWeights &w = I->layers[l];
+        const TrainState::Saved &sv = t.saved[l];
+        if (l == 0)
+            fwd(IEFWD_K_LN, "cast", [&] { return launch_cast_bf16(x, sv.hb, (size_t)T * d, s); });
+        const QkvDst qd{sv.q, sv.k, sv.vt, S, 0, S, spad, H, dh, d};
+        fwd(IEFWD_K_QKV, "qkv gemm",
+            [&] { return launch_gemm(Epi::Qkv, sv.hb, w.wqkv, w.bqkv, nullptr, nullptr, T, 3 * d, d, &qd, s); });
+        fwd(IEFWD_K_ATTN, "attention",
+            [&] { return launch_attention(sv.q, sv.k, sv.vt, sv.ctx, B, H, S, dh, causal, s, S, spad); });
+        if (l == 0) {
+            fwd(IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
+                return launch_gemm(Epi::BiasResidF32, sv.ctx, w.wo, w.bo, x, sv.z1, T, d, d, nullptr, s);
+            });
+        } else {
+            const LayerWeights &pw = I->layers[l - 1];
+            const LnResid r{t.saved[l - 1].z2, t.saved[l - 1].st2, pw.g2, pw.be2};
+            fwd(IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
+                return launch_gemm(Epi::BiasLnResidF32, sv.ctx, w.wo, w.bo, nullptr, sv.z1, T, d, d, nullptr, s, &r);
+            });
+        }
+        fwd(IEFWD_K_LN, "layernorm",
+            [&] { return launch_layernorm(sv.z1, w.g1, w.be1, nullptr, sv.h1b, T, d, eps, s, sv.st1); });
+        fwd(IEFWD_K_FFN1, "ffn1 gemm",
+            [&] { return launch_gemm(Epi::BiasBf16, sv.h1b, w.w1, w.b1, nullptr, sv.v, T, F, d, nullptr, s); });
+        fwd(IEFWD_K_FFN1, "gelu", [&] { return launch_gelu(sv.v, sv.u, (size_t)T * F, s); });
+        const LnResid r1{sv.z1, sv.st1, w.g1, w.be1};
+        fwd(IEFWD_K_FFN2, "ffn2 gemm", [&] {
+            return launch_gemm(Epi::BiasLnResidF32, sv.u, w.w2, w.b2, nullptr, sv.z2, T, d, F, nullptr, s, &r1);
+        });
+        if (l + 1 < L)
+            fwd(IEFWD_K_LN, "layernorm", [&] {
+                return launch_layernorm(sv.z2, w.g2, w.be2, nullptr, t.saved[l + 1].hb, T, d, eps, s, sv.st2);
+            });
+    }
+    // last LayerNorm + head + cross-entropy; dX of the last layer's output into dxa
+    {
+        const LayerWeights &w = I->layers[L - 1];
+        const TrainState::Saved &sv = t.saved[L - 1];
+        fwd(IEFWD_K_LN, "head + loss", [&] {
+            return launch_head_loss(sv.z2, w.g2, w.be2, I->wh, I->bh, t.labels, t.xl, sv.st2, I->out, t.loss_t,
+                                    t.dlogits, t.dxa, T, d, no, eps, 1.0f / (float)T, s);
+        });
+        bwd("head partials", [&] { return launch_head_partials(t.dlogits, t.xl, t.part, T, d, no, s); });
+        const int parts = colsum_partials(T);
+        bwd("column sums", [&] { return launch_colsum(t.part, false, t.grad + t.off_wh, parts, no * d, parts, s); });
+        colsum(t.dlogits, false, T, no, t.grad + t.off_bh);
+        colsum(t.loss_t, false, T, 1, t.loss_sum);
+    }
+
+    // ---- backward, last layer first; dxa holds dL/d(layer output)
+    auto ln_grads = [&](const float *dy, const float *z, const float *st, size_t off_g, size_t off_b) {
+        const int parts = colsum_partials(T);
+        bwd("layernorm param partials",
+            [&] { return launch_ln_param_partials(dy, z, st, t.part, t.part + (size_t)parts * d, T, d, s); });
+        bwd("column sums", [&] { return launch_colsum(t.part, false, t.grad + off_g, parts, d, parts, s); });
+        bwd("column sums",
+            [&] { return launch_colsum(t.part + (size_t)parts * d, false, t.grad + off_b, parts, d, parts, s); });
+    };
+    for (int l = L - 1; l >= 0; --l) {
+        const LayerWeights &w = I->layers[l];
+        const TrainState::Saved &sv = t.saved[l];
+        const TrainState::Transposed &wt = t.wt[l];
+        const auto &o = t.off[l];
+        // LN2: dz2 (fp32 in dz, bf16 in dzb)
+        bwd("layernorm backward", [&] { return launch_ln_backward(t.dxa, sv.z2, sv.st2, w.g2, t.dz, t.dzb, T, d, s); });
+        ln_grads(t.dxa, sv.z2, sv.st2, o[10], o[11]);
+        // FFN-down: dW2 = dz2^T u, db2, dv = (dz2 W2) GELU'(v)
+        colsum(t.dz, false, T, d, t.grad + o[9]);
+        bwd("transpose", [&] { return launch_transpose_bf16(t.dzb, t.ta, T, d, s); });
+        bwd("transpose", [&] { return launch_transpose_bf16(sv.u, t.tb, T, F, s); });
+        bwd_gemm("dW2 gemm", [&] {
+            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[8], d, F, T, nullptr, s);
+        });
+        bwd_gemm("dv gemm", [&] {
+            return launch_gemm(Epi::GeluBwdBf16, t.dzb, wt.w2, nullptr, nullptr, t.dvb, T, F, d, nullptr, s, nullptr,
+                               sv.v);
+        });
+        // FFN-up: dW1 = dv^T X1, db1, dX1 = dz2 + dv W1
+        colsum(t.dvb, true, T, F, t.grad + o[7]);
+        bwd("transpose", [&] { return launch_transpose_bf16(t.dvb, t.ta, T, F, s); });
+        bwd("transpose", [&] { return launch_transpose_bf16(sv.h1b, t.tb, T, d, s); });
+        bwd_gemm("dW1 gemm", [&] {
+            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[6], F, d, T, nullptr, s);
+        });
+        bwd_gemm("dX1 gemm", [&] {
+            return launch_gemm(Epi::BiasResidF32, t.dvb, wt.w1, t.zero_bias, t.dz, t.dxb, T, d, F, nullptr, s);
+        });
+        // LN1: dz1
+        bwd("layernorm backward", [&] { return launch_ln_backward(t.dxb, sv.z1, sv.st1, w.g1, t.dz, t.dzb, T, d, s); });
+        ln_grads(t.dxb, sv.z1, sv.st1, o[4], o[5]);
+        // out-projection: dWo = dz1^T ctx, dbo, dctx = dz1 Wo
+        colsum(t.dz, false, T, d, t.grad + o[3]);
+        bwd("transpose", [&] { return launch_transpose_bf16(t.dzb, t.ta, T, d, s); });
+        bwd("transpose", [&] { return launch_transpose_bf16(sv.ctx, t.tb, T, d, s); });
+        bwd_gemm("dWo gemm", [&] {
+            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[2], d, d, T, nullptr, s);
+        });
+        bwd_gemm("dctx gemm", [&] {
+            return launch_gemm(Epi::BiasBf16, t.dzb, wt.wo, t.zero_bias, nullptr, t.dctx, T, d, d, nullptr, s);
+        });
+        // attention
+        bwd("attention backward", [&] {
+            return launch_attention_backward(sv.q, sv.k, sv.vt, sv.ctx, t.dctx, t.dqkv, B, H, S, dh, spad, causal, s);
+        });
+        // QKV: dWqkv = dqkv^T X, dbqkv, dX = dz1 + dqkv Wqkv
+        colsum(t.dqkv, true, T, 3 * d, t.grad + o[1]);
+        bwd("transpose", [&] { return launch_transpose_bf16(t.dqkv, t.ta, T, 3 * d, s); });
+        bwd("transpose", [&] { return launch_transpose_bf16(sv.hb, t.tb, T, d, s); });
+        bwd_gemm("dWqkv gemm", [&] {
+            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[0], 3 * d, d, T, nullptr, s);
+        });
+        if (l > 0)
+            bwd_gemm("dX gemm", [&] {
+                return launch_gemm(Epi::BiasResidF32, t.dqkv, wt.wqkv, t.zero_bias, t.dz, t.dxa, T, d, 3 * d, nullptr,
+                                   s);
+            });
+    }
+
+    // ---- AdamW over every parameter, then W^T for the next step's input gradients
+    t.steps += 1;
+    AdamStep st{};
+    st.lr = t.hp.lr;
+    st.beta1 = t.hp.beta1;
+    st.beta2 = t.hp.beta2;
+    st.eps = t.hp.eps;
+    st.weight_decay = t.hp.weight_decay;
+    st.c1 = (float)(1.0 / (1.0 - std::pow((double)t.hp.beta1, (double)t.steps)));
+    st.c2 = (float)(1.0 / (1.0 - std::pow((double)t.hp.beta2, (double)t.steps)));
+    launch(I, IEFWD_K_OPTIM, "adamw", [&] {
+        return launch_adamw(t.master, t.grad, t.mom1, t.mom2, t.segs_d, t.blk_seg_d, t.n_blocks, st, s);
+    });
+    for (int l = 0; l < L; ++l) {
+        const LayerWeights &w = I->layers[l];
+        const TrainState::Transposed &wt = t.wt[l];
+        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transpose_bf16(w.wqkv, wt.wqkv, 3 * d, d, s); });
+        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transpose_bf16(w.wo, wt.wo, d, d, s); });
+        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transpose_bf16(w.w1, wt.w1, F, d, s); });
+        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transpose_bf16(w.w2, wt.w2, d, F, s); });
+    }
+    hip_check(hipMemcpyAsync(t.loss_host, t.loss_sum, 4, hipMemcpyDeviceToHost, s), "loss copy");
+}
+
 }  // namespace
 
 iefwd_instance::~iefwd_instance() {
@@ -545,6 +900,7 @@ iefwd_instance::~iefwd_instance() {
     for (hipEvent_t e : event_pool) (void)hipEventDestroy(e);
     for (hipEvent_t e : {ev_start, ev_end, ev_copy})
         if (e) (void)hipEventDestroy(e);
+    train.reset();
     if (wsblob) (void)hipFree(wsblob);
     if (kvblob) (void)hipFree(kvblob);
     if (wblob) (void)hipFree(wblob);
@@ -579,12 +935,15 @@ int iefwd_build_cu_mask(uint32_t n_cu, uint32_t n_xcd, uint32_t quota, uint32_t 
     });
 }
 
-int iefwd_create(const iefwd_config *cfg, int device, iefwd_instance **out) {
+namespace {
+
+int create_instance(const iefwd_config *cfg, const iefwd_train_params *tp, int device, iefwd_instance **out) {
     if (out) *out = nullptr;
     iefwd_instance *inst = nullptr;
     const int st = guarded([&] {
         if (!cfg || !out) fail(IEFWD_EINVAL, "NULL argument");
         validate_config(*cfg);
+        if (tp) validate_train(*cfg, *tp);
         const DeviceInfo dev = query_device(device);
         hip_check(hipSetDevice(device), "hipSetDevice");
         inst = new iefwd_instance();
@@ -602,6 +961,7 @@ int iefwd_create(const iefwd_config *cfg, int device, iefwd_instance **out) {
             fail(IEFWD_ENODEV, "device CU count is not a multiple of its XCD count");
         hip_check(inst->streams.acquire(all, &inst->stream), "hipExtStreamCreateWithCUMask");
         inst->mask = all;
+        if (tp) train_alloc(inst, *tp);
     });
     if (st != IEFWD_OK) {
         delete inst;
@@ -609,6 +969,130 @@ int iefwd_create(const iefwd_config *cfg, int device, iefwd_instance **out) {
     }
     *out = inst;
     return IEFWD_OK;
+}
+
+}  // namespace
+
+int iefwd_create(const iefwd_config *cfg, int device, iefwd_instance **out) {
+    return create_instance(cfg, nullptr, device, out);
+}
+
+void iefwd_train_params_init(iefwd_train_params *tp) {
+    if (!tp) return;
+    std::memset(tp, 0, sizeof *tp);
+    tp->abi_version = IEFWD_ABI_VERSION;
+    tp->lr = 1e-4f;
+    tp->beta1 = 0.9f;
+    tp->beta2 = 0.999f;
+    tp->eps = 1e-8f;
+    tp->weight_decay = 0.01f;
+}
+
+int iefwd_train_create(const iefwd_config *cfg, const iefwd_train_params *tp, int device, iefwd_instance **out) {
+    if (!tp) {
+        if (out) *out = nullptr;
+        return guarded([&] { fail(IEFWD_EINVAL, "train params are NULL"); });
+    }
+    return create_instance(cfg, tp, device, out);
+}
+
+int iefwd_train_step(iefwd_instance *inst, const float *x, const int32_t *labels, uint32_t batch, uint32_t seq,
+                     int inputs_are_device) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!inst->train) fail(IEFWD_ESTATE, "not a training instance (iefwd_train_create)");
+        if (!x || !labels) fail(IEFWD_EINVAL, "x or labels is NULL");
+        if (batch < 1 || batch > inst->cfg.max_batch) fail(IEFWD_EINVAL, "batch out of range [1, max_batch]");
+        if (seq < 1 || seq > inst->cfg.max_seq) fail(IEFWD_EINVAL, "seq out of range [1, max_seq]");
+        if (((uint64_t)batch * seq) % 64) fail(IEFWD_EINVAL, "batch * seq must be a multiple of 64");
+        if (inst->state == iefwd_instance::State::InFlight)
+            fail(IEFWD_ESTATE, "a step is already in flight; call iefwd_wait or iefwd_train_loss first");
+        on_device(inst, [&] {
+            apply_pending_quota(inst);
+            inst->batch = batch;
+            inst->seq = seq;
+            const size_t T = (size_t)batch * seq, n = T * inst->cfg.d_model;
+            const float *xin = x;
+            const hipMemcpyKind kind = inputs_are_device ? hipMemcpyDeviceToDevice : hipMemcpyHostToDevice;
+            hip_check(hipMemcpyAsync(inst->train->labels, labels, T * 4, kind, inst->stream), "label copy");
+            if (!inputs_are_device) {
+                hip_check(hipMemcpyAsync(inst->xstage, x, n * 4, hipMemcpyHostToDevice, inst->stream), "input copy");
+                xin = inst->xstage;
+            }
+            if (!inputs_are_device) {
+                hip_check(hipEventRecord(inst->ev_copy, inst->stream), "hipEventRecord");
+                hip_check(hipEventSynchronize(inst->ev_copy), "hipEventSynchronize");
+            }
+            hip_check(hipEventRecord(inst->ev_start, inst->stream), "hipEventRecord");
+            train_run(inst, xin);
+            hip_check(hipEventRecord(inst->ev_end, inst->stream), "hipEventRecord");
+            inst->state = iefwd_instance::State::InFlight;
+            inst->have_batch = true;
+        });
+    });
+}
+
+int iefwd_train_loss(iefwd_instance *inst, float *loss) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!loss) fail(IEFWD_EINVAL, "loss is NULL");
+        if (!inst->train) fail(IEFWD_ESTATE, "not a training instance (iefwd_train_create)");
+        if (inst->train->steps == 0) fail(IEFWD_ESTATE, "no training step has run");
+        on_device(inst, [&] { wait_batch(inst); });
+        *loss = inst->train->loss_host[0] / (float)((uint64_t)inst->batch * inst->seq);
+    });
+}
+
+int iefwd_train_steps(const iefwd_instance *inst, uint64_t *steps) {
+    return guarded([&] {
+        if (!inst || !steps) fail(IEFWD_EINVAL, "NULL argument");
+        *steps = inst->train ? inst->train->steps : 0;
+    });
+}
+
+int iefwd_train_export(iefwd_instance *inst, uint32_t layer, uint32_t slot, uint32_t what, float *host_dst,
+                       size_t n_floats) {
+    return guarded([&] {
+        check_alive(inst);
+        if (!host_dst) fail(IEFWD_EINVAL, "host_dst is NULL");
+        if (!inst->train) fail(IEFWD_ESTATE, "not a training instance (iefwd_train_create)");
+        if (what > IEFWD_TRAIN_MOMENT2) fail(IEFWD_EINVAL, "unknown optimiser tensor");
+        const iefwd_config &c = inst->cfg;
+        const TrainState &t = *inst->train;
+        const size_t d = c.d_model, F = c.d_ff;
+        size_t off = 0, rows = 1, cols = 0;   // logical [rows = in, cols = out]; stored [out, in]
+        bool matrix = false;
+        if (layer < c.n_layers) {
+            if (slot > 11) fail(IEFWD_EINVAL, "per-layer slot must be 0..11");
+            off = t.off[layer][slot];
+            const size_t in[12] = {d, 1, d, 1, 1, 1, d, 1, F, 1, 1, 1};
+            const size_t outn[12] = {3 * d, 3 * d, d, d, d, d, F, F, d, d, d, d};
+            rows = in[slot];
+            cols = outn[slot];
+            matrix = slot == 0 || slot == 2 || slot == 6 || slot == 8;
+        } else if (layer == c.n_layers && (slot == 14 || slot == 15)) {
+            off = slot == 14 ? t.off_wh : t.off_bh;
+            rows = slot == 14 ? d : 1;
+            cols = c.n_out;
+            matrix = slot == 14;
+        } else {
+            fail(IEFWD_EINVAL, "layer / slot out of range (the head is slots 14, 15 of layer n_layers)");
+        }
+        if (n_floats != rows * cols) fail(IEFWD_EINVAL, "n_floats does not match the tensor size");
+        const float *base[4] = {t.master, t.grad, t.mom1, t.mom2};
+        on_device(inst, [&] {
+            wait_batch(inst);
+            std::vector<float> stored(rows * cols);
+            hip_check(hipMemcpy(stored.data(), base[what] + off, stored.size() * 4, hipMemcpyDeviceToHost),
+                      "export copy");
+            if (!matrix) {
+                std::memcpy(host_dst, stored.data(), stored.size() * 4);
+                return;
+            }
+            for (size_t o = 0; o < cols; ++o)
+                for (size_t i = 0; i < rows; ++i) host_dst[i * cols + o] = stored[o * rows + i];
+        });
+    });
 }
 
 int iefwd_destroy(iefwd_instance *inst) {

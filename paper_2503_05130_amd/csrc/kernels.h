@@ -45,6 +45,8 @@ enum class Epi : int {
     BiasResidF32 = 2,   // out f32  = resid + acc + b
     Qkv = 3,            // acc + b scattered to Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad]
     BiasLnResidF32 = 4, // out f32  = LN(z) + acc + b, LN(z) rebuilt from z and its row stats
+    F32 = 5,            // out f32  = acc                      (weight gradients)
+    GeluBwdBf16 = 6,    // out bf16 = acc * GELU'(aux), aux bf16 [M, N] (the GELU's input)
 };
 
 // Row statistics a LayerNorm kernel leaves for a later consumer: the residual
@@ -82,7 +84,8 @@ inline int attn_seq_pad(int seq) { return (seq + 63) / 64 * 64; }
 // Requires N % 64 == 0, K % 64 == 0, M >= 1.
 hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
                        const float *resid, void *out, int M, int N, int K,
-                       const QkvDst *qkv, hipStream_t stream, const LnResid *ln = nullptr);
+                       const QkvDst *qkv, hipStream_t stream, const LnResid *ln = nullptr,
+                       const bf16_t *aux = nullptr);
 
 // Activations given as LayerNorm(z): z fp32 [M, K] rows, gamma / beta fp32 [K].
 struct LnIn {
@@ -125,6 +128,61 @@ int decode_attention_chunks(int n_keys);
 hipError_t launch_decode_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx,
                                    int batch, int n_heads, int n_keys, int head_dim, int k_rows,
                                    int vt_stride, float *partials, hipStream_t stream);
+
+// ---- training step (csrc/train.hip) ----
+// bf16 [R, C] -> [C, R]; R % 64 == 0, C % 64 == 0.
+hipError_t launch_transpose_bf16(const bf16_t *src, bf16_t *dst, int R, int C, hipStream_t stream);
+// u = GELU(v) elementwise, bf16; n % 8 == 0.
+hipError_t launch_gelu(const bf16_t *v, bf16_t *u, size_t n, hipStream_t stream);
+// LayerNorm backward per row: dz = rstd (g - mean(g) - x^ mean(g x^)), g = dy gamma,
+// x^ = (z - mean) rstd with the forward's {mean, rstd}.  dz (fp32, may be null)
+// and dzb (bf16) [rows, d]; d % 4 == 0.
+hipError_t launch_ln_backward(const float *dy, const float *z, const float *stats, const float *gamma, float *dz,
+                              bf16_t *dzb, int rows, int d, hipStream_t stream);
+// Column-sum partials over blocks of 64 rows: colsum_partials(rows) of them.
+int colsum_partials(int rows);
+// part_g[b][f] = sum_r dy x^, part_b[b][f] = sum_r dy over the rows of block b.
+hipError_t launch_ln_param_partials(const float *dy, const float *z, const float *stats, float *part_g,
+                                    float *part_b, int rows, int d, hipStream_t stream);
+// dst[b][f] = sum of src[r][f] over rows b * rows_per_part .. (b + 1) * rows_per_part - 1, in row order.
+hipError_t launch_colsum(const void *src, bool src_bf16, float *dst, int rows, int n, int rows_per_part,
+                         hipStream_t stream);
+// Per token: the last LayerNorm of z (two-pass statistics), logits = X Wh^T + bh,
+// softmax cross-entropy against labels, dlogits = (p - onehot) * inv_n, dX = dlogits Wh.
+// Writes xl = X (fp32 [rows, d]), stats, logits and dlogits [rows, n_out],
+// loss_t [rows] (the token's loss) and dx [rows, d].  n_out <= 16.
+hipError_t launch_head_loss(const float *z, const float *gamma, const float *beta, const bf16_t *wh,
+                            const bf16_t *bh, const int32_t *labels, float *xl, float *stats, float *logits,
+                            float *loss_t, float *dlogits, float *dx, int rows, int d, int n_out, float eps,
+                            float inv_n, hipStream_t stream);
+// part[b][c * d + f] = sum over block b's rows of dlogits[r][c] xl[r][f].
+hipError_t launch_head_partials(const float *dlogits, const float *xl, float *part, int rows, int d, int n_out,
+                                hipStream_t stream);
+// Attention backward for seq <= 128, head_dim 64: from Q, K [B,H,S,dh], V^T
+// [B,H,dh,vt_stride], the forward's context and its gradient (bf16 [B*S, H*dh])
+// to dQ | dK | dV as bf16 [B*S, 3 H dh] (the QKV product's column order).
+hipError_t launch_attention_backward(const bf16_t *q, const bf16_t *k, const bf16_t *vt, const bf16_t *ctx,
+                                     const bf16_t *dctx, bf16_t *dqkv, int batch, int n_heads, int seq, int head_dim,
+                                     int vt_stride, bool causal, hipStream_t stream);
+
+// One parameter tensor of the flat AdamW state: elements offset .. offset +
+// count - 1 (offset a multiple of adamw_block()); after the update the new
+// value is also written to out[k] (bf16 when out_bf16, else fp32).
+struct AdamSegment {
+    size_t offset;
+    size_t count;
+    void *out;
+    int32_t out_bf16;
+    int32_t decay;
+};
+// Hyper-parameters of one step; c1 = 1 / (1 - beta1^t), c2 = 1 / (1 - beta2^t).
+struct AdamStep {
+    float lr, beta1, beta2, eps, weight_decay, c1, c2;
+};
+int adamw_block();
+hipError_t launch_adamw(float *w, const float *g, float *m, float *v, const AdamSegment *segs,
+                        const uint32_t *blk_seg, int n_blocks, const AdamStep &st, hipStream_t stream);
+hipError_t launch_bf16_to_f32(const bf16_t *src, float *dst, size_t n, hipStream_t stream);
 
 // Row LayerNorm, d % 128 == 0, d <= 4096.  out_f32 / out_bf16 / stats may be
 // null; stats receives {mean, rstd} per row.

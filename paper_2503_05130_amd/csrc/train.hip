@@ -1,0 +1,531 @@
+// Training-step kernels for gfx950: what a post-LN encoder's backward pass and
+// optimiser need beyond the forward kernels and the GEMM.
+//
+//   transpose          bf16 [R, C] -> [C, R] through 64 x 64 LDS tiles (the
+//                      GEMM contracts over its operands' contiguous dimension,
+//                      so weight gradients, which contract over tokens, read
+//                      transposed activations)
+//   gelu               u = GELU(v), bf16 -> bf16
+//   ln_backward        dz = rstd (g - mean(g) - x^ mean(g x^)), g = dy gamma,
+//                      one wave per row, fp32; writes fp32 and bf16
+//   ln_param_partials  per 64-row block: sum dy x^ and sum dy per column
+//   colsum             per row block: column sums (fp32 or bf16 input), fixed order
+//   head_loss          per token: the last LayerNorm, logits = X Wh^T + bh,
+//                      softmax cross-entropy, dlogits = (p - onehot) / N,
+//                      dX = dlogits Wh
+//   head_partials      per 64-row block: sum dlogits^T X (the head's gradient)
+//   attention_backward per (batch, head), S <= 128: P recomputed from Q and K,
+//                      dS = P (dP - D), D = rowsum(dO O); dQ, dK, dV
+//   adamw              one pass over every parameter (fp32 master, moments),
+//                      writing the forward's bf16 (or fp32) copy
+// Every reduction runs in a fixed order, so a training step is deterministic.
+#include "gelu.h"
+#include "kernels.h"
+
+namespace iefwd {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ inline float bf(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+__device__ inline uint16_t to_bf(float f) {
+    __bf16 b = (__bf16)f;   // round to nearest even
+    return __builtin_bit_cast(uint16_t, b);
+}
+
+__device__ inline float wave_sum(float v) {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+    return v;
+}
+
+// ------------------------------------------------------------------ transpose
+constexpr int kTile = 64;
+
+__global__ __launch_bounds__(256) void transpose_kernel(const uint16_t *__restrict__ src, uint16_t *__restrict__ dst,
+                                                        int R, int C) {
+    __shared__ uint16_t tile[kTile][kTile + 2];
+    const int r0 = blockIdx.y * kTile, c0 = blockIdx.x * kTile, tid = threadIdx.x;
+    // in: rows r0 + tid / 8 (+ 32), 8 columns each (16 bytes)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int r = tid / 8 + 32 * h, c = (tid % 8) * 8;
+        const u32x4 v = *reinterpret_cast<const u32x4 *>(src + (size_t)(r0 + r) * C + c0 + c);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            tile[r][c + 2 * e] = (uint16_t)(v[e] & 0xffffu);
+            tile[r][c + 2 * e + 1] = (uint16_t)(v[e] >> 16);
+        }
+    }
+    __syncthreads();
+    // out: rows c0 + tid / 8 (+ 32) of dst, 8 source rows each
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int cc = tid / 8 + 32 * h, rr = (tid % 8) * 8;
+        u32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (uint32_t)tile[rr + 2 * e][cc] | ((uint32_t)tile[rr + 2 * e + 1][cc] << 16);
+        *reinterpret_cast<u32x4 *>(dst + (size_t)(c0 + cc) * R + r0 + rr) = v;
+    }
+}
+
+// ------------------------------------------------------------------ GELU
+__global__ __launch_bounds__(256) void gelu_kernel(const uint16_t *__restrict__ v, uint16_t *__restrict__ u,
+                                                   size_t n8) {
+    const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n8) return;
+    const u32x4 x = reinterpret_cast<const u32x4 *>(v)[i];
+    u32x4 y;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float lo = gelu(__uint_as_float(x[e] << 16)), hi = gelu(__uint_as_float(x[e] & 0xffff0000u));
+        y[e] = (uint32_t)to_bf(lo) | ((uint32_t)to_bf(hi) << 16);
+    }
+    reinterpret_cast<u32x4 *>(u)[i] = y;
+}
+
+// ------------------------------------------------------------------ LayerNorm backward
+constexpr int kRowsPerBlock = 4;   // one wave per row
+
+// Two passes over the row (the second re-reads dy and z from the cache):
+// sums of g and g x^, then dz.  x^ = (z - mean) rstd with the forward's
+// statistics.  d % 4 == 0.
+__global__ __launch_bounds__(64 * kRowsPerBlock) void ln_backward_kernel(
+    const float *__restrict__ dy, const float *__restrict__ z, const float *__restrict__ stats,
+    const float *__restrict__ gamma, float *__restrict__ dz, uint16_t *__restrict__ dzb, int rows, int d) {
+    const int lane = threadIdx.x & 63, row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const float mean = stats[2 * (size_t)row], rstd = stats[2 * (size_t)row + 1];
+    const f32x4 *dyr = reinterpret_cast<const f32x4 *>(dy + (size_t)row * d);
+    const f32x4 *zr = reinterpret_cast<const f32x4 *>(z + (size_t)row * d);
+    const f32x4 *g4 = reinterpret_cast<const f32x4 *>(gamma);
+    const int nv = d / 4;
+    float sg = 0.f, sgx = 0.f;
+    for (int i = lane; i < nv; i += 64) {
+        const f32x4 a = dyr[i], zz = zr[i], g = g4[i];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float gg = a[e] * g[e], xh = (zz[e] - mean) * rstd;
+            sg += gg;
+            sgx += gg * xh;
+        }
+    }
+    const float inv_d = 1.0f / (float)d;
+    const float mg = wave_sum(sg) * inv_d, mgx = wave_sum(sgx) * inv_d;
+    for (int i = lane; i < nv; i += 64) {
+        const f32x4 a = dyr[i], zz = zr[i], g = g4[i];
+        f32x4 o;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float xh = (zz[e] - mean) * rstd;
+            o[e] = rstd * (a[e] * g[e] - mg - xh * mgx);
+        }
+        if (dz) reinterpret_cast<f32x4 *>(dz + (size_t)row * d)[i] = o;
+        reinterpret_cast<u32x2 *>(dzb + (size_t)row * d)[i] =
+            u32x2{(uint32_t)to_bf(o[0]) | ((uint32_t)to_bf(o[1]) << 16), (uint32_t)to_bf(o[2]) | ((uint32_t)to_bf(o[3]) << 16)};
+    }
+}
+
+// ------------------------------------------------------------------ column sums
+constexpr int kColRows = 64;   // rows per partial
+
+// partial_g[b][f] = sum over rows of block b of dy x^, partial_b[b][f] = sum dy
+__global__ __launch_bounds__(256) void ln_param_partials_kernel(
+    const float *__restrict__ dy, const float *__restrict__ z, const float *__restrict__ stats,
+    float *__restrict__ part_g, float *__restrict__ part_b, int rows, int d) {
+    const int f = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+    if (f >= d) return;
+    float sg = 0.f, sb = 0.f;
+    const int r1 = min(rows, (b + 1) * kColRows);
+    for (int r = b * kColRows; r < r1; ++r) {
+        const float a = dy[(size_t)r * d + f];
+        sg += a * ((z[(size_t)r * d + f] - stats[2 * (size_t)r]) * stats[2 * (size_t)r + 1]);
+        sb += a;
+    }
+    part_g[(size_t)b * d + f] = sg;
+    part_b[(size_t)b * d + f] = sb;
+}
+
+template <typename T>
+__device__ inline float load_as_f32(const T *p, size_t i);
+template <>
+__device__ inline float load_as_f32<float>(const float *p, size_t i) { return p[i]; }
+template <>
+__device__ inline float load_as_f32<uint16_t>(const uint16_t *p, size_t i) { return bf(p[i]); }
+
+// dst[b][f] = sum of src rows b * rb .. b * rb + rb - 1, column f, in row order
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_kernel(const T *__restrict__ src, float *__restrict__ dst, int rows,
+                                                     int n, int rb) {
+    const int f = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+    if (f >= n) return;
+    float s = 0.f;
+    const int r1 = min(rows, (b + 1) * rb);
+    for (int r = b * rb; r < r1; ++r) s += load_as_f32(src, (size_t)r * n + f);
+    dst[(size_t)b * n + f] = s;
+}
+
+// ------------------------------------------------------------------ head + loss
+// One wave per token.  The last LayerNorm (two-pass statistics, the forward
+// LayerNorm kernel's expression), logits = X Wh^T + bh, softmax cross-entropy
+// against the label, dlogits = (p - onehot) * inv_n, dX = dlogits Wh.
+// Writes X (fp32), the statistics, logits, per-token loss, dlogits and dX.
+// d % 4 == 0, n_out <= 16.
+__global__ __launch_bounds__(64 * kRowsPerBlock) void head_loss_kernel(
+    const float *__restrict__ z, const float *__restrict__ gamma, const float *__restrict__ beta,
+    const uint16_t *__restrict__ wh, const uint16_t *__restrict__ bh, const int32_t *__restrict__ labels,
+    float *__restrict__ xl, float *__restrict__ stats, float *__restrict__ logits, float *__restrict__ loss_t,
+    float *__restrict__ dlogits, float *__restrict__ dx, int rows, int d, int n_out, float eps, float inv_n) {
+    const int lane = threadIdx.x & 63, row = blockIdx.x * kRowsPerBlock + (threadIdx.x >> 6);
+    if (row >= rows) return;
+    const int nv = d / 4;
+    const f32x4 *zr = reinterpret_cast<const f32x4 *>(z + (size_t)row * d);
+    float s = 0.f;
+    for (int i = lane; i < nv; i += 64) {
+        const f32x4 a = zr[i];
+        s += a[0] + a[1] + a[2] + a[3];
+    }
+    const float inv_d = 1.0f / (float)d;
+    const float mean = wave_sum(s) * inv_d;
+    float ss = 0.f;
+    for (int i = lane; i < nv; i += 64) {
+        const f32x4 a = zr[i];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const float c = a[e] - mean;
+            ss += c * c;
+        }
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(ss) * inv_d + eps);
+    float acc[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c) acc[c] = 0.f;
+    for (int i = lane; i < nv; i += 64) {
+        const f32x4 a = zr[i], g = reinterpret_cast<const f32x4 *>(gamma)[i], b = reinterpret_cast<const f32x4 *>(beta)[i];
+        f32x4 x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = __builtin_fmaf(g[e], (a[e] - mean) * rstd, b[e]);
+        reinterpret_cast<f32x4 *>(xl + (size_t)row * d)[i] = x;
+#pragma unroll
+        for (int c = 0; c < 16; ++c)
+            if (c < n_out) {
+                const u32x2 w = *reinterpret_cast<const u32x2 *>(wh + (size_t)c * d + 4 * i);
+                acc[c] += x[0] * __uint_as_float(w[0] << 16) + x[1] * __uint_as_float(w[0] & 0xffff0000u) +
+                          x[2] * __uint_as_float(w[1] << 16) + x[3] * __uint_as_float(w[1] & 0xffff0000u);
+            }
+    }
+    float lg[16], mx = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+        if (c < n_out) {
+            lg[c] = wave_sum(acc[c]) + bf(bh[c]);
+            mx = fmaxf(mx, lg[c]);
+        }
+    float se = 0.f;
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+        if (c < n_out) se += __expf(lg[c] - mx);
+    const float lse = mx + __logf(se);
+    const int label = labels[row];
+    float dl[16];
+#pragma unroll
+    for (int c = 0; c < 16; ++c)
+        if (c < n_out) dl[c] = (__expf(lg[c] - lse) - (c == label ? 1.0f : 0.0f)) * inv_n;
+    if (lane < n_out) {
+        float l = 0.f, g = 0.f;
+#pragma unroll
+        for (int c = 0; c < 16; ++c)
+            if (c == lane) {
+                l = lg[c];
+                g = dl[c];
+            }
+        logits[(size_t)row * n_out + lane] = l;
+        dlogits[(size_t)row * n_out + lane] = g;
+    }
+    if (lane == 0) {
+        float ll = 0.f;
+#pragma unroll
+        for (int c = 0; c < 16; ++c)
+            if (c == label) ll = lg[c];
+        loss_t[row] = lse - ll;
+        stats[2 * (size_t)row] = mean;
+        stats[2 * (size_t)row + 1] = rstd;
+    }
+    for (int i = lane; i < nv; i += 64) {
+        f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < 16; ++c)
+            if (c < n_out) {
+                const u32x2 w = *reinterpret_cast<const u32x2 *>(wh + (size_t)c * d + 4 * i);
+                o[0] += dl[c] * __uint_as_float(w[0] << 16);
+                o[1] += dl[c] * __uint_as_float(w[0] & 0xffff0000u);
+                o[2] += dl[c] * __uint_as_float(w[1] << 16);
+                o[3] += dl[c] * __uint_as_float(w[1] & 0xffff0000u);
+            }
+        reinterpret_cast<f32x4 *>(dx + (size_t)row * d)[i] = o;
+    }
+}
+
+// part[b][c * d + f] = sum over rows of block b of dlogits[r][c] * xl[r][f]
+__global__ __launch_bounds__(256) void head_partials_kernel(const float *__restrict__ dlogits,
+                                                            const float *__restrict__ xl, float *__restrict__ part,
+                                                            int rows, int d, int n_out) {
+    const int idx = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
+    if (idx >= n_out * d) return;
+    const int c = idx / d, f = idx - c * d;
+    float s = 0.f;
+    const int r1 = min(rows, (b + 1) * kColRows);
+    for (int r = b * kColRows; r < r1; ++r) s += dlogits[(size_t)r * n_out + c] * xl[(size_t)r * d + f];
+    part[(size_t)b * n_out * d + idx] = s;
+}
+
+// ------------------------------------------------------------------ attention backward
+// One workgroup (256 threads) per (batch, head); S <= 128 keys, DH in {64, 128}.
+// K, V, Q and dO of the head live in LDS as bf16; query rows go in blocks of
+// 32: P and dS of the block in LDS (fp32), then dQ of the block, and the
+// block's contributions to dK and dV, which each thread accumulates for its
+// (key, half of dh) in registers.  fp32 arithmetic throughout.
+constexpr int kAbSeq = 128, kAbQb = 32;
+
+template <int DH>
+__global__ __launch_bounds__(256) void attention_backward_kernel(
+    const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K, const uint16_t *__restrict__ Vt,
+    const uint16_t *__restrict__ ctx, const uint16_t *__restrict__ dctx, uint16_t *__restrict__ dqkv, int n_heads,
+    int S, int vt_stride, int causal, float scale) {
+    constexpr int LD = DH + 8;                 // bf16 row stride in LDS
+    __shared__ uint16_t sq[kAbSeq * LD], sk[kAbSeq * LD], sv[kAbSeq * LD], sdo[kAbSeq * LD];
+    __shared__ float sp[kAbQb][kAbSeq + 1], sds[kAbQb][kAbSeq + 1];
+    __shared__ float sD[kAbSeq];
+    const int tid = threadIdx.x, bh = blockIdx.x, b = bh / n_heads, h = bh - b * n_heads;
+    const int d = n_heads * DH;
+    const size_t tok0 = (size_t)b * S;
+    const uint16_t *Qh = Q + (size_t)bh * S * DH, *Kh = K + (size_t)bh * S * DH, *Vh = Vt + (size_t)bh * DH * vt_stride;
+
+    // load the head's operands; D_i = sum_c dO[i][c] O[i][c]
+    for (int idx = tid; idx < S * DH; idx += 256) {
+        const int i = idx / DH, c = idx - i * DH;
+        sq[i * LD + c] = Qh[idx];
+        sk[i * LD + c] = Kh[idx];
+        sv[i * LD + c] = Vh[(size_t)c * vt_stride + i];
+        sdo[i * LD + c] = dctx[(tok0 + i) * d + h * DH + c];
+    }
+    for (int i = tid; i < S; i += 256) {
+        float s = 0.f;
+        for (int c = 0; c < DH; ++c) s += bf(dctx[(tok0 + i) * d + h * DH + c]) * bf(ctx[(tok0 + i) * d + h * DH + c]);
+        sD[i] = s;
+    }
+    __syncthreads();
+
+    // this thread's dK / dV accumulators: key j, columns c0 .. c0 + DH/2 - 1
+    const int aj = tid >> 1, ac0 = (tid & 1) * (DH / 2);
+    float dk[DH / 2], dv[DH / 2];
+#pragma unroll
+    for (int c = 0; c < DH / 2; ++c) dk[c] = dv[c] = 0.f;
+
+    for (int q0 = 0; q0 < S; q0 += kAbQb) {
+        // P and dS of rows q0 .. q0 + 31: thread (row tid / 8, keys tid % 8 + 8 k)
+        {
+            const int il = tid >> 3, i = q0 + il, j0 = tid & 7;
+            float s[kAbSeq / 8], dp[kAbSeq / 8];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int k = 0; k < kAbSeq / 8; ++k) {
+                const int j = j0 + 8 * k;
+                float a = -INFINITY, g = 0.f;
+                if (i < S && j < S && (!causal || j <= i)) {
+                    a = 0.f;
+                    for (int c = 0; c < DH; ++c) {
+                        a += bf(sq[i * LD + c]) * bf(sk[j * LD + c]);
+                        g += bf(sdo[i * LD + c]) * bf(sv[j * LD + c]);
+                    }
+                    a *= scale;
+                }
+                s[k] = a;
+                dp[k] = g;
+                mx = fmaxf(mx, a);
+            }
+#pragma unroll
+            for (int m = 4; m >= 1; m >>= 1) mx = fmaxf(mx, __shfl_xor(mx, m));
+            float l = 0.f;
+#pragma unroll
+            for (int k = 0; k < kAbSeq / 8; ++k) {
+                s[k] = s[k] == -INFINITY ? 0.f : __expf(s[k] - mx);
+                l += s[k];
+            }
+#pragma unroll
+            for (int m = 4; m >= 1; m >>= 1) l += __shfl_xor(l, m);
+            const float inv_l = i < S ? 1.0f / l : 0.f;
+            const float Di = i < S ? sD[i] : 0.f;
+#pragma unroll
+            for (int k = 0; k < kAbSeq / 8; ++k) {
+                const float p = s[k] * inv_l;
+                sp[il][j0 + 8 * k] = p;
+                sds[il][j0 + 8 * k] = p * (dp[k] - Di);
+            }
+        }
+        __syncthreads();
+        // dQ of the block: thread (row tid / 8, columns tid % 8 + 8 k)
+        {
+            const int il = tid >> 3, i = q0 + il, c0 = tid & 7;
+            if (i < S) {
+                for (int k = 0; k < DH / 8; ++k) {
+                    const int c = c0 + 8 * k;
+                    float a = 0.f;
+                    for (int j = 0; j < S; ++j) a += sds[il][j] * bf(sk[j * LD + c]);
+                    dqkv[(tok0 + i) * 3 * d + h * DH + c] = to_bf(a * scale);
+                }
+            }
+        }
+        // dK += dS^T Q, dV += P^T dO over the block's rows
+        if (aj < S) {
+            const int i1 = min(kAbQb, S - q0);
+            for (int il = 0; il < i1; ++il) {
+                const float ds = sds[il][aj], p = sp[il][aj];
+                const uint16_t *qr = sq + (q0 + il) * LD + ac0, *dor = sdo + (q0 + il) * LD + ac0;
+#pragma unroll
+                for (int c = 0; c < DH / 2; ++c) {
+                    dk[c] += ds * bf(qr[c]);
+                    dv[c] += p * bf(dor[c]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+    if (aj < S) {
+#pragma unroll
+        for (int c = 0; c < DH / 2; ++c) {
+            dqkv[(tok0 + aj) * 3 * d + d + h * DH + ac0 + c] = to_bf(dk[c] * scale);
+            dqkv[(tok0 + aj) * 3 * d + 2 * d + h * DH + ac0 + c] = to_bf(dv[c]);
+        }
+    }
+}
+
+// ------------------------------------------------------------------ AdamW
+// One thread per 4 parameters; block b covers parameters of segment
+// blk_seg[b] only (segments start at multiples of kAdamBlock elements).
+constexpr int kAdamBlock = 1024;
+
+__global__ __launch_bounds__(256) void adamw_kernel(float *__restrict__ w, const float *__restrict__ g,
+                                                    float *__restrict__ m, float *__restrict__ v,
+                                                    const AdamSegment *__restrict__ segs,
+                                                    const uint32_t *__restrict__ blk_seg, AdamStep st) {
+    const AdamSegment sg = segs[blk_seg[blockIdx.x]];
+    const size_t base = (size_t)blockIdx.x * kAdamBlock;
+    const size_t i0 = base + threadIdx.x * 4;
+    if (i0 >= sg.offset + sg.count) return;
+    const float decay = sg.decay ? 1.0f - st.lr * st.weight_decay : 1.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const size_t i = i0 + e;
+        if (i >= sg.offset + sg.count) break;
+        const float gg = g[i];
+        const float mm = st.beta1 * m[i] + (1.0f - st.beta1) * gg;
+        const float vv = st.beta2 * v[i] + (1.0f - st.beta2) * gg * gg;
+        m[i] = mm;
+        v[i] = vv;
+        const float upd = (mm * st.c1) / (sqrtf(vv * st.c2) + st.eps);
+        const float ww = w[i] * decay - st.lr * upd;
+        w[i] = ww;
+        const size_t k = i - sg.offset;
+        if (sg.out_bf16) static_cast<uint16_t *>(sg.out)[k] = to_bf(ww);
+        else static_cast<float *>(sg.out)[k] = ww;
+    }
+}
+
+__global__ __launch_bounds__(256) void bf16_to_f32_kernel(const uint16_t *__restrict__ src, float *__restrict__ dst,
+                                                          size_t n) {
+    const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) dst[i] = bf(src[i]);
+}
+
+}  // namespace
+
+hipError_t launch_transpose_bf16(const bf16_t *src, bf16_t *dst, int R, int C, hipStream_t stream) {
+    if (R <= 0 || C <= 0) return hipSuccess;
+    if (R % kTile || C % kTile) return hipErrorInvalidValue;
+    return launch_kernel(transpose_kernel, dim3(C / kTile, R / kTile), dim3(256), stream, src, dst, R, C);
+}
+
+hipError_t launch_gelu(const bf16_t *v, bf16_t *u, size_t n, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    if (n % 8) return hipErrorInvalidValue;
+    const size_t n8 = n / 8;
+    return launch_kernel(gelu_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), stream, v, u, n8);
+}
+
+hipError_t launch_ln_backward(const float *dy, const float *z, const float *stats, const float *gamma, float *dz,
+                              bf16_t *dzb, int rows, int d, hipStream_t stream) {
+    if (rows <= 0) return hipSuccess;
+    if (d % 4) return hipErrorInvalidValue;
+    return launch_kernel(ln_backward_kernel, dim3((rows + kRowsPerBlock - 1) / kRowsPerBlock),
+                         dim3(64 * kRowsPerBlock), stream, dy, z, stats, gamma, dz, dzb, rows, d);
+}
+
+int colsum_partials(int rows) { return (rows + kColRows - 1) / kColRows; }
+
+hipError_t launch_ln_param_partials(const float *dy, const float *z, const float *stats, float *part_g,
+                                    float *part_b, int rows, int d, hipStream_t stream) {
+    if (rows <= 0) return hipSuccess;
+    return launch_kernel(ln_param_partials_kernel, dim3((d + 255) / 256, colsum_partials(rows)), dim3(256), stream,
+                         dy, z, stats, part_g, part_b, rows, d);
+}
+
+hipError_t launch_colsum(const void *src, bool src_bf16, float *dst, int rows, int n, int rows_per_part,
+                         hipStream_t stream) {
+    if (rows <= 0) return hipSuccess;
+    const dim3 grid((n + 255) / 256, (rows + rows_per_part - 1) / rows_per_part);
+    if (src_bf16)
+        return launch_kernel(colsum_kernel<uint16_t>, grid, dim3(256), stream, static_cast<const uint16_t *>(src), dst,
+                             rows, n, rows_per_part);
+    return launch_kernel(colsum_kernel<float>, grid, dim3(256), stream, static_cast<const float *>(src), dst, rows, n,
+                         rows_per_part);
+}
+
+hipError_t launch_head_loss(const float *z, const float *gamma, const float *beta, const bf16_t *wh,
+                            const bf16_t *bh, const int32_t *labels, float *xl, float *stats, float *logits,
+                            float *loss_t, float *dlogits, float *dx, int rows, int d, int n_out, float eps,
+                            float inv_n, hipStream_t stream) {
+    if (rows <= 0) return hipSuccess;
+    if (d % 4 || n_out < 1 || n_out > 16) return hipErrorInvalidValue;
+    return launch_kernel(head_loss_kernel, dim3((rows + kRowsPerBlock - 1) / kRowsPerBlock), dim3(64 * kRowsPerBlock),
+                         stream, z, gamma, beta, wh, bh, labels, xl, stats, logits, loss_t, dlogits, dx, rows, d,
+                         n_out, eps, inv_n);
+}
+
+hipError_t launch_head_partials(const float *dlogits, const float *xl, float *part, int rows, int d, int n_out,
+                                hipStream_t stream) {
+    if (rows <= 0) return hipSuccess;
+    return launch_kernel(head_partials_kernel, dim3((n_out * d + 255) / 256, colsum_partials(rows)), dim3(256), stream,
+                         dlogits, xl, part, rows, d, n_out);
+}
+
+hipError_t launch_attention_backward(const bf16_t *q, const bf16_t *k, const bf16_t *vt, const bf16_t *ctx,
+                                     const bf16_t *dctx, bf16_t *dqkv, int batch, int n_heads, int seq, int head_dim,
+                                     int vt_stride, bool causal, hipStream_t stream) {
+    if (batch <= 0) return hipSuccess;
+    if (seq < 1 || seq > kAbSeq || vt_stride < seq) return hipErrorInvalidValue;
+    const dim3 grid(batch * n_heads), block(256);
+    const float scale = 1.0f / sqrtf((float)head_dim);
+    if (head_dim == 64)
+        return launch_kernel(attention_backward_kernel<64>, grid, block, stream, q, k, vt, ctx, dctx, dqkv, n_heads,
+                             seq, vt_stride, causal ? 1 : 0, scale);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_adamw(float *w, const float *g, float *m, float *v, const AdamSegment *segs,
+                        const uint32_t *blk_seg, int n_blocks, const AdamStep &st, hipStream_t stream) {
+    if (n_blocks <= 0) return hipSuccess;
+    return launch_kernel(adamw_kernel, dim3(n_blocks), dim3(kAdamBlock / 4), stream, w, g, m, v, segs, blk_seg, st);
+}
+
+int adamw_block() { return kAdamBlock; }
+
+hipError_t launch_bf16_to_f32(const bf16_t *src, float *dst, size_t n, hipStream_t stream) {
+    if (n == 0) return hipSuccess;
+    return launch_kernel(bf16_to_f32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), stream, src, dst, n);
+}
+
+}  // namespace iefwd
