@@ -15,10 +15,12 @@ CU quotas 64/192, 128/128 and 192/64 against one alone, and the fp64 CPU oracle
 timed on a bounded sample, the per-batch cost of re-masking the
 instance's stream between batches, throughput and MFMA utilisation at CU
 quotas (BERT-base batch 32; the RoBERTa-large-sized causal decoder at batch 8,
-S 512), and the four GEMM classes against hipBLASLt on the same shapes.
+S 512), the four GEMM classes against hipBLASLt on the same shapes, and a
+training step of the same encoder (batch 32, AdamW).
 
   python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline] [--no-colocated] [--no-remask]
-                  [--no-quota-sweep] [--no-gemm-reference] [--decode | --decode-only]
+                  [--no-quota-sweep] [--no-gemm-reference] [--no-train | --train-only]
+                  [--decode | --decode-only]
 """
 from __future__ import annotations
 
@@ -303,6 +305,62 @@ def gemm_reference(ie, inst, x, B, S, shape, reps=20):
     return out
 
 
+def train_flops(L, d, F, H, S, n_out, causal=False):
+    """Algorithmic FLOPs of one training step per sequence: the forward, and a
+    backward of twice the forward's products (input and weight gradients of
+    every GEMM, the four attention products' gradients, the head's)."""
+    return 3 * forward_flops(L, d, F, H, S, n_out, causal)
+
+
+def train_leg(ie, W, batch=32, steps=10, warmup=3):
+    """Training steps of the BERT-base-shaped post-LN encoder (batch 32, seq
+    128, 2-class per-token cross-entropy, AdamW) at the full quota: device time
+    per step, sequences/s, MFMA utilisation of the step's algorithmic FLOPs,
+    and the split over kernel classes."""
+    import torch
+
+    name = WORKLOAD
+    shape = W.model_shape(name)
+    S = W.WORKLOADS[name]["seq"]
+    cfg = {k: shape[k] for k in ("n_layers", "d_model", "n_heads", "d_ff", "pre_ln", "causal", "n_out", "ln_eps",
+                                 "w_std", "b_std", "ln_std", "qk_std", "seed")}
+    tr = ie.Trainer(device=0, max_batch=batch, max_seq=S, **cfg)
+    x = torch.from_numpy(W.make_input(7100, batch, S, shape["d_model"])).to("cuda:0")
+    lab = torch.from_numpy(W.make_labels(7101, batch, S, shape["n_out"])).to("cuda:0")
+    for _ in range(warmup):
+        tr.step(x, lab)
+        tr.wait()
+    ms, losses = [], []
+    for _ in range(steps):
+        tr.step(x, lab)
+        losses.append(tr.loss())
+        ms.append(tr.last_batch_ms())
+    kinds = {"forward": (ie.K_QKV, ie.K_ATTN, ie.K_OUTPROJ, ie.K_FFN1, ie.K_FFN2, ie.K_LN),
+             "backward_gemm": (ie.K_BWD_GEMM,), "backward_other": (ie.K_BWD,), "optimizer": (ie.K_OPTIM,)}
+    for ks in kinds.values():
+        for k in ks:
+            tr.time_kernel(k, True)
+    for _ in range(3):
+        tr.step(x, lab)
+        tr.wait()
+    split = {}
+    for nm, ks in kinds.items():
+        tot = 0.0
+        for k in ks:
+            t, _ = tr.kernel_time(k)
+            tr.time_kernel(k, False)
+            tot += t
+        split[nm] = round(tot / 3, 3)
+    tr.close()
+    t = float(np.median(ms))
+    fl = train_flops(shape["n_layers"], shape["d_model"], shape["d_ff"], shape["n_heads"], S, shape["n_out"]) * batch
+    return {"workload": f"{name} training step, batch {batch}, 2-class per-token cross-entropy, AdamW",
+            "ms_per_step": round(t, 4), "sequences_s": round(batch / (t * 1e-3), 1),
+            "tokens_s": round(batch * S / (t * 1e-3), 1),
+            "mfma_util_pct": round(fl / (t * 1e-3) / (PEAK_BF16_TFLOPS * 1e12) * 100, 2),
+            "loss_first_last": [round(losses[0], 5), round(losses[-1], 5)], "ms_by_class": split}
+
+
 def copy_calibration(mib: int) -> None:
     """A plain device-to-device copy of `mib` MiB, for scaling the FETCH_SIZE /
     WRITE_SIZE counters of a profiling run (read once, written once)."""
@@ -328,6 +386,9 @@ def main() -> int:
     ap.add_argument("--no-remask", action="store_true")
     ap.add_argument("--no-quota-sweep", action="store_true")
     ap.add_argument("--no-gemm-reference", action="store_true")
+    ap.add_argument("--no-train", action="store_true")
+    ap.add_argument("--train-only", action="store_true",
+                    help="time only the training step (a profiling aid: prints {\"train\": ...})")
     ap.add_argument("--decode", action="store_true", help="also time the decode phase of the d=2048 decoder")
     ap.add_argument("--decode-only", action="store_true",
                     help="time only the decode phase (a profiling aid: prints {\"decode\": ...})")
@@ -348,6 +409,9 @@ def main() -> int:
         copy_calibration(args.copy_calibration_mib)
     if args.decode_only:
         print(json.dumps({"decode": decode_leg(ie, W)}))
+        return 0
+    if args.train_only:
+        print(json.dumps({"train": train_leg(ie, W)}))
         return 0
     w = W.WORKLOADS[WORKLOAD]
     shape = W.model_shape(WORKLOAD)
@@ -425,6 +489,8 @@ def main() -> int:
         result["colocated"] = colocated(ie, W, shape, cfg, [(64, 192), (128, 128), (192, 64)])
     if args.decode:
         result["decode"] = decode_leg(ie, W)
+    if not args.no_train:
+        result["train"] = train_leg(ie, W)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(shape, args.cpu_sample)
     print(json.dumps(result))

@@ -164,7 +164,7 @@ struct TrainState {
     float *dxa = nullptr, *dxb = nullptr, *dz = nullptr, *xl = nullptr, *loss_t = nullptr, *dlogits = nullptr;
     float *part = nullptr, *part2 = nullptr, *loss_sum = nullptr;
     bf16_t *dzb = nullptr, *dvb = nullptr, *dctx = nullptr, *dqkv = nullptr, *ta = nullptr, *tb = nullptr;
-    bf16_t *zero_bias = nullptr;
+    bf16_t *zero_bias = nullptr, *attn_scratch = nullptr;
     int32_t *labels = nullptr;
 
     ~TrainState() {
@@ -644,6 +644,7 @@ void train_alloc(iefwd_instance *I, const iefwd_train_params &hp) {
     const size_t o_dzb = reserve(T * d * 2), o_dvb = reserve(T * F * 2), o_dctx = reserve(T * d * 2);
     const size_t o_dqkv = reserve(T * 3 * d * 2), o_ta = reserve(wide * T * 2), o_tb = reserve(wide * T * 2);
     const size_t o_zero = reserve(wide * 2), o_lab = reserve(T * 4);
+    const size_t o_ascr = reserve(attention_backward_scratch((int)c.max_batch, (int)c.n_heads) * 2);
     if (hipMalloc(&t.blob, bytes) != hipSuccess) {
         (void)hipGetLastError();
         t.blob = nullptr;
@@ -672,7 +673,7 @@ void train_alloc(iefwd_instance *I, const iefwd_train_params &hp) {
     t.dxa = f32(o_dxa); t.dxb = f32(o_dxb); t.dz = f32(o_dz); t.xl = f32(o_xl); t.loss_t = f32(o_loss);
     t.dlogits = f32(o_dl); t.part = f32(o_part); t.part2 = f32(o_part2); t.loss_sum = f32(o_lsum);
     t.dzb = b16(o_dzb); t.dvb = b16(o_dvb); t.dctx = b16(o_dctx); t.dqkv = b16(o_dqkv); t.ta = b16(o_ta);
-    t.tb = b16(o_tb); t.zero_bias = b16(o_zero);
+    t.tb = b16(o_tb); t.zero_bias = b16(o_zero); t.attn_scratch = b16(o_ascr);
     t.labels = reinterpret_cast<int32_t *>(b + o_lab);
 
     // segments: where each tensor's updated value goes (the forward's copy)
@@ -739,7 +740,7 @@ void train_run(iefwd_instance *I, const float *x) {
     // column sums of a [rows, n] matrix into dst [n], two fixed-order stages
     auto colsum = [&](const void *src, bool is_bf16, int rows, int n, float *dst) {
         const int parts = colsum_partials(rows);
-        bwd("column sums", [&] { return launch_colsum(src, is_bf16, t.part2, rows, n, 64, s); });
+        bwd("column sums", [&] { return launch_colsum(src, is_bf16, t.part2, rows, n, 256, s); });
         bwd("column sums", [&] { return launch_colsum(t.part2, false, dst, parts, n, parts, s); });
     };
 
@@ -847,7 +848,8 @@ void train_run(iefwd_instance *I, const float *x) {
         });
         // attention
         bwd("attention backward", [&] {
-            return launch_attention_backward(sv.q, sv.k, sv.vt, sv.ctx, t.dctx, t.dqkv, B, H, S, dh, spad, causal, s);
+            return launch_attention_backward(sv.q, sv.k, sv.vt, sv.ctx, t.dctx, t.dqkv, t.attn_scratch, B, H, S, dh,
+                                             spad, causal, s);
         });
         // QKV: dWqkv = dqkv^T X, dbqkv, dX = dz1 + dqkv Wqkv
         colsum(t.dqkv, true, T, 3 * d, t.grad + o[1]);

@@ -139,9 +139,9 @@ hipError_t launch_gelu(const bf16_t *v, bf16_t *u, size_t n, hipStream_t stream)
 // and dzb (bf16) [rows, d]; d % 4 == 0.
 hipError_t launch_ln_backward(const float *dy, const float *z, const float *stats, const float *gamma, float *dz,
                               bf16_t *dzb, int rows, int d, hipStream_t stream);
-// Column-sum partials over blocks of 64 rows: colsum_partials(rows) of them.
+// Column-sum partials over chunks of 256 rows: colsum_partials(rows) of them.
 int colsum_partials(int rows);
-// part_g[b][f] = sum_r dy x^, part_b[b][f] = sum_r dy over the rows of block b.
+// part_g[b][f] = sum_r dy x^, part_b[b][f] = sum_r dy over the rows of chunk b.
 hipError_t launch_ln_param_partials(const float *dy, const float *z, const float *stats, float *part_g,
                                     float *part_b, int rows, int d, hipStream_t stream);
 // dst[b][f] = sum of src[r][f] over rows b * rows_per_part .. (b + 1) * rows_per_part - 1, in row order.
@@ -155,15 +155,17 @@ hipError_t launch_head_loss(const float *z, const float *gamma, const float *bet
                             const bf16_t *bh, const int32_t *labels, float *xl, float *stats, float *logits,
                             float *loss_t, float *dlogits, float *dx, int rows, int d, int n_out, float eps,
                             float inv_n, hipStream_t stream);
-// part[b][c * d + f] = sum over block b's rows of dlogits[r][c] xl[r][f].
+// part[b][c * d + f] = sum over chunk b's rows of dlogits[r][c] xl[r][f].
 hipError_t launch_head_partials(const float *dlogits, const float *xl, float *part, int rows, int d, int n_out,
                                 hipStream_t stream);
 // Attention backward for seq <= 128, head_dim 64: from Q, K [B,H,S,dh], V^T
 // [B,H,dh,vt_stride], the forward's context and its gradient (bf16 [B*S, H*dh])
 // to dQ | dK | dV as bf16 [B*S, 3 H dh] (the QKV product's column order).
+// scratch: attention_backward_scratch(batch, n_heads) bf16 elements.
+size_t attention_backward_scratch(int batch, int n_heads);
 hipError_t launch_attention_backward(const bf16_t *q, const bf16_t *k, const bf16_t *vt, const bf16_t *ctx,
-                                     const bf16_t *dctx, bf16_t *dqkv, int batch, int n_heads, int seq, int head_dim,
-                                     int vt_stride, bool causal, hipStream_t stream);
+                                     const bf16_t *dctx, bf16_t *dqkv, bf16_t *scratch, int batch, int n_heads,
+                                     int seq, int head_dim, int vt_stride, bool causal, hipStream_t stream);
 
 // One parameter tensor of the flat AdamW state: elements offset .. offset +
 // count - 1 (offset a multiple of adamw_block()); after the update the new

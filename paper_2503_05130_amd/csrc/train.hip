@@ -8,14 +8,14 @@
 //   gelu               u = GELU(v), bf16 -> bf16
 //   ln_backward        dz = rstd (g - mean(g) - x^ mean(g x^)), g = dy gamma,
 //                      one wave per row, fp32; writes fp32 and bf16
-//   ln_param_partials  per 64-row block: sum dy x^ and sum dy per column
+//   ln_param_partials  per 256-row chunk: sum dy x^ and sum dy per column
 //   colsum             per row block: column sums (fp32 or bf16 input), fixed order
 //   head_loss          per token: the last LayerNorm, logits = X Wh^T + bh,
 //                      softmax cross-entropy, dlogits = (p - onehot) / N,
 //                      dX = dlogits Wh
-//   head_partials      per 64-row block: sum dlogits^T X (the head's gradient)
-//   attention_backward per (batch, head), S <= 128: P recomputed from Q and K,
-//                      dS = P (dP - D), D = rowsum(dO O); dQ, dK, dV
+//   head_partials      per 256-row chunk: sum dlogits^T X (the head's gradient)
+//   attention_backward per (batch, head), S <= 128, MFMA: P recomputed from Q
+//                      and K, dS = P (dP - D), D = rowsum(dO O); dQ, dK, dV
 //   adamw              one pass over every parameter (fp32 master, moments),
 //                      writing the forward's bf16 (or fp32) copy
 // Every reduction runs in a fixed order, so a training step is deterministic.
@@ -130,23 +130,41 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void ln_backward_kernel(
 }
 
 // ------------------------------------------------------------------ column sums
-constexpr int kColRows = 64;   // rows per partial
+// A workgroup sums 64 columns over one chunk of kColRows rows: thread (column
+// c, lane g of 4) adds rows g, g + 4, ... of the chunk in order, then lane 0
+// adds the 4 lanes' sums in order.  Fixed order, so the sums are deterministic.
+constexpr int kColRows = 256;   // rows per partial
+constexpr int kColLanes = 4;
 
-// partial_g[b][f] = sum over rows of block b of dy x^, partial_b[b][f] = sum dy
+__device__ inline float lane_total(float v, int c, int g, float (&red)[kColLanes][64]) {
+    red[g][c] = v;
+    __syncthreads();
+    return red[0][c] + red[1][c] + red[2][c] + red[3][c];
+}
+
+// partial_g[b][f] = sum over rows of chunk b of dy x^, partial_b[b][f] = sum dy
 __global__ __launch_bounds__(256) void ln_param_partials_kernel(
     const float *__restrict__ dy, const float *__restrict__ z, const float *__restrict__ stats,
     float *__restrict__ part_g, float *__restrict__ part_b, int rows, int d) {
-    const int f = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
-    if (f >= d) return;
+    __shared__ float red[kColLanes][64];
+    const int c = threadIdx.x & 63, g = threadIdx.x >> 6, f = blockIdx.x * 64 + c, b = blockIdx.y;
     float sg = 0.f, sb = 0.f;
-    const int r1 = min(rows, (b + 1) * kColRows);
-    for (int r = b * kColRows; r < r1; ++r) {
-        const float a = dy[(size_t)r * d + f];
-        sg += a * ((z[(size_t)r * d + f] - stats[2 * (size_t)r]) * stats[2 * (size_t)r + 1]);
-        sb += a;
+    if (f < d) {
+        const int r1 = min(rows, (b + 1) * kColRows);
+#pragma unroll 4
+        for (int r = b * kColRows + g; r < r1; r += kColLanes) {
+            const float a = dy[(size_t)r * d + f];
+            sg += a * ((z[(size_t)r * d + f] - stats[2 * (size_t)r]) * stats[2 * (size_t)r + 1]);
+            sb += a;
+        }
     }
-    part_g[(size_t)b * d + f] = sg;
-    part_b[(size_t)b * d + f] = sb;
+    const float tg = lane_total(sg, c, g, red);
+    __syncthreads();
+    const float tb = lane_total(sb, c, g, red);
+    if (g == 0 && f < d) {
+        part_g[(size_t)b * d + f] = tg;
+        part_b[(size_t)b * d + f] = tb;
+    }
 }
 
 template <typename T>
@@ -156,16 +174,20 @@ __device__ inline float load_as_f32<float>(const float *p, size_t i) { return p[
 template <>
 __device__ inline float load_as_f32<uint16_t>(const uint16_t *p, size_t i) { return bf(p[i]); }
 
-// dst[b][f] = sum of src rows b * rb .. b * rb + rb - 1, column f, in row order
+// dst[b][f] = sum of src rows b * rb .. b * rb + rb - 1, column f
 template <typename T>
 __global__ __launch_bounds__(256) void colsum_kernel(const T *__restrict__ src, float *__restrict__ dst, int rows,
                                                      int n, int rb) {
-    const int f = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
-    if (f >= n) return;
+    __shared__ float red[kColLanes][64];
+    const int c = threadIdx.x & 63, g = threadIdx.x >> 6, f = blockIdx.x * 64 + c, b = blockIdx.y;
     float s = 0.f;
-    const int r1 = min(rows, (b + 1) * rb);
-    for (int r = b * rb; r < r1; ++r) s += load_as_f32(src, (size_t)r * n + f);
-    dst[(size_t)b * n + f] = s;
+    if (f < n) {
+        const int r1 = min(rows, (b + 1) * rb);
+#pragma unroll 4
+        for (int r = b * rb + g; r < r1; r += kColLanes) s += load_as_f32(src, (size_t)r * n + f);
+    }
+    const float t = lane_total(s, c, g, red);
+    if (g == 0 && f < n) dst[(size_t)b * n + f] = t;
 }
 
 // ------------------------------------------------------------------ head + loss
@@ -269,138 +291,195 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void head_loss_kernel(
     }
 }
 
-// part[b][c * d + f] = sum over rows of block b of dlogits[r][c] * xl[r][f]
+// part[b][k * d + f] = sum over rows of chunk b of dlogits[r][k] * xl[r][f]
 __global__ __launch_bounds__(256) void head_partials_kernel(const float *__restrict__ dlogits,
                                                             const float *__restrict__ xl, float *__restrict__ part,
                                                             int rows, int d, int n_out) {
-    const int idx = blockIdx.x * 256 + threadIdx.x, b = blockIdx.y;
-    if (idx >= n_out * d) return;
-    const int c = idx / d, f = idx - c * d;
+    __shared__ float red[kColLanes][64];
+    const int c = threadIdx.x & 63, g = threadIdx.x >> 6, idx = blockIdx.x * 64 + c, b = blockIdx.y;
     float s = 0.f;
-    const int r1 = min(rows, (b + 1) * kColRows);
-    for (int r = b * kColRows; r < r1; ++r) s += dlogits[(size_t)r * n_out + c] * xl[(size_t)r * d + f];
-    part[(size_t)b * n_out * d + idx] = s;
+    if (idx < n_out * d) {
+        const int k = idx / d, f = idx - k * d;
+        const int r1 = min(rows, (b + 1) * kColRows);
+#pragma unroll 4
+        for (int r = b * kColRows + g; r < r1; r += kColLanes) s += dlogits[(size_t)r * n_out + k] * xl[(size_t)r * d + f];
+    }
+    const float t = lane_total(s, c, g, red);
+    if (g == 0 && idx < n_out * d) part[(size_t)b * n_out * d + idx] = t;
 }
 
 // ------------------------------------------------------------------ attention backward
-// One workgroup (256 threads) per (batch, head); S <= 128 keys, DH in {64, 128}.
-// K, V, Q and dO of the head live in LDS as bf16; query rows go in blocks of
-// 32: P and dS of the block in LDS (fp32), then dQ of the block, and the
-// block's contributions to dK and dV, which each thread accumulates for its
-// (key, half of dh) in registers.  fp32 arithmetic throughout.
-constexpr int kAbSeq = 128, kAbQb = 32;
+// One workgroup (4 waves) per (batch, head); S <= 128 keys, head dim 64, all
+// five products on v_mfma_f32_32x32x16_bf16.  (32x32x16 operands: lane l holds
+// A[l % 32][8 (l / 32) .. +8] and B[8 (l / 32) .. +8][l % 32]; accumulator
+// entry r of lane l is C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].)
+//   load     Q, K, V, dO of the head into LDS in row layout ([token][c]) and Q,
+//            K, dO also transposed ([c][token]); D_i = sum_c dO[i][c] O[i][c].
+//            Rows past S are zero.
+//   phase 1  wave w, queries 32 w .. 32 w + 31: S^T = K Q^T and dP^T = V dO^T
+//            (keys as rows, so a lane holds 64 of its query's 128 keys, its
+//            partner lane l ^ 32 the rest); softmax over keys in registers
+//            (causal: keys j <= i), dS = P (dP - D_i).  P^T and dS^T ([key]
+//            [query]) and dS ([query][key]) go to a per-head scratch in global
+//            memory (L2-resident), the layouts phase 2 reads as A operands.
+//   phase 2  wave w: dV = P^T dO and dK = dS^T Q for keys 32 w .. 32 w + 31,
+//            dQ = dS K for queries 32 w .. 32 w + 31 (dQ and dK times
+//            1 / sqrt(dh)).
+// fp32 accumulation and softmax; P and dS are rounded to bf16 for phase 2.
+constexpr int kAbSeq = 128, kAbDh = 64;
+constexpr int kAbLd = kAbDh + 8, kAbLdT = kAbSeq + 8;   // LDS row strides (bf16)
+constexpr size_t kAbScratch = 3 * (size_t)kAbSeq * kAbSeq;   // bf16 elements per head
 
-template <int DH>
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ inline bf16x8 ld8(const uint16_t *p) { return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p)); }
+
 __global__ __launch_bounds__(256) void attention_backward_kernel(
     const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K, const uint16_t *__restrict__ Vt,
-    const uint16_t *__restrict__ ctx, const uint16_t *__restrict__ dctx, uint16_t *__restrict__ dqkv, int n_heads,
-    int S, int vt_stride, int causal, float scale) {
-    constexpr int LD = DH + 8;                 // bf16 row stride in LDS
-    __shared__ uint16_t sq[kAbSeq * LD], sk[kAbSeq * LD], sv[kAbSeq * LD], sdo[kAbSeq * LD];
-    __shared__ float sp[kAbQb][kAbSeq + 1], sds[kAbQb][kAbSeq + 1];
+    const uint16_t *__restrict__ ctx, const uint16_t *__restrict__ dctx, uint16_t *__restrict__ dqkv,
+    uint16_t *__restrict__ scratch, int n_heads, int S, int vt_stride, int causal, float scale) {
+    __shared__ __attribute__((aligned(16))) uint16_t sQ[kAbSeq * kAbLd], sK[kAbSeq * kAbLd], sV[kAbSeq * kAbLd],
+        sdO[kAbSeq * kAbLd];
+    __shared__ __attribute__((aligned(16))) uint16_t sQt[kAbDh * kAbLdT], sKt[kAbDh * kAbLdT], sdOt[kAbDh * kAbLdT];
     __shared__ float sD[kAbSeq];
-    const int tid = threadIdx.x, bh = blockIdx.x, b = bh / n_heads, h = bh - b * n_heads;
-    const int d = n_heads * DH;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5, col = lane & 31;
+    const int bh = blockIdx.x, b = bh / n_heads, h = bh - b * n_heads;
+    const int d = n_heads * kAbDh;
     const size_t tok0 = (size_t)b * S;
-    const uint16_t *Qh = Q + (size_t)bh * S * DH, *Kh = K + (size_t)bh * S * DH, *Vh = Vt + (size_t)bh * DH * vt_stride;
+    const uint16_t *Qh = Q + (size_t)bh * S * kAbDh, *Kh = K + (size_t)bh * S * kAbDh;
+    const uint16_t *Vh = Vt + (size_t)bh * kAbDh * vt_stride;
+    uint16_t *Pt = scratch + (size_t)bh * kAbScratch, *dSt = Pt + kAbSeq * kAbSeq, *dS = dSt + kAbSeq * kAbSeq;
 
-    // load the head's operands; D_i = sum_c dO[i][c] O[i][c]
-    for (int idx = tid; idx < S * DH; idx += 256) {
-        const int i = idx / DH, c = idx - i * DH;
-        sq[i * LD + c] = Qh[idx];
-        sk[i * LD + c] = Kh[idx];
-        sv[i * LD + c] = Vh[(size_t)c * vt_stride + i];
-        sdo[i * LD + c] = dctx[(tok0 + i) * d + h * DH + c];
+    // ---- load: 8-element vectors, row i = v / 8, columns c0 .. c0 + 7
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    for (int v = tid; v < kAbSeq * kAbDh / 8; v += 256) {
+        const int i = v / 8, c0 = (v % 8) * 8;
+        const bool in = i < S;
+        const u32x4 q = in ? *reinterpret_cast<const u32x4 *>(Qh + (size_t)i * kAbDh + c0) : zero;
+        const u32x4 k = in ? *reinterpret_cast<const u32x4 *>(Kh + (size_t)i * kAbDh + c0) : zero;
+        const u32x4 g = in ? *reinterpret_cast<const u32x4 *>(dctx + (tok0 + i) * d + h * kAbDh + c0) : zero;
+        const u32x4 o = in ? *reinterpret_cast<const u32x4 *>(ctx + (tok0 + i) * d + h * kAbDh + c0) : zero;
+        *reinterpret_cast<u32x4 *>(sQ + i * kAbLd + c0) = q;
+        *reinterpret_cast<u32x4 *>(sK + i * kAbLd + c0) = k;
+        *reinterpret_cast<u32x4 *>(sdO + i * kAbLd + c0) = g;
+        float dot = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sQt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(q[e] & 0xffffu);
+            sQt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(q[e] >> 16);
+            sKt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(k[e] & 0xffffu);
+            sKt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(k[e] >> 16);
+            sdOt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(g[e] & 0xffffu);
+            sdOt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(g[e] >> 16);
+            dot += __uint_as_float(g[e] << 16) * __uint_as_float(o[e] << 16) +
+                   __uint_as_float(g[e] & 0xffff0000u) * __uint_as_float(o[e] & 0xffff0000u);
+        }
+        // the 8 vectors of row i are 8 consecutive lanes
+#pragma unroll
+        for (int m = 4; m >= 1; m >>= 1) dot += __shfl_xor(dot, m);
+        if (v % 8 == 0) sD[i] = dot;
     }
-    for (int i = tid; i < S; i += 256) {
-        float s = 0.f;
-        for (int c = 0; c < DH; ++c) s += bf(dctx[(tok0 + i) * d + h * DH + c]) * bf(ctx[(tok0 + i) * d + h * DH + c]);
-        sD[i] = s;
+    // V from V^T [c][j]: vector v = 8 keys j0 .. j0 + 7 of column c; keys past S are zero
+    for (int v = tid; v < kAbDh * kAbSeq / 8; v += 256) {
+        const int c = v / (kAbSeq / 8), j0 = (v % (kAbSeq / 8)) * 8;
+        u32x4 x = j0 < S ? *reinterpret_cast<const u32x4 *>(Vh + (size_t)c * vt_stride + j0) : zero;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const uint16_t val = j0 + e < S ? (uint16_t)(x[e / 2] >> (16 * (e % 2))) : (uint16_t)0;
+            sV[(j0 + e) * kAbLd + c] = val;
+        }
     }
     __syncthreads();
 
-    // this thread's dK / dV accumulators: key j, columns c0 .. c0 + DH/2 - 1
-    const int aj = tid >> 1, ac0 = (tid & 1) * (DH / 2);
-    float dk[DH / 2], dv[DH / 2];
+    // ---- phase 1: queries of this wave against all keys
+    const int iq = 32 * wave + col;          // this lane's query
+    f32x16 st[4], dpt[4];
 #pragma unroll
-    for (int c = 0; c < DH / 2; ++c) dk[c] = dv[c] = 0.f;
+    for (int jb = 0; jb < 4; ++jb) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) st[jb][r] = dpt[jb][r] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < kAbDh / 16; ++ks) {
+            const int kc = 16 * ks + 8 * half;
+            st[jb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld8(sK + (32 * jb + col) * kAbLd + kc),
+                                                             ld8(sQ + iq * kAbLd + kc), st[jb], 0, 0, 0);
+            dpt[jb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ld8(sV + (32 * jb + col) * kAbLd + kc),
+                                                              ld8(sdO + iq * kAbLd + kc), dpt[jb], 0, 0, 0);
+        }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int j = 32 * jb + 8 * (r / 4) + 4 * half + r % 4;
+            const bool ok = iq < S && j < S && (!causal || j <= iq);
+            st[jb][r] = ok ? st[jb][r] * scale : -INFINITY;
+            mx = fmaxf(mx, st[jb][r]);
+        }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    float l = 0.f;
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const float p = st[jb][r] == -INFINITY ? 0.f : __expf(st[jb][r] - mx);
+            st[jb][r] = p;
+            l += p;
+        }
+    l += __shfl_xor(l, 32);
+    const float inv_l = iq < S ? 1.0f / l : 0.f;
+    const float Di = sD[iq];
+#pragma unroll
+    for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+            uint16_t dsv[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int r = 4 * q4 + e, j = 32 * jb + 8 * q4 + 4 * half + e;
+                const float p = st[jb][r] * inv_l, ds = p * (dpt[jb][r] - Di);
+                Pt[j * kAbSeq + iq] = to_bf(p);
+                dsv[e] = to_bf(ds);
+                dSt[j * kAbSeq + iq] = dsv[e];
+            }
+            *reinterpret_cast<u32x2 *>(dS + iq * kAbSeq + 32 * jb + 8 * q4 + 4 * half) =
+                u32x2{(uint32_t)dsv[0] | ((uint32_t)dsv[1] << 16), (uint32_t)dsv[2] | ((uint32_t)dsv[3] << 16)};
+        }
+    __syncthreads();   // the scratch is complete (workgroup scope)
 
-    for (int q0 = 0; q0 < S; q0 += kAbQb) {
-        // P and dS of rows q0 .. q0 + 31: thread (row tid / 8, keys tid % 8 + 8 k)
-        {
-            const int il = tid >> 3, i = q0 + il, j0 = tid & 7;
-            float s[kAbSeq / 8], dp[kAbSeq / 8];
-            float mx = -INFINITY;
+    // ---- phase 2: keys 32 w .. 32 w + 31 (dV, dK) and queries 32 w .. 32 w + 31 (dQ)
+    f32x16 dv[2], dk[2], dq[2];
 #pragma unroll
-            for (int k = 0; k < kAbSeq / 8; ++k) {
-                const int j = j0 + 8 * k;
-                float a = -INFINITY, g = 0.f;
-                if (i < S && j < S && (!causal || j <= i)) {
-                    a = 0.f;
-                    for (int c = 0; c < DH; ++c) {
-                        a += bf(sq[i * LD + c]) * bf(sk[j * LD + c]);
-                        g += bf(sdo[i * LD + c]) * bf(sv[j * LD + c]);
-                    }
-                    a *= scale;
-                }
-                s[k] = a;
-                dp[k] = g;
-                mx = fmaxf(mx, a);
-            }
+    for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-            for (int m = 4; m >= 1; m >>= 1) mx = fmaxf(mx, __shfl_xor(mx, m));
-            float l = 0.f;
+        for (int r = 0; r < 16; ++r) dv[cb][r] = dk[cb][r] = dq[cb][r] = 0.f;
+    const int row = 32 * wave + col;
 #pragma unroll
-            for (int k = 0; k < kAbSeq / 8; ++k) {
-                s[k] = s[k] == -INFINITY ? 0.f : __expf(s[k] - mx);
-                l += s[k];
-            }
+    for (int ks = 0; ks < kAbSeq / 16; ++ks) {
+        const int kc = 16 * ks + 8 * half;
+        const bf16x8 a_p = ld8(Pt + row * kAbSeq + kc), a_dst = ld8(dSt + row * kAbSeq + kc);
+        const bf16x8 a_ds = ld8(dS + row * kAbSeq + kc);
 #pragma unroll
-            for (int m = 4; m >= 1; m >>= 1) l += __shfl_xor(l, m);
-            const float inv_l = i < S ? 1.0f / l : 0.f;
-            const float Di = i < S ? sD[i] : 0.f;
-#pragma unroll
-            for (int k = 0; k < kAbSeq / 8; ++k) {
-                const float p = s[k] * inv_l;
-                sp[il][j0 + 8 * k] = p;
-                sds[il][j0 + 8 * k] = p * (dp[k] - Di);
-            }
-        }
-        __syncthreads();
-        // dQ of the block: thread (row tid / 8, columns tid % 8 + 8 k)
-        {
-            const int il = tid >> 3, i = q0 + il, c0 = tid & 7;
-            if (i < S) {
-                for (int k = 0; k < DH / 8; ++k) {
-                    const int c = c0 + 8 * k;
-                    float a = 0.f;
-                    for (int j = 0; j < S; ++j) a += sds[il][j] * bf(sk[j * LD + c]);
-                    dqkv[(tok0 + i) * 3 * d + h * DH + c] = to_bf(a * scale);
-                }
-            }
-        }
-        // dK += dS^T Q, dV += P^T dO over the block's rows
-        if (aj < S) {
-            const int i1 = min(kAbQb, S - q0);
-            for (int il = 0; il < i1; ++il) {
-                const float ds = sds[il][aj], p = sp[il][aj];
-                const uint16_t *qr = sq + (q0 + il) * LD + ac0, *dor = sdo + (q0 + il) * LD + ac0;
-#pragma unroll
-                for (int c = 0; c < DH / 2; ++c) {
-                    dk[c] += ds * bf(qr[c]);
-                    dv[c] += p * bf(dor[c]);
-                }
-            }
-        }
-        __syncthreads();
-    }
-    if (aj < S) {
-#pragma unroll
-        for (int c = 0; c < DH / 2; ++c) {
-            dqkv[(tok0 + aj) * 3 * d + d + h * DH + ac0 + c] = to_bf(dk[c] * scale);
-            dqkv[(tok0 + aj) * 3 * d + 2 * d + h * DH + ac0 + c] = to_bf(dv[c]);
+        for (int cb = 0; cb < 2; ++cb) {
+            const int c = 32 * cb + col;
+            dv[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_p, ld8(sdOt + c * kAbLdT + kc), dv[cb], 0, 0, 0);
+            dk[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_dst, ld8(sQt + c * kAbLdT + kc), dk[cb], 0, 0, 0);
+            dq[cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_ds, ld8(sKt + c * kAbLdT + kc), dq[cb], 0, 0, 0);
         }
     }
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const int t = 32 * wave + 8 * (r / 4) + 4 * half + r % 4, c = 32 * cb + col;
+            if (t >= S) continue;
+            uint16_t *o = dqkv + (tok0 + t) * 3 * d + h * kAbDh + c;
+            o[0] = to_bf(dq[cb][r] * scale);
+            o[d] = to_bf(dk[cb][r] * scale);
+            o[2 * d] = to_bf(dv[cb][r]);
+        }
 }
 
 // ------------------------------------------------------------------ AdamW
@@ -469,14 +548,14 @@ int colsum_partials(int rows) { return (rows + kColRows - 1) / kColRows; }
 hipError_t launch_ln_param_partials(const float *dy, const float *z, const float *stats, float *part_g,
                                     float *part_b, int rows, int d, hipStream_t stream) {
     if (rows <= 0) return hipSuccess;
-    return launch_kernel(ln_param_partials_kernel, dim3((d + 255) / 256, colsum_partials(rows)), dim3(256), stream,
+    return launch_kernel(ln_param_partials_kernel, dim3((d + 63) / 64, colsum_partials(rows)), dim3(256), stream,
                          dy, z, stats, part_g, part_b, rows, d);
 }
 
 hipError_t launch_colsum(const void *src, bool src_bf16, float *dst, int rows, int n, int rows_per_part,
                          hipStream_t stream) {
     if (rows <= 0) return hipSuccess;
-    const dim3 grid((n + 255) / 256, (rows + rows_per_part - 1) / rows_per_part);
+    const dim3 grid((n + 63) / 64, (rows + rows_per_part - 1) / rows_per_part);
     if (src_bf16)
         return launch_kernel(colsum_kernel<uint16_t>, grid, dim3(256), stream, static_cast<const uint16_t *>(src), dst,
                              rows, n, rows_per_part);
@@ -498,21 +577,20 @@ hipError_t launch_head_loss(const float *z, const float *gamma, const float *bet
 hipError_t launch_head_partials(const float *dlogits, const float *xl, float *part, int rows, int d, int n_out,
                                 hipStream_t stream) {
     if (rows <= 0) return hipSuccess;
-    return launch_kernel(head_partials_kernel, dim3((n_out * d + 255) / 256, colsum_partials(rows)), dim3(256), stream,
+    return launch_kernel(head_partials_kernel, dim3((n_out * d + 63) / 64, colsum_partials(rows)), dim3(256), stream,
                          dlogits, xl, part, rows, d, n_out);
 }
 
+size_t attention_backward_scratch(int batch, int n_heads) { return (size_t)batch * n_heads * kAbScratch; }
+
 hipError_t launch_attention_backward(const bf16_t *q, const bf16_t *k, const bf16_t *vt, const bf16_t *ctx,
-                                     const bf16_t *dctx, bf16_t *dqkv, int batch, int n_heads, int seq, int head_dim,
-                                     int vt_stride, bool causal, hipStream_t stream) {
+                                     const bf16_t *dctx, bf16_t *dqkv, bf16_t *scratch, int batch, int n_heads,
+                                     int seq, int head_dim, int vt_stride, bool causal, hipStream_t stream) {
     if (batch <= 0) return hipSuccess;
-    if (seq < 1 || seq > kAbSeq || vt_stride < seq) return hipErrorInvalidValue;
-    const dim3 grid(batch * n_heads), block(256);
-    const float scale = 1.0f / sqrtf((float)head_dim);
-    if (head_dim == 64)
-        return launch_kernel(attention_backward_kernel<64>, grid, block, stream, q, k, vt, ctx, dctx, dqkv, n_heads,
-                             seq, vt_stride, causal ? 1 : 0, scale);
-    return hipErrorInvalidValue;
+    if (seq < 1 || seq > kAbSeq || vt_stride < seq || vt_stride % 8 || head_dim != kAbDh || !scratch)
+        return hipErrorInvalidValue;
+    return launch_kernel(attention_backward_kernel, dim3(batch * n_heads), dim3(256), stream, q, k, vt, ctx, dctx, dqkv,
+                         scratch, n_heads, seq, vt_stride, causal ? 1 : 0, 1.0f / sqrtf((float)head_dim));
 }
 
 hipError_t launch_adamw(float *w, const float *g, float *m, float *v, const AdamSegment *segs,
