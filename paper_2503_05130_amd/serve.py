@@ -5,6 +5,7 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
 
   python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 static proportional shared]
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--small]
+                                       [--mix inference|train]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
 batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
@@ -143,6 +144,80 @@ class Served:
                                       if self.klc_log else None)}
 
 
+class Trainee:
+    """A training instance co-located with inference (the paper's train-inf
+    collocation, Sec. 5.2): whole training steps back to back on a fixed
+    synthetic batch, with the same quota hand-off and controller reports as
+    an inference instance.  Its KLC is the step time relative to its fastest
+    step on the same quota; it always has work, so its queue length is 1."""
+
+    def __init__(self, idx, name, shape, seq, batch, request, limit, seed):
+        self.idx, self.name, self.seq, self.max_batch, self.rate = idx, name, seq, batch, 0.0
+        self.request, self.limit, self.slo = request, limit, False
+        self.inst = ie.Trainer(device=0, max_batch=batch, max_seq=seq, seed=seed, **shape)
+        self.x = torch.from_numpy(np.random.default_rng(6000 + idx).standard_normal(
+            (batch, seq, shape["d_model"]), dtype=np.float32)).to("cuda:0")
+        self.labels = torch.from_numpy(np.random.default_rng(6100 + idx).integers(
+            0, shape["n_out"], size=(batch, seq), dtype=np.int32)).to("cuda:0")
+        self.pool = self.x
+        self.lock = threading.Lock()
+
+    def reset(self, horizon):
+        self.done_at = []                   # completion times of the steps
+        self.step_ms = []
+        self.best_ms = {}
+        self.kernels = self.inst.kernels_launched()
+        self.ratios = []
+        self.pending = None
+        self.inst.set_quota(ie.device_info(0)[0], 0)
+        self.applied = (ie.device_info(0)[0], 0)
+        self.batches = 0
+        self.changes = 0
+        self.klc_log = []
+        self.plans = set()
+
+    def queue_len(self, now):
+        return 1
+
+    def warm(self):
+        self.inst.step(self.x, self.labels)
+        self.inst.wait()
+
+    def run(self, t0, horizon, stop):
+        while not stop.is_set():
+            if time.perf_counter() - t0 > horizon:
+                return
+            with self.lock:
+                pend, self.pending = self.pending, None
+            if pend is not None and pend != self.applied:
+                self.inst.set_quota(*pend)
+                self.applied = pend
+                self.changes += 1
+                self.plans.add(pend)
+            self.inst.step(self.x, self.labels)
+            self.inst.wait()
+            self.done_at.append(time.perf_counter() - t0)
+            ms = self.inst.last_batch_ms()
+            self.step_ms.append(ms)
+            self.batches += 1
+            best = min(self.best_ms.get(self.applied[0], ms), ms)
+            self.best_ms[self.applied[0]] = best
+            with self.lock:
+                self.kernels = self.inst.kernels_launched()
+                self.ratios.append(ms / best)
+
+    def stats(self, warmup, horizon):
+        done = np.array(self.done_at)
+        n = int(((done >= warmup) & (done <= horizon)).sum())
+        return {"name": self.name, "training": True, "steps": n,
+                "steps_s": round(n / max(horizon - warmup, 1e-9), 2),
+                "sequences_s": round(n * self.max_batch / max(horizon - warmup, 1e-9), 1),
+                "step_ms_p50": round(float(np.median(self.step_ms)), 3) if self.step_ms else None,
+                "quota_changes": self.changes, "distinct_placements": len(self.plans),
+                "klc_ratio_p50_p90": ([round(float(np.percentile(self.klc_log, p)), 3) for p in (50, 90)]
+                                      if self.klc_log else None)}
+
+
 GRANULE = 32   # quota granularity of the dynamic policies: 4 CUs per XCD, few distinct masks
 
 
@@ -203,8 +278,11 @@ def control_loop(policy, served, t0, horizon, period, stop, history):
 def run_policy(policy, served, horizon, warmup, period):
     for s in served:
         s.reset(horizon)
-        s.inst.submit(s.pool[:1])              # warm the instance and its full-device stream
-        s.inst.wait()
+        if isinstance(s, Trainee):
+            s.warm()
+        else:
+            s.inst.submit(s.pool[:1])          # warm the instance and its full-device stream
+            s.inst.wait()
     torch.cuda.synchronize()
     stop, history = threading.Event(), []
     t0 = time.perf_counter()
@@ -219,7 +297,7 @@ def run_policy(policy, served, horizon, warmup, period):
     qs = np.array([h[1] for h in history]) if history else np.zeros((0, len(served)))
     states = [h[2] for h in history]
     return {"policy": policy, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
-            "instances": [s.stats(warmup) for s in served],
+            "instances": [s.stats(warmup, horizon) if isinstance(s, Trainee) else s.stats(warmup) for s in served],
             "mean_quota": [round(float(v), 1) for v in qs.mean(0)] if len(qs) else None,
             "periods": len(history),
             "state_counts": {str(k): states.count(k) for k in sorted(set(states))}}
@@ -229,6 +307,50 @@ def build_mix(mix):
     return [Served(i, *m) for i, m in enumerate(mix)]
 
 
+def train_mix(small: bool = False):
+    """The train-inf collocation mix: one BERT-base-shaped inference instance
+    (batches of up to 4, latency-sensitive) beside one training instance of the
+    same shape (batch 32 x 128, best effort)."""
+    shape, seq = (SMALL, 64) if small else (BERT, 128)
+    inf = Served(0, "bert_inf", shape, seq, 4, 200.0, 0.25, 0.5, True, 51)
+    trn = Trainee(1, "bert_train", shape, seq, 8 if small else 32, 0.75, 1.0, 55)
+    return [inf, trn]
+
+
+def run_train_mix(policies, horizon, warmup, period, small=False):
+    """Each policy with both instances, then each instance alone on the whole
+    GPU ("exclusive"); the paper compares co-location against exclusive."""
+    served = train_mix(small)
+    out = []
+    try:
+        for pol in policies:
+            name, _, per = pol.partition("@")
+            res = run_policy(name, served, horizon, warmup, (float(per) if per else period) / 1e3)
+            out.append(res)
+            print(json.dumps(res), flush=True)
+        for one in served:
+            res = run_policy("shared", [one], horizon, warmup, period / 1e3)
+            res["policy"] = f"exclusive:{one.name}"
+            out.append(res)
+            print(json.dumps(res), flush=True)
+    finally:
+        for s in served:
+            s.inst.close()
+    excl = {r["instances"][0]["name"]: r["instances"][0] for r in out if r["policy"].startswith("exclusive")}
+    summary = {}
+    for r in out:
+        if r["policy"].startswith("exclusive"):
+            continue
+        inf, trn = r["instances"]
+        e_inf, e_trn = excl["bert_inf"], excl["bert_train"]
+        summary[r["policy"]] = {
+            "inference_p50_vs_exclusive": round(inf["p50_ms"] / e_inf["p50_ms"], 3) if inf["p50_ms"] else None,
+            "inference_p99_vs_exclusive": round(inf["p99_ms"] / e_inf["p99_ms"], 3) if inf["p99_ms"] else None,
+            "training_throughput_vs_exclusive": round(trn["steps_s"] / e_trn["steps_s"], 3) if e_trn["steps_s"] else None}
+    print(json.dumps({"train_inf_summary": summary}), flush=True)
+    return out, summary
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--policy", nargs="+", default=["shared", "static", "proportional", "alg2"])
@@ -236,7 +358,12 @@ def main() -> int:
     ap.add_argument("--warmup", type=float, default=2.0)
     ap.add_argument("--period-ms", type=float, default=20.0)
     ap.add_argument("--small", action="store_true", help="small models (quick functional run)")
+    ap.add_argument("--mix", choices=["inference", "train"], default="inference",
+                    help="inference: the four-instance serving mix; train: inference beside a training instance")
     args = ap.parse_args()
+    if args.mix == "train":
+        run_train_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small)
+        return 0
     t = time.perf_counter()
     served = build_mix(default_mix(args.small))
     print(json.dumps({"setup_s": round(time.perf_counter() - t, 1),

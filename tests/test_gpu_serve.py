@@ -30,3 +30,21 @@ def test_policy_serves_every_request(served, policy):
     assert np.all((q >= 8) & (q <= 256))
     if policy == "alg2":
         assert sum(res["state_counts"].values()) == res["periods"]
+
+
+def test_training_beside_inference():
+    """The train-inf mix (small models): the inference instance serves every
+    request and the training instance completes steps under each policy, and
+    both also alone."""
+    out, summary = serve.run_train_mix(["static", "alg2"], horizon=1.5, warmup=0.2, period=10.0, small=True)
+    names = [r["policy"] for r in out]
+    assert names == ["static", "alg2", "exclusive:bert_inf", "exclusive:bert_train"]
+    for r in out:
+        for st in r["instances"]:
+            if st.get("training"):
+                assert st["steps"] > 0 and st["steps_s"] > 0
+            else:
+                assert st["dropped"] == 0 and st["requests"] > 0
+    for pol in ("static", "alg2"):
+        v = summary[pol]
+        assert v["inference_p50_vs_exclusive"] > 0 and v["training_throughput_vs_exclusive"] > 0

@@ -85,3 +85,61 @@ def test_frontier_visits_smallest_feasible_smr_per_ibs():
 def test_unknown_walk_rejected():
     with pytest.raises(ValueError):
         P.hgss(convex, 100.0, walk="spiral")
+
+
+# ------------------------------------------------------------------ training profiling (binary search)
+def saturating(knee_cus, t_max=1000.0):
+    """Throughput linear in the quota up to the knee, flat after it."""
+    return lambda q: t_max * min(q, knee_cus) / knee_cus
+
+
+def test_train_binary_search_follows_the_printed_rule():
+    from paper_2503_05130_amd.profiler import train_binary_search
+    calls = []
+
+    def measure(q):
+        calls.append(q)
+        return saturating(128)(q)
+    r = train_binary_search(measure, 0.8)
+    # T1 at 100%, then mid = 50% (128 CUs): 1000 >= 800 + 20 -> high = 50; mid = 25% (64 CUs): 500 -> low = 25 ...
+    assert calls[0] == 256 and calls[1] == 128 and calls[2] == 64
+    assert abs(r["quota_cus"] - 0.8 * 128) <= 8             # the knee times p, to one XCD granule
+    assert r["t1"] == 1000.0
+    assert r["trials"] <= 8
+
+
+def test_train_binary_search_stops_inside_the_band():
+    from paper_2503_05130_amd.profiler import train_binary_search
+    # saturating at 64 CUs: 50% is already full throughput, inside the p = 100% band: the printed rule stops there
+    r = train_binary_search(saturating(64), 1.0)
+    assert r["path"] == [(100.0, 256), (50.0, 128)] and r["quota_cus"] == 128
+    # a knee above 50%: bisects upward until a setting is inside the band
+    r = train_binary_search(saturating(200), 1.0)
+    assert saturating(200)(r["quota_cus"]) >= 980.0 and r["quota_cus"] >= 200
+
+
+def test_train_binary_search_tight_finds_the_knee():
+    from paper_2503_05130_amd.profiler import train_binary_search
+    for knee in (64, 96, 200, 256):
+        r = train_binary_search(saturating(knee), 1.0, tight=True)
+        assert knee - 16 <= r["quota_cus"] <= knee + 8, (knee, r)
+
+
+def test_train_binary_search_against_traversal():
+    import numpy as np
+
+    from paper_2503_05130_amd.profiler import train_binary_search, train_traversal
+    rng = np.random.default_rng(1)
+    for _ in range(20):
+        knee = int(rng.integers(2, 33)) * 8
+        f = saturating(knee)
+        for p in (0.8, 1.0):
+            tv = train_traversal(f, p)
+            assert tv["trials"] == 32
+            for tight in (False, True):
+                bs = train_binary_search(f, p, tight=tight)
+                assert bs["trials"] < tv["trials"]
+                # the setting delivers throughput no lower than the band below p * T1 (to one XCD granule)
+                assert f(bs["quota_cus"]) >= (p - 0.02) * 1000.0 - 1000.0 * 8 / knee
+                assert bs["quota_cus"] >= tv["quota_cus"] - 8
+            assert abs(train_binary_search(f, p, tight=True)["quota_cus"] - tv["quota_cus"]) <= 16
