@@ -48,6 +48,8 @@ def gemm_bound(a64, w64, K):
     (256, 768, 3072),    # long K: split (even/odd) K order, 64 x 96
     (130, 512, 2048),    # split order, 64 x 128, ragged M
     (2048, 2048, 2048),  # split order, 128 x 128
+    (4096, 768, 3072),   # split order, 64 x 96 (the BERT-base FFN-down product)
+    (4133, 768, 2048),   # split order, 64 x 96, ragged M
 ])
 @pytest.mark.parametrize("epi", [ie.EPI_BIAS_BF16, ie.EPI_BIAS_GELU_BF16, ie.EPI_BIAS_RESID_F32])
 def test_gemm_epilogues(M, N, K, epi):
@@ -83,6 +85,7 @@ def test_gemm_epilogues(M, N, K, epi):
     (512, 768, 768),      # 64 x 64 tiles throughout
     (4096, 3072, 768),    # 128 x 192 tiles (8 waves) for the full batch, 64 x 64 / 64 x 96 for the slices
     (4096, 1024, 4096),   # split K order: 128 x 128 for the full batch, 64 x 128 for the slices
+    (4096, 768, 3072),    # split K order, 64 x 96 tiles (the BERT-base FFN-down product)
 ])
 def test_gemm_batch_invariance(M, N, K):
     # rows computed in a large batch equal the same rows computed alone, bit for
