@@ -40,7 +40,7 @@ WORKLOAD = "bert_base_l12_d768_s128"
 # HBM bytes per launch of the FFN-down kernel (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 KiB,
 # factors from a 256 MiB device copy in the same runs), valid only for the GEMM source
 # and build flags they were counted on; any other source reports null.
-FFN2_TRAFFIC = {"source_sha256_16": "44063643aeb1d6c0", "bytes": (36983.3 * 2.0 + 14573.1 * 1.0) * 1024}
+FFN2_TRAFFIC = {"source_sha256_16": "0fb9db58756c7b6b", "bytes": (36991.7 * 2.0 + 14825.2 * 1.0) * 1024}
 GEMM_SOURCES = ("paper_2503_05130_amd/csrc/gemm.hip", "paper_2503_05130_amd/csrc/kernels.h",
                 "paper_2503_05130_amd/build.py")
 
@@ -380,7 +380,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--batch", type=int, default=32)
     ap.add_argument("--quota", type=int, default=256)
-    ap.add_argument("--cpu-sample", type=int, default=4)
+    ap.add_argument("--cpu-sample", type=int, default=96)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-colocated", action="store_true")
     ap.add_argument("--no-remask", action="store_true")
