@@ -219,3 +219,66 @@ def test_kernel_entry_points_validate_shapes():
     assert L.iefwd_test_ln_head(p, p, p, p, p, p, 4, 128, 0, 1e-5, None) == ie.EINVAL
     assert L.iefwd_test_cu_probe(None, 0, p) == ie.EINVAL
     assert L.iefwd_test_gemm_qkv(p, p, p, p, p, p, 1, 4, 100, 2, None) == ie.EINVAL
+
+
+# ------------------------------------------------------------------ training ABI (host-side decisions)
+def test_train_params_layout_and_defaults(tmp_path):
+    fields = [f for f, _ in ie.TrainParams._fields_]
+    prog = tmp_path / "tlayout.c"
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "iefwd.h"', "int main(void) {",
+             '  printf("size %zu\\n", sizeof(iefwd_train_params));']
+    for f in fields:
+        lines.append(f'  printf("{f} %zu\\n", offsetof(iefwd_train_params, {f}));')
+    lines.append("  return 0; }")
+    prog.write_text("\n".join(lines))
+    exe = tmp_path / "tlayout"
+    subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", f"-I{ROOT}/include", str(prog), "-o", str(exe)],
+                   check=True)
+    out = dict(line.split() for line in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                       check=True).stdout.splitlines())
+    assert int(out["size"]) == ctypes.sizeof(ie.TrainParams)
+    for f in fields:
+        assert int(out[f]) == getattr(ie.TrainParams, f).offset, f
+    tp = ie.train_params()
+    assert tp.abi_version == ie.ABI_VERSION
+    assert (tp.lr, tp.beta1, tp.beta2, tp.eps, tp.weight_decay) == pytest.approx((1e-4, 0.9, 0.999, 1e-8, 0.01))
+    with pytest.raises(ValueError):
+        ie.train_params(momentum=0.9)
+
+
+TRAIN_BASE = dict(BASE, pre_ln=0, causal=0, n_out=2)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(pre_ln=1),                         # post-LN stacks only
+    dict(n_out=0),                          # needs a head (classes)
+    dict(d_model=256, n_heads=2),           # head dim 128
+    dict(max_seq=256),                      # attention backward covers S <= 128
+])
+def test_train_create_rejects_bad_config(bad):
+    with pytest.raises(ie.IefwdError) as e:
+        ie.Trainer(**dict(TRAIN_BASE, **bad))
+    assert e.value.status == ie.EINVAL
+
+
+@pytest.mark.parametrize("bad", [dict(lr=-1.0), dict(beta1=1.0), dict(beta2=-0.1), dict(eps=0.0),
+                                 dict(weight_decay=float("nan"))])
+def test_train_create_rejects_bad_params(bad):
+    with pytest.raises(ie.IefwdError) as e:
+        ie.Trainer(train=bad, **TRAIN_BASE)
+    assert e.value.status == ie.EINVAL
+
+
+def test_train_null_and_version():
+    L = ie.lib()
+    cfg = ie.make_config(**TRAIN_BASE)
+    h = ctypes.c_void_p()
+    assert L.iefwd_train_create(ctypes.byref(cfg), None, 0, ctypes.byref(h)) == ie.EINVAL
+    assert h.value is None
+    tp = ie.train_params()
+    tp.abi_version = 99
+    assert L.iefwd_train_create(ctypes.byref(cfg), ctypes.byref(tp), 0, ctypes.byref(h)) == ie.EVERSION
+    assert L.iefwd_train_step(None, None, None, 1, 64, 0) == ie.EINVAL
+    assert L.iefwd_train_loss(None, None) == ie.EINVAL
+    assert L.iefwd_train_steps(None, None) == ie.EINVAL
+    assert L.iefwd_train_export(None, 0, 0, 0, None, 0) == ie.EINVAL
