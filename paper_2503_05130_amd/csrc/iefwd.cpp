@@ -162,7 +162,7 @@ struct TrainState {
     std::vector<Saved> saved;
     // backward scratch
     float *dxa = nullptr, *dxb = nullptr, *dz = nullptr, *xl = nullptr, *loss_t = nullptr, *dlogits = nullptr;
-    float *part = nullptr, *part2 = nullptr, *loss_sum = nullptr;
+    float *colpart = nullptr, *loss_sum = nullptr;   // column-sum partials of one layer; the loss
     bf16_t *dzb = nullptr, *dvb = nullptr, *dctx = nullptr, *dqkv = nullptr, *ta = nullptr, *tb = nullptr;
     bf16_t *zero_bias = nullptr, *attn_scratch = nullptr;
     int32_t *labels = nullptr;
@@ -639,8 +639,9 @@ void train_alloc(iefwd_instance *I, const iefwd_train_params &hp) {
     const size_t wide = std::max(F, 3 * d), parts = (size_t)colsum_partials((int)T);
     const size_t o_dxa = reserve(T * d * 4), o_dxb = reserve(T * d * 4), o_dz = reserve(T * d * 4);
     const size_t o_xl = reserve(T * d * 4), o_loss = reserve(T * 4), o_dl = reserve(T * no * 4);
-    const size_t o_part = reserve(parts * std::max(wide, no * d) * 4), o_part2 = reserve(parts * std::max(wide, no * d) * 4);
-    const size_t o_lsum = reserve(parts * 4 + 4);
+    // partial column sums of every bias / LayerNorm gradient of one layer (or of the head), each [parts, n]
+    const size_t o_colpart = reserve(parts * std::max(9 * d + F, no * d + no + 1) * 4);
+    const size_t o_lsum = reserve(4);
     const size_t o_dzb = reserve(T * d * 2), o_dvb = reserve(T * F * 2), o_dctx = reserve(T * d * 2);
     const size_t o_dqkv = reserve(T * 3 * d * 2), o_ta = reserve(wide * T * 2), o_tb = reserve(wide * T * 2);
     const size_t o_zero = reserve(wide * 2), o_lab = reserve(T * 4);
@@ -671,7 +672,7 @@ void train_alloc(iefwd_instance *I, const iefwd_train_params &hp) {
                            f32(o.z1), f32(o.st1), f32(o.z2), f32(o.st2)});
     }
     t.dxa = f32(o_dxa); t.dxb = f32(o_dxb); t.dz = f32(o_dz); t.xl = f32(o_xl); t.loss_t = f32(o_loss);
-    t.dlogits = f32(o_dl); t.part = f32(o_part); t.part2 = f32(o_part2); t.loss_sum = f32(o_lsum);
+    t.dlogits = f32(o_dl); t.colpart = f32(o_colpart); t.loss_sum = f32(o_lsum);
     t.dzb = b16(o_dzb); t.dvb = b16(o_dvb); t.dctx = b16(o_dctx); t.dqkv = b16(o_dqkv); t.ta = b16(o_ta);
     t.tb = b16(o_tb); t.zero_bias = b16(o_zero); t.attn_scratch = b16(o_ascr);
     t.labels = reinterpret_cast<int32_t *>(b + o_lab);
@@ -737,11 +738,22 @@ void train_run(iefwd_instance *I, const float *x) {
     auto fwd = [&](uint32_t kind, const char *what, auto &&f) { launch(I, kind, what, f); };
     auto bwd_gemm = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD_GEMM, what, f); };
     auto bwd = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD, what, f); };
-    // column sums of a [rows, n] matrix into dst [n], two fixed-order stages
-    auto colsum = [&](const void *src, bool is_bf16, int rows, int n, float *dst) {
-        const int parts = colsum_partials(rows);
-        bwd("column sums", [&] { return launch_colsum(src, is_bf16, t.part2, rows, n, 256, s); });
-        bwd("column sums", [&] { return launch_colsum(t.part2, false, dst, parts, n, parts, s); });
+    // Column sums of [T, n] matrices into dst [n], two fixed-order stages: the
+    // per-256-row partials when the source is ready (into t.colpart at column
+    // offset `col`), the last stages of a layer's sums together in one launch.
+    const int parts = colsum_partials(T);
+    std::vector<ColsumJob> finals;
+    auto region = [&](int col) { return t.colpart + (size_t)parts * col; };
+    auto colsum = [&](const void *src, bool is_bf16, int n, float *dst, int col) {
+        bwd("column sums", [&] { return launch_colsum(src, is_bf16, region(col), T, n, 256, s); });
+        finals.push_back({region(col), dst, parts, n});
+    };
+    auto flush_finals = [&] {
+        bwd("column sums", [&] { return launch_colsums(finals.data(), (int)finals.size(), s); });
+        finals.clear();
+    };
+    auto transposes = [&](std::initializer_list<TransposeJob> jobs) {
+        bwd("transpose", [&] { return launch_transposes(jobs.begin(), (int)jobs.size(), s); });
     };
 
     // ---- forward, saving what the backward needs
@@ -788,22 +800,22 @@ void train_run(iefwd_instance *I, const float *x) {
             return launch_head_loss(sv.z2, w.g2, w.be2, I->wh, I->bh, t.labels, t.xl, sv.st2, I->out, t.loss_t,
                                     t.dlogits, t.dxa, T, d, no, eps, 1.0f / (float)T, s);
         });
-        bwd("head partials", [&] { return launch_head_partials(t.dlogits, t.xl, t.part, T, d, no, s); });
-        const int parts = colsum_partials(T);
-        bwd("column sums", [&] { return launch_colsum(t.part, false, t.grad + t.off_wh, parts, no * d, parts, s); });
-        colsum(t.dlogits, false, T, no, t.grad + t.off_bh);
-        colsum(t.loss_t, false, T, 1, t.loss_sum);
+        bwd("head partials", [&] { return launch_head_partials(t.dlogits, t.xl, region(0), T, d, no, s); });
+        finals.push_back({region(0), t.grad + t.off_wh, parts, no * d});
+        colsum(t.dlogits, false, no, t.grad + t.off_bh, no * d);
+        colsum(t.loss_t, false, 1, t.loss_sum, no * d + no);
+        flush_finals();
     }
 
     // ---- backward, last layer first; dxa holds dL/d(layer output)
-    auto ln_grads = [&](const float *dy, const float *z, const float *st, size_t off_g, size_t off_b) {
-        const int parts = colsum_partials(T);
+    auto ln_grads = [&](const float *dy, const float *z, const float *st, size_t off_g, size_t off_b, int col) {
         bwd("layernorm param partials",
-            [&] { return launch_ln_param_partials(dy, z, st, t.part, t.part + (size_t)parts * d, T, d, s); });
-        bwd("column sums", [&] { return launch_colsum(t.part, false, t.grad + off_g, parts, d, parts, s); });
-        bwd("column sums",
-            [&] { return launch_colsum(t.part + (size_t)parts * d, false, t.grad + off_b, parts, d, parts, s); });
+            [&] { return launch_ln_param_partials(dy, z, st, region(col), region(col + d), T, d, s); });
+        finals.push_back({region(col), t.grad + off_g, parts, d});
+        finals.push_back({region(col + d), t.grad + off_b, parts, d});
     };
+    // column offsets of a layer's partial sums in t.colpart
+    const int c_ln2 = 0, c_b2 = 2 * d, c_b1 = 3 * d, c_ln1 = 3 * d + F, c_bo = 5 * d + F, c_bqkv = 6 * d + F;
     for (int l = L - 1; l >= 0; --l) {
         const LayerWeights &w = I->layers[l];
         const TrainState::Saved &sv = t.saved[l];
@@ -811,11 +823,10 @@ void train_run(iefwd_instance *I, const float *x) {
         const auto &o = t.off[l];
         // LN2: dz2 (fp32 in dz, bf16 in dzb)
         bwd("layernorm backward", [&] { return launch_ln_backward(t.dxa, sv.z2, sv.st2, w.g2, t.dz, t.dzb, T, d, s); });
-        ln_grads(t.dxa, sv.z2, sv.st2, o[10], o[11]);
+        ln_grads(t.dxa, sv.z2, sv.st2, o[10], o[11], c_ln2);
         // FFN-down: dW2 = dz2^T u, db2, dv = (dz2 W2) GELU'(v)
-        colsum(t.dz, false, T, d, t.grad + o[9]);
-        bwd("transpose", [&] { return launch_transpose_bf16(t.dzb, t.ta, T, d, s); });
-        bwd("transpose", [&] { return launch_transpose_bf16(sv.u, t.tb, T, F, s); });
+        colsum(t.dz, false, d, t.grad + o[9], c_b2);
+        transposes({{t.dzb, t.ta, T, d}, {sv.u, t.tb, T, F}});
         bwd_gemm("dW2 gemm", [&] {
             return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[8], d, F, T, nullptr, s);
         });
@@ -824,9 +835,8 @@ void train_run(iefwd_instance *I, const float *x) {
                                sv.v);
         });
         // FFN-up: dW1 = dv^T X1, db1, dX1 = dz2 + dv W1
-        colsum(t.dvb, true, T, F, t.grad + o[7]);
-        bwd("transpose", [&] { return launch_transpose_bf16(t.dvb, t.ta, T, F, s); });
-        bwd("transpose", [&] { return launch_transpose_bf16(sv.h1b, t.tb, T, d, s); });
+        colsum(t.dvb, true, F, t.grad + o[7], c_b1);
+        transposes({{t.dvb, t.ta, T, F}, {sv.h1b, t.tb, T, d}});
         bwd_gemm("dW1 gemm", [&] {
             return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[6], F, d, T, nullptr, s);
         });
@@ -835,11 +845,10 @@ void train_run(iefwd_instance *I, const float *x) {
         });
         // LN1: dz1
         bwd("layernorm backward", [&] { return launch_ln_backward(t.dxb, sv.z1, sv.st1, w.g1, t.dz, t.dzb, T, d, s); });
-        ln_grads(t.dxb, sv.z1, sv.st1, o[4], o[5]);
+        ln_grads(t.dxb, sv.z1, sv.st1, o[4], o[5], c_ln1);
         // out-projection: dWo = dz1^T ctx, dbo, dctx = dz1 Wo
-        colsum(t.dz, false, T, d, t.grad + o[3]);
-        bwd("transpose", [&] { return launch_transpose_bf16(t.dzb, t.ta, T, d, s); });
-        bwd("transpose", [&] { return launch_transpose_bf16(sv.ctx, t.tb, T, d, s); });
+        colsum(t.dz, false, d, t.grad + o[3], c_bo);
+        transposes({{t.dzb, t.ta, T, d}, {sv.ctx, t.tb, T, d}});
         bwd_gemm("dWo gemm", [&] {
             return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[2], d, d, T, nullptr, s);
         });
@@ -852,9 +861,8 @@ void train_run(iefwd_instance *I, const float *x) {
                                              spad, causal, s);
         });
         // QKV: dWqkv = dqkv^T X, dbqkv, dX = dz1 + dqkv Wqkv
-        colsum(t.dqkv, true, T, 3 * d, t.grad + o[1]);
-        bwd("transpose", [&] { return launch_transpose_bf16(t.dqkv, t.ta, T, 3 * d, s); });
-        bwd("transpose", [&] { return launch_transpose_bf16(sv.hb, t.tb, T, d, s); });
+        colsum(t.dqkv, true, 3 * d, t.grad + o[1], c_bqkv);
+        transposes({{t.dqkv, t.ta, T, 3 * d}, {sv.hb, t.tb, T, d}});
         bwd_gemm("dWqkv gemm", [&] {
             return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[0], 3 * d, d, T, nullptr, s);
         });
@@ -863,6 +871,7 @@ void train_run(iefwd_instance *I, const float *x) {
                 return launch_gemm(Epi::BiasResidF32, t.dqkv, wt.wqkv, t.zero_bias, t.dz, t.dxa, T, d, 3 * d, nullptr,
                                    s);
             });
+        flush_finals();
     }
 
     // ---- AdamW over every parameter, then W^T for the next step's input gradients
@@ -878,13 +887,18 @@ void train_run(iefwd_instance *I, const float *x) {
     launch(I, IEFWD_K_OPTIM, "adamw", [&] {
         return launch_adamw(t.master, t.grad, t.mom1, t.mom2, t.segs_d, t.blk_seg_d, t.n_blocks, st, s);
     });
+    std::vector<TransposeJob> wjobs;
     for (int l = 0; l < L; ++l) {
         const LayerWeights &w = I->layers[l];
         const TrainState::Transposed &wt = t.wt[l];
-        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transpose_bf16(w.wqkv, wt.wqkv, 3 * d, d, s); });
-        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transpose_bf16(w.wo, wt.wo, d, d, s); });
-        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transpose_bf16(w.w1, wt.w1, F, d, s); });
-        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transpose_bf16(w.w2, wt.w2, d, F, s); });
+        wjobs.push_back({w.wqkv, wt.wqkv, 3 * d, d});
+        wjobs.push_back({w.wo, wt.wo, d, d});
+        wjobs.push_back({w.w1, wt.w1, F, d});
+        wjobs.push_back({w.w2, wt.w2, d, F});
+    }
+    for (size_t j = 0; j < wjobs.size(); j += kMaxTransposeJobs) {
+        const int n = (int)std::min(wjobs.size() - j, (size_t)kMaxTransposeJobs);
+        launch(I, IEFWD_K_OPTIM, "transpose", [&] { return launch_transposes(wjobs.data() + j, n, s); });
     }
     hip_check(hipMemcpyAsync(t.loss_host, t.loss_sum, 4, hipMemcpyDeviceToHost, s), "loss copy");
 }

@@ -132,6 +132,14 @@ hipError_t launch_decode_attention(const bf16_t *q, const bf16_t *k, const bf16_
 // ---- training step (csrc/train.hip) ----
 // bf16 [R, C] -> [C, R]; R % 64 == 0, C % 64 == 0.
 hipError_t launch_transpose_bf16(const bf16_t *src, bf16_t *dst, int R, int C, hipStream_t stream);
+// Up to kMaxTransposeJobs such transposes (bf16 src [rows, cols] -> dst [cols, rows]) in one launch.
+struct TransposeJob {
+    const bf16_t *src;
+    bf16_t *dst;
+    int32_t rows, cols;
+};
+constexpr int kMaxTransposeJobs = 48;
+hipError_t launch_transposes(const TransposeJob *jobs, int n_jobs, hipStream_t stream);
 // u = GELU(v) elementwise, bf16; n % 8 == 0.
 hipError_t launch_gelu(const bf16_t *v, bf16_t *u, size_t n, hipStream_t stream);
 // LayerNorm backward per row: dz = rstd (g - mean(g) - x^ mean(g x^)), g = dy gamma,
@@ -147,6 +155,15 @@ hipError_t launch_ln_param_partials(const float *dy, const float *z, const float
 // dst[b][f] = sum of src[r][f] over rows b * rows_per_part .. (b + 1) * rows_per_part - 1, in row order.
 hipError_t launch_colsum(const void *src, bool src_bf16, float *dst, int rows, int n, int rows_per_part,
                          hipStream_t stream);
+// Up to kMaxColsumJobs whole-column sums of fp32 [rows, n] matrices in one launch:
+// dst[f] = sum of src[r][f] over all rows, the order of launch_colsum with rows_per_part = rows.
+struct ColsumJob {
+    const float *src;
+    float *dst;
+    int32_t rows, n;
+};
+constexpr int kMaxColsumJobs = 16;
+hipError_t launch_colsums(const ColsumJob *jobs, int n_jobs, hipStream_t stream);
 // Per token: the last LayerNorm of z (two-pass statistics), logits = X Wh^T + bh,
 // softmax cross-entropy against labels, dlogits = (p - onehot) * inv_n, dX = dlogits Wh.
 // Writes xl = X (fp32 [rows, d]), stats, logits and dlogits [rows, n_out],

@@ -4,12 +4,13 @@
 //   transpose          bf16 [R, C] -> [C, R] through 64 x 64 LDS tiles (the
 //                      GEMM contracts over its operands' contiguous dimension,
 //                      so weight gradients, which contract over tokens, read
-//                      transposed activations)
+//                      transposed activations); several in one launch
+//   colsum             per row block: column sums (fp32 or bf16 input), fixed
+//                      order; the last stages of several sums in one launch
 //   gelu               u = GELU(v), bf16 -> bf16
 //   ln_backward        dz = rstd (g - mean(g) - x^ mean(g x^)), g = dy gamma,
 //                      one wave per row, fp32; writes fp32 and bf16
 //   ln_param_partials  per 256-row chunk: sum dy x^ and sum dy per column
-//   colsum             per row block: column sums (fp32 or bf16 input), fixed order
 //   head_loss          per token: the last LayerNorm, logits = X Wh^T + bh,
 //                      softmax cross-entropy, dlogits = (p - onehot) / N,
 //                      dX = dlogits Wh
@@ -45,10 +46,10 @@ __device__ inline float wave_sum(float v) {
 // ------------------------------------------------------------------ transpose
 constexpr int kTile = 64;
 
-__global__ __launch_bounds__(256) void transpose_kernel(const uint16_t *__restrict__ src, uint16_t *__restrict__ dst,
-                                                        int R, int C) {
-    __shared__ uint16_t tile[kTile][kTile + 2];
-    const int r0 = blockIdx.y * kTile, c0 = blockIdx.x * kTile, tid = threadIdx.x;
+// One 64 x 64 tile of a bf16 [R, C] -> [C, R] transpose: rows r0.., columns c0.. of src.
+__device__ inline void transpose_tile(const uint16_t *__restrict__ src, uint16_t *__restrict__ dst, int R, int C,
+                                      int r0, int c0, uint16_t (&tile)[kTile][kTile + 2]) {
+    const int tid = threadIdx.x;
     // in: rows r0 + tid / 8 (+ 32), 8 columns each (16 bytes)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -70,6 +71,29 @@ __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t *__restri
         for (int e = 0; e < 4; ++e) v[e] = (uint32_t)tile[rr + 2 * e][cc] | ((uint32_t)tile[rr + 2 * e + 1][cc] << 16);
         *reinterpret_cast<u32x4 *>(dst + (size_t)(c0 + cc) * R + r0 + rr) = v;
     }
+}
+
+__global__ __launch_bounds__(256) void transpose_kernel(const uint16_t *__restrict__ src, uint16_t *__restrict__ dst,
+                                                        int R, int C) {
+    __shared__ uint16_t tile[kTile][kTile + 2];
+    transpose_tile(src, dst, R, C, blockIdx.y * kTile, blockIdx.x * kTile, tile);
+}
+
+// Several transposes in one launch: workgroup b takes tile b - first[j] of the
+// job j with first[j] <= b < first[j + 1] (tiles numbered row-major per job).
+struct TransposeBatch {
+    TransposeJob job[kMaxTransposeJobs];
+    int32_t first[kMaxTransposeJobs + 1];
+    int32_t n;
+};
+
+__global__ __launch_bounds__(256) void transpose_jobs_kernel(TransposeBatch b) {
+    __shared__ uint16_t tile[kTile][kTile + 2];
+    int j = 0;
+    while (j + 1 < b.n && (int)blockIdx.x >= b.first[j + 1]) ++j;
+    const int t = (int)blockIdx.x - b.first[j], tiles_c = b.job[j].cols / kTile;
+    transpose_tile(reinterpret_cast<const uint16_t *>(b.job[j].src), reinterpret_cast<uint16_t *>(b.job[j].dst),
+                   b.job[j].rows, b.job[j].cols, (t / tiles_c) * kTile, (t % tiles_c) * kTile, tile);
 }
 
 // ------------------------------------------------------------------ GELU
@@ -174,12 +198,12 @@ __device__ inline float load_as_f32<float>(const float *p, size_t i) { return p[
 template <>
 __device__ inline float load_as_f32<uint16_t>(const uint16_t *p, size_t i) { return bf(p[i]); }
 
-// dst[b][f] = sum of src rows b * rb .. b * rb + rb - 1, column f
+// One workgroup's column block: dst[b * n + f] = sum of src rows b * rb ..
+// min(rows, b * rb + rb) - 1 of column f, f = 64 cb .. 64 cb + 63
 template <typename T>
-__global__ __launch_bounds__(256) void colsum_kernel(const T *__restrict__ src, float *__restrict__ dst, int rows,
-                                                     int n, int rb) {
-    __shared__ float red[kColLanes][64];
-    const int c = threadIdx.x & 63, g = threadIdx.x >> 6, f = blockIdx.x * 64 + c, b = blockIdx.y;
+__device__ inline void colsum_block(const T *__restrict__ src, float *__restrict__ dst, int rows, int n, int rb,
+                                    int cb, int b, float (&red)[kColLanes][64]) {
+    const int c = threadIdx.x & 63, g = threadIdx.x >> 6, f = cb * 64 + c;
     float s = 0.f;
     if (f < n) {
         const int r1 = min(rows, (b + 1) * rb);
@@ -188,6 +212,29 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T *__restrict__ src, 
     }
     const float t = lane_total(s, c, g, red);
     if (g == 0 && f < n) dst[(size_t)b * n + f] = t;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_kernel(const T *__restrict__ src, float *__restrict__ dst, int rows,
+                                                     int n, int rb) {
+    __shared__ float red[kColLanes][64];
+    colsum_block(src, dst, rows, n, rb, blockIdx.x, blockIdx.y, red);
+}
+
+// Several whole-column sums in one launch (one row block per job):
+// workgroup b takes column block b - first[j] of job j.
+struct ColsumBatch {
+    ColsumJob job[kMaxColsumJobs];
+    int32_t first[kMaxColsumJobs + 1];
+    int32_t n;
+};
+
+__global__ __launch_bounds__(256) void colsum_jobs_kernel(ColsumBatch b) {
+    __shared__ float red[kColLanes][64];
+    int j = 0;
+    while (j + 1 < b.n && (int)blockIdx.x >= b.first[j + 1]) ++j;
+    colsum_block(b.job[j].src, b.job[j].dst, b.job[j].rows, b.job[j].n, b.job[j].rows, (int)blockIdx.x - b.first[j],
+                 0, red);
 }
 
 // ------------------------------------------------------------------ head + loss
@@ -483,9 +530,22 @@ __global__ __launch_bounds__(256) void attention_backward_kernel(
 }
 
 // ------------------------------------------------------------------ AdamW
-// One thread per 4 parameters; block b covers parameters of segment
-// blk_seg[b] only (segments start at multiples of kAdamBlock elements).
+// One thread per 4 consecutive parameters (16-byte loads and stores; the
+// scalar form for a segment's last, partial group); block b covers parameters
+// of segment blk_seg[b] only (segments start at multiples of kAdamBlock
+// elements, and every out pointer is 16-byte aligned).
 constexpr int kAdamBlock = 1024;
+
+struct AdamOne {
+    float w, m, v;
+};
+
+__device__ inline AdamOne adam_one(float w, float g, float m, float v, float decay, const AdamStep &st) {
+    const float mm = st.beta1 * m + (1.0f - st.beta1) * g;
+    const float vv = st.beta2 * v + (1.0f - st.beta2) * g * g;
+    const float upd = (mm * st.c1) / (sqrtf(vv * st.c2) + st.eps);
+    return {w * decay - st.lr * upd, mm, vv};
+}
 
 __global__ __launch_bounds__(256) void adamw_kernel(float *__restrict__ w, const float *__restrict__ g,
                                                     float *__restrict__ m, float *__restrict__ v,
@@ -493,24 +553,41 @@ __global__ __launch_bounds__(256) void adamw_kernel(float *__restrict__ w, const
                                                     const uint32_t *__restrict__ blk_seg, AdamStep st) {
     const AdamSegment sg = segs[blk_seg[blockIdx.x]];
     const size_t base = (size_t)blockIdx.x * kAdamBlock;
-    const size_t i0 = base + threadIdx.x * 4;
-    if (i0 >= sg.offset + sg.count) return;
+    const size_t i0 = base + threadIdx.x * 4, end = sg.offset + sg.count;
+    if (i0 >= end) return;
     const float decay = sg.decay ? 1.0f - st.lr * st.weight_decay : 1.0f;
+    const size_t k0 = i0 - sg.offset;
+    if (i0 + 4 <= end) {
+        const f32x4 gg = *reinterpret_cast<const f32x4 *>(g + i0);
+        const f32x4 mm = *reinterpret_cast<const f32x4 *>(m + i0);
+        const f32x4 vv = *reinterpret_cast<const f32x4 *>(v + i0);
+        const f32x4 ww = *reinterpret_cast<const f32x4 *>(w + i0);
+        f32x4 nw, nm, nv;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const size_t i = i0 + e;
-        if (i >= sg.offset + sg.count) break;
-        const float gg = g[i];
-        const float mm = st.beta1 * m[i] + (1.0f - st.beta1) * gg;
-        const float vv = st.beta2 * v[i] + (1.0f - st.beta2) * gg * gg;
-        m[i] = mm;
-        v[i] = vv;
-        const float upd = (mm * st.c1) / (sqrtf(vv * st.c2) + st.eps);
-        const float ww = w[i] * decay - st.lr * upd;
-        w[i] = ww;
-        const size_t k = i - sg.offset;
-        if (sg.out_bf16) static_cast<uint16_t *>(sg.out)[k] = to_bf(ww);
-        else static_cast<float *>(sg.out)[k] = ww;
+        for (int e = 0; e < 4; ++e) {
+            const AdamOne r = adam_one(ww[e], gg[e], mm[e], vv[e], decay, st);
+            nw[e] = r.w;
+            nm[e] = r.m;
+            nv[e] = r.v;
+        }
+        *reinterpret_cast<f32x4 *>(m + i0) = nm;
+        *reinterpret_cast<f32x4 *>(v + i0) = nv;
+        *reinterpret_cast<f32x4 *>(w + i0) = nw;
+        if (sg.out_bf16)
+            *reinterpret_cast<u32x2 *>(static_cast<uint16_t *>(sg.out) + k0) =
+                u32x2{(uint32_t)to_bf(nw[0]) | ((uint32_t)to_bf(nw[1]) << 16),
+                      (uint32_t)to_bf(nw[2]) | ((uint32_t)to_bf(nw[3]) << 16)};
+        else
+            *reinterpret_cast<f32x4 *>(static_cast<float *>(sg.out) + k0) = nw;
+        return;
+    }
+    for (size_t i = i0; i < end; ++i) {
+        const AdamOne r = adam_one(w[i], g[i], m[i], v[i], decay, st);
+        m[i] = r.m;
+        v[i] = r.v;
+        w[i] = r.w;
+        if (sg.out_bf16) static_cast<uint16_t *>(sg.out)[i - sg.offset] = to_bf(r.w);
+        else static_cast<float *>(sg.out)[i - sg.offset] = r.w;
     }
 }
 
@@ -526,6 +603,40 @@ hipError_t launch_transpose_bf16(const bf16_t *src, bf16_t *dst, int R, int C, h
     if (R <= 0 || C <= 0) return hipSuccess;
     if (R % kTile || C % kTile) return hipErrorInvalidValue;
     return launch_kernel(transpose_kernel, dim3(C / kTile, R / kTile), dim3(256), stream, src, dst, R, C);
+}
+
+hipError_t launch_transposes(const TransposeJob *jobs, int n_jobs, hipStream_t stream) {
+    if (n_jobs <= 0) return hipSuccess;
+    if (n_jobs > kMaxTransposeJobs) return hipErrorInvalidValue;
+    TransposeBatch b{};
+    b.n = n_jobs;
+    long tiles = 0;
+    for (int j = 0; j < n_jobs; ++j) {
+        const TransposeJob &jb = jobs[j];
+        if (jb.rows <= 0 || jb.cols <= 0 || jb.rows % kTile || jb.cols % kTile) return hipErrorInvalidValue;
+        b.job[j] = jb;
+        b.first[j] = (int32_t)tiles;
+        tiles += (long)(jb.rows / kTile) * (jb.cols / kTile);
+        if (tiles > 0x7fffffffL) return hipErrorInvalidValue;
+    }
+    b.first[n_jobs] = (int32_t)tiles;
+    return launch_kernel(transpose_jobs_kernel, dim3((unsigned)tiles), dim3(256), stream, b);
+}
+
+hipError_t launch_colsums(const ColsumJob *jobs, int n_jobs, hipStream_t stream) {
+    if (n_jobs <= 0) return hipSuccess;
+    if (n_jobs > kMaxColsumJobs) return hipErrorInvalidValue;
+    ColsumBatch b{};
+    b.n = n_jobs;
+    int blocks = 0;
+    for (int j = 0; j < n_jobs; ++j) {
+        if (jobs[j].rows <= 0 || jobs[j].n <= 0) return hipErrorInvalidValue;
+        b.job[j] = jobs[j];
+        b.first[j] = blocks;
+        blocks += (jobs[j].n + 63) / 64;
+    }
+    b.first[n_jobs] = blocks;
+    return launch_kernel(colsum_jobs_kernel, dim3(blocks), dim3(256), stream, b);
 }
 
 hipError_t launch_gelu(const bf16_t *v, bf16_t *u, size_t n, hipStream_t stream) {

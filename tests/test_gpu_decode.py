@@ -31,7 +31,9 @@ def check(got, ref, what=""):
     (1, 1, 1, 64, 1, 64),
     (2, 3, 7, 64, 16, 64),
     (3, 2, 513, 64, 600, 640),
-    (1, 1, 64, 128, 64, 64),                # one full chunk of 64
+    (1, 1, 64, 128, 64, 64),
+    (2, 5, 1000, 128, 1000, 1024),
+    (1, 3, 1024, 64, 1024, 1024),
     (2, 16, 1025, 128, 1100, 1152),
     (1, 2, 2048, 64, 2048, 2048),           # 32 chunks of 64: the most chunks
     (2, 2, 2049, 64, 2100, 2112),           # first length split into chunks of 256

@@ -148,6 +148,8 @@ def attn_inputs(B, H, S, dh, seed, scale=1.0):
     (2, 4, 512, 64, True),     # decoder prefill, several workgroups per head
     (1, 2, 1024, 128, True),
     (1, 2, 300, 128, False),
+    (24, 12, 230, 64, True),   # 576 heads x 128-query groups: 4-wave workgroups
+    (6, 16, 700, 128, False),
 ])
 @pytest.mark.parametrize("scale", [0.5, 2.0])
 def test_attention(B, H, S, dh, causal, scale):
@@ -167,6 +169,25 @@ def test_attention(B, H, S, dh, causal, scale):
     tol = 2.5 * UBF * vmax + UBF * 1.01 * np.abs(ref) + 1e-4 * vmax
     assert np.all(np.isfinite(got))
     assert np.all(np.abs(got - ref) <= tol), float(np.max(np.abs(got - ref) - tol))
+
+
+@pytest.mark.parametrize("dh,causal", [(64, False), (64, True), (128, True)])
+def test_attention_batch_invariant(dh, causal):
+    """A head's context does not depend on how many other heads share the
+    launch: a large batch (128-query workgroups) and a one-sequence launch
+    (64-query workgroups) give the same bits."""
+    B, H, S = 40, 13, 200
+    print(f"attention batch invariance dh={dh} causal={causal}", flush=True)
+    q, k, v = attn_inputs(B, H, S, dh, seed=dh + 7)
+    vt = torch.zeros((B, H, dh, 256), dtype=torch.bfloat16)
+    vt[..., :S] = v.transpose(2, 3)
+    full = torch.empty((B, S, H * dh), dtype=torch.bfloat16, device=DEV)
+    ie.test_attention(to_dev(q), to_dev(k), to_dev(vt), full, B, H, S, dh, causal)
+    for b in (0, 17, B - 1):
+        one = torch.empty((1, S, H * dh), dtype=torch.bfloat16, device=DEV)
+        ie.test_attention(to_dev(q[b:b + 1]), to_dev(k[b:b + 1]), to_dev(vt[b:b + 1]), one, 1, H, S, dh, causal)
+        sync()
+        assert torch.equal(one[0].view(torch.int16), full[b].view(torch.int16)), b
 
 
 def test_attention_uniform_closed_form():
