@@ -360,15 +360,18 @@ __global__ __launch_bounds__(256) void head_partials_kernel(const float *__restr
 // five products on v_mfma_f32_32x32x16_bf16.  (32x32x16 operands: lane l holds
 // A[l % 32][8 (l / 32) .. +8] and B[8 (l / 32) .. +8][l % 32]; accumulator
 // entry r of lane l is C[8 (r / 4) + 4 (l / 32) + r % 4][l % 32].)
-//   load     Q, K, V, dO of the head into LDS in row layout ([token][c]) and Q,
-//            K, dO also transposed ([c][token]); D_i = sum_c dO[i][c] O[i][c].
-//            Rows past S are zero.
+//   load     Q, K, V, dO of the head into LDS in row layout ([token][c]);
+//            D_i = sum_c dO[i][c] O[i][c].  Rows past S are zero.
 //   phase 1  wave w, queries 32 w .. 32 w + 31: S^T = K Q^T and dP^T = V dO^T
 //            (keys as rows, so a lane holds 64 of its query's 128 keys, its
 //            partner lane l ^ 32 the rest); softmax over keys in registers
 //            (causal: keys j <= i), dS = P (dP - D_i).  P^T and dS^T ([key]
 //            [query]) and dS ([query][key]) go to a per-head scratch in global
 //            memory (L2-resident), the layouts phase 2 reads as A operands.
+//   relayout Q, K and dO move from the row copies (through registers) to
+//            transposed copies ([c][token]) in the same LDS, which phase 2
+//            reads as B operands.  Only one layout is ever resident, so a
+//            workgroup takes 74 KB of LDS and two share a CU.
 //   phase 2  wave w: dV = P^T dO and dK = dS^T Q for keys 32 w .. 32 w + 31,
 //            dQ = dS K for queries 32 w .. 32 w + 31 (dQ and dK times
 //            1 / sqrt(dh)).
@@ -386,10 +389,12 @@ __global__ __launch_bounds__(256) void attention_backward_kernel(
     const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K, const uint16_t *__restrict__ Vt,
     const uint16_t *__restrict__ ctx, const uint16_t *__restrict__ dctx, uint16_t *__restrict__ dqkv,
     uint16_t *__restrict__ scratch, int n_heads, int S, int vt_stride, int causal, float scale) {
-    __shared__ __attribute__((aligned(16))) uint16_t sQ[kAbSeq * kAbLd], sK[kAbSeq * kAbLd], sV[kAbSeq * kAbLd],
-        sdO[kAbSeq * kAbLd];
-    __shared__ __attribute__((aligned(16))) uint16_t sQt[kAbDh * kAbLdT], sKt[kAbDh * kAbLdT], sdOt[kAbDh * kAbLdT];
+    // row copies for phase 1; the transposed copies of phase 2 reuse the same space
+    static_assert(3 * kAbDh * kAbLdT <= 4 * kAbSeq * kAbLd, "transposed copies fit the row copies' space");
+    __shared__ __attribute__((aligned(16))) uint16_t lds[4 * kAbSeq * kAbLd];
     __shared__ float sD[kAbSeq];
+    uint16_t *sQ = lds, *sK = sQ + kAbSeq * kAbLd, *sV = sK + kAbSeq * kAbLd, *sdO = sV + kAbSeq * kAbLd;
+    uint16_t *sQt = lds, *sKt = sQt + kAbDh * kAbLdT, *sdOt = sKt + kAbDh * kAbLdT;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, half = lane >> 5, col = lane & 31;
     const int bh = blockIdx.x, b = bh / n_heads, h = bh - b * n_heads;
     const int d = n_heads * kAbDh;
@@ -412,16 +417,9 @@ __global__ __launch_bounds__(256) void attention_backward_kernel(
         *reinterpret_cast<u32x4 *>(sdO + i * kAbLd + c0) = g;
         float dot = 0.f;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            sQt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(q[e] & 0xffffu);
-            sQt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(q[e] >> 16);
-            sKt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(k[e] & 0xffffu);
-            sKt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(k[e] >> 16);
-            sdOt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(g[e] & 0xffffu);
-            sdOt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(g[e] >> 16);
+        for (int e = 0; e < 4; ++e)
             dot += __uint_as_float(g[e] << 16) * __uint_as_float(o[e] << 16) +
                    __uint_as_float(g[e] & 0xffff0000u) * __uint_as_float(o[e] & 0xffff0000u);
-        }
         // the 8 vectors of row i are 8 consecutive lanes
 #pragma unroll
         for (int m = 4; m >= 1; m >>= 1) dot += __shfl_xor(dot, m);
@@ -494,7 +492,32 @@ __global__ __launch_bounds__(256) void attention_backward_kernel(
             *reinterpret_cast<u32x2 *>(dS + iq * kAbSeq + 32 * jb + 8 * q4 + 4 * half) =
                 u32x2{(uint32_t)dsv[0] | ((uint32_t)dsv[1] << 16), (uint32_t)dsv[2] | ((uint32_t)dsv[3] << 16)};
         }
-    __syncthreads();   // the scratch is complete (workgroup scope)
+
+    // ---- relayout: Q, K, dO rows -> registers -> transposed copies over the same LDS
+    constexpr int kVecs = kAbSeq * kAbDh / 8 / 256;   // 8-element row vectors per thread and matrix
+    u32x4 rq[kVecs], rk[kVecs], rg[kVecs];
+#pragma unroll
+    for (int u = 0; u < kVecs; ++u) {
+        const int v = tid + 256 * u, i = v / 8, c0 = (v % 8) * 8;
+        rq[u] = *reinterpret_cast<const u32x4 *>(sQ + i * kAbLd + c0);
+        rk[u] = *reinterpret_cast<const u32x4 *>(sK + i * kAbLd + c0);
+        rg[u] = *reinterpret_cast<const u32x4 *>(sdO + i * kAbLd + c0);
+    }
+    __syncthreads();   // every wave is done with the row copies
+#pragma unroll
+    for (int u = 0; u < kVecs; ++u) {
+        const int v = tid + 256 * u, i = v / 8, c0 = (v % 8) * 8;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            sQt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(rq[u][e] & 0xffffu);
+            sQt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(rq[u][e] >> 16);
+            sKt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(rk[u][e] & 0xffffu);
+            sKt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(rk[u][e] >> 16);
+            sdOt[(c0 + 2 * e) * kAbLdT + i] = (uint16_t)(rg[u][e] & 0xffffu);
+            sdOt[(c0 + 2 * e + 1) * kAbLdT + i] = (uint16_t)(rg[u][e] >> 16);
+        }
+    }
+    __syncthreads();   // the transposed copies and the scratch are complete (workgroup scope)
 
     // ---- phase 2: keys 32 w .. 32 w + 31 (dV, dK) and queries 32 w .. 32 w + 31 (dQ)
     f32x16 dv[2], dk[2], dq[2];
