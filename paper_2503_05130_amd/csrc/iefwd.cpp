@@ -636,11 +636,12 @@ void train_alloc(iefwd_instance *I, const iefwd_train_params &hp) {
         o_sv[l] = {reserve(T * d * 2), reserve(T * d * 2), reserve(T * d * 2), reserve(c.max_batch * d * spad * 2),
                    reserve(T * d * 2), reserve(T * d * 2), reserve(T * F * 2), reserve(T * F * 2),
                    reserve(T * d * 4), reserve(T * 8), reserve(T * d * 4), reserve(T * 8)};
-    const size_t wide = std::max(F, 3 * d), parts = (size_t)colsum_partials((int)T);
+    const size_t wide = std::max(F, 3 * d);
     const size_t o_dxa = reserve(T * d * 4), o_dxb = reserve(T * d * 4), o_dz = reserve(T * d * 4);
     const size_t o_xl = reserve(T * d * 4), o_loss = reserve(T * 4), o_dl = reserve(T * no * 4);
-    // partial column sums of every bias / LayerNorm gradient of one layer (or of the head), each [parts, n]
-    const size_t o_colpart = reserve(parts * std::max(9 * d + F, no * d + no + 1) * 4);
+    // partial column sums of every bias / LayerNorm gradient of one layer (or of the head), each at most
+    // [T / 64, n] (a step has T % 64 == 0)
+    const size_t o_colpart = reserve(T / 64 * std::max(9 * d + F, no * d + no + 1) * 4);
     const size_t o_lsum = reserve(4);
     const size_t o_dzb = reserve(T * d * 2), o_dvb = reserve(T * F * 2), o_dctx = reserve(T * d * 2);
     const size_t o_dqkv = reserve(T * 3 * d * 2), o_ta = reserve(wide * T * 2), o_tb = reserve(wide * T * 2);
@@ -739,11 +740,14 @@ void train_run(iefwd_instance *I, const float *x) {
     auto bwd_gemm = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD_GEMM, what, f); };
     auto bwd = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD, what, f); };
     // Column sums of [T, n] matrices into dst [n], two fixed-order stages: the
-    // per-256-row partials when the source is ready (into t.colpart at column
-    // offset `col`), the last stages of a layer's sums together in one launch.
-    const int parts = colsum_partials(T);
+    // partials of row blocks when the source is ready (into t.colpart at column
+    // offset `col`, T / 64 rows per region), the last stages of a layer's sums
+    // together in one launch.  Bias gradients take their partials from the
+    // transpose of the output gradient (64-row blocks), the others from
+    // 256-row chunks.
+    const int parts = colsum_partials(T), blocks64 = T / 64;
     std::vector<ColsumJob> finals;
-    auto region = [&](int col) { return t.colpart + (size_t)parts * col; };
+    auto region = [&](int col) { return t.colpart + (size_t)blocks64 * col; };
     auto colsum = [&](const void *src, bool is_bf16, int n, float *dst, int col) {
         bwd("column sums", [&] { return launch_colsum(src, is_bf16, region(col), T, n, 256, s); });
         finals.push_back({region(col), dst, parts, n});
@@ -825,8 +829,8 @@ void train_run(iefwd_instance *I, const float *x) {
         bwd("layernorm backward", [&] { return launch_ln_backward(t.dxa, sv.z2, sv.st2, w.g2, t.dz, t.dzb, T, d, s); });
         ln_grads(t.dxa, sv.z2, sv.st2, o[10], o[11], c_ln2);
         // FFN-down: dW2 = dz2^T u, db2, dv = (dz2 W2) GELU'(v)
-        colsum(t.dz, false, d, t.grad + o[9], c_b2);
-        transposes({{t.dzb, t.ta, T, d}, {sv.u, t.tb, T, F}});
+        transposes({{t.dzb, t.ta, T, d, region(c_b2)}, {sv.u, t.tb, T, F}});
+        finals.push_back({region(c_b2), t.grad + o[9], blocks64, d});
         bwd_gemm("dW2 gemm", [&] {
             return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[8], d, F, T, nullptr, s);
         });
@@ -835,8 +839,8 @@ void train_run(iefwd_instance *I, const float *x) {
                                sv.v);
         });
         // FFN-up: dW1 = dv^T X1, db1, dX1 = dz2 + dv W1
-        colsum(t.dvb, true, F, t.grad + o[7], c_b1);
-        transposes({{t.dvb, t.ta, T, F}, {sv.h1b, t.tb, T, d}});
+        transposes({{t.dvb, t.ta, T, F, region(c_b1)}, {sv.h1b, t.tb, T, d}});
+        finals.push_back({region(c_b1), t.grad + o[7], blocks64, F});
         bwd_gemm("dW1 gemm", [&] {
             return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[6], F, d, T, nullptr, s);
         });
@@ -847,8 +851,8 @@ void train_run(iefwd_instance *I, const float *x) {
         bwd("layernorm backward", [&] { return launch_ln_backward(t.dxb, sv.z1, sv.st1, w.g1, t.dz, t.dzb, T, d, s); });
         ln_grads(t.dxb, sv.z1, sv.st1, o[4], o[5], c_ln1);
         // out-projection: dWo = dz1^T ctx, dbo, dctx = dz1 Wo
-        colsum(t.dz, false, d, t.grad + o[3], c_bo);
-        transposes({{t.dzb, t.ta, T, d}, {sv.ctx, t.tb, T, d}});
+        transposes({{t.dzb, t.ta, T, d, region(c_bo)}, {sv.ctx, t.tb, T, d}});
+        finals.push_back({region(c_bo), t.grad + o[3], blocks64, d});
         bwd_gemm("dWo gemm", [&] {
             return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[2], d, d, T, nullptr, s);
         });
@@ -861,8 +865,8 @@ void train_run(iefwd_instance *I, const float *x) {
                                              spad, causal, s);
         });
         // QKV: dWqkv = dqkv^T X, dbqkv, dX = dz1 + dqkv Wqkv
-        colsum(t.dqkv, true, 3 * d, t.grad + o[1], c_bqkv);
-        transposes({{t.dqkv, t.ta, T, 3 * d}, {sv.hb, t.tb, T, d}});
+        transposes({{t.dqkv, t.ta, T, 3 * d, region(c_bqkv)}, {sv.hb, t.tb, T, d}});
+        finals.push_back({region(c_bqkv), t.grad + o[1], blocks64, 3 * d});
         bwd_gemm("dWqkv gemm", [&] {
             return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[0], 3 * d, d, T, nullptr, s);
         });

@@ -133,10 +133,13 @@ hipError_t launch_decode_attention(const bf16_t *q, const bf16_t *k, const bf16_
 // bf16 [R, C] -> [C, R]; R % 64 == 0, C % 64 == 0.
 hipError_t launch_transpose_bf16(const bf16_t *src, bf16_t *dst, int R, int C, hipStream_t stream);
 // Up to kMaxTransposeJobs such transposes (bf16 src [rows, cols] -> dst [cols, rows]) in one launch.
+// With colsum non-null the job also writes the column sums of each 64-row block
+// of src: colsum[b * cols + c] = sum of src[64 b .. 64 b + 63][c] (fp32, a fixed order).
 struct TransposeJob {
     const bf16_t *src;
     bf16_t *dst;
     int32_t rows, cols;
+    float *colsum = nullptr;
 };
 constexpr int kMaxTransposeJobs = 48;
 hipError_t launch_transposes(const TransposeJob *jobs, int n_jobs, hipStream_t stream);

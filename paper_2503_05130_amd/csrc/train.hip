@@ -4,7 +4,9 @@
 //   transpose          bf16 [R, C] -> [C, R] through 64 x 64 LDS tiles (the
 //                      GEMM contracts over its operands' contiguous dimension,
 //                      so weight gradients, which contract over tokens, read
-//                      transposed activations); several in one launch
+//                      transposed activations); several in one launch; on
+//                      request also the per-64-row column sums of the source
+//                      (the bias gradients' first stage)
 //   colsum             per row block: column sums (fp32 or bf16 input), fixed
 //                      order; the last stages of several sums in one launch
 //   gelu               u = GELU(v), bf16 -> bf16
@@ -47,8 +49,12 @@ __device__ inline float wave_sum(float v) {
 constexpr int kTile = 64;
 
 // One 64 x 64 tile of a bf16 [R, C] -> [C, R] transpose: rows r0.., columns c0.. of src.
+// With colsum non-null, also colsum[(r0 / 64) * C + c0 + c] = sum over the tile's
+// rows of column c: thread (c, q) adds rows 16 q .. 16 q + 15 in order, then the
+// four partial sums are added in q order.
 __device__ inline void transpose_tile(const uint16_t *__restrict__ src, uint16_t *__restrict__ dst, int R, int C,
-                                      int r0, int c0, uint16_t (&tile)[kTile][kTile + 2]) {
+                                      int r0, int c0, uint16_t (&tile)[kTile][kTile + 2], float *__restrict__ colsum,
+                                      float (&red)[4][kTile]) {
     const int tid = threadIdx.x;
     // in: rows r0 + tid / 8 (+ 32), 8 columns each (16 bytes)
 #pragma unroll
@@ -71,12 +77,22 @@ __device__ inline void transpose_tile(const uint16_t *__restrict__ src, uint16_t
         for (int e = 0; e < 4; ++e) v[e] = (uint32_t)tile[rr + 2 * e][cc] | ((uint32_t)tile[rr + 2 * e + 1][cc] << 16);
         *reinterpret_cast<u32x4 *>(dst + (size_t)(c0 + cc) * R + r0 + rr) = v;
     }
+    if (colsum) {   // uniform over the workgroup
+        const int c = tid & 63, q = tid >> 6;
+        float sum = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sum += bf(tile[16 * q + r][c]);
+        red[q][c] = sum;
+        __syncthreads();
+        if (q == 0) colsum[(size_t)(r0 / kTile) * C + c0 + c] = red[0][c] + red[1][c] + red[2][c] + red[3][c];
+    }
 }
 
 __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t *__restrict__ src, uint16_t *__restrict__ dst,
                                                         int R, int C) {
     __shared__ uint16_t tile[kTile][kTile + 2];
-    transpose_tile(src, dst, R, C, blockIdx.y * kTile, blockIdx.x * kTile, tile);
+    __shared__ float red[4][kTile];
+    transpose_tile(src, dst, R, C, blockIdx.y * kTile, blockIdx.x * kTile, tile, nullptr, red);
 }
 
 // Several transposes in one launch: workgroup b takes tile b - first[j] of the
@@ -89,11 +105,13 @@ struct TransposeBatch {
 
 __global__ __launch_bounds__(256) void transpose_jobs_kernel(TransposeBatch b) {
     __shared__ uint16_t tile[kTile][kTile + 2];
+    __shared__ float red[4][kTile];
     int j = 0;
     while (j + 1 < b.n && (int)blockIdx.x >= b.first[j + 1]) ++j;
     const int t = (int)blockIdx.x - b.first[j], tiles_c = b.job[j].cols / kTile;
     transpose_tile(reinterpret_cast<const uint16_t *>(b.job[j].src), reinterpret_cast<uint16_t *>(b.job[j].dst),
-                   b.job[j].rows, b.job[j].cols, (t / tiles_c) * kTile, (t % tiles_c) * kTile, tile);
+                   b.job[j].rows, b.job[j].cols, (t / tiles_c) * kTile, (t % tiles_c) * kTile, tile, b.job[j].colsum,
+                   red);
 }
 
 // ------------------------------------------------------------------ GELU
