@@ -597,6 +597,13 @@ void validate_train(const iefwd_config &c, const iefwd_train_params &p) {
 
 // Allocates the training state and initialises the fp32 master weights from
 // the instance's stored bf16 / fp32 weights, the moments to zero and W^T.
+// Rows of each column-sum partials region for T tokens: the most any first
+// stage writes (bias gradients: T / 64; LayerNorm parameters:
+// ln_backward_partials; the head: colsum_partials).
+int colpart_rows(int T, int d) {
+    return std::max({T / 64, ln_backward_partials(T, d), colsum_partials(T)});
+}
+
 void train_alloc(iefwd_instance *I, const iefwd_train_params &hp) {
     const iefwd_config &c = I->cfg;
     auto ts = std::make_unique<TrainState>();
@@ -640,8 +647,8 @@ void train_alloc(iefwd_instance *I, const iefwd_train_params &hp) {
     const size_t o_dxa = reserve(T * d * 4), o_dxb = reserve(T * d * 4), o_dz = reserve(T * d * 4);
     const size_t o_xl = reserve(T * d * 4), o_loss = reserve(T * 4), o_dl = reserve(T * no * 4);
     // partial column sums of every bias / LayerNorm gradient of one layer (or of the head), each at most
-    // [T / 64, n] (a step has T % 64 == 0)
-    const size_t o_colpart = reserve(T / 64 * std::max(9 * d + F, no * d + no + 1) * 4);
+    // [colpart_rows, n]
+    const size_t o_colpart = reserve((size_t)colpart_rows((int)T, (int)d) * std::max(9 * d + F, no * d + no + 1) * 4);
     const size_t o_lsum = reserve(4);
     const size_t o_dzb = reserve(T * d * 2), o_dvb = reserve(T * F * 2), o_dctx = reserve(T * d * 2);
     const size_t o_dqkv = reserve(T * 3 * d * 2), o_ta = reserve(wide * T * 2), o_tb = reserve(wide * T * 2);
@@ -745,9 +752,9 @@ void train_run(iefwd_instance *I, const float *x) {
     // together in one launch.  Bias gradients take their partials from the
     // transpose of the output gradient (64-row blocks), the others from
     // 256-row chunks.
-    const int parts = colsum_partials(T), blocks64 = T / 64;
+    const int parts = colsum_partials(T), blocks64 = T / 64, ln_parts = ln_backward_partials(T, d);
     std::vector<ColsumJob> finals;
-    auto region = [&](int col) { return t.colpart + (size_t)blocks64 * col; };
+    auto region = [&](int col) { return t.colpart + (size_t)colpart_rows(T, d) * col; };
     auto colsum = [&](const void *src, bool is_bf16, int n, float *dst, int col) {
         bwd("column sums", [&] { return launch_colsum(src, is_bf16, region(col), T, n, 256, s); });
         finals.push_back({region(col), dst, parts, n});
@@ -812,11 +819,14 @@ void train_run(iefwd_instance *I, const float *x) {
     }
 
     // ---- backward, last layer first; dxa holds dL/d(layer output)
-    auto ln_grads = [&](const float *dy, const float *z, const float *st, size_t off_g, size_t off_b, int col) {
-        bwd("layernorm param partials",
-            [&] { return launch_ln_param_partials(dy, z, st, region(col), region(col + d), T, d, s); });
-        finals.push_back({region(col), t.grad + off_g, parts, d});
-        finals.push_back({region(col + d), t.grad + off_b, parts, d});
+    // LayerNorm backward (dz fp32 and bf16) with its parameters' partial sums
+    auto ln_backward = [&](const float *dy, const float *z, const float *st, const float *gamma, size_t off_g,
+                           size_t off_b, int col) {
+        bwd("layernorm backward", [&] {
+            return launch_ln_backward_params(dy, z, st, gamma, t.dz, t.dzb, region(col), region(col + d), T, d, s);
+        });
+        finals.push_back({region(col), t.grad + off_g, ln_parts, d});
+        finals.push_back({region(col + d), t.grad + off_b, ln_parts, d});
     };
     // column offsets of a layer's partial sums in t.colpart
     const int c_ln2 = 0, c_b2 = 2 * d, c_b1 = 3 * d, c_ln1 = 3 * d + F, c_bo = 5 * d + F, c_bqkv = 6 * d + F;
@@ -826,8 +836,7 @@ void train_run(iefwd_instance *I, const float *x) {
         const TrainState::Transposed &wt = t.wt[l];
         const auto &o = t.off[l];
         // LN2: dz2 (fp32 in dz, bf16 in dzb)
-        bwd("layernorm backward", [&] { return launch_ln_backward(t.dxa, sv.z2, sv.st2, w.g2, t.dz, t.dzb, T, d, s); });
-        ln_grads(t.dxa, sv.z2, sv.st2, o[10], o[11], c_ln2);
+        ln_backward(t.dxa, sv.z2, sv.st2, w.g2, o[10], o[11], c_ln2);
         // FFN-down: dW2 = dz2^T u, db2, dv = (dz2 W2) GELU'(v)
         transposes({{t.dzb, t.ta, T, d, region(c_b2)}, {sv.u, t.tb, T, F}});
         finals.push_back({region(c_b2), t.grad + o[9], blocks64, d});
@@ -848,8 +857,7 @@ void train_run(iefwd_instance *I, const float *x) {
             return launch_gemm(Epi::BiasResidF32, t.dvb, wt.w1, t.zero_bias, t.dz, t.dxb, T, d, F, nullptr, s);
         });
         // LN1: dz1
-        bwd("layernorm backward", [&] { return launch_ln_backward(t.dxb, sv.z1, sv.st1, w.g1, t.dz, t.dzb, T, d, s); });
-        ln_grads(t.dxb, sv.z1, sv.st1, o[4], o[5], c_ln1);
+        ln_backward(t.dxb, sv.z1, sv.st1, w.g1, o[4], o[5], c_ln1);
         // out-projection: dWo = dz1^T ctx, dbo, dctx = dz1 Wo
         transposes({{t.dzb, t.ta, T, d, region(c_bo)}, {sv.ctx, t.tb, T, d}});
         finals.push_back({region(c_bo), t.grad + o[3], blocks64, d});

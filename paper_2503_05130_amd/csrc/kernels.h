@@ -155,6 +155,13 @@ int colsum_partials(int rows);
 // part_g[b][f] = sum_r dy x^, part_b[b][f] = sum_r dy over the rows of chunk b.
 hipError_t launch_ln_param_partials(const float *dy, const float *z, const float *stats, float *part_g,
                                     float *part_b, int rows, int d, hipStream_t stream);
+// launch_ln_backward and the parameter partials together: part_g / part_b get
+// ln_backward_partials(rows, d) rows (row blocks of 16 rows for d <= 1024,
+// one pass over dy and z; else the 256-row chunks of launch_ln_param_partials).
+int ln_backward_partials(int rows, int d);
+hipError_t launch_ln_backward_params(const float *dy, const float *z, const float *stats, const float *gamma,
+                                     float *dz, bf16_t *dzb, float *part_g, float *part_b, int rows, int d,
+                                     hipStream_t stream);
 // dst[b][f] = sum of src[r][f] over rows b * rows_per_part .. (b + 1) * rows_per_part - 1, in row order.
 hipError_t launch_colsum(const void *src, bool src_bf16, float *dst, int rows, int n, int rows_per_part,
                          hipStream_t stream);

@@ -13,6 +13,8 @@
 //   ln_backward        dz = rstd (g - mean(g) - x^ mean(g x^)), g = dy gamma,
 //                      one wave per row, fp32; writes fp32 and bf16
 //   ln_param_partials  per 256-row chunk: sum dy x^ and sum dy per column
+//   ln_backward_params ln_backward with the parameter partials of 16-row
+//                      blocks (d <= 1024: one pass over dy and z)
 //   head_loss          per token: the last LayerNorm, logits = X Wh^T + bh,
 //                      softmax cross-entropy, dlogits = (p - onehot) / N,
 //                      dX = dlogits Wh
@@ -170,6 +172,84 @@ __global__ __launch_bounds__(64 * kRowsPerBlock) void ln_backward_kernel(
             u32x2{(uint32_t)to_bf(o[0]) | ((uint32_t)to_bf(o[1]) << 16), (uint32_t)to_bf(o[2]) | ((uint32_t)to_bf(o[3]) << 16)};
     }
 }
+
+// LayerNorm backward fused with the first stage of its parameter gradients,
+// for d <= 256 NV: a workgroup of 4 waves takes 4 RPW consecutive rows (wave w
+// rows w RPW .. w RPW + RPW - 1, each as in ln_backward_kernel) and keeps, per
+// lane, the running sums of dy x^ and dy over its rows for its columns; the
+// four waves' sums are added in wave order into the block's partial row.
+template <int NV, int RPW>
+__global__ __launch_bounds__(256) void ln_backward_params_kernel(
+    const float *__restrict__ dy, const float *__restrict__ z, const float *__restrict__ stats,
+    const float *__restrict__ gamma, float *__restrict__ dz, uint16_t *__restrict__ dzb, float *__restrict__ part_g,
+    float *__restrict__ part_b, int rows, int d) {
+    __shared__ float red[2][4][256 * NV];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nv = d / 4, blk = blockIdx.x;
+    const f32x4 *g4 = reinterpret_cast<const f32x4 *>(gamma);
+    f32x4 gm[NV], pg[NV], pb[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) {
+        const int i = v * 64 + lane;
+        gm[v] = i < nv ? g4[i] : f32x4{0.f, 0.f, 0.f, 0.f};
+        pg[v] = pb[v] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const float inv_d = 1.0f / (float)d;
+    for (int k = 0; k < RPW; ++k) {
+        const int row = (blk * 4 + wave) * RPW + k;
+        if (row >= rows) break;   // wave-uniform
+        const float mean = stats[2 * (size_t)row], rstd = stats[2 * (size_t)row + 1];
+        const f32x4 *dyr = reinterpret_cast<const f32x4 *>(dy + (size_t)row * d);
+        const f32x4 *zr = reinterpret_cast<const f32x4 *>(z + (size_t)row * d);
+        f32x4 a[NV], xh[NV];
+        float sg = 0.f, sgx = 0.f;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const int i = v * 64 + lane;
+            a[v] = xh[v] = f32x4{0.f, 0.f, 0.f, 0.f};
+            if (i < nv) {
+                a[v] = dyr[i];
+                const f32x4 zz = zr[i];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) xh[v][e] = (zz[e] - mean) * rstd;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float gg = a[v][e] * gm[v][e];
+                sg += gg;
+                sgx += gg * xh[v][e];
+            }
+        }
+        const float mg = wave_sum(sg) * inv_d, mgx = wave_sum(sgx) * inv_d;
+#pragma unroll
+        for (int v = 0; v < NV; ++v) {
+            const int i = v * 64 + lane;
+            if (i >= nv) continue;
+            f32x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                o[e] = rstd * (a[v][e] * gm[v][e] - mg - xh[v][e] * mgx);
+                pg[v][e] += a[v][e] * xh[v][e];
+                pb[v][e] += a[v][e];
+            }
+            if (dz) reinterpret_cast<f32x4 *>(dz + (size_t)row * d)[i] = o;
+            reinterpret_cast<u32x2 *>(dzb + (size_t)row * d)[i] =
+                u32x2{(uint32_t)to_bf(o[0]) | ((uint32_t)to_bf(o[1]) << 16), (uint32_t)to_bf(o[2]) | ((uint32_t)to_bf(o[3]) << 16)};
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < NV; ++v)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            red[0][wave][4 * (v * 64 + lane) + e] = pg[v][e];
+            red[1][wave][4 * (v * 64 + lane) + e] = pb[v][e];
+        }
+    __syncthreads();
+    for (int f = threadIdx.x; f < d; f += 256) {
+        part_g[(size_t)blk * d + f] = red[0][0][f] + red[0][1][f] + red[0][2][f] + red[0][3][f];
+        part_b[(size_t)blk * d + f] = red[1][0][f] + red[1][1][f] + red[1][2][f] + red[1][3][f];
+    }
+}
+constexpr int kLnbRowsPerWave = 4;
 
 // ------------------------------------------------------------------ column sums
 // A workgroup sums 64 columns over one chunk of kColRows rows: thread (column
@@ -696,6 +776,35 @@ hipError_t launch_ln_backward(const float *dy, const float *z, const float *stat
 }
 
 int colsum_partials(int rows) { return (rows + kColRows - 1) / kColRows; }
+
+int ln_backward_partials(int rows, int d) {
+    return d <= 1024 ? (rows + 4 * kLnbRowsPerWave - 1) / (4 * kLnbRowsPerWave) : colsum_partials(rows);
+}
+
+hipError_t launch_ln_backward_params(const float *dy, const float *z, const float *stats, const float *gamma,
+                                     float *dz, bf16_t *dzb, float *part_g, float *part_b, int rows, int d,
+                                     hipStream_t stream) {
+    if (rows <= 0) return hipSuccess;
+    if (d % 4) return hipErrorInvalidValue;
+    if (d > 1024) {   // registers hold at most 16 columns per lane: the two-kernel form
+        const hipError_t e = launch_ln_backward(dy, z, stats, gamma, dz, dzb, rows, d, stream);
+        if (e != hipSuccess) return e;
+        return launch_ln_param_partials(dy, z, stats, part_g, part_b, rows, d, stream);
+    }
+    const dim3 grid(ln_backward_partials(rows, d)), block(256);
+    const int nv = d / 4;
+    if (nv <= 64)
+        return launch_kernel(ln_backward_params_kernel<1, kLnbRowsPerWave>, grid, block, stream, dy, z, stats, gamma,
+                             dz, dzb, part_g, part_b, rows, d);
+    if (nv <= 128)
+        return launch_kernel(ln_backward_params_kernel<2, kLnbRowsPerWave>, grid, block, stream, dy, z, stats, gamma,
+                             dz, dzb, part_g, part_b, rows, d);
+    if (nv <= 192)
+        return launch_kernel(ln_backward_params_kernel<3, kLnbRowsPerWave>, grid, block, stream, dy, z, stats, gamma,
+                             dz, dzb, part_g, part_b, rows, d);
+    return launch_kernel(ln_backward_params_kernel<4, kLnbRowsPerWave>, grid, block, stream, dy, z, stats, gamma, dz,
+                         dzb, part_g, part_b, rows, d);
+}
 
 hipError_t launch_ln_param_partials(const float *dy, const float *z, const float *stats, float *part_g,
                                     float *part_b, int rows, int d, hipStream_t stream) {

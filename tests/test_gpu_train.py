@@ -90,6 +90,25 @@ def test_one_step_matches_oracle(causal, B, S):
         assert tr.steps() == 1
 
 
+@pytest.mark.parametrize("d", [512, 1024, 2048])
+def test_one_step_wide_models(d):
+    """One layer at widths that take the other LayerNorm-backward forms (d 512
+    and 1024: 2 and 4 column vectors per lane; d 2048: the two-kernel form)."""
+    shape = shape_of(dict(SMALL, n_layers=1, d_model=d, n_heads=d // 64, d_ff=2 * d))
+    print(f"train step d={d}", flush=True)
+    x, labels = make_batch(shape, 1, 64, 500 + d)
+    params = T.initial_params(shape)
+    loss_ref, grads_ref, _ = T.loss_and_grads(params, x, labels, shape)
+    with ie.Trainer(**instance_config(shape, 1, 64)) as tr:
+        tr.step(x, labels)
+        assert abs(tr.loss() - loss_ref) <= LOSS_REL * abs(loss_ref)
+        for layer, slot, name, ref in oracle_tensors(grads_ref, shape):
+            g = tr.export(layer, slot, ie.TRAIN_GRAD, ref.shape)
+            e = rel_l2(g, ref)
+            assert np.all(np.isfinite(g)), name
+            assert e <= GRAD_REL_L2, (name, e)
+
+
 def test_steps_deterministic_across_quotas():
     shape = shape_of(SMALL)
     x, labels = make_batch(shape, 2, 32, 77)
