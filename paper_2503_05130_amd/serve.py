@@ -5,7 +5,7 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
 
   python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 static proportional shared]
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--small]
-                                       [--mix inference|train]
+                                       [--mix inference|train|decode]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
 batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
@@ -218,6 +218,99 @@ class Trainee:
                                       if self.klc_log else None)}
 
 
+class Generator:
+    """A decoding instance co-located with inference (the decode phase beside
+    prefill-type work): requests of a P-token prompt per sequence (one prefill
+    batch) followed by G decode steps of one token per sequence, back to back,
+    over a KV cache.  Every prefill and every decode step is an iteration: a
+    pending quota is applied before it, and its KLC is its device time
+    relative to the fastest iteration of the same kind on the same quota.  It
+    always has work, so its queue length is 1."""
+
+    def __init__(self, idx, name, shape, batch, prompt, gen, request, limit, slo, seed):
+        self.idx, self.name, self.max_batch, self.rate = idx, name, batch, 0.0
+        self.prompt, self.gen = prompt, gen
+        self.request, self.limit, self.slo = request, limit, slo
+        self.inst = ie.Instance(device=0, max_batch=batch, max_seq=prompt + gen, seed=seed, kv_cache=1, **shape)
+        x = np.random.default_rng(7000 + idx).standard_normal((batch, prompt + gen, shape["d_model"]),
+                                                              dtype=np.float32)
+        self.x_prompt = torch.from_numpy(np.ascontiguousarray(x[:, :prompt])).to("cuda:0")
+        self.x_steps = [torch.from_numpy(np.ascontiguousarray(x[:, prompt + g])).to("cuda:0") for g in range(gen)]
+        self.pool = self.x_prompt
+        self.lock = threading.Lock()
+
+    def reset(self, horizon):
+        self.step_done, self.step_ms = [], []      # decode steps: completion time, wall time
+        self.prefill_ms = []
+        self.best_ms = {}
+        self.kernels = self.inst.kernels_launched()
+        self.ratios = []
+        self.pending = None
+        self.inst.set_quota(ie.device_info(0)[0], 0)
+        self.applied = (ie.device_info(0)[0], 0)
+        self.batches = 0
+        self.changes = 0
+        self.klc_log = []
+        self.plans = set()
+
+    def queue_len(self, now):
+        return 1
+
+    def warm(self):
+        self.inst.submit(self.x_prompt)
+        self.inst.wait()
+        self.inst.decode(self.x_steps[0], self.prompt)
+        self.inst.wait()
+
+    def _iteration(self, kind, launch):
+        with self.lock:
+            pend, self.pending = self.pending, None
+        if pend is not None and pend != self.applied:
+            self.inst.set_quota(*pend)
+            self.applied = pend
+            self.changes += 1
+            self.plans.add(pend)
+        t = time.perf_counter()
+        launch()
+        self.inst.wait()
+        wall = (time.perf_counter() - t) * 1e3
+        ms = self.inst.last_batch_ms()
+        self.batches += 1
+        key = (kind, self.applied[0])
+        best = min(self.best_ms.get(key, ms), ms)
+        self.best_ms[key] = best
+        with self.lock:
+            self.kernels = self.inst.kernels_launched()
+            self.ratios.append(ms / best)
+        return wall
+
+    def run(self, t0, horizon, stop):
+        while not stop.is_set():
+            if time.perf_counter() - t0 > horizon:
+                return
+            self.prefill_ms.append(self._iteration("prefill", lambda: self.inst.submit(self.x_prompt)))
+            for g in range(self.gen):
+                if stop.is_set() or time.perf_counter() - t0 > horizon:
+                    return
+                wall = self._iteration("decode", lambda: self.inst.decode(self.x_steps[g], self.prompt + g))
+                self.step_done.append(time.perf_counter() - t0)
+                self.step_ms.append(wall)
+
+    def stats(self, warmup, horizon):
+        done = np.array(self.step_done)
+        keep = (done >= warmup) & (done <= horizon)
+        tpot = np.array(self.step_ms)[keep] if len(done) else np.zeros(0)
+        n = int(keep.sum())
+        return {"name": self.name, "decoding": True, "steps": n,
+                "tokens_s": round(n * self.max_batch / max(horizon - warmup, 1e-9), 1),
+                "tpot_p50_ms": round(float(np.percentile(tpot, 50)), 3) if n else None,
+                "tpot_p99_ms": round(float(np.percentile(tpot, 99)), 3) if n else None,
+                "prefill_p50_ms": round(float(np.median(self.prefill_ms)), 3) if self.prefill_ms else None,
+                "quota_changes": self.changes, "distinct_placements": len(self.plans),
+                "klc_ratio_p50_p90": ([round(float(np.percentile(self.klc_log, q)), 3) for q in (50, 90)]
+                                      if self.klc_log else None)}
+
+
 GRANULE = 32   # quota granularity of the dynamic policies: 4 CUs per XCD, few distinct masks
 
 
@@ -278,7 +371,7 @@ def control_loop(policy, served, t0, horizon, period, stop, history):
 def run_policy(policy, served, horizon, warmup, period):
     for s in served:
         s.reset(horizon)
-        if isinstance(s, Trainee):
+        if isinstance(s, (Trainee, Generator)):
             s.warm()
         else:
             s.inst.submit(s.pool[:1])          # warm the instance and its full-device stream
@@ -297,7 +390,8 @@ def run_policy(policy, served, horizon, warmup, period):
     qs = np.array([h[1] for h in history]) if history else np.zeros((0, len(served)))
     states = [h[2] for h in history]
     return {"policy": policy, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
-            "instances": [s.stats(warmup, horizon) if isinstance(s, Trainee) else s.stats(warmup) for s in served],
+            "instances": [s.stats(warmup, horizon) if isinstance(s, (Trainee, Generator)) else s.stats(warmup)
+                          for s in served],
             "mean_quota": [round(float(v), 1) for v in qs.mean(0)] if len(qs) else None,
             "periods": len(history),
             "state_counts": {str(k): states.count(k) for k in sorted(set(states))}}
@@ -351,6 +445,55 @@ def run_train_mix(policies, horizon, warmup, period, small=False):
     return out, summary
 
 
+def decode_mix(small: bool = False):
+    """Decode beside prefill-type work: one BERT-base-shaped inference instance
+    (batches of up to 4, 200 requests/s, latency-sensitive) and one d = 2048
+    decoder generating 64 tokens after a 512-token prompt for 2 sequences at a
+    time, back to back (latency-sensitive: its time per output token)."""
+    if small:
+        inf = Served(0, "bert_inf", SMALL, 64, 4, 200.0, 0.25, 0.5, True, 51)
+        gen = Generator(1, "decoder_gen", dict(SMALL, pre_ln=1, causal=1), 2, 64, 8, 0.5, 0.75, True, 56)
+    else:
+        inf = Served(0, "bert_inf", BERT, 128, 4, 200.0, 0.25, 0.5, True, 51)
+        gen = Generator(1, "decoder_gen", DECODER, 2, 512, 64, 0.5, 0.75, True, 56)
+    return [inf, gen]
+
+
+def run_decode_mix(policies, horizon, warmup, period, small=False):
+    """Each policy with both instances, then each alone on the whole GPU."""
+    served = decode_mix(small)
+    out = []
+    try:
+        for pol in policies:
+            name, _, per = pol.partition("@")
+            res = run_policy(name, served, horizon, warmup, (float(per) if per else period) / 1e3)
+            out.append(res)
+            print(json.dumps(res), flush=True)
+        for one in served:
+            res = run_policy("shared", [one], horizon, warmup, period / 1e3)
+            res["policy"] = f"exclusive:{one.name}"
+            out.append(res)
+            print(json.dumps(res), flush=True)
+    finally:
+        for s in served:
+            s.inst.close()
+    excl = {r["instances"][0]["name"]: r["instances"][0] for r in out if r["policy"].startswith("exclusive")}
+    summary = {}
+    for r in out:
+        if r["policy"].startswith("exclusive"):
+            continue
+        inf, gen = r["instances"]
+        e_inf, e_gen = excl["bert_inf"], excl["decoder_gen"]
+        summary[r["policy"]] = {
+            "inference_p50_vs_exclusive": round(inf["p50_ms"] / e_inf["p50_ms"], 3) if inf["p50_ms"] else None,
+            "inference_p99_vs_exclusive": round(inf["p99_ms"] / e_inf["p99_ms"], 3) if inf["p99_ms"] else None,
+            "tpot_p50_vs_exclusive": round(gen["tpot_p50_ms"] / e_gen["tpot_p50_ms"], 3) if gen["tpot_p50_ms"] else None,
+            "tpot_p99_vs_exclusive": round(gen["tpot_p99_ms"] / e_gen["tpot_p99_ms"], 3) if gen["tpot_p99_ms"] else None,
+            "decode_tokens_vs_exclusive": round(gen["tokens_s"] / e_gen["tokens_s"], 3) if e_gen["tokens_s"] else None}
+    print(json.dumps({"decode_inf_summary": summary}), flush=True)
+    return out, summary
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--policy", nargs="+", default=["shared", "static", "proportional", "alg2"])
@@ -358,11 +501,15 @@ def main() -> int:
     ap.add_argument("--warmup", type=float, default=2.0)
     ap.add_argument("--period-ms", type=float, default=20.0)
     ap.add_argument("--small", action="store_true", help="small models (quick functional run)")
-    ap.add_argument("--mix", choices=["inference", "train"], default="inference",
-                    help="inference: the four-instance serving mix; train: inference beside a training instance")
+    ap.add_argument("--mix", choices=["inference", "train", "decode"], default="inference",
+                    help="inference: the four-instance serving mix; train: inference beside a training instance; "
+                         "decode: inference beside a token-by-token decoder")
     args = ap.parse_args()
     if args.mix == "train":
         run_train_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small)
+        return 0
+    if args.mix == "decode":
+        run_decode_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small)
         return 0
     t = time.perf_counter()
     served = build_mix(default_mix(args.small))

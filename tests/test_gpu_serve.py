@@ -48,3 +48,21 @@ def test_training_beside_inference():
     for pol in ("static", "alg2"):
         v = summary[pol]
         assert v["inference_p50_vs_exclusive"] > 0 and v["training_throughput_vs_exclusive"] > 0
+
+
+def test_decode_beside_inference():
+    """The decode mix (small models): the inference instance serves every
+    request and the decoder completes decode steps under each policy, and both
+    also alone."""
+    out, summary = serve.run_decode_mix(["static", "alg2"], horizon=1.5, warmup=0.2, period=10.0, small=True)
+    names = [r["policy"] for r in out]
+    assert names == ["static", "alg2", "exclusive:bert_inf", "exclusive:decoder_gen"]
+    for r in out:
+        for st in r["instances"]:
+            if st.get("decoding"):
+                assert st["steps"] > 0 and st["tokens_s"] > 0 and st["tpot_p99_ms"] >= st["tpot_p50_ms"] > 0
+            else:
+                assert st["dropped"] == 0 and st["requests"] > 0
+    for pol in ("static", "alg2"):
+        v = summary[pol]
+        assert v["inference_p50_vs_exclusive"] > 0 and v["tpot_p50_vs_exclusive"] > 0
