@@ -166,7 +166,8 @@ hipError_t launch_ln_backward_params(const float *dy, const float *z, const floa
 hipError_t launch_colsum(const void *src, bool src_bf16, float *dst, int rows, int n, int rows_per_part,
                          hipStream_t stream);
 // Up to kMaxColsumJobs whole-column sums of fp32 [rows, n] matrices in one launch:
-// dst[f] = sum of src[r][f] over all rows, the order of launch_colsum with rows_per_part = rows.
+// dst[f] = sum of src[r][f] over all rows, in a fixed order (8 interleaved row
+// lanes, each in row order, then the lanes in order).
 struct ColsumJob {
     const float *src;
     float *dst;

@@ -319,8 +319,12 @@ __global__ __launch_bounds__(256) void colsum_kernel(const T *__restrict__ src, 
     colsum_block(src, dst, rows, n, rb, blockIdx.x, blockIdx.y, red);
 }
 
-// Several whole-column sums in one launch (one row block per job):
-// workgroup b takes column block b - first[j] of job j.
+// Several whole-column sums in one launch (the last stage of a layer's sums:
+// a few hundred partial rows each).  Workgroup b takes 32 columns of job j
+// (first[j] <= b < first[j + 1]); thread (column c, lane g of 8) adds rows g,
+// g + 8, ... in order, then lane 0 adds the 8 lanes' sums in order.
+constexpr int kFinCols = 32, kFinLanes = 8;
+
 struct ColsumBatch {
     ColsumJob job[kMaxColsumJobs];
     int32_t first[kMaxColsumJobs + 1];
@@ -328,11 +332,26 @@ struct ColsumBatch {
 };
 
 __global__ __launch_bounds__(256) void colsum_jobs_kernel(ColsumBatch b) {
-    __shared__ float red[kColLanes][64];
+    __shared__ float red[kFinLanes][kFinCols];
     int j = 0;
     while (j + 1 < b.n && (int)blockIdx.x >= b.first[j + 1]) ++j;
-    colsum_block(b.job[j].src, b.job[j].dst, b.job[j].rows, b.job[j].n, b.job[j].rows, (int)blockIdx.x - b.first[j],
-                 0, red);
+    const float *__restrict__ src = b.job[j].src;
+    const int rows = b.job[j].rows, n = b.job[j].n;
+    const int c = threadIdx.x % kFinCols, g = threadIdx.x / kFinCols;
+    const int f = ((int)blockIdx.x - b.first[j]) * kFinCols + c;
+    float sum = 0.f;
+    if (f < n) {
+#pragma unroll 4
+        for (int r = g; r < rows; r += kFinLanes) sum += src[(size_t)r * n + f];
+    }
+    red[g][c] = sum;
+    __syncthreads();
+    if (g == 0 && f < n) {
+        float t = red[0][c];
+#pragma unroll
+        for (int k = 1; k < kFinLanes; ++k) t += red[k][c];
+        b.job[j].dst[f] = t;
+    }
 }
 
 // ------------------------------------------------------------------ head + loss
@@ -754,10 +773,10 @@ hipError_t launch_colsums(const ColsumJob *jobs, int n_jobs, hipStream_t stream)
         if (jobs[j].rows <= 0 || jobs[j].n <= 0) return hipErrorInvalidValue;
         b.job[j] = jobs[j];
         b.first[j] = blocks;
-        blocks += (jobs[j].n + 63) / 64;
+        blocks += (jobs[j].n + kFinCols - 1) / kFinCols;
     }
     b.first[n_jobs] = blocks;
-    return launch_kernel(colsum_jobs_kernel, dim3(blocks), dim3(256), stream, b);
+    return launch_kernel(colsum_jobs_kernel, dim3(blocks), dim3(kFinCols * kFinLanes), stream, b);
 }
 
 hipError_t launch_gelu(const bf16_t *v, bf16_t *u, size_t n, hipStream_t stream) {
