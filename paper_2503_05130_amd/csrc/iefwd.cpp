@@ -748,10 +748,11 @@ void train_run(iefwd_instance *I, const float *x) {
     auto bwd = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD, what, f); };
     // Column sums of [T, n] matrices into dst [n], two fixed-order stages: the
     // partials of row blocks when the source is ready (into t.colpart at column
-    // offset `col`, T / 64 rows per region), the last stages of a layer's sums
-    // together in one launch.  Bias gradients take their partials from the
-    // transpose of the output gradient (64-row blocks), the others from
-    // 256-row chunks.
+    // offset `col`, colpart_rows(T, d) rows per region), the last stages of a
+    // layer's sums together in one launch.  Bias gradients take their partials
+    // from the transpose of the output gradient (64-row blocks), LayerNorm
+    // parameters from the LayerNorm backward (16-row blocks for d <= 1024), the
+    // head's sums from 256-row chunks.
     const int parts = colsum_partials(T), blocks64 = T / 64, ln_parts = ln_backward_partials(T, d);
     std::vector<ColsumJob> finals;
     auto region = [&](int col) { return t.colpart + (size_t)colpart_rows(T, d) * col; };
