@@ -28,7 +28,7 @@
 // -- never on the tile shape, the ring depth, the grid, the CU mask or the
 // other rows in the batch.  No atomics, no cross-workgroup split-K.
 #include "gelu.h"
-#include "kernels.h"
+#include "gemm.h"
 
 #include <algorithm>
 

@@ -3,111 +3,10 @@
 // checks live in the callers (executor and test entry points).
 #pragma once
 
-#include <hip/hip_ext.h>
-#include <hip/hip_runtime.h>
-
-#include <cstddef>
-#include <cstdint>
+#include "gemm.h"
+#include "launch.h"
 
 namespace iefwd {
-
-// Kernel-only timing: when a pair of events is armed on this host thread, the
-// next kernel launch records its own dispatch start and end into them (the
-// timestamps of the kernel itself, not of markers around it) and disarms.
-struct LaunchEvents {
-    hipEvent_t start = nullptr, stop = nullptr;
-};
-// Events armed by the caller for the next launches on this thread: the first
-// kernel records `start` as it begins, and every kernel records `stop` as it
-// ends, so for an operation of several kernels the pair spans all of them.
-LaunchEvents &armed_launch_events();
-// Kernels launched by this thread so far.
-uint64_t &launch_count();
-
-template <typename F, typename... Args>
-hipError_t launch_kernel(F kernel, dim3 grid, dim3 block, hipStream_t stream, Args... args) {
-    LaunchEvents &ev = armed_launch_events();
-    if (ev.stop) {
-        hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, ev.start, ev.stop, 0, args...);
-        ev.start = nullptr;
-    } else {
-        hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
-    }
-    ++launch_count();
-    return hipGetLastError();
-}
-
-using bf16_t = uint16_t;   // bf16 storage: the upper half of an fp32 bit pattern
-
-enum class Epi : int {
-    BiasBf16 = 0,       // out bf16 = acc + b
-    BiasGeluBf16 = 1,   // out bf16 = GELU(acc + b)
-    BiasResidF32 = 2,   // out f32  = resid + acc + b
-    Qkv = 3,            // acc + b scattered to Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad]
-    BiasLnResidF32 = 4, // out f32  = LN(z) + acc + b, LN(z) rebuilt from z and its row stats
-    F32 = 5,            // out f32  = acc                      (weight gradients)
-    GeluBwdBf16 = 6,    // out bf16 = acc * GELU'(aux), aux bf16 [M, N] (the GELU's input)
-};
-
-// Row statistics a LayerNorm kernel leaves for a later consumer: the residual
-// LN(z)[t, f] = gamma[f] * ((z[t, f] - mean[t]) * rstd[t]) + beta[f] is rebuilt
-// from them with exactly the LayerNorm kernel's arithmetic.
-struct LnResid {
-    const float *z;       // [M, N] fp32 pre-normalisation rows
-    const float *stats;   // [M, 2] fp32 {mean, rstd}
-    const float *gamma;   // [N]
-    const float *beta;    // [N]
-};
-
-// Destination of the QKV epilogue.
-// Where the QKV epilogue puts each token's Q, K and V.  Token t of a launch is
-// position pos0 + t % seq of sequence t / seq.  Q goes to the per-launch
-// buffer [B, H, seq, dh]; K and V^T go to buffers that may be a KV cache:
-// K [B, H, k_rows, dh] at row pos0 + t % seq, V^T [B, H, dh, vt_stride] at
-// column pos0 + t % seq.  A prefill without a cache has pos0 = 0,
-// k_rows = seq, vt_stride = S rounded up to a multiple of 64.
-struct QkvDst {
-    bf16_t *q, *k, *vt;
-    int seq;        // tokens per sequence in this launch
-    int pos0;       // position of the launch's first token of each sequence
-    int k_rows;     // rows of K per (batch, head)
-    int vt_stride;  // row stride of V^T (a multiple of 64)
-    int n_heads;
-    int head_dim;
-    int d_model;
-};
-
-// S rounded up to the attention kernel's 64-key chunk (the row stride of V^T).
-inline int attn_seq_pad(int seq) { return (seq + 63) / 64 * 64; }
-
-// out = epi(A W^T + b).  A bf16 [M,K], W bf16 [N,K], bias bf16 [N].
-// Requires N % 64 == 0, K % 64 == 0, M >= 1.
-hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
-                       const float *resid, void *out, int M, int N, int K,
-                       const QkvDst *qkv, hipStream_t stream, const LnResid *ln = nullptr,
-                       const bf16_t *aux = nullptr);
-
-// Activations given as LayerNorm(z): z fp32 [M, K] rows, gamma / beta fp32 [K].
-struct LnIn {
-    const float *z;
-    const float *gamma;
-    const float *beta;
-    float eps;
-};
-
-// The same product for M <= 16 rows (a decode step), bound by reading W once:
-// N % 16 == 0, K % 32 == 0; every epilogue but BiasLnResidF32.  Its K
-// summation order differs from launch_gemm's (the two agree within rounding).
-// With ln_in the activations are LayerNorm(z), normalised in the kernel (then
-// `a` is unused); that needs skinny_ln_fits(M, K).
-hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
-                              const float *resid, void *out, int M, int N, int K, const QkvDst *qkv,
-                              hipStream_t stream, const LnIn *ln_in = nullptr);
-bool skinny_ln_fits(int M, int K);
-// K-groups per MFMA the skinny product uses for this shape (1, 2 or 4), with
-// or without the LayerNorm prologue; its summation order depends on K and
-// this number.
-int skinny_groups(int M, int N, int K, bool ln);
 
 // ctx bf16 [B, S, H*dh] from Q, K [B,H,S,dh] and V^T [B,H,dh,S_pad].
 // k_rows: rows of K per (batch, head) (0: seq); vt_stride: row stride of V^T
