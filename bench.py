@@ -502,6 +502,8 @@ def main() -> int:
     inst.close()
     if not args.no_colocated:
         result["colocated"] = colocated(ie, W, shape, cfg, [(64, 192), (128, 128), (192, 64)])
+        # the same pairs at the headline batch: two batch-32 instances against one
+        result["colocated_b32"] = colocated(ie, W, shape, cfg, [(64, 192), (128, 128), (192, 64)], batch=B)
     if args.decode:
         result["decode"] = decode_leg(ie, W)
     if not args.no_train:
