@@ -320,6 +320,38 @@ def gemm_reference(ie, inst, x, B, S, shape, reps=20):
     return out
 
 
+def hbm_kernels(ie, inst, x, B, S, shape, reps=20):
+    """Achieved HBM bandwidth of the forward's memory-bound kernels: algorithmic
+    bytes over device time per launch (HIP events around each launch, on the
+    instance's stream).  LayerNorm class of a post-LN forward: the input cast
+    (4 B in, 2 B out per element), 2L - 1 LayerNorms (4 B in, 2 B out per
+    element, 8 B of statistics per row) and the last LayerNorm fused with the
+    head (4 B in per element, the logits out).  Attention: Q, K and V^T read
+    once (2 B each per element of the [T, d] activations), the context written
+    once (2 B)."""
+    T, d, L = B * S, shape["d_model"], shape["n_layers"]
+    if shape["pre_ln"]:
+        return None
+    ln_bytes = T * d * 6 + (2 * L - 1) * (T * d * 6 + T * 8) + T * d * 4 + T * shape["n_out"] * 4
+    attn_bytes = L * (3 * T * d * 2 + T * d * 2)
+    kinds = {"layernorm": (ie.K_LN, ln_bytes, 2 * L + 1), "attention": (ie.K_ATTN, attn_bytes, L)}
+    for k, _, _ in kinds.values():
+        inst.time_kernel(k, True)
+    for _ in range(reps):
+        inst.submit(x)
+        inst.wait()
+    out = {}
+    for nm, (k, nbytes, per_fwd) in kinds.items():
+        ms, n = inst.kernel_time(k)
+        inst.time_kernel(k, False)
+        fwd = n / per_fwd
+        gbs = nbytes * fwd / (ms * 1e-3) / 1e9
+        out[nm] = {"launches": n, "avg_us": round(ms * 1e3 / max(n, 1), 2),
+                   "bytes_per_launch": round(nbytes / per_fwd), "achieved_GBps": round(gbs, 1),
+                   "frac_of_hbm_peak": round(gbs / 8000.0, 3)}
+    return out
+
+
 def train_flops(L, d, F, H, S, n_out, causal=False):
     """Algorithmic FLOPs of one training step per sequence: the forward, and a
     backward of twice the forward's products (input and weight gradients of
@@ -499,6 +531,7 @@ def main() -> int:
         result["quota_sweep"] = quota_sweep(ie, W, inst, x, B, S, shape)
     if not args.no_gemm_reference:
         result["gemm_reference"] = gemm_reference(ie, inst, x, B, S, shape)
+    result["hbm_kernels"] = hbm_kernels(ie, inst, x, B, S, shape)
     inst.close()
     if not args.no_colocated:
         result["colocated"] = colocated(ie, W, shape, cfg, [(64, 192), (128, 128), (192, 64)])
