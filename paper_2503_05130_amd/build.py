@@ -63,7 +63,7 @@ def _check_stubs(lib: str) -> None:
 
     clang's host pass can drop a kernel's stub without a diagnostic when the
     kernel body holds a device-only construct it cannot check on the host; the
-    library would then fail to load on the GPU machine."""
+    library would then fail to load at run time."""
     res = subprocess.run(["nm", "-D", "--undefined-only", lib], capture_output=True, text=True, check=True)
     missing = [line.split()[-1] for line in res.stdout.splitlines() if "__device_stub" in line]
     if missing:
