@@ -10,6 +10,7 @@ import workloads
 from oracle import forward as F
 from oracle import init_spec as I
 from oracle import scalar as SC
+from tests.golden_data import rows
 
 
 # ----------------------------------------------------------------------------- matmul
@@ -68,9 +69,8 @@ def test_layernorm_invariants():
 
 # ----------------------------------------------------------------------------- GELU
 def test_gelu_textbook_values_and_identities():
-    # GELU(u) = u * Phi(u).  Phi(1) = 0.8413447460685429, Phi(2) = 0.9772498680518208,
-    # Phi(-0.5) = 0.3085375387259869 (standard normal table, Abramowitz & Stegun 26.2)
-    for u, phi in ((1.0, 0.8413447460685429), (2.0, 0.9772498680518208), (-0.5, 0.3085375387259869)):
+    # GELU(u) = u * Phi(u), Phi from the standard normal table (tests/golden/normal_cdf_table.txt)
+    for u, phi in ((float(x), float(p)) for x, p in rows("normal_cdf_table.txt")):
         assert F.gelu(np.array(u)) == pytest.approx(u * phi, abs=1e-15)
     u = np.linspace(-6, 6, 241)
     assert np.allclose(F.gelu(u), u * ndtr(u), rtol=0, atol=1e-15)      # library normal CDF

@@ -5,6 +5,7 @@ import math
 import pytest
 
 from paper_2503_05130_amd import profiler as P
+from tests.golden_data import rows
 
 
 def test_smr_to_cus():
@@ -14,13 +15,16 @@ def test_smr_to_cus():
 
 
 def test_paper_example_path():
-    # the paper's GPT2-large example (100 ms SLO): <1,10>, <2,20>, <4,30> meet
-    # the SLO, <8,40> violates it and the search stops there
+    # the paper's GPT2-large example (100 ms SLO, tests/golden/hgss_printed_path.txt):
+    # <1,10>, <2,20>, <4,30> meet the SLO, <8,40> violates it and the search stops there
+    printed = [(int(b), float(s), m == "1") for b, s, m in rows("hgss_printed_path.txt")]
+
     def measure(ibs, smr):
         return 60.0 if ibs >= 8 else 20.0 * ibs / (smr / 10.0)
     r = P.hgss(measure, slo_ms=100.0)
-    assert r["path"] == [(1, 10.0), (2, 20.0), (4, 30.0), (8, 40.0)]
-    assert r["trials"] == 4
+    assert r["path"] == [(b, s) for b, s, _ in printed]
+    assert [measure(b, s) <= 100.0 / 2 for b, s in r["path"]] == [m for _, _, m in printed]   # t_exec = SLO / 2
+    assert r["trials"] == len(printed)
     # TE = IBS / (t * SMR): 1/(0.02*10) = 5, 2/(0.02*20) = 5, 4/(0.02667*30) = 5  -> ties: first max
     tes = [P.throughput_efficacy(b, measure(b, s), s) for b, s in r["path"][:3]]
     assert tes == pytest.approx([5.0, 5.0, 5.0])
@@ -71,6 +75,23 @@ def test_walks_against_traversal():
     assert (f["ibs"], f["request_smr"]) == (t["ibs"], t["request_smr"])
     assert d["best"]["te"] < t["best"]["te"]
 
+
+
+def test_printed_traversal_grid_and_trial_counts():
+    # Table "Inference function profiling comparison" (tests/golden/profiling_trials_table.txt):
+    # the traversal costs 60 trials per model, HGSS 6 to 9.  The grid that gives 60 is IBS
+    # 1 .. 32 (doubling) times SMR 10 .. 100 (steps of 10); on it the diagonal walk stays
+    # within the printed HGSS counts for surfaces from light to heavy.
+    table = {r[0]: [int(v) for v in r[1:]] for r in rows("profiling_trials_table.txt")}
+    ibs_list = [1 << k for k in range(6)]
+    smr_list = [10.0 * k for k in range(1, 11)]
+    for scale in (0.5, 1.0, 4.0, 16.0):
+        def m(b, s, sc=scale):
+            return sc * convex(b, s)
+        t = P.traversal(m, 100.0, ibs_list, smr_list)
+        d = P.hgss(m, 100.0, max_ibs=32)
+        assert t["trials"] == table["traversal"][0] == 60
+        assert d["trials"] <= max(table["hgss"]), (scale, d["trials"])
 
 def test_frontier_visits_smallest_feasible_smr_per_ibs():
     f = P.hgss(convex, 100.0, max_ibs=256, walk="frontier")
