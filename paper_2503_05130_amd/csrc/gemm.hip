@@ -480,8 +480,9 @@ using CfgF = Cfg<64, 64, 2, 2, 3>;     // 4 waves, 32 x 32
 using SplitC = Cfg<64, 96, 2, 2, 2>;   // split order: two 4-wave groups
 using SplitE = Cfg<64, 128, 2, 2, 2>;
 using SplitD = Cfg<128, 128, 2, 2, 2>;
+using SplitG = Cfg<32, 64, 1, 2, 2>;   // two 2-wave groups, 32 x 32 per wave: small products
 
-enum class Tile { A, D, B, C, E, F, SplitC, SplitE, SplitD };
+enum class Tile { A, D, B, C, E, F, SplitC, SplitE, SplitD, SplitG };
 
 // K summation order from the weight shape (N, K) only: K >= 2048 uses the
 // split (even/odd) order, shorter K the sequential order.  So a given weight
@@ -497,6 +498,10 @@ long tiles_of(int M, int N, int bm, int bn) { return (long)((M + bm - 1) / bm) *
 // the QKV scatter, so that no tile straddles the Q / K / V boundaries).
 Tile choose_tile(int M, int N, int K, int align) {
     if (split_k_order(N, K)) {
+        // a product too small to give three quarters of the CUs a 64 x 96 or 64 x 128
+        // tile takes 32 x 64 tiles (the same even / odd K order)
+        const bool small = (align % 96 == 0 ? tiles_of(M, N, 64, 96) : tiles_of(M, N, 64, 128)) < 192;
+        if (small && align % 64 == 0) return Tile::SplitG;
         if (align % 96 == 0) return Tile::SplitC;
         if (align % 128 == 0 && tiles_of(M, N, 64, 128) < 512) return Tile::SplitE;
         if (align % 128 == 0) return Tile::SplitD;
@@ -796,6 +801,7 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
     case Tile::SplitC: return launch_tile<SplitC, true>(epi, p, stream);
     case Tile::SplitE: return launch_tile<SplitE, true>(epi, p, stream);
     case Tile::SplitD: return launch_tile<SplitD, true>(epi, p, stream);
+    case Tile::SplitG: return launch_tile<SplitG, true>(epi, p, stream);
     }
     return hipErrorInvalidValue;
 }

@@ -46,7 +46,10 @@ def gemm_bound(a64, w64, K):
     (2000, 1024, 512),   # 64 x 128 tiles, ragged M
     (300, 1024, 1024),   # 64 x 64 tiles, ragged M
     (256, 768, 3072),    # long K: split (even/odd) K order, 64 x 96
-    (130, 512, 2048),    # split order, 64 x 128, ragged M
+    (130, 512, 2048),    # split order, small product: 32 x 64, ragged M
+    (768, 768, 4096),    # split order, small product: 32 x 64 (an out-projection weight gradient)
+    (1000, 1024, 2048),  # split order, small product: 32 x 64, ragged M
+    (2000, 768, 2048),   # split order, 64 x 96, ragged M (just past the small-product limit)
     (2048, 2048, 2048),  # split order, 128 x 128
     (4096, 768, 3072),   # split order, 64 x 96 (the BERT-base FFN-down product)
     (4133, 768, 2048),   # split order, 64 x 96, ragged M
@@ -84,8 +87,10 @@ def test_gemm_epilogues(M, N, K, epi):
 @pytest.mark.parametrize("M,N,K", [
     (512, 768, 768),      # 64 x 64 tiles throughout
     (4096, 3072, 768),    # 128 x 192 tiles (8 waves) for the full batch, 64 x 64 / 64 x 96 for the slices
-    (4096, 1024, 4096),   # split K order: 128 x 128 for the full batch, 64 x 128 for the slices
-    (4096, 768, 3072),    # split K order, 64 x 96 tiles (the BERT-base FFN-down product)
+    (4096, 1024, 4096),   # split K order: 128 x 128 for the full batch, 32 x 64 for the slices
+    (4096, 768, 3072),    # split K order: 64 x 96 for the full batch (the BERT-base FFN-down
+                          # product), 32 x 64 for the slices
+    (2048, 768, 4096),    # split K order: 64 x 96 for the full batch, 32 x 64 for the slices
 ])
 def test_gemm_batch_invariance(M, N, K):
     # rows computed in a large batch equal the same rows computed alone, bit for
