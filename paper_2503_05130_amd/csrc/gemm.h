@@ -48,11 +48,13 @@ struct QkvDst {
 inline int attn_seq_pad(int seq) { return (seq + 63) / 64 * 64; }
 
 // out = epi(A W^T + b).  A bf16 [M,K], W bf16 [N,K], bias bf16 [N].
-// Requires N % 64 == 0, K % 64 == 0, M >= 1.
+// Requires N % 64 == 0, K % 64 == 0, M >= 1.  n_cu: the CUs the stream's mask
+// enables; it may change the tile shape, never the result (every tile shape
+// of a K order adds the same terms in the same order).
 hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
                        const float *resid, void *out, int M, int N, int K,
                        const QkvDst *qkv, hipStream_t stream, const LnResid *ln = nullptr,
-                       const bf16_t *aux = nullptr);
+                       const bf16_t *aux = nullptr, int n_cu = 256);
 
 // Activations given as LayerNorm(z): z fp32 [M, K] rows, gamma / beta fp32 [K].
 struct LnIn {

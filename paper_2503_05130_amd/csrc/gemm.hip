@@ -492,15 +492,18 @@ bool split_k_order(int /*N*/, int K) { return K >= 2048; }
 
 long tiles_of(int M, int N, int bm, int bn) { return (long)((M + bm - 1) / bm) * (N / bn); }
 
-// Tile shape from (M, N, K) only -- never the current CU quota.  The largest
-// tile that still gives at least one workgroup per CU (256 tiles); if none
-// does, the one with the most tiles.  Tile widths divide `align` (d_model for
-// the QKV scatter, so that no tile straddles the Q / K / V boundaries).
-Tile choose_tile(int M, int N, int K, int align) {
+// Tile shape.  The K order comes from (N, K) alone (split_k_order) and every
+// tile shape of an order adds the same terms in the same sequence, so the
+// shape may follow the launch (M, and the n_cu CUs the stream may use)
+// without changing a bit.  Sequential order: the largest tile that still
+// gives at least one workgroup per CU (256 tiles); if none does, the one with
+// the most tiles.  Split order: 64 x 96 (or 64 x 128 / 128 x 128) tiles, or
+// 32 x 64 ones when the product is too small to give three quarters of the
+// CUs a larger tile.  Tile widths divide `align` (d_model for the QKV
+// scatter, so that no tile straddles the Q / K / V boundaries).
+Tile choose_tile(int M, int N, int K, int align, int n_cu) {
     if (split_k_order(N, K)) {
-        // a product too small to give three quarters of the CUs a 64 x 96 or 64 x 128
-        // tile takes 32 x 64 tiles (the same even / odd K order)
-        const bool small = (align % 96 == 0 ? tiles_of(M, N, 64, 96) : tiles_of(M, N, 64, 128)) < 192;
+        const bool small = (align % 96 == 0 ? tiles_of(M, N, 64, 96) : tiles_of(M, N, 64, 128)) < 3L * n_cu / 4;
         if (small && align % 64 == 0) return Tile::SplitG;
         if (align % 96 == 0) return Tile::SplitC;
         if (align % 128 == 0 && tiles_of(M, N, 64, 128) < 512) return Tile::SplitE;
@@ -781,7 +784,7 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
 
 hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
                        const float *resid, void *out, int M, int N, int K, const QkvDst *qkv,
-                       hipStream_t stream, const LnResid *ln, const bf16_t *aux) {
+                       hipStream_t stream, const LnResid *ln, const bf16_t *aux, int n_cu) {
     if (M <= 0) return hipSuccess;
     if (epi == Epi::GeluBwdBf16 && !aux) return hipErrorInvalidValue;
     GemmParams p{};
@@ -791,7 +794,7 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
     if (ln) p.ln = *ln;
     // N is a multiple of 64 (checked by the callers); d_model a multiple of 128
     const int align = epi == Epi::Qkv ? p.qkv.d_model : N;
-    switch (choose_tile(M, N, K, align)) {
+    switch (choose_tile(M, N, K, align, n_cu)) {
     case Tile::A: return launch_tile<CfgA, false>(epi, p, stream);
     case Tile::D: return launch_tile<CfgD, false>(epi, p, stream);
     case Tile::B: return launch_tile<CfgB, false>(epi, p, stream);

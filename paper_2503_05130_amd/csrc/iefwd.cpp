@@ -322,10 +322,11 @@ void run_forward(iefwd_instance *I, const float *x, int decode_pos = -1) {
     // block's LayerNorm fused into the product that consumes it)
     const bool skinny = decode && T <= 16;
     const bool fuse_ln = skinny && c.pre_ln && skinny_ln_fits(T, d);
+    const int n_cu = (int)mask_popcount(I->mask, I->dev.n_cu);   // the quota this batch runs on
     auto gemm = [&](Epi epi, const bf16_t *a, const bf16_t *wt, const bf16_t *bias, const float *resid, void *out,
                     int N, int K, const QkvDst *qkv, const LnResid *ln_resid, const LnIn *ln_in = nullptr) {
         if (skinny && !ln_resid) return launch_gemm_skinny(epi, a, wt, bias, resid, out, T, N, K, qkv, s, ln_in);
-        return launch_gemm(epi, a, wt, bias, resid, out, T, N, K, qkv, s, ln_resid);
+        return launch_gemm(epi, a, wt, bias, resid, out, T, N, K, qkv, s, ln_resid, nullptr, n_cu);
     };
     auto attention_block = [&](int l, const bf16_t *y_bf16, const LayerWeights &w, const float *resid,
                                const LnResid *ln_resid, float *dst, const LnIn *ln_in = nullptr) {
@@ -743,6 +744,7 @@ void train_run(iefwd_instance *I, const float *x) {
     const float eps = c.ln_eps;
     const bool causal = c.causal != 0;
     hipStream_t s = I->stream;
+    const int n_cu = (int)mask_popcount(I->mask, I->dev.n_cu);   // the quota this step runs on
     auto fwd = [&](uint32_t kind, const char *what, auto &&f) { launch(I, kind, what, f); };
     auto bwd_gemm = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD_GEMM, what, f); };
     auto bwd = [&](const char *what, auto &&f) { launch(I, IEFWD_K_BWD, what, f); };
@@ -776,28 +778,35 @@ void train_run(iefwd_instance *I, const float *x) {
             fwd(IEFWD_K_LN, "cast", [&] { return launch_cast_bf16(x, sv.hb, (size_t)T * d, s); });
         const QkvDst qd{sv.q, sv.k, sv.vt, S, 0, S, spad, H, dh, d};
         fwd(IEFWD_K_QKV, "qkv gemm",
-            [&] { return launch_gemm(Epi::Qkv, sv.hb, w.wqkv, w.bqkv, nullptr, nullptr, T, 3 * d, d, &qd, s); });
+            [&] {
+                return launch_gemm(Epi::Qkv, sv.hb, w.wqkv, w.bqkv, nullptr, nullptr, T, 3 * d, d, &qd, s, nullptr,
+                                   nullptr, n_cu);
+            });
         fwd(IEFWD_K_ATTN, "attention",
             [&] { return launch_attention(sv.q, sv.k, sv.vt, sv.ctx, B, H, S, dh, causal, s, S, spad); });
         if (l == 0) {
             fwd(IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
-                return launch_gemm(Epi::BiasResidF32, sv.ctx, w.wo, w.bo, x, sv.z1, T, d, d, nullptr, s);
+                return launch_gemm(Epi::BiasResidF32, sv.ctx, w.wo, w.bo, x, sv.z1, T, d, d, nullptr, s,
+                                   nullptr, nullptr, n_cu);
             });
         } else {
             const LayerWeights &pw = I->layers[l - 1];
             const LnResid r{t.saved[l - 1].z2, t.saved[l - 1].st2, pw.g2, pw.be2};
             fwd(IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
-                return launch_gemm(Epi::BiasLnResidF32, sv.ctx, w.wo, w.bo, nullptr, sv.z1, T, d, d, nullptr, s, &r);
+                return launch_gemm(Epi::BiasLnResidF32, sv.ctx, w.wo, w.bo, nullptr, sv.z1, T, d, d, nullptr, s,
+                                   &r, nullptr, n_cu);
             });
         }
         fwd(IEFWD_K_LN, "layernorm",
             [&] { return launch_layernorm(sv.z1, w.g1, w.be1, nullptr, sv.h1b, T, d, eps, s, sv.st1); });
         fwd(IEFWD_K_FFN1, "ffn1 gemm",
-            [&] { return launch_gemm(Epi::BiasBf16, sv.h1b, w.w1, w.b1, nullptr, sv.v, T, F, d, nullptr, s); });
+            [&] { return launch_gemm(Epi::BiasBf16, sv.h1b, w.w1, w.b1, nullptr, sv.v, T, F, d, nullptr, s,
+                                     nullptr, nullptr, n_cu); });
         fwd(IEFWD_K_FFN1, "gelu", [&] { return launch_gelu(sv.v, sv.u, (size_t)T * F, s); });
         const LnResid r1{sv.z1, sv.st1, w.g1, w.be1};
         fwd(IEFWD_K_FFN2, "ffn2 gemm", [&] {
-            return launch_gemm(Epi::BiasLnResidF32, sv.u, w.w2, w.b2, nullptr, sv.z2, T, d, F, nullptr, s, &r1);
+            return launch_gemm(Epi::BiasLnResidF32, sv.u, w.w2, w.b2, nullptr, sv.z2, T, d, F, nullptr, s,
+                               &r1, nullptr, n_cu);
         });
         if (l + 1 < L)
             fwd(IEFWD_K_LN, "layernorm", [&] {
@@ -842,20 +851,23 @@ void train_run(iefwd_instance *I, const float *x) {
         transposes({{t.dzb, t.ta, T, d, region(c_b2)}, {sv.u, t.tb, T, F}});
         finals.push_back({region(c_b2), t.grad + o[9], blocks64, d});
         bwd_gemm("dW2 gemm", [&] {
-            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[8], d, F, T, nullptr, s);
+            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[8], d, F, T, nullptr, s,
+                               nullptr, nullptr, n_cu);
         });
         bwd_gemm("dv gemm", [&] {
             return launch_gemm(Epi::GeluBwdBf16, t.dzb, wt.w2, nullptr, nullptr, t.dvb, T, F, d, nullptr, s, nullptr,
-                               sv.v);
+                               sv.v, n_cu);
         });
         // FFN-up: dW1 = dv^T X1, db1, dX1 = dz2 + dv W1
         transposes({{t.dvb, t.ta, T, F, region(c_b1)}, {sv.h1b, t.tb, T, d}});
         finals.push_back({region(c_b1), t.grad + o[7], blocks64, F});
         bwd_gemm("dW1 gemm", [&] {
-            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[6], F, d, T, nullptr, s);
+            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[6], F, d, T, nullptr, s,
+                               nullptr, nullptr, n_cu);
         });
         bwd_gemm("dX1 gemm", [&] {
-            return launch_gemm(Epi::BiasResidF32, t.dvb, wt.w1, t.zero_bias, t.dz, t.dxb, T, d, F, nullptr, s);
+            return launch_gemm(Epi::BiasResidF32, t.dvb, wt.w1, t.zero_bias, t.dz, t.dxb, T, d, F, nullptr, s,
+                               nullptr, nullptr, n_cu);
         });
         // LN1: dz1
         ln_backward(t.dxb, sv.z1, sv.st1, w.g1, o[4], o[5], c_ln1);
@@ -863,10 +875,12 @@ void train_run(iefwd_instance *I, const float *x) {
         transposes({{t.dzb, t.ta, T, d, region(c_bo)}, {sv.ctx, t.tb, T, d}});
         finals.push_back({region(c_bo), t.grad + o[3], blocks64, d});
         bwd_gemm("dWo gemm", [&] {
-            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[2], d, d, T, nullptr, s);
+            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[2], d, d, T, nullptr, s,
+                               nullptr, nullptr, n_cu);
         });
         bwd_gemm("dctx gemm", [&] {
-            return launch_gemm(Epi::BiasBf16, t.dzb, wt.wo, t.zero_bias, nullptr, t.dctx, T, d, d, nullptr, s);
+            return launch_gemm(Epi::BiasBf16, t.dzb, wt.wo, t.zero_bias, nullptr, t.dctx, T, d, d, nullptr, s,
+                               nullptr, nullptr, n_cu);
         });
         // attention
         bwd("attention backward", [&] {
@@ -877,12 +891,13 @@ void train_run(iefwd_instance *I, const float *x) {
         transposes({{t.dqkv, t.ta, T, 3 * d, region(c_bqkv)}, {sv.hb, t.tb, T, d}});
         finals.push_back({region(c_bqkv), t.grad + o[1], blocks64, 3 * d});
         bwd_gemm("dWqkv gemm", [&] {
-            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[0], 3 * d, d, T, nullptr, s);
+            return launch_gemm(Epi::F32, t.ta, t.tb, nullptr, nullptr, t.grad + o[0], 3 * d, d, T, nullptr, s,
+                               nullptr, nullptr, n_cu);
         });
         if (l > 0)
             bwd_gemm("dX gemm", [&] {
                 return launch_gemm(Epi::BiasResidF32, t.dqkv, wt.wqkv, t.zero_bias, t.dz, t.dxa, T, d, 3 * d, nullptr,
-                                   s);
+                                   s, nullptr, nullptr, n_cu);
             });
         flush_finals();
     }
