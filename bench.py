@@ -40,7 +40,7 @@ WORKLOAD = "bert_base_l12_d768_s128"
 # HBM bytes per launch of the FFN-down kernel (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 KiB,
 # factors from a 256 MiB device copy in the same runs), valid only for the GEMM source
 # and build flags they were counted on; any other source reports null.
-FFN2_TRAFFIC = {"source_sha256_16": "a713fe81397ee0a7", "bytes": (36998.4 * 2.0 + 14079.4 * 1.0) * 1024}
+FFN2_TRAFFIC = {"source_sha256_16": "c90f012751a46252", "bytes": (37014.7 * 2.0 + 14028.3 * 1.0) * 1024}
 GEMM_SOURCES = ("paper_2503_05130_amd/csrc/gemm.hip", "paper_2503_05130_amd/csrc/gemm.h",
                 "paper_2503_05130_amd/csrc/launch.h", "paper_2503_05130_amd/csrc/gelu.h",
                 "paper_2503_05130_amd/build.py")

@@ -496,8 +496,8 @@ long tiles_of(int M, int N, int bm, int bn) { return (long)((M + bm - 1) / bm) *
 // tile shape of an order adds the same terms in the same sequence, so the
 // shape may follow the launch (M, and the n_cu CUs the stream may use)
 // without changing a bit.  Sequential order: the largest tile that still
-// gives at least one workgroup per CU (256 tiles); if none does, the one with
-// the most tiles.  Split order: 64 x 96 (or 64 x 128 / 128 x 128) tiles, or
+// gives min(256, 2 n_cu) tiles (one per CU of the device, two per CU of a
+// share up to 128 CUs); if none does, the one with the most tiles.  Split order: 64 x 96 (or 64 x 128 / 128 x 128) tiles, or
 // 32 x 64 ones when the product is too small to give three quarters of the
 // CUs a larger tile.  Tile widths divide `align` (d_model for the QKV
 // scatter, so that no tile straddles the Q / K / V boundaries).
@@ -515,10 +515,11 @@ Tile choose_tile(int M, int N, int K, int align, int n_cu) {
         {Tile::C, 64, 96}, {Tile::E, 64, 128}, {Tile::F, 64, 64}};
     Tile best = Tile::F;
     long best_n = 0;
+    const long enough = std::min(256, 2 * n_cu);   // two tiles per CU on a share of <= 128 CUs
     for (const Cand &c : cands) {
         if (align % c.bn) continue;
         const long n = tiles_of(M, N, c.bm, c.bn);
-        if (n >= 256) return c.t;
+        if (n >= enough) return c.t;
         if (n > best_n) { best = c.t; best_n = n; }
     }
     return best;
