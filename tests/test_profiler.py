@@ -15,7 +15,7 @@ def test_smr_to_cus():
 
 
 def test_paper_example_path():
-    # the paper's GPT2-large example (100 ms SLO, tests/golden/hgss_printed_path.txt):
+    # the GPT2-large example of the draft text of Sec. 3.2 (100 ms SLO, tests/golden/hgss_printed_path.txt):
     # <1,10>, <2,20>, <4,30> meet the SLO, <8,40> violates it and the search stops there
     printed = [(int(b), float(s), m == "1") for b, s, m in rows("hgss_printed_path.txt")]
 
