@@ -220,17 +220,33 @@ def test_colocated_equals_solo():
 
 
 # ------------------------------------------------------------------------ causal decoders, full size
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name,prefix", [("decoder_l24_d1024_s512", 64), ("decoder_l24_d2048_s1024", 32)])
-def test_decoder_prefix_matches_oracle(name, prefix):
-    # causal: outputs at positions < p depend only on tokens < p, so the oracle
-    # runs on a prefix while the GPU runs the full-size batch
+def test_decoder_full_sequence_matches_oracle(name, prefix):
+    # the full-size batch on the GPU; the oracle runs the first sequence at its
+    # full length (every position, so every key chunk of the online softmax and
+    # every query workgroup), and the last sequence on a prefix (causal: outputs
+    # at positions < p depend only on tokens < p)
     w = W.WORKLOADS[name]
     shape = W.model_shape(name)
     B, S = w["batch"], w["seq"]
-    print(f"decoder {name} B={B} S={S} prefix={prefix}", flush=True)
+    print(f"decoder {name} B={B} S={S}: sequence 0 whole, sequence {B - 1} prefix {prefix}", flush=True)
     x = W.make_input(w["input_seed"], B, S, shape["d_model"])
     with ie.Instance(**instance_config(shape, B, S)) as inst:
         got = run_instance(inst, x)
     assert np.all(np.isfinite(got))
-    for b in sorted({0, B - 1}):
-        check(got[b:b + 1, :prefix], F.forward(x[b:b + 1, :prefix], shape), f"seq {b}")
+    check(got[B - 1:B, :prefix], F.forward(x[B - 1:B, :prefix], shape), f"seq {B - 1} prefix")
+    check(got[0:1], F.forward(x[0:1], shape), "seq 0 whole")
+
+
+@pytest.mark.timeout(600)
+def test_bert_base_batch32_stress_init_matches_oracle():
+    # stress init (biases, LN affine, peaked attention) at the headline batch:
+    # 8 sequences spread over the batch against the oracle
+    shape = W.model_shape("bert_base_l12_d768_s128", **W.STRESS_INIT)
+    x = bert_x(32, k=9)
+    print("bert B=32 stress init", flush=True)
+    with ie.Instance(**instance_config(shape, 32, 128)) as inst:
+        got = run_instance(inst, x)
+    idx = [0, 5, 9, 14, 18, 23, 27, 31]
+    check(got[idx], F.forward(x[idx], shape), "8 sequences")
