@@ -26,7 +26,11 @@
  *    caller; distinct instances are independent and may be driven from
  *    different threads.
  *  - Results are a function of (config, seed, input) only: bit-identical
- *    across CU quotas, co-location, repeats and batch composition.
+ *    across CU quotas, co-location, repeats and batch composition.  One
+ *    exception: a decode step (iefwd_decode) sums its products in an order
+ *    chosen by the batch-size class (1-4, 5-8 or 9-16 sequences), so its bits
+ *    may differ between classes (never across quotas or co-location); prefill
+ *    and decode agree within rounding, not bit for bit.
  *  - Device pointers are HIP device addresses on the instance's device.
  *  - After a HIP runtime error an instance is poisoned: every later call on it
  *    returns IEFWD_EHIP; destroy and re-create it (weights are a pure function
@@ -397,6 +401,17 @@ int iefwd_ctl_state(const iefwd_ctl *ctl, int32_t *state);
 int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void *bias,
                     const float *resid, void *out, uint32_t M, uint32_t N, uint32_t K,
                     void *stream);
+
+/* Pure host function: how iefwd_test_gemm and the forward pass run an
+ * M x N x K product on a stream with n_cu CUs.  k_order: the K summation order
+ * of the weight shape (0 = sequential 64-wide K tiles, 1 = even and odd K
+ * tiles summed separately, then added); tile_order: the order the chosen tile
+ * sums in, always equal to k_order; tile_m x tile_n: the output tile (tokens x
+ * features).  align: the width every tile must divide (d_model for the QKV
+ * product, else N).  EINVAL unless 1 <= M <= 2^24, N and K are multiples of 64
+ * in [64, 65536], align is a multiple of 64 dividing N and 1 <= n_cu <= 1024. */
+int iefwd_test_gemm_plan(uint32_t M, uint32_t N, uint32_t K, uint32_t align, uint32_t n_cu, uint32_t *k_order,
+                         uint32_t *tile_order, uint32_t *tile_m, uint32_t *tile_n);
 
 /* The decode-step product for M <= 16 activation rows: the same operands and
  * epilogues as iefwd_test_gemm, N % 16 == 0, K % 32 == 0.  Its K summation

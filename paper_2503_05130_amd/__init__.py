@@ -68,6 +68,8 @@ SIGNATURES = {
     "iefwd_last_error": (ctypes.c_char_p, []),
     "iefwd_status_string": (ctypes.c_char_p, [_i32]),
     "iefwd_test_gemm": (_i32, [_u32, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp]),
+    "iefwd_test_gemm_plan": (_i32, [_u32, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32), ctypes.POINTER(_u32),
+                                     ctypes.POINTER(_u32), ctypes.POINTER(_u32)]),
     "iefwd_test_gemm_skinny": (_i32, [_u32, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp, _vp, _vp, _f32, _vp]),
     "iefwd_test_gemm_qkv": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _vp]),
     "iefwd_test_attention": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _i32, _vp]),
@@ -342,6 +344,13 @@ def test_decode_attention(q, k, vt, ctx, batch, n_heads, n_keys, head_dim, k_row
     _check(lib().iefwd_test_decode_attention(_ptr(q), _ptr(k), _ptr(vt), _ptr(ctx), batch, n_heads, n_keys,
                                              head_dim, k_rows, vt_stride, _stream(stream)),
            "iefwd_test_decode_attention")
+
+
+def test_gemm_plan(M: int, N: int, K: int, align: int, n_cu: int) -> tuple[int, int, int, int]:
+    """(k_order, tile_order, tile_m, tile_n) of an M x N x K product on n_cu CUs."""
+    o = [_u32() for _ in range(4)]
+    _check(lib().iefwd_test_gemm_plan(M, N, K, align, n_cu, *[ctypes.byref(v) for v in o]), "iefwd_test_gemm_plan")
+    return tuple(v.value for v in o)
 
 
 def test_cu_probe(n_groups: int, out, stream=None) -> None:

@@ -56,6 +56,16 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
                        const QkvDst *qkv, hipStream_t stream, const LnResid *ln = nullptr,
                        const bf16_t *aux = nullptr, int n_cu = 256);
 
+// How launch_gemm runs a product: the K summation order (a function of the
+// weight shape (N, K) alone), the order the chosen tile sums in, and the tile.
+// align: the width every tile must divide (d_model for the QKV scatter, else N).
+struct GemmPlan {
+    bool split_order;   // K >= 2048: even / odd K tiles summed separately, then added
+    bool tile_split;    // the chosen tile's order (must equal split_order)
+    int bm, bn;         // output tile, tokens x features
+};
+GemmPlan gemm_plan(int M, int N, int K, int align, int n_cu);
+
 // Activations given as LayerNorm(z): z fp32 [M, K] rows, gamma / beta fp32 [K].
 struct LnIn {
     const float *z;

@@ -4,29 +4,31 @@
 //   A: activations, bf16 [M, K] row-major (tokens x features-in)
 //   W: weights stored output-major, bf16 [N, K] row-major
 //
-// Data movement.  K is walked in 64-wide tiles.  Each tile of A and W is copied
-// from global memory straight into LDS with global_load_lds_dwordx4 (gfx950's
-// 16-byte global->LDS DMA: no VGPR staging), into an S-stage ring, so S-1
-// tiles are in flight while one is consumed.  Each wave copies whole 8-row
-// groups (one 1 KB DMA per group); LDS rows are 128 bytes with the 16-byte
-// chunks XOR-swizzled per row, chosen so that the 16 rows read by one
-// ds_read_b128 fragment load fall in distinct bank groups.  The swizzle is
-// applied on the source side: lane i of a DMA fetches the global chunk that
-// belongs at its fixed LDS slot.  The wave waits for its own DMAs of the tile
-// it is about to read (s_waitcnt vmcnt), then a workgroup barrier makes every
-// wave's copies visible and frees the slot the next DMA will overwrite.
+// Data movement.  K is walked in BK-wide tiles (64, or 32 for a deeper ring).
+// Each tile of A and W is copied from global memory straight into LDS with
+// global_load_lds_dwordx4 (gfx950's 16-byte global->LDS DMA: no VGPR
+// staging) into an S-slot ring shared by the workgroup's wave groups; a
+// tile's 1 KB copies are spread over all waves.  LDS rows hold BK elements
+// with the 16-byte chunks XOR-swizzled per row, so that the 16 rows read by
+// one ds_read_b128 fragment load fall in distinct banks; the swizzle is
+// applied on the source side (lane i of a DMA fetches the global chunk that
+// belongs at its fixed LDS slot).  Each wave waits for its own copies of the
+// tiles it is about to read (s_waitcnt vmcnt), then a workgroup barrier makes
+// every wave's copies visible and frees the slots the next copies overwrite.
+// The MFMAs of each 32-deep half tile are issued before the LDS reads of the
+// next half, so fragment reads overlap the matrix unit's work.
 //
 // Math.  v_mfma_f32_16x16x32_bf16 on C^T blocks (features x tokens): the W
 // fragment is the MFMA "A" operand, the activation fragment the "B" operand,
 // so each lane ends up owning 4 consecutive output features of one token and
-// stores them with one vector store.  4 waves in a 2 x 2 grid over the tile.
+// stores them with one vector store.
 //
 // Determinism and batch invariance: every configuration uses the same MFMA
-// instruction; the K summation order (sequential 64-wide K tiles, or the
-// workgroup-internal even/odd split for long K) is a function of the weight
-// shape (N, K) alone.  So out[t, f] depends only on row t of A and row f of W
-// -- never on the tile shape, the ring depth, the grid, the CU mask or the
-// other rows in the batch.  No atomics, no cross-workgroup split-K.
+// instruction; the K summation order (32-wide K chunks in sequence, or the
+// workgroup-internal even/odd split of 64-wide tiles for long K) is a function
+// of the weight shape (N, K) alone.  So out[t, f] depends only on row t of A
+// and row f of W -- never on the tile shape, the ring depth, the grid, the CU
+// mask or the other rows in the batch.  No atomics, no cross-workgroup split-K.
 #include "gelu.h"
 #include "gemm.h"
 
@@ -41,8 +43,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void *lds_ptr_t;
-
-constexpr int kBK = 64;               // K tile (bf16 elements) = one 128-byte LDS row
 
 struct GemmParams {
     const bf16_t *a;
@@ -97,114 +97,200 @@ __device__ inline float wave_sum(float v) {
     return v;
 }
 
-// 16-byte chunk position of logical chunk 0 in LDS row r (row r holds its
-// chunk c at position c ^ swizzle(r)).  Consecutive rows alternate between the
-// two 128-byte halves of a 256-byte bank line, and within each parity the 8
-// rows of a 16-row fragment get 8 distinct positions.
-__device__ inline int swizzle(int r) { return ((r >> 1) & 7) ^ ((r & 1) << 2); }
+// 16-byte chunk position of logical chunk 0 in LDS row r of a BK-wide K tile
+// (row r holds its chunk c at position c ^ swizzle<BK>(r)), chosen so that the
+// 16 rows one ds_read_b128 fragment load reads fall in distinct banks:
+//  - 128-byte rows (BK = 64): consecutive rows alternate between the two
+//    128-byte halves of a 256-byte bank line, and within each parity the 8
+//    rows of a 16-row fragment get 8 distinct positions;
+//  - 64-byte rows (BK = 32): rows r, r + 4, r + 8, r + 12 share a bank offset
+//    and get the 4 distinct positions.
+template <int BK>
+__device__ inline int swizzle(int r) {
+    if constexpr (BK == 64) return ((r >> 1) & 7) ^ ((r & 1) << 2);
+    else return (r >> 2) & 3;
+}
 
-// s_waitcnt immediate that waits until at most n vector-memory operations of
-// this wave are outstanding (expcnt and lgkmcnt left unconstrained).
-constexpr int vmcnt_imm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+// One global->LDS copy of 16 bytes per lane (1 KB per wave) to the
+// wave-uniform LDS byte address `lds`.  Issued through inline asm: the
+// compiler's wait-count model treats these copies as LDS traffic that may
+// complete out of order with LDS reads, and would then drain every
+// outstanding LDS read before each use of any of them; the main loop orders
+// the copies itself (s_waitcnt vmcnt before each barrier).  The M0 write
+// needs one wait state before the copy reads it.
+__device__ inline void dma16(const void *src, uint32_t lds) {
+    uint32_t m0;   // the asm writes M0; naming it as an output tells the compiler so
+    asm volatile("s_mov_b32 %0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 : "={m0}"(m0)
+                 : "v"(src), "s"(lds)
+                 : "memory");
+    (void)m0;
+}
 
-// Tile configuration: BM x BN output tile, WGM x WGN waves, S-slot LDS ring.
-template <int BM_, int BN_, int WGM_, int WGN_, int S_>
+// s_waitcnt immediate: wait until at most vm vector-memory and lgkm LDS
+// operations of this wave are outstanding (expcnt left unconstrained).
+constexpr int waitcnt_imm(int vm, int lgkm) { return (vm & 15) | (7 << 4) | ((lgkm & 15) << 8) | ((vm >> 4) << 14); }
+
+// Tile configuration: BM x BN output tile; G wave groups of WGM x WGN waves;
+// one S-slot LDS ring of BK-wide K tiles (BK = 32 or 64) shared by the groups.
+// The MFMA sums 32 K at a time; G is the K order: G = 1 adds the 32-wide K
+// chunks in sequence (the same order for either BK), G = 2 (BK = 64 only) has
+// group g sum the 64-wide K tiles with index = g (mod 2) in sequence, then
+// adds the two partial sums.
+template <int BM_, int BN_, int WGM_, int WGN_, int G_, int S_, int BK_>
 struct Cfg {
-    static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, S = S_;
-    static constexpr int NW = WGM * WGN, NT = 64 * NW;
+    static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_, G = G_, S = S_, BK = BK_;
+    static constexpr int NWG = WGM * WGN;                      // waves per group
+    static constexpr int NW = G * NWG, NT = 64 * NW;           // waves / threads per workgroup
     static constexpr int TM = BM / WGM, TN = BN / WGN;         // per-wave tile (tokens x features)
     static constexpr int FM = TM / 16, FN = TN / 16;           // 16 x 16 MFMA blocks per wave
-    static constexpr int STAGE = (BM + BN) * kBK;              // bf16 elements per ring slot
-    static constexpr int G = (BM + BN) / 8;                    // 1 KB (8-row) DMA groups per slot
-    static constexpr int GPW = (G + NW - 1) / NW, REM = G % NW;  // groups per wave (first REM waves: GPW)
-    static_assert(TM % 16 == 0 && TN % 16 == 0 && BM % 8 == 0 && BN % 8 == 0, "tile");
-    static_assert(S >= 2 && (S - 2) * GPW <= 63, "ring depth");
+    static constexpr int H = BK / 32;                          // 32-deep MFMA steps per K tile
+    static constexpr int CPR = BK / 8;                         // 16-byte chunks per LDS row
+    static constexpr int RPG = 64 / CPR;                       // rows per 1 KB DMA (64 lanes x 16 B)
+    static constexpr int STAGE = (BM + BN) * BK;               // bf16 elements per ring slot
+    static constexpr int DG = (BM + BN) / RPG;                 // 1 KB DMA groups per slot
+    static constexpr int DPW = (DG + NW - 1) / NW;             // DMA groups per wave per slot (at most)
+    // waves per SIMD the register budget is sized for: as many workgroups as
+    // the LDS ring allows share a CU (160 KB), at most 4 waves per SIMD
+    static constexpr int WG_CU = 163840 / (S * STAGE * 2);
+    static constexpr int WPE = WG_CU * NW / 4 >= 4 ? 4 : WG_CU * NW / 4 < 1 ? 1 : WG_CU * NW / 4;
+    static_assert(TM % 16 == 0 && TN % 16 == 0 && BM % RPG == 0 && BN % RPG == 0, "tile");
+    static_assert(BK == 32 || BK == 64, "K tile");
+    static_assert(G == 1 || (G == 2 && BK == 64), "K order");
+    static_assert(S >= 2 * G && (S - 1) * DPW <= 63, "ring depth (vmcnt holds 6 bits)");
 };
 
-// One wave group's main loop over the K tiles kt_first, kt_first + kt_stride,
-// ... (n_mine of them) through its own S-slot LDS ring, accumulating into acc.
-// Every wave of the workgroup runs n_steps iterations (>= n_mine), so the
-// workgroup barriers line up even when two groups own different tile counts.
+// Waits until at most `t` K tiles' worth of this wave's copies (`per` DMAs
+// each) are still in flight: the copies of tiles issued after the ones about
+// to be read.  t in [0, S - 1]; the s_waitcnt immediate must be a constant,
+// hence the recursion over the possible counts.
+template <class C, int c = C::S - 1>
+__device__ inline void wait_tiles(int t, int per) {
+    if constexpr (c == 0) {
+        __builtin_amdgcn_s_waitcnt(waitcnt_imm(0, 15));
+    } else {
+        if (t >= c) {
+            if constexpr (C::DPW > 1) {
+                if (per != C::DPW) {
+                    __builtin_amdgcn_s_waitcnt(waitcnt_imm(c * (C::DPW - 1), 15));
+                    return;
+                }
+            }
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm(c * C::DPW, 15));
+            return;
+        }
+        wait_tiles<C, c - 1>(t, per);
+    }
+}
+
+// The main loop over the K tiles through the shared ring.  Tile t lives in
+// slot t % S; step j has group g multiply tile jG + g, 32 K at a time (H =
+// BK / 32 halves per tile).  Each half's MFMAs are issued before the LDS
+// reads of the next half, so those reads run while the matrix unit works
+// through the MFMAs just queued; the barrier sits between a step's last
+// reads and the next step's first ones:
+//
+//   MFMAs of half h                   (fragments read before)
+//   h < H - 1: read half h + 1 of my tile
+//   h = H - 1: wait for my copies of the next step's tiles and my LDS reads;
+//              barrier (next tiles visible to all; no wave reads this
+//              step's slots any more); refill this step's slots with tiles
+//              jG + S .. jG + S + G - 1; read half 0 of my next tile
+//
+// so S - G tiles are in flight behind the ones being read.  Each tile's 1 KB
+// copies are spread over all the workgroup's waves.
 template <class C>
 __device__ inline void main_loop(const GemmParams &p, bf16_t *ring0, int wave, int lane, int m0, int n0,
-                                 int kt_first, int kt_stride, int n_mine, int n_steps,
                                  f32x4 (&acc)[C::FN][C::FM]) {
-    constexpr int NW = C::NW, GPW = C::GPW, G = C::G;
-    const int wm = wave % C::WGM, wn = wave / C::WGM;
+    constexpr int NW = C::NW, DPW = C::DPW, DG = C::DG, S = C::S, G = C::G, FM = C::FM, FN = C::FN;
+    constexpr int BK = C::BK, H = C::H, CPR = C::CPR, RPG = C::RPG;
+    const int grp = wave / C::NWG, gw = wave % C::NWG;
+    const int wm = gw % C::WGM, wn = gw / C::WGM;
 
-    // DMA sources of this lane: DMA i of this wave copies the 8-row group
-    // g = wave + NW i (A rows first, then W rows); lane l fills row 8 g + l / 8
-    // of the slot at chunk position l % 8.  Rows past M are clamped to the
-    // last valid row (never stored); N is a multiple of BN.
-    uint32_t src[GPW];
-    const bf16_t *base[GPW];
+    // DMA sources of this lane: DMA i of this wave copies the RPG-row group
+    // d = wave + NW i of a slot (A rows first, then W rows); lane l fills row
+    // RPG d + l / CPR of the slot at chunk position l % CPR.  Rows past M are
+    // clamped to the last valid row (never stored); N is a multiple of BN.
+    uint32_t src[DPW];
+    const bf16_t *base[DPW];
+    int per = 0;   // DMAs this wave issues per tile
 #pragma unroll
-    for (int i = 0; i < GPW; ++i) {
-        const int g = min(wave + NW * i, G - 1);
-        if (g < C::BM / 8) {
-            const int r = 8 * g + (lane >> 3);
-            src[i] = (uint32_t)min(m0 + r, p.M - 1) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
+    for (int i = 0; i < DPW; ++i) {
+        const int d = min(wave + NW * i, DG - 1);
+        per += wave + NW * i < DG;
+        if (d < C::BM / RPG) {
+            const int r = RPG * d + lane / CPR;
+            src[i] = (uint32_t)min(m0 + r, p.M - 1) * (uint32_t)p.K + (((lane % CPR) ^ swizzle<BK>(r)) * 8);
             base[i] = p.a;
         } else {
-            const int r = 8 * (g - C::BM / 8) + (lane >> 3);
-            src[i] = (uint32_t)(n0 + r) * (uint32_t)p.K + (((lane & 7) ^ swizzle(r)) * 8);
+            const int r = RPG * (d - C::BM / RPG) + lane / CPR;
+            src[i] = (uint32_t)(n0 + r) * (uint32_t)p.K + (((lane % CPR) ^ swizzle<BK>(r)) * 8);
             base[i] = p.w;
         }
     }
-#define IEFWD_ISSUE(kt, slot)                                                                           \
-    do {                                                                                                \
-        const int k0_ = (kt) * kBK;                                                                     \
-        bf16_t *ring_ = ring0 + (slot) * C::STAGE;                                                      \
-        _Pragma("unroll") for (int i = 0; i < GPW; ++i)                                                 \
-            if (wave + NW * i < G)                                                                      \
-                __builtin_amdgcn_global_load_lds((const void *)(base[i] + src[i] + k0_),                \
-                                                 (lds_ptr_t)(ring_ + (wave + NW * i) * 512), 16, 0, 0); \
-    } while (0)
-
+    const int n_kt = p.K / BK;
+    auto issue = [&](int t) {   // copies of K tile t into slot t % S
+        const int k0 = t * BK;
+        bf16_t *ring = ring0 + (t % S) * C::STAGE;
 #pragma unroll
-    for (int s = 0; s < C::S - 1; ++s)
-        if (s < n_mine) IEFWD_ISSUE(kt_first + s * kt_stride, s);
-
-    // fragment rows: lane % 16 of each 16-row block; 16-byte chunk 4 ks + lane / 16
+        for (int i = 0; i < DPW; ++i)
+            if (wave + NW * i < DG)
+                dma16(base[i] + src[i] + k0, (uint32_t)(size_t)(lds_ptr_t)(ring + (wave + NW * i) * 512));
+    };
+    // fragment rows: lane % 16 of each 16-row block; 16-byte chunk 4 half + lane / 16
     const int ra = wm * C::TM + (lane & 15), rw = wn * C::TN + (lane & 15);
-    const bool full = C::REM == 0 || wave < C::REM;   // this wave issues GPW DMAs per slot, else GPW - 1
-    for (int it = 0; it < n_steps; ++it) {
-        // this wave's copies of its tile `it` are done once at most the later
-        // tiles' copies are outstanding; the barrier then publishes every wave's
-        // copies and guarantees the slot reused below is no longer being read
-        if (it + C::S - 2 < n_mine) {
-            if (full) __builtin_amdgcn_s_waitcnt(vmcnt_imm((C::S - 2) * GPW));
-            else __builtin_amdgcn_s_waitcnt(vmcnt_imm((C::S - 2) * (GPW - 1)));
-        } else {
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    auto read = [&](bf16x8 (&af)[FM], bf16x8 (&wf)[FN], int t, int half) {
+        const bf16_t *ring = ring0 + (t % S) * C::STAGE;
+        const int c = half * 4 + (lane >> 4);
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            const int r = ra + i * 16;
+            af[i] = *reinterpret_cast<const bf16x8 *>(ring + r * BK + ((c ^ swizzle<BK>(r)) * 8));
         }
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");   // keep LDS accesses on their side of the barrier
-        if (it + C::S - 1 < n_mine) IEFWD_ISSUE(kt_first + (it + C::S - 1) * kt_stride, (it + C::S - 1) % C::S);
-        if (it >= n_mine) continue;
-        const bf16_t *ring = ring0 + (it % C::S) * C::STAGE;
 #pragma unroll
-        for (int ks = 0; ks < kBK / 32; ++ks) {
-            const int c = ks * 4 + (lane >> 4);
-            bf16x8 af[C::FM], wf[C::FN];
-#pragma unroll
-            for (int i = 0; i < C::FM; ++i) {
-                const int r = ra + i * 16;
-                af[i] = *reinterpret_cast<const bf16x8 *>(ring + r * kBK + ((c ^ swizzle(r)) * 8));
-            }
-#pragma unroll
-            for (int j = 0; j < C::FN; ++j) {
-                const int r = rw + j * 16;
-                wf[j] = *reinterpret_cast<const bf16x8 *>(ring + C::BM * kBK + r * kBK + ((c ^ swizzle(r)) * 8));
-            }
-#pragma unroll
-            for (int j = 0; j < C::FN; ++j)
-#pragma unroll
-                for (int i = 0; i < C::FM; ++i)
-                    acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[j], af[i], acc[j][i], 0, 0, 0);
+        for (int jj = 0; jj < FN; ++jj) {
+            const int r = rw + jj * 16;
+            wf[jj] = *reinterpret_cast<const bf16x8 *>(ring + C::BM * BK + r * BK + ((c ^ swizzle<BK>(r)) * 8));
         }
+    };
+    auto mfma = [&](const bf16x8 (&af)[FM], const bf16x8 (&wf)[FN]) {
+#pragma unroll
+        for (int jj = 0; jj < FN; ++jj)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+                acc[jj][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[jj], af[i], acc[jj][i], 0, 0, 0);
+    };
+
+#pragma unroll
+    for (int t = 0; t < S; ++t)
+        if (t < n_kt) issue(t);
+    bf16x8 a0[FM], w0[FN], a1[FM], w1[FN];
+    wait_tiles<C>(min(n_kt, S) - min(n_kt, G), per);   // the first step's tiles have landed
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");   // keep LDS accesses on their side of the barrier
+    if (grp < n_kt) read(a0, w0, grp, 0);
+    const int n_steps = (n_kt + G - 1) / G, n_q = n_steps * H;
+    // half-step q: step q / H, half q % H of this group's tile
+    auto half = [&](bf16x8 (&ca)[FM], bf16x8 (&cw)[FN], bf16x8 (&na)[FM], bf16x8 (&nw)[FN], int q) {
+        const int j = q / H, h = q % H, t = j * G + grp;
+        if (t < n_kt) mfma(ca, cw);
+        if (h + 1 < H) {
+            if (t < n_kt) read(na, nw, t, h + 1);
+        } else if (j + 1 < n_steps) {
+            wait_tiles<C>(min(n_kt, j * G + S) - min(n_kt, (j + 2) * G), per);
+            __builtin_amdgcn_s_waitcnt(waitcnt_imm(63, 0));   // my reads of this step's slots have returned
+            __builtin_amdgcn_s_barrier();
+            asm volatile("" ::: "memory");
+#pragma unroll
+            for (int u = 0; u < G; ++u)
+                if (j * G + S + u < n_kt) issue(j * G + S + u);
+            if (t + G < n_kt) read(na, nw, t + G, 0);
+        }
+    };
+    for (int q = 0; q < n_q; q += 2) {
+        half(a0, w0, a1, w1, q);
+        if (q + 1 < n_q) half(a1, w1, a0, w0, q + 1);
     }
-#undef IEFWD_ISSUE
 }
 
 // bf16 outputs (bias, bias + GELU, the QKV scatter) leave through LDS: each wave
@@ -223,19 +309,19 @@ constexpr bool has_bias(Epi e) { return e != Epi::F32 && e != Epi::GeluBwdBf16; 
 // tiles (<= 6 blocks); larger tiles, and the split workgroups (whose register
 // budget is shared by both groups), would trade occupancy for it and load them
 // in the epilogue instead.
-template <class C, Epi EPI, bool SPLIT>
+template <class C, Epi EPI>
 struct EpiInputs {
     static constexpr int FM = C::FM, FN = C::FN;
     static constexpr bool kZ =
-        (EPI == Epi::BiasResidF32 || EPI == Epi::BiasLnResidF32) && FN * FM <= 6 && C::NW == 4 && !SPLIT;
+        (EPI == Epi::BiasResidF32 || EPI == Epi::BiasLnResidF32) && FN * FM <= 6 && C::NW == 4 && C::G == 1;
     u32x2 bias[FN];
     f32x4 z[kZ ? FN : 1][kZ ? FM : 1];
     f32x2 stats[EPI == Epi::BiasLnResidF32 ? FM : 1];
     f32x4 gamma[EPI == Epi::BiasLnResidF32 ? FN : 1], beta[EPI == Epi::BiasLnResidF32 ? FN : 1];
 };
 
-template <class C, Epi EPI, bool SPLIT>
-__device__ inline void epilogue_prefetch(const GemmParams &p, EpiInputs<C, EPI, SPLIT> &in, int wave, int lane,
+template <class C, Epi EPI>
+__device__ inline void epilogue_prefetch(const GemmParams &p, EpiInputs<C, EPI> &in, int wave, int lane,
                                          int m0, int n0) {
     const int wm = wave % C::WGM, wn = wave / C::WGM;
 #pragma unroll
@@ -247,7 +333,7 @@ __device__ inline void epilogue_prefetch(const GemmParams &p, EpiInputs<C, EPI, 
             in.gamma[j] = *reinterpret_cast<const f32x4 *>(p.ln.gamma + f);
             in.beta[j] = *reinterpret_cast<const f32x4 *>(p.ln.beta + f);
         }
-        if constexpr (EpiInputs<C, EPI, SPLIT>::kZ) {
+        if constexpr (EpiInputs<C, EPI>::kZ) {
             const float *src = EPI == Epi::BiasResidF32 ? p.resid : p.ln.z;
 #pragma unroll
             for (int i = 0; i < C::FM; ++i) {
@@ -274,9 +360,9 @@ template <class C> constexpr int kColStride = C::BM + 8;
 // Epilogue of one wave.  Lane owns features f..f+3 of token t in every block.
 // fp32 outputs are stored directly (one 16-byte store per block); bf16 outputs
 // go to the LDS tile `ctile` (token-major, or feature-major when `vt_tile`).
-template <class C, Epi EPI, bool SPLIT>
+template <class C, Epi EPI>
 __device__ inline void epilogue(const GemmParams &p, const f32x4 (&acc)[C::FN][C::FM],
-                                const EpiInputs<C, EPI, SPLIT> &in, int wave, int lane, int m0, int n0,
+                                const EpiInputs<C, EPI> &in, int wave, int lane, int m0, int n0,
                                 bf16_t *ctile, bool vt_tile) {
     const int wm = wave % C::WGM, wn = wave / C::WGM;
 #pragma unroll
@@ -318,14 +404,14 @@ __device__ inline void epilogue(const GemmParams &p, const f32x4 (&acc)[C::FN][C
             } else if constexpr (EPI == Epi::BiasResidF32) {
                 if (t >= p.M) continue;
                 f32x4 r;
-                if constexpr (EpiInputs<C, EPI, SPLIT>::kZ) r = in.z[j][i];
+                if constexpr (EpiInputs<C, EPI>::kZ) r = in.z[j][i];
                 else r = *reinterpret_cast<const f32x4 *>(p.resid + (size_t)t * p.N + f);
                 *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + (size_t)t * p.N + f) =
                     f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
             } else {   // Epi::BiasLnResidF32: residual = LN(z) rebuilt with the LayerNorm kernel's expression
                 if (t >= p.M) continue;
                 f32x4 z;
-                if constexpr (EpiInputs<C, EPI, SPLIT>::kZ) z = in.z[j][i];
+                if constexpr (EpiInputs<C, EPI>::kZ) z = in.z[j][i];
                 else z = *reinterpret_cast<const f32x4 *>(p.ln.z + (size_t)t * p.N + f);
                 const float mean = in.stats[i][0], rstd = in.stats[i][1];
                 f32x4 r;
@@ -387,100 +473,74 @@ __device__ inline void store_tile(const GemmParams &p, const bf16_t *ctile, bool
     }
 }
 
-// Sequential K order: one wave group, one ring, K tiles 0, 1, 2, ... into one accumulator.
+// One output tile per workgroup.  With two wave groups (the even / odd K
+// order) group 1 hands its partial sums to group 0 through LDS once the ring
+// is drained, and group 0 adds them (even-tile sum + odd-tile sum, always in
+// that order) and runs the epilogue.
 template <class C, Epi EPI>
-__global__ __launch_bounds__(C::NT) void gemm_kernel(GemmParams p) {
+__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::WPE))) void gemm_kernel(GemmParams p) {
+    constexpr int FN = C::FN, FM = C::FM;
     __shared__ __attribute__((aligned(1024))) bf16_t lds[C::S * C::STAGE];
     static_assert(!staged(EPI) || (C::BM * kRowStride<C> <= C::S * C::STAGE &&
                                    C::BN * kColStride<C> <= C::S * C::STAGE), "staged tile fits in the ring");
+    static_assert(C::G == 1 || FN * FM * 4 * C::NWG * 64 * 4 <= C::S * C::STAGE * 2, "hand-off space");
     int tm, tn;
     grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
     const int m0 = tm * C::BM, n0 = tn * C::BN;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    f32x4 acc[C::FN][C::FM];
+    // the wave index is uniform across the wave: held in a scalar register, so
+    // that every branch on it (group, tile, copy counts) is a scalar branch
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int grp = wave / C::NWG, gw = wave % C::NWG;   // group, wave within the group
+    f32x4 acc[FN][FM];
 #pragma unroll
-    for (int j = 0; j < C::FN; ++j)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int i = 0; i < C::FM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    EpiInputs<C, EPI, false> in;
-    epilogue_prefetch<C, EPI, false>(p, in, wave, lane, m0, n0);
-    const int kt_count = p.K / kBK;
-    main_loop<C>(p, lds, wave, lane, m0, n0, 0, 1, kt_count, kt_count, acc);
+        for (int i = 0; i < FM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    EpiInputs<C, EPI> in;
+    if (grp == 0) epilogue_prefetch<C, EPI>(p, in, gw, lane, m0, n0);
+    main_loop<C>(p, lds, wave, lane, m0, n0, acc);
+    __syncthreads();   // every wave is done reading the ring (and every copy has landed)
+    if constexpr (C::G == 2) {
+        float *handoff = reinterpret_cast<float *>(lds) + (gw * 64 + lane) * (FN * FM * 4);
+        if (grp == 1) {
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int i = 0; i < FM; ++i) *reinterpret_cast<f32x4 *>(handoff + (j * FM + i) * 4) = acc[j][i];
+        }
+        __syncthreads();
+        if (grp == 0) {
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+#pragma unroll
+                for (int i = 0; i < FM; ++i) acc[j][i] += *reinterpret_cast<const f32x4 *>(handoff + (j * FM + i) * 4);
+        }
+        if constexpr (staged(EPI)) __syncthreads();   // the hand-off is consumed before the tile overwrites it
+    }
     const bool vt_tile = EPI == Epi::Qkv && n0 >= 2 * p.qkv.d_model;
-    if constexpr (staged(EPI)) __syncthreads();   // every wave is done reading the ring
-    epilogue<C, EPI, false>(p, acc, in, wave, lane, m0, n0, lds, vt_tile);
+    if (grp == 0) epilogue<C, EPI>(p, acc, in, gw, lane, m0, n0, lds, vt_tile);
     if constexpr (staged(EPI)) {
         __syncthreads();
         store_tile<C, EPI>(p, lds, vt_tile, threadIdx.x, C::NT, m0, n0);
     }
 }
 
-// Split K order: two wave groups over the same output tile; group g
-// accumulates the K tiles kt = g (mod 2) through its own ring, then group 1
-// hands its partial sums to group 0 through LDS and group 0 adds them
-// (even-tile sum + odd-tile sum, always in that order) and runs the epilogue.
-// Twice the waves per CU for the long K loop.
-template <class C, Epi EPI>
-__global__ __launch_bounds__(2 * C::NT) void gemm_split_kernel(GemmParams p) {
-    constexpr int FN = C::FN, FM = C::FM;
-    __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * C::S * C::STAGE];
-    static_assert(FN * FM * 4 * C::NT * 4 <= 2 * C::S * C::STAGE * 2, "hand-off space");
-    static_assert(!staged(EPI) || (C::BM * kRowStride<C> <= 2 * C::S * C::STAGE &&
-                                   C::BN * kColStride<C> <= 2 * C::S * C::STAGE), "staged tile fits in the rings");
-    int tm, tn;
-    grouped_tile(xcd_contiguous(blockIdx.x, gridDim.x), p.tiles_m, p.tiles_n, tm, tn);
-    const int m0 = tm * C::BM, n0 = tn * C::BN;
-    const int lane = threadIdx.x & 63, grp = threadIdx.x / C::NT, wave = (threadIdx.x >> 6) % C::NW;
-    f32x4 acc[FN][FM];
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int i = 0; i < FM; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    EpiInputs<C, EPI, true> in;
-    if (grp == 0) epilogue_prefetch<C, EPI, true>(p, in, wave, lane, m0, n0);
-    const int kt_count = p.K / kBK;
-    const int n_mine = (kt_count - grp + 1) / 2;
-    main_loop<C>(p, lds + grp * C::S * C::STAGE, wave, lane, m0, n0, grp, 2, n_mine, (kt_count + 1) / 2, acc);
-    __syncthreads();   // both rings drained: reuse the LDS for the hand-off
-    float *handoff = reinterpret_cast<float *>(lds) + (wave * 64 + lane) * (FN * FM * 4);
-    if (grp == 1) {
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int i = 0; i < FM; ++i) *reinterpret_cast<f32x4 *>(handoff + (j * FM + i) * 4) = acc[j][i];
-    }
-    __syncthreads();
-    if (grp == 0) {
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int i = 0; i < FM; ++i) acc[j][i] += *reinterpret_cast<const f32x4 *>(handoff + (j * FM + i) * 4);
-    }
-    const bool vt_tile = EPI == Epi::Qkv && n0 >= 2 * p.qkv.d_model;
-    if constexpr (staged(EPI)) {
-        __syncthreads();   // the hand-off is consumed before the tile overwrites it
-        if (grp == 0) epilogue<C, EPI, true>(p, acc, in, wave, lane, m0, n0, lds, vt_tile);
-        __syncthreads();
-        store_tile<C, EPI>(p, lds, vt_tile, threadIdx.x, 2 * C::NT, m0, n0);
-    } else if (grp == 0) {
-        epilogue<C, EPI, true>(p, acc, in, wave, lane, m0, n0, lds, vt_tile);
-    }
-}
-
 // Tile configurations.  8-wave workgroups for large tiles: two waves per SIMD
 // and a 128-row tile halve the operand bytes each CU pulls through its L1 per
-// MFMA compared with 64-row 4-wave tiles (the per-CU load path, ~62 B/clk,
-// bounds small tiles below the MFMA rate).
-using CfgA = Cfg<128, 192, 2, 4, 2>;   // 8 waves, 64 x 48 per wave
-using CfgD = Cfg<128, 128, 2, 4, 2>;   // 8 waves, 64 x 32
-using CfgB = Cfg<128, 96, 4, 2, 2>;    // 8 waves, 32 x 48
-using CfgC = Cfg<64, 96, 2, 2, 2>;     // 4 waves, 32 x 48
-using CfgE = Cfg<64, 128, 2, 2, 2>;    // 4 waves, 32 x 64
-using CfgF = Cfg<64, 64, 2, 2, 3>;     // 4 waves, 32 x 32
-using SplitC = Cfg<64, 96, 2, 2, 2>;   // split order: two 4-wave groups
-using SplitE = Cfg<64, 128, 2, 2, 2>;
-using SplitD = Cfg<128, 128, 2, 2, 2>;
-using SplitG = Cfg<32, 64, 1, 2, 2>;   // two 2-wave groups, 32 x 32 per wave: small products
+// MFMA compared with 64-row 4-wave tiles (the per-CU load path moves about
+// 43 B/clk of global->LDS copies, which bounds small tiles below the MFMA rate).
+//                BM   BN  WGM WGN G  S  BK
+using CfgA = Cfg<128, 192, 2, 4, 1, 2, 64>;   // 8 waves, 64 x 48 per wave; 2 per CU
+using CfgD = Cfg<128, 128, 2, 4, 1, 2, 64>;   // 8 waves, 64 x 32
+using CfgB = Cfg<128, 96, 4, 2, 1, 2, 64>;    // 8 waves, 32 x 48
+using CfgC = Cfg<64, 96, 2, 2, 1, 2, 64>;     // 4 waves, 32 x 48
+using CfgE = Cfg<64, 128, 2, 2, 1, 2, 64>;    // 4 waves, 32 x 64
+using CfgF = Cfg<64, 64, 2, 2, 1, 3, 64>;     // 4 waves, 32 x 32
+// even / odd K order: two wave groups sharing one ring
+using SplitC = Cfg<64, 96, 2, 2, 2, 4, 64>;   // 8 waves, 32 x 48
+using SplitE = Cfg<64, 128, 2, 2, 2, 4, 64>;
+using SplitD = Cfg<128, 128, 2, 2, 2, 4, 64>;
+using SplitG = Cfg<32, 64, 1, 2, 2, 4, 64>;   // 4 waves, 32 x 32: small products
 
 enum class Tile { A, D, B, C, E, F, SplitC, SplitE, SplitD, SplitG };
 
@@ -497,18 +557,21 @@ long tiles_of(int M, int N, int bm, int bn) { return (long)((M + bm - 1) / bm) *
 // shape may follow the launch (M, and the n_cu CUs the stream may use)
 // without changing a bit.  Sequential order: the largest tile that still
 // gives min(256, 2 n_cu) tiles (one per CU of the device, two per CU of a
-// share up to 128 CUs); if none does, the one with the most tiles.  Split order: 64 x 96 (or 64 x 128 / 128 x 128) tiles, or
-// 32 x 64 ones when the product is too small to give three quarters of the
-// CUs a larger tile.  Tile widths divide `align` (d_model for the QKV
-// scatter, so that no tile straddles the Q / K / V boundaries).
+// share up to 128 CUs); if none does, the one with the most tiles.  Split
+// order: 64 x 96 (or 64 x 128 / 128 x 128) tiles, or 32 x 64 ones when the
+// product is too small to give three quarters of the CUs a larger tile.  Tile widths
+// divide `align` (d_model for the QKV scatter, so that no tile straddles the
+// Q / K / V boundaries).
 Tile choose_tile(int M, int N, int K, int align, int n_cu) {
     if (split_k_order(N, K)) {
+        // every split-order product takes a split-order tile: SplitG (64 wide)
+        // serves any width the others do not divide, whatever M and n_cu are
+        if (align % 96 && align % 128) return Tile::SplitG;
         const bool small = (align % 96 == 0 ? tiles_of(M, N, 64, 96) : tiles_of(M, N, 64, 128)) < 3L * n_cu / 4;
-        if (small && align % 64 == 0) return Tile::SplitG;
+        if (small) return Tile::SplitG;
         if (align % 96 == 0) return Tile::SplitC;
-        if (align % 128 == 0 && tiles_of(M, N, 64, 128) < 512) return Tile::SplitE;
-        if (align % 128 == 0) return Tile::SplitD;
-        return Tile::F;
+        if (tiles_of(M, N, 64, 128) < 512) return Tile::SplitE;
+        return Tile::SplitD;
     }
     struct Cand { Tile t; int bm, bn; } cands[] = {
         {Tile::A, 128, 192}, {Tile::D, 128, 128}, {Tile::B, 128, 96},
@@ -525,25 +588,40 @@ Tile choose_tile(int M, int N, int K, int align, int n_cu) {
     return best;
 }
 
-template <class C, Epi E, bool SPLIT>
-constexpr auto kernel_for() {
-    if constexpr (SPLIT) return gemm_split_kernel<C, E>;
-    else return gemm_kernel<C, E>;
+struct TileDims { int bm, bn; bool split; };
+
+template <class C>
+constexpr TileDims dims_of() { return {C::BM, C::BN, C::G == 2}; }
+
+TileDims tile_dims(Tile t) {
+    switch (t) {
+    case Tile::A: return dims_of<CfgA>();
+    case Tile::D: return dims_of<CfgD>();
+    case Tile::B: return dims_of<CfgB>();
+    case Tile::C: return dims_of<CfgC>();
+    case Tile::E: return dims_of<CfgE>();
+    case Tile::F: return dims_of<CfgF>();
+    case Tile::SplitC: return dims_of<SplitC>();
+    case Tile::SplitE: return dims_of<SplitE>();
+    case Tile::SplitD: return dims_of<SplitD>();
+    case Tile::SplitG: return dims_of<SplitG>();
+    }
+    return {0, 0, false};
 }
 
-template <class C, bool SPLIT>
+template <class C>
 hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
     p.tiles_m = (p.M + C::BM - 1) / C::BM;
     p.tiles_n = p.N / C::BN;
-    const dim3 grid(p.tiles_m * p.tiles_n), block(SPLIT ? 2 * C::NT : C::NT);
+    const dim3 grid(p.tiles_m * p.tiles_n), block(C::NT);
     switch (epi) {
-    case Epi::BiasBf16: return launch_kernel(kernel_for<C, Epi::BiasBf16, SPLIT>(), grid, block, s, p);
-    case Epi::BiasGeluBf16: return launch_kernel(kernel_for<C, Epi::BiasGeluBf16, SPLIT>(), grid, block, s, p);
-    case Epi::BiasResidF32: return launch_kernel(kernel_for<C, Epi::BiasResidF32, SPLIT>(), grid, block, s, p);
-    case Epi::Qkv: return launch_kernel(kernel_for<C, Epi::Qkv, SPLIT>(), grid, block, s, p);
-    case Epi::BiasLnResidF32: return launch_kernel(kernel_for<C, Epi::BiasLnResidF32, SPLIT>(), grid, block, s, p);
-    case Epi::F32: return launch_kernel(kernel_for<C, Epi::F32, SPLIT>(), grid, block, s, p);
-    case Epi::GeluBwdBf16: return launch_kernel(kernel_for<C, Epi::GeluBwdBf16, SPLIT>(), grid, block, s, p);
+    case Epi::BiasBf16: return launch_kernel(gemm_kernel<C, Epi::BiasBf16>, grid, block, s, p);
+    case Epi::BiasGeluBf16: return launch_kernel(gemm_kernel<C, Epi::BiasGeluBf16>, grid, block, s, p);
+    case Epi::BiasResidF32: return launch_kernel(gemm_kernel<C, Epi::BiasResidF32>, grid, block, s, p);
+    case Epi::Qkv: return launch_kernel(gemm_kernel<C, Epi::Qkv>, grid, block, s, p);
+    case Epi::BiasLnResidF32: return launch_kernel(gemm_kernel<C, Epi::BiasLnResidF32>, grid, block, s, p);
+    case Epi::F32: return launch_kernel(gemm_kernel<C, Epi::F32>, grid, block, s, p);
+    case Epi::GeluBwdBf16: return launch_kernel(gemm_kernel<C, Epi::GeluBwdBf16>, grid, block, s, p);
     }
     return hipErrorInvalidValue;
 }
@@ -783,10 +861,16 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
 
 }  // namespace
 
+GemmPlan gemm_plan(int M, int N, int K, int align, int n_cu) {
+    const TileDims d = tile_dims(choose_tile(M, N, K, align, n_cu));
+    return GemmPlan{split_k_order(N, K), d.split, d.bm, d.bn};
+}
+
 hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
                        const float *resid, void *out, int M, int N, int K, const QkvDst *qkv,
                        hipStream_t stream, const LnResid *ln, const bf16_t *aux, int n_cu) {
     if (M <= 0) return hipSuccess;
+    if (N % 64 || K % 64 || N <= 0 || K <= 0) return hipErrorInvalidValue;
     if (epi == Epi::GeluBwdBf16 && !aux) return hipErrorInvalidValue;
     GemmParams p{};
     p.a = a; p.w = w; p.bias = bias; p.resid = resid; p.out = out; p.aux = aux;
@@ -796,16 +880,16 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
     // N is a multiple of 64 (checked by the callers); d_model a multiple of 128
     const int align = epi == Epi::Qkv ? p.qkv.d_model : N;
     switch (choose_tile(M, N, K, align, n_cu)) {
-    case Tile::A: return launch_tile<CfgA, false>(epi, p, stream);
-    case Tile::D: return launch_tile<CfgD, false>(epi, p, stream);
-    case Tile::B: return launch_tile<CfgB, false>(epi, p, stream);
-    case Tile::C: return launch_tile<CfgC, false>(epi, p, stream);
-    case Tile::E: return launch_tile<CfgE, false>(epi, p, stream);
-    case Tile::F: return launch_tile<CfgF, false>(epi, p, stream);
-    case Tile::SplitC: return launch_tile<SplitC, true>(epi, p, stream);
-    case Tile::SplitE: return launch_tile<SplitE, true>(epi, p, stream);
-    case Tile::SplitD: return launch_tile<SplitD, true>(epi, p, stream);
-    case Tile::SplitG: return launch_tile<SplitG, true>(epi, p, stream);
+    case Tile::A: return launch_tile<CfgA>(epi, p, stream);
+    case Tile::D: return launch_tile<CfgD>(epi, p, stream);
+    case Tile::B: return launch_tile<CfgB>(epi, p, stream);
+    case Tile::C: return launch_tile<CfgC>(epi, p, stream);
+    case Tile::E: return launch_tile<CfgE>(epi, p, stream);
+    case Tile::F: return launch_tile<CfgF>(epi, p, stream);
+    case Tile::SplitC: return launch_tile<SplitC>(epi, p, stream);
+    case Tile::SplitE: return launch_tile<SplitE>(epi, p, stream);
+    case Tile::SplitD: return launch_tile<SplitD>(epi, p, stream);
+    case Tile::SplitG: return launch_tile<SplitG>(epi, p, stream);
     }
     return hipErrorInvalidValue;
 }

@@ -950,6 +950,22 @@ iefwd_instance::~iefwd_instance() {
     if (wblob) (void)hipFree(wblob);
 }
 
+// ================================================================= shared validation
+
+namespace {
+
+void check_decode_attention_args(const void *q, const void *k, const void *vt, void *ctx, uint32_t batch,
+                                 uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
+                                 uint32_t vt_stride) {
+    if (!q || !k || !vt || !ctx) fail(IEFWD_EINVAL, "NULL pointer");
+    if (batch == 0 || n_heads == 0 || (uint64_t)batch * n_heads > 65535) fail(IEFWD_EINVAL, "bad batch / heads");
+    if (head_dim != 64 && head_dim != 128) fail(IEFWD_EINVAL, "head_dim must be 64 or 128");
+    if (n_keys == 0 || n_keys > 8192 || k_rows < n_keys || vt_stride < n_keys || vt_stride % 64)
+        fail(IEFWD_EINVAL, "need 1 <= n_keys <= 8192, k_rows >= n_keys, vt_stride >= n_keys and % 64 == 0");
+}
+
+}  // namespace
+
 // =================================================================================== ABI
 
 extern "C" {
@@ -1501,6 +1517,22 @@ int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void 
     });
 }
 
+int iefwd_test_gemm_plan(uint32_t M, uint32_t N, uint32_t K, uint32_t align, uint32_t n_cu, uint32_t *k_order,
+                         uint32_t *tile_order, uint32_t *tile_m, uint32_t *tile_n) {
+    return guarded([&] {
+        if (!k_order || !tile_order || !tile_m || !tile_n) fail(IEFWD_EINVAL, "NULL pointer");
+        if (M == 0 || M > (1u << 24) || N == 0 || N % 64 || N > 65536 || K == 0 || K % 64 || K > 65536)
+            fail(IEFWD_EINVAL, "need 1 <= M <= 2^24 and N, K multiples of 64 in [64, 65536]");
+        if (align == 0 || align % 64 || N % align) fail(IEFWD_EINVAL, "align must be a multiple of 64 dividing N");
+        if (n_cu == 0 || n_cu > 1024) fail(IEFWD_EINVAL, "n_cu must be in [1, 1024]");
+        const GemmPlan p = gemm_plan((int)M, (int)N, (int)K, (int)align, (int)n_cu);
+        *k_order = p.split_order ? 1u : 0u;
+        *tile_order = p.tile_split ? 1u : 0u;
+        *tile_m = (uint32_t)p.bm;
+        *tile_n = (uint32_t)p.bn;
+    });
+}
+
 int iefwd_test_gemm_skinny(uint32_t epilogue, const void *a, const void *w, const void *bias, const float *resid,
                            void *out, uint32_t M, uint32_t N, uint32_t K, const float *ln_z, const float *ln_gamma,
                            const float *ln_beta, float ln_eps, void *stream) {
@@ -1583,11 +1615,7 @@ int iefwd_test_decode_attention(const void *q, const void *k, const void *vt, vo
                                 uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
                                 uint32_t vt_stride, void *stream) {
     return guarded([&] {
-        if (!q || !k || !vt || !ctx) fail(IEFWD_EINVAL, "NULL pointer");
-        if (batch == 0 || n_heads == 0 || (uint64_t)batch * n_heads > 65535) fail(IEFWD_EINVAL, "bad batch / heads");
-        if (head_dim != 64 && head_dim != 128) fail(IEFWD_EINVAL, "head_dim must be 64 or 128");
-        if (n_keys == 0 || n_keys > 8192 || k_rows < n_keys || vt_stride < n_keys || vt_stride % 64)
-            fail(IEFWD_EINVAL, "need 1 <= n_keys <= 8192, k_rows >= n_keys, vt_stride >= n_keys and % 64 == 0");
+        check_decode_attention_args(q, k, vt, ctx, batch, n_heads, n_keys, head_dim, k_rows, vt_stride);
         // scratch for this call only: allocated, released after the stream drains
         const size_t bh = (size_t)batch * n_heads;
         const size_t pbytes = round_up(bh * kDecodeMaxChunks * (head_dim + 2) * 4, 256);

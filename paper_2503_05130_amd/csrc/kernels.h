@@ -20,8 +20,9 @@ hipError_t launch_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, 
 // ctx bf16 [B, H * dh].  fp32 scores, softmax and sums.  n_keys <= 8192.
 // The keys are split into decode_attention_chunks(n_keys) <= kDecodeMaxChunks
 // chunks, one workgroup each; with more than one chunk a second kernel
-// combines them.  partials: at least B * H * kDecodeMaxChunks * (dh + 2)
-// floats of scratch; launches sharing it must not overlap.
+// combines them.  partials: at least B * H * decode_attention_chunks(n_keys)
+// * (dh + 2) floats of scratch, every one of them written before it is read
+// (nothing needs clearing); launches sharing it must not overlap.
 constexpr int kDecodeMaxChunks = 32;
 int decode_attention_chunks(int n_keys);
 hipError_t launch_decode_attention(const bf16_t *q, const bf16_t *k, const bf16_t *vt, bf16_t *ctx,

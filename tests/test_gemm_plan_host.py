@@ -1,0 +1,57 @@
+"""Host checks of the GEMM launch plan (no GPU needed): the K summation order
+of a product is a function of the weight shape (N, K) alone, and the tile the
+library picks always sums in that order, whatever the batch (M), the CU
+quota or the width the tiles must divide.  This is what makes an output
+element's bits independent of the quota and of the other rows in the batch."""
+import itertools
+
+import pytest
+
+import paper_2503_05130_amd as ie
+
+MS = [1, 2, 7, 16, 64, 100, 128, 256, 512, 1000, 2048, 4096, 8192, 16384]
+N_CUS = [8, 16, 32, 64, 96, 128, 160, 192, 224, 256]
+KS = [64, 128, 768, 1024, 1984, 2048, 2112, 3072, 4096, 8192, 8384, 16384]
+# widths (features) of the products of every model the library accepts: 3d, d, d_ff; plus the
+# widths that are multiples of 64 but of neither 96 nor 128 (d_ff = 8384, 320, 704, ...)
+NS = [64, 128, 192, 320, 384, 704, 768, 1024, 1088, 2304, 3072, 4096, 6144, 8192, 8384, 12288, 16448]
+
+
+def _plan(M, N, K, align, n_cu):
+    return ie.test_gemm_plan(M, N, K, align, n_cu)
+
+
+def test_k_order_depends_on_weight_shape_only():
+    for N, K in itertools.product(NS, KS):
+        orders = set()
+        for M, n_cu in itertools.product(MS, N_CUS):
+            k_order, tile_order, bm, bn = _plan(M, N, K, N, n_cu)
+            assert tile_order == k_order, (M, N, K, n_cu, bm, bn)
+            assert N % bn == 0 and bm > 0
+            orders.add(k_order)
+        assert len(orders) == 1, (N, K, orders)
+        assert orders == {1 if K >= 2048 else 0}
+
+
+@pytest.mark.parametrize("d", [128, 256, 768, 1024, 2048, 4096])
+def test_qkv_tiles_do_not_straddle_q_k_v(d):
+    # the QKV product's tiles divide d_model, so no tile mixes Q, K and V columns
+    for M, n_cu in itertools.product(MS, N_CUS):
+        k_order, tile_order, bm, bn = _plan(M, 3 * d, d, d, n_cu)
+        assert d % bn == 0 and tile_order == k_order
+
+
+def test_the_width_that_once_broke_the_order():
+    # d_model 2048 with d_ff 8384: FFN-up N = 8384, K = 2048 (split order), at
+    # every batch and quota; before the fix 64-128 CUs took a sequential tile
+    for M in (128, 1024, 8192):
+        for n_cu in (64, 128, 192, 256):
+            assert _plan(M, 8384, 2048, 8384, n_cu)[:2] == (1, 1)
+
+
+def test_plan_rejects_bad_arguments():
+    for args in [(0, 64, 64, 64, 256), (1, 96, 64, 96, 256), (1, 64, 96, 64, 256), (1, 128, 64, 96, 256),
+                 (1, 128, 64, 128, 0)]:
+        with pytest.raises(ie.IefwdError) as e:
+            _plan(*args)
+        assert e.value.status == ie.EINVAL
