@@ -466,6 +466,23 @@ int iefwd_test_decode_attention(const void *q, const void *k, const void *vt, vo
                                 uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
                                 uint32_t vt_stride, void *stream);
 
+/* Allocation-free variant of iefwd_test_decode_attention, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc).  Same arguments, kernels and
+ * results (bit for bit); the chunks' partial results go to a fixed device
+ * scratch of 8 MiB that the library holds on each GPU it runs on until the
+ * process ends, instead of a per-call allocation.  Needs
+ * batch * n_heads * chunks * (head_dim + 2) * 4 <= 8 MiB, chunks =
+ * ceil(n_keys / 64) up to 2048 keys, else ceil(n_keys / 256) (EINVAL
+ * otherwise).  Runs on the current device (stream must belong to it) and
+ * returns without synchronising.  The call allocates nothing and frees
+ * nothing.  Every call on one GPU uses the same scratch: calls that overlap
+ * on one GPU (on different streams, or from different threads) race and
+ * must be serialised by the caller. */
+int iefwd_decode_attention_noalloc(const void *q, const void *k, const void *vt, void *ctx, uint32_t batch,
+                                   uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
+                                   uint32_t vt_stride, void *stream);
+
 /* CU residency probe: launches n_groups workgroups of 64 threads on `stream`;
  * workgroup g writes out[2g] = XCC id, out[2g+1] = the hardware id register
  * (CU, SIMD, shader-array and shader-engine fields).  out: device uint32

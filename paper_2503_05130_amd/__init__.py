@@ -77,6 +77,7 @@ SIGNATURES = {
     "iefwd_test_ln_head": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _f32, _vp]),
     "iefwd_test_cu_probe": (_i32, [_vp, _u32, _vp]),
     "iefwd_test_decode_attention": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _u32, _u32, _vp]),
+    "iefwd_decode_attention_noalloc": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _u32, _u32, _vp]),
 }
 
 
@@ -351,6 +352,13 @@ def test_gemm_plan(M: int, N: int, K: int, align: int, n_cu: int) -> tuple[int, 
     o = [_u32() for _ in range(4)]
     _check(lib().iefwd_test_gemm_plan(M, N, K, align, n_cu, *[ctypes.byref(v) for v in o]), "iefwd_test_gemm_plan")
     return tuple(v.value for v in o)
+
+
+def decode_attention_noalloc(q, k, vt, ctx, batch, n_heads, n_keys, head_dim, k_rows, vt_stride,
+                             stream=None) -> None:
+    _check(lib().iefwd_decode_attention_noalloc(_ptr(q), _ptr(k), _ptr(vt), _ptr(ctx), batch, n_heads, n_keys,
+                                                head_dim, k_rows, vt_stride, _stream(stream)),
+           "iefwd_decode_attention_noalloc")
 
 
 def test_cu_probe(n_groups: int, out, stream=None) -> None:

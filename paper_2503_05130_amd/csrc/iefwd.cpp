@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <array>
 #include <memory>
+#include <mutex>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -950,9 +951,38 @@ iefwd_instance::~iefwd_instance() {
     if (wblob) (void)hipFree(wblob);
 }
 
-// ================================================================= shared validation
+// ========================================================================== fixed scratch
 
 namespace {
+
+// Device scratch of the allocation-free decode attention entry point: the
+// per-chunk partial results (max, sum, unnormalised context) of one call.
+// Each GPU the library runs on holds its own copy until the process ends; all
+// calls on a GPU share it.  In host code `scratch` names a host-side stand-in,
+// never the device memory: kernels get the address hipGetSymbolAddress returns
+// for the current device.
+constexpr size_t kNoallocScratchBytes = size_t(8) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_dev[kMaxScratchDevices];   // device address of `scratch` per device, once looked up
+
+// Address of the current device's `scratch`, looked up on the first call on
+// that device (with that device current).
+void *scratch_on_current_device() {
+    int dev = 0;
+    hip_check(hipGetDevice(&dev), "hipGetDevice");
+    if (dev < 0 || dev >= kMaxScratchDevices) fail(IEFWD_ENODEV, "device index beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void *ptr = nullptr;
+        hip_check(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+        if (!ptr) fail(IEFWD_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+        g_scratch_dev[dev] = ptr;
+    }
+    return g_scratch_dev[dev];
+}
 
 void check_decode_attention_args(const void *q, const void *k, const void *vt, void *ctx, uint32_t batch,
                                  uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
@@ -1630,6 +1660,23 @@ int iefwd_test_decode_attention(const void *q, const void *k, const void *vt, vo
                                           (int)vt_stride, static_cast<float *>(scratch), (hipStream_t)stream),
                   "decode attention launch");
         hip_check(hipStreamSynchronize((hipStream_t)stream), "hipStreamSynchronize");
+    });
+}
+
+int iefwd_decode_attention_noalloc(const void *q, const void *k, const void *vt, void *ctx, uint32_t batch,
+                                   uint32_t n_heads, uint32_t n_keys, uint32_t head_dim, uint32_t k_rows,
+                                   uint32_t vt_stride, void *stream) {
+    return guarded([&] {
+        check_decode_attention_args(q, k, vt, ctx, batch, n_heads, n_keys, head_dim, k_rows, vt_stride);
+        const size_t need = (size_t)batch * n_heads * decode_attention_chunks((int)n_keys) * (head_dim + 2) * 4;
+        if (need > kNoallocScratchBytes)
+            fail(IEFWD_EINVAL, "batch * heads * chunks * (head_dim + 2) * 4 = " + std::to_string(need) +
+                                   " bytes exceeds the fixed scratch of " + std::to_string(kNoallocScratchBytes));
+        float *partials = static_cast<float *>(scratch_on_current_device());
+        hip_check(launch_decode_attention((const bf16_t *)q, (const bf16_t *)k, (const bf16_t *)vt, (bf16_t *)ctx,
+                                          (int)batch, (int)n_heads, (int)n_keys, (int)head_dim, (int)k_rows,
+                                          (int)vt_stride, partials, (hipStream_t)stream),
+                  "decode attention launch");
     });
 }
 
