@@ -150,6 +150,18 @@ int iefwd_set_quota(iefwd_instance *inst, uint32_t n_cu);
  * hardware queue.  EINVAL as iefwd_set_quota_at. */
 int iefwd_prepare_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first);
 
+/* Sets how many masked streams (hardware queues) the instance keeps cached:
+ * 1 .. 16, default 2 (the one in use and one more).  Lowering it destroys the
+ * least recently used streams beyond the new size (never the one in use).
+ * Measured on MI355X, and the reason the cache is small: creating or
+ * destroying a masked queue stalls every other queue of the process for
+ * about 3 ms, and with more than about 20-24 live queues in a process the
+ * hardware scheduler time-slices them (12-33 ms stalls).  A serving loop that
+ * moves quotas every control period should therefore prepare a fixed set of
+ * placements once (iefwd_prepare_quota_at), size the cache to hold them, and
+ * keep the whole process within that queue budget.  EINVAL outside 1 .. 16. */
+int iefwd_set_stream_cache(iefwd_instance *inst, uint32_t capacity);
+
 /* Requests an explicit CU mask (n_words 32-bit words, bit order as above);
  * same timing as iefwd_set_quota.  EINVAL if the mask enables no existing CU. */
 int iefwd_set_cu_mask(iefwd_instance *inst, const uint32_t *mask, uint32_t n_words);

@@ -40,6 +40,7 @@ SIGNATURES = {
     "iefwd_set_quota_at": (_i32, [_vp, _u32, _u32]),
     "iefwd_decode": (_i32, [_vp, _vp, _u32, _u32, _i32]),
     "iefwd_prepare_quota_at": (_i32, [_vp, _u32, _u32]),
+    "iefwd_set_stream_cache": (_i32, [_vp, _u32]),
     "iefwd_kernels_launched": (_i32, [_vp, ctypes.POINTER(ctypes.c_uint64)]),
     "iefwd_ctl_params_init": (_i32, [_vp]),
     "iefwd_ctl_create": (_i32, [_vp, ctypes.POINTER(_vp)]),
@@ -212,6 +213,10 @@ class Instance:
         """Create the masked stream for (n_cu, first) ahead of time; may be called
         from another thread while this instance serves."""
         _check(lib().iefwd_prepare_quota_at(self._h, n_cu, first), "iefwd_prepare_quota_at")
+
+    def set_stream_cache(self, capacity: int) -> None:
+        """Number of masked streams (hardware queues) the instance keeps cached."""
+        _check(lib().iefwd_set_stream_cache(self._h, capacity), "iefwd_set_stream_cache")
 
     def set_cu_mask(self, mask) -> None:
         buf = (_u32 * len(mask))(*mask)

@@ -1217,6 +1217,15 @@ int iefwd_prepare_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first) 
     });
 }
 
+int iefwd_set_stream_cache(iefwd_instance *inst, uint32_t capacity) {
+    return guarded([&] {
+        check_alive(inst);
+        if (capacity < 1 || capacity > 16) fail(IEFWD_EINVAL, "capacity must be in [1, 16]");
+        hip_check(hipSetDevice(inst->device), "hipSetDevice");
+        hip_check(inst->streams.set_capacity(capacity), "hipStreamDestroy");
+    });
+}
+
 int iefwd_set_cu_mask(iefwd_instance *inst, const uint32_t *mask, uint32_t n_words) {
     return guarded([&] {
         check_alive(inst);

@@ -105,6 +105,25 @@ hipError_t MaskedStreams::acquire(const std::vector<uint32_t> &mask, hipStream_t
     return hipSuccess;
 }
 
+hipError_t MaskedStreams::set_capacity(size_t capacity) {
+    std::lock_guard<std::mutex> lock(mu_);
+    capacity_ = capacity < 1 ? 1 : capacity;
+    while (entries_.size() > capacity_) {
+        size_t victim = entries_.size();
+        for (size_t i = 0; i < entries_.size(); ++i) {
+            if (entries_[i].stream == current_) continue;
+            if (victim == entries_.size() || entries_[i].last_use < entries_[victim].last_use) victim = i;
+        }
+        if (victim == entries_.size()) break;
+        hipError_t err = hipStreamSynchronize(entries_[victim].stream);
+        if (err != hipSuccess) return err;
+        err = hipStreamDestroy(entries_[victim].stream);
+        if (err != hipSuccess) return err;
+        entries_.erase(entries_.begin() + (long)victim);
+    }
+    return hipSuccess;
+}
+
 hipError_t MaskedStreams::prepare(const std::vector<uint32_t> &mask) {
     hipStream_t s = nullptr;
     return get(mask, &s);

@@ -32,11 +32,15 @@ uint32_t mask_popcount(const std::vector<uint32_t> &mask, uint32_t n_cu);
 // Small LRU cache of CU-masked streams for one instance.  Creating a masked
 // stream creates a hardware queue (about 5 ms on MI355X), so it is kept off
 // the batch path: once a mask has been seen, or prepared ahead of time from
-// another thread, switching to it costs one event wait.  The default keeps two
-// (the stream in use and the next one): with several co-located instances,
-// more live queues per instance made batches after a switch stall more often.  Streams are created
-// at the default priority.  Thread-safe: prepare() may run concurrently with
-// acquire(); stream creation happens outside the lock.
+// another thread, switching to it costs one event wait.  Measured on MI355X:
+// creating or destroying a masked queue stalls the work of every other queue
+// of the process for about 3 ms (the hardware scheduler rewrites its queue
+// list), and with more than about 20-24 live queues in a process the
+// scheduler time-slices them (batches stall 12-33 ms).  So the cache is
+// small (2 by default: the stream in use and the next one) and a serving
+// loop should switch among a fixed set of prepared masks.  Streams are
+// created at the default priority.  Thread-safe: prepare() may run
+// concurrently with acquire(); stream creation happens outside the lock.
 class MaskedStreams {
 public:
     explicit MaskedStreams(size_t capacity = 2) : capacity_(capacity) {}
@@ -50,6 +54,9 @@ public:
     // Makes sure a stream with this mask is cached (creating it if missing)
     // without changing the stream in use.
     hipError_t prepare(const std::vector<uint32_t> &mask);
+    // Keeps at most `capacity` streams (>= 1), destroying the least recently
+    // used ones beyond it (never the stream in use).
+    hipError_t set_capacity(size_t capacity);
     void clear();   // synchronises and destroys every cached stream
 
 private:

@@ -3,8 +3,8 @@ instances, one dispatcher thread per instance, and a quota policy that
 re-masks the instances every control period (the paper's setting of
 Sec. 3.4 and its inference-inference experiments, Sec. 5).
 
-  python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 static proportional shared]
-                                       [--horizon 20] [--warmup 2] [--period-ms 20] [--small]
+  python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 static proportional shared paired]
+                                       [--horizon 20] [--warmup 2] [--period-ms 20] [--granule 32] [--small]
                                        [--mix inference|train|decode]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
@@ -22,6 +22,18 @@ Policies (each period):
   alg2         the fast scale-up/down controller (iefwd_ctl_*, 32-CU
                granule): kernels launched in the period and the per-batch
                time go in, quotas and placements come out
+  paired       quotas from a fixed vocabulary: instances are paired (each
+               SLO-sensitive one with a best-effort one) and each pair owns
+               a fixed 128-CU region whose split point moves in 32-CU steps
+               (32 / 96, 64 / 64, 96 / 32) in proportion to the two queue
+               lengths.  Every placement is prepared before the run and the
+               stream caches hold all of them, so no hardware queue is
+               created or destroyed while the instances serve (creating or
+               destroying one stalls every queue of the process for ~3 ms on
+               MI355X, and more than ~20-24 live queues per process make the
+               hardware scheduler time-slice them)
+
+--granule sets the quota granularity (in CUs) of proportional and alg2.
 
 A new quota's masked stream is created by the control thread
 (iefwd_prepare_quota_at) before the quota is posted, so a dispatcher only
@@ -92,6 +104,8 @@ class Served:
         self.pending = None                 # (quota, first) posted by the control thread
         self.inst.set_quota(ie.device_info(0)[0], 0)
         self.applied = (ie.device_info(0)[0], 0)
+        self.busy = False                   # a batch is in flight (on `applied`)
+        self.batch_log = []                 # (completion time, device ms, quota, first batch after a switch)
         self.batches = 0
         self.changes = 0                    # quota switches applied
         self.klc_log = []                   # KLC ratios reported to the controller
@@ -110,22 +124,29 @@ class Served:
                 time.sleep(min(self.arrivals[self.next] - now, 0.002))
                 continue
             k = min(self.max_batch, self.queue_len(now))
-            with self.lock:
+            with self.lock:                 # taking the quota and marking the batch start together
                 pend, self.pending = self.pending, None
-            if pend is not None and pend != self.applied:
+                self.busy = True
+            switched = pend is not None and pend != self.applied
+            if switched:
                 self.inst.set_quota(*pend)
-                self.applied = pend
                 self.changes += 1
                 self.plans.add(pend)
+            with self.lock:
+                if pend is not None:
+                    self.applied = pend
             x = self.pool[slot:slot + k]
             slot = (slot + k) % (len(self.pool) - self.max_batch + 1)
             self.inst.submit(x)
             self.inst.wait()
+            with self.lock:
+                self.busy = False
             done = time.perf_counter() - t0
             self.latency[self.next:self.next + k] = done - self.arrivals[self.next:self.next + k]
             self.next += k
             self.batches += 1
             ms = self.inst.last_batch_ms()
+            self.batch_log.append((done, ms, self.applied[0] if self.applied else 0, switched))
             key = (k, self.applied[0] if self.applied else 0)
             best = min(self.best_ms.get(key, ms), ms)
             self.best_ms[key] = best
@@ -133,10 +154,21 @@ class Served:
                 self.kernels = self.inst.kernels_launched()
                 self.ratios.append(ms / best)
 
+    def batch_stats(self, warmup):
+        """Device time per batch (ms): first batches after a quota switch and the others."""
+        log = [b for b in self.batch_log if b[0] >= warmup]
+        out = {}
+        for key, sel in (("after_switch", [b[1] for b in log if b[3]]), ("other", [b[1] for b in log if not b[3]])):
+            if sel:
+                out[key] = {"n": len(sel), "p50_ms": round(float(np.percentile(sel, 50)), 3),
+                            "p99_ms": round(float(np.percentile(sel, 99)), 3), "max_ms": round(float(max(sel)), 3)}
+        return out
+
     def stats(self, warmup):
         keep = (self.arrivals >= warmup) & np.isfinite(self.latency)
         lat = self.latency[keep] * 1e3
         return {"name": self.name, "requests": int(keep.sum()), "dropped": int(np.isnan(self.latency).sum()),
+                "batch_device_ms": self.batch_stats(warmup),
                 "p50_ms": round(float(np.percentile(lat, 50)), 3) if len(lat) else None,
                 "p99_ms": round(float(np.percentile(lat, 99)), 3) if len(lat) else None,
                 "batches": self.batches, "quota_changes": self.changes, "distinct_placements": len(self.plans),
@@ -311,18 +343,42 @@ class Generator:
                                       if self.klc_log else None)}
 
 
-GRANULE = 32   # quota granularity of the dynamic policies: 4 CUs per XCD, few distinct masks
+GRANULE = 32   # default quota granularity of the dynamic policies: 4 CUs per XCD, few distinct masks
+PAIR_SPLITS = (32, 64, 96)   # CUs of the first instance of a pair in its 128-CU region
 
 
-def control_loop(policy, served, t0, horizon, period, stop, history):
+def pairs_of(served):
+    """(first, second) index pairs for the paired policy: each SLO-sensitive
+    instance with a best-effort one, in order; leftovers pair among themselves."""
+    slo = [i for i, s in enumerate(served) if s.slo]
+    other = [i for i, s in enumerate(served) if not s.slo]
+    pairs = list(zip(slo, other))
+    rest = slo[len(pairs):] + other[len(pairs):]
+    pairs += list(zip(rest[0::2], rest[1::2]))
+    return pairs
+
+
+def placements_disjoint(p, q, n_cu):
+    """Whether two (quota, first bit) runs of mask bits share no CU."""
+    bits = lambda r: {(r[1] + i) % n_cu for i in range(r[0])}
+    return not (bits(p) & bits(q))
+
+
+def paired_placement(n_cu, pair_idx, split, second):
+    """(quota, first bit) of one member of pair `pair_idx` at a given split."""
+    base = (128 * pair_idx) % n_cu
+    return (128 - split, base + split) if second else (split, base)
+
+
+def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRANULE):
     n_cu = ie.device_info(0)[0]
     ctl = None
     if policy == "alg2":
-        ctl = ie.Controller(max_tokens=n_cu, granule=GRANULE, min_quota=GRANULE)
+        ctl = ie.Controller(max_tokens=n_cu, granule=granule, min_quota=granule)
         for s in served:
             ctl.add(s.request, s.limit, s.slo)
     last_k = [s.kernels for s in served]
-    posted = [None] * len(served)
+    posted = [s.applied if policy == "paired" else None for s in served]
     while not stop.is_set():
         now = time.perf_counter() - t0
         if now > horizon:
@@ -338,14 +394,37 @@ def control_loop(policy, served, t0, horizon, period, stop, history):
         elif policy == "proportional":
             ql = np.array([max(s.queue_len(now), 0) for s in served], dtype=np.float64)
             share = np.full(len(served), 1.0 / len(served)) if ql.sum() == 0 else ql / ql.sum()
-            qs = np.maximum(GRANULE, np.floor(share * n_cu / GRANULE) * GRANULE).astype(int)
+            qs = np.maximum(granule, np.floor(share * n_cu / granule) * granule).astype(int)
             while qs.sum() > n_cu:
-                qs[int(np.argmax(qs))] -= GRANULE
+                qs[int(np.argmax(qs))] -= granule
             qs[int(np.argmax(share))] += n_cu - qs.sum()
             plan, first = [], 0
             for q in qs:
                 plan.append((int(q), first))
                 first = (first + int(q)) % n_cu
+        elif policy == "paired":
+            # Hand-over in order: a member may shrink at once, but it grows only
+            # onto CUs its partner has already left (the partner's current or
+            # last batch ran on `applied`; a quota change takes effect at a batch
+            # boundary, and a decoder batch runs for tens of ms).
+            plan = list(posted)
+            for pi, (a, b) in enumerate(pairs_of(served)):
+                la, lb = max(served[a].queue_len(now), 0), max(served[b].queue_len(now), 0)
+                share = 0.5 if la + lb == 0 else la / (la + lb)
+                split = min(PAIR_SPLITS, key=lambda sp: abs(sp / 128.0 - share))
+                want = {a: paired_placement(n_cu, pi, split, False), b: paired_placement(n_cu, pi, split, True)}
+                grow = [i for i in (a, b) if want[i][0] > posted[i][0]]
+                for i in (a, b):                # the shrinking (or unchanged) member: posted at once
+                    if i not in grow:
+                        plan[i] = want[i]
+                        with served[i].lock:
+                            served[i].pending = want[i]
+                for i in grow:                  # the growing one: once its partner has left the CUs
+                    other = b if i == a else a
+                    with served[other].lock:
+                        held, busy = served[other].applied, served[other].busy
+                    if not busy or placements_disjoint(want[i], held, n_cu):
+                        plan[i] = want[i]
         else:
             for i, s in enumerate(served):
                 with s.lock:
@@ -358,9 +437,13 @@ def control_loop(policy, served, t0, horizon, period, stop, history):
                 last_k[i] = k
             _, qs, firsts = ctl.issue()
             plan = list(zip(qs, firsts))
-        for i, (s, p) in enumerate(zip(served, plan)):
+        # shrinking instances first, so that none starts a batch on CUs just handed to another
+        order = sorted(range(len(served)), key=lambda i: plan[i][0] - (posted[i] or plan[i])[0])
+        for i in order:
+            s, p = served[i], plan[i]
             if p != posted[i]:
-                s.inst.prepare_quota(*p)       # hardware queue created here, not on the batch path
+                if policy != "paired":         # paired: every placement was prepared before the run
+                    s.inst.prepare_quota(*p)   # hardware queue created here, not on the batch path
                 posted[i] = p
             with s.lock:
                 s.pending = p
@@ -368,7 +451,26 @@ def control_loop(policy, served, t0, horizon, period, stop, history):
         time.sleep(period)
 
 
-def run_policy(policy, served, horizon, warmup, period):
+def prepare_paired(served):
+    """Prepares every placement the paired policy can issue, sizes each stream
+    cache to hold exactly them (the full-device stream is dropped), and starts
+    every instance on the even split."""
+    n_cu = ie.device_info(0)[0]
+    for pi, (a, b) in enumerate(pairs_of(served)):
+        for idx, second in ((a, False), (b, True)):
+            inst = served[idx].inst
+            inst.set_stream_cache(len(PAIR_SPLITS) + 1)
+            for sp in PAIR_SPLITS:
+                inst.prepare_quota(*paired_placement(n_cu, pi, sp, second))
+            start = paired_placement(n_cu, pi, 64, second)
+            inst.set_quota(*start)
+            served[idx].applied = start
+            inst.submit(served[idx].pool[:1])   # moves the instance onto its placement
+            inst.wait()
+            inst.set_stream_cache(len(PAIR_SPLITS))
+
+
+def run_policy(policy, served, horizon, warmup, period, granule=GRANULE):
     for s in served:
         s.reset(horizon)
         if isinstance(s, (Trainee, Generator)):
@@ -376,11 +478,13 @@ def run_policy(policy, served, horizon, warmup, period):
         else:
             s.inst.submit(s.pool[:1])          # warm the instance and its full-device stream
             s.inst.wait()
+    if policy == "paired":
+        prepare_paired(served)
     torch.cuda.synchronize()
     stop, history = threading.Event(), []
     t0 = time.perf_counter()
     threads = [threading.Thread(target=s.run, args=(t0, horizon, stop)) for s in served]
-    ctl = threading.Thread(target=control_loop, args=(policy, served, t0, horizon, period, stop, history))
+    ctl = threading.Thread(target=control_loop, args=(policy, served, t0, horizon, period, stop, history, granule))
     for t in threads + [ctl]:
         t.start()
     for t in threads:
@@ -389,7 +493,17 @@ def run_policy(policy, served, horizon, warmup, period):
     ctl.join()
     qs = np.array([h[1] for h in history]) if history else np.zeros((0, len(served)))
     states = [h[2] for h in history]
+    if policy == "paired":
+        for s in served:
+            s.inst.set_stream_cache(2)
+    lat = [s.latency[(s.arrivals >= warmup) & np.isfinite(s.latency)] * 1e3 for s in served
+           if isinstance(s, Served)]
+    allat = np.concatenate(lat) if lat else np.zeros(0)
+    aggregate = {"requests_s": round(len(allat) / max(horizon - warmup, 1e-9), 1),
+                 "p50_ms": round(float(np.percentile(allat, 50)), 3) if len(allat) else None,
+                 "p99_ms": round(float(np.percentile(allat, 99)), 3) if len(allat) else None}
     return {"policy": policy, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
+            "granule": granule if policy in ("proportional", "alg2") else None, "aggregate": aggregate,
             "instances": [s.stats(warmup, horizon) if isinstance(s, (Trainee, Generator)) else s.stats(warmup)
                           for s in served],
             "mean_quota": [round(float(v), 1) for v in qs.mean(0)] if len(qs) else None,
@@ -500,6 +614,7 @@ def main() -> int:
     ap.add_argument("--horizon", type=float, default=20.0)
     ap.add_argument("--warmup", type=float, default=2.0)
     ap.add_argument("--period-ms", type=float, default=20.0)
+    ap.add_argument("--granule", type=int, default=GRANULE, help="quota granularity (CUs) of proportional and alg2")
     ap.add_argument("--small", action="store_true", help="small models (quick functional run)")
     ap.add_argument("--mix", choices=["inference", "train", "decode"], default="inference",
                     help="inference: the four-instance serving mix; train: inference beside a training instance; "
@@ -520,7 +635,7 @@ def main() -> int:
         for pol in args.policy:
             name, _, per = pol.partition("@")          # "alg2@100": policy with its own period in ms
             period = float(per) if per else args.period_ms
-            res = run_policy(name, served, args.horizon, args.warmup, period / 1e3)
+            res = run_policy(name, served, args.horizon, args.warmup, period / 1e3, args.granule)
             print(json.dumps(res), flush=True)
     finally:
         for s in served:

@@ -195,6 +195,7 @@ def test_null_arguments():
     assert L.iefwd_set_quota_at(None, 8, 0) == ie.EINVAL
     assert L.iefwd_decode(None, None, 1, 0, 1) == ie.EINVAL
     assert L.iefwd_prepare_quota_at(None, 8, 0) == ie.EINVAL
+    assert L.iefwd_set_stream_cache(None, 2) == ie.EINVAL
     assert L.iefwd_submit(None, None, 1, 1, 0) == ie.EINVAL
     assert L.iefwd_wait(None) == ie.EINVAL
     assert L.iefwd_read_logits(None, None, 0, 0) == ie.EINVAL

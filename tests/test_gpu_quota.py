@@ -93,3 +93,30 @@ def test_prepare_from_another_thread():
             cus = observed_cus(inst.stream_handle())
             print(f"prepared quota {q} at {f}: first batch {ms:.2f} ms, {len(cus)} CUs", flush=True)
             assert len(cus) == q
+
+
+def test_stream_cache_capacity():
+    # a cache sized for a fixed set of placements: switching among them gives the
+    # same bits and the right masks; shrinking it keeps the stream in use
+    shape = W.model_shape("encoder_l1_d128_s32_b2")
+    x = W.make_input(7, 2, 32, 128)
+    with ie.Instance(**instance_config(shape, 2, 32)) as inst:
+        ref = run_instance(inst, x)
+        for bad in (0, 17):
+            with pytest.raises(ie.IefwdError) as e:
+                inst.set_stream_cache(bad)
+            assert e.value.status == ie.EINVAL
+        inst.set_stream_cache(4)
+        places = [(32, 0), (64, 32), (96, 96)]
+        for p in places:
+            inst.prepare_quota(*p)
+        for rep in range(2):
+            for q, f in places:
+                inst.set_quota(q, f)
+                got = run_instance(inst, x)
+                assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+                assert inst.get_cu_mask() == ie.build_cu_mask(256, 8, q, f)
+        inst.set_stream_cache(1)
+        got = run_instance(inst, x)
+        assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
+        assert inst.get_cu_mask() == ie.build_cu_mask(256, 8, 96, 96)

@@ -17,7 +17,7 @@ def served():
         x.inst.close()
 
 
-@pytest.mark.parametrize("policy", ["shared", "static", "proportional", "alg2"])
+@pytest.mark.parametrize("policy", ["shared", "static", "proportional", "alg2", "paired"])
 def test_policy_serves_every_request(served, policy):
     print(f"serve policy={policy}", flush=True)
     res = serve.run_policy(policy, served, horizon=1.5, warmup=0.2, period=0.01)
@@ -30,6 +30,13 @@ def test_policy_serves_every_request(served, policy):
     assert np.all((q >= 8) & (q <= 256))
     if policy == "alg2":
         assert sum(res["state_counts"].values()) == res["periods"]
+    if policy == "paired":
+        # quotas from the fixed vocabulary only: each instance uses at most the 3 placements of its pair
+        for st in res["instances"]:
+            assert st["distinct_placements"] <= 3, st
+        assert np.all((q >= 32) & (q <= 96))        # means of quotas in {32, 64, 96}
+    agg = res["aggregate"]
+    assert agg["requests_s"] > 0 and agg["p99_ms"] >= agg["p50_ms"] > 0
 
 
 def test_training_beside_inference():
