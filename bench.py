@@ -37,10 +37,11 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2516.6     # 256 CU x 4096 FLOP/clk x 2.4 GHz, dense bf16 MFMA
 WORKLOAD = "bert_base_l12_d768_s128"
-# HBM bytes per launch of the FFN-down kernel (FETCH_SIZE x 2.000 + WRITE_SIZE x 1.000 KiB,
-# factors from a 256 MiB device copy in the same runs), valid only for the GEMM source
-# and build flags they were counted on; any other source reports null.
-FFN2_TRAFFIC = {"source_sha256_16": "c90f012751a46252", "bytes": (37014.7 * 2.0 + 14028.3 * 1.0) * 1024}
+# Bytes per launch of the FFN-down kernel between the L2s and the memory side (FETCH_SIZE x
+# 2.000 + WRITE_SIZE x 1.000 KiB, factors from a 256 MiB device copy in the same runs): L2
+# misses, which the 256 MB MALL may serve without touching HBM.  Valid only for the GEMM
+# source and build flags they were counted on; any other source reports null.
+FFN2_TRAFFIC = {"source_sha256_16": "ced883f3aca9b4c9", "bytes": (37100.5 * 2.0 + 13388.4 * 1.0) * 1024}
 GEMM_SOURCES = ("paper_2503_05130_amd/csrc/gemm.hip", "paper_2503_05130_amd/csrc/gemm.h",
                 "paper_2503_05130_amd/csrc/launch.h", "paper_2503_05130_amd/csrc/gelu.h",
                 "paper_2503_05130_amd/build.py")
@@ -63,6 +64,21 @@ def forward_flops(L, d, F, H, S, n_out, causal=False):
     return L * (gemm + attn) + 2 * S * d * n_out
 
 
+def host_info(blas) -> dict:
+    """nproc, CPU model and the BLAS library NumPy calls (threadpoolctl's view)."""
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"nproc": len(os.sched_getaffinity(0)), "cpu_count": os.cpu_count(), "cpu_model": model,
+            "blas": [{"api": p.get("internal_api"), "version": p.get("version"), "threads": p.get("num_threads"),
+                      "library": os.path.basename(p.get("filepath", ""))} for p in blas]}
+
+
 def cpu_baseline(shape, batch_sample: int):
     """The fp64 oracle on `batch_sample` sequences of the same workload."""
     from threadpoolctl import threadpool_info
@@ -78,12 +94,55 @@ def cpu_baseline(shape, batch_sample: int):
     t0 = time.perf_counter()
     F.forward_with(x, shape, lambda l: layers[l], glob)
     dt = time.perf_counter() - t0
-    threads = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("internal_api") == "openblas"]
-                  or [os.cpu_count() or 1])
+    blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+    threads = max([p.get("num_threads", 1) for p in blas] or [os.cpu_count() or 1])
     return {"value": round(batch_sample / dt, 4), "unit": "inferences/s", "cores": int(threads),
-            "kind": "oracle",
+            "kind": "oracle", "host": host_info(blas),
             "sample": f"{batch_sample} sequences of the same workload (seq 128), NumPy fp64 forward, "
                       f"weights pre-generated; {dt:.2f} s"}
+
+
+def oracle_timing() -> dict:
+    """The fp64 oracle timed on this host's cores on every workload of the
+    plan: the single-layer encoder (batch 2), BERT-base at batch 1 / 8 / 32
+    (median of 3 runs), the RoBERTa-large-sized causal decoder at batch 8 and
+    the d = 2048 decoder at batch 2 (one run each), plus single-thread runs of
+    the two smallest.  Weights are generated before the clock starts; inputs
+    are the workloads' seeded inputs.  inferences/s = batch / wall time."""
+    import statistics
+
+    from threadpoolctl import threadpool_info, threadpool_limits
+
+    import workloads as W
+    from oracle import forward as F
+    from oracle import init_spec as I
+
+    plan = [("encoder_l1_d128_s32_b2", 2, 3, None), ("encoder_l1_d128_s32_b2", 2, 3, 1),
+            ("bert_base_l12_d768_s128", 1, 3, None), ("bert_base_l12_d768_s128", 1, 3, 1),
+            ("bert_base_l12_d768_s128", 8, 3, None), ("bert_base_l12_d768_s128", 32, 3, None),
+            ("decoder_l24_d1024_s512", 8, 1, None), ("decoder_l24_d2048_s1024", 2, 1, None)]
+    rows, weights = [], {}
+    for name, batch, runs, threads in plan:
+        shape = W.model_shape(name)
+        w = W.WORKLOADS[name]
+        if name not in weights:
+            weights.clear()
+            weights[name] = ([I.layer_weights(shape, l) for l in range(shape["n_layers"])], I.global_weights(shape))
+        layers, glob = weights[name]
+        x = W.make_input(w["input_seed"], batch, w["seq"], shape["d_model"])
+        times = []
+        with threadpool_limits(limits=threads):
+            used = max([p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"] or [1])
+            for _ in range(runs):
+                t0 = time.perf_counter()
+                F.forward_with(x, shape, lambda l: layers[l], glob)
+                times.append(time.perf_counter() - t0)
+        t = statistics.median(times)
+        rows.append({"workload": name, "batch": batch, "blas_threads": used, "runs": runs,
+                     "seconds": round(t, 3), "inferences_s": round(batch / t, 4)})
+        print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
+    blas = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+    return {"kind": "oracle", "host": host_info(blas), "rows": rows}
 
 
 def colocated(ie, W, shape, cfg, quota_pairs, batch=8, window_s=1.0):
@@ -420,6 +479,65 @@ def copy_calibration(mib: int) -> None:
     torch.cuda.synchronize()
 
 
+def start_clock_sampler(path: str):
+    """Starts `amd-smi metric --clock` in a loop (each sample preceded by a
+    wall-clock timestamp) as a child process.  Called before this process
+    touches the GPU, so no process that holds a GPU context starts another
+    program.  Returns the Popen handle, or None if amd-smi is unavailable or a
+    profiler is attached (its preloaded library initialises the GPU first)."""
+    import shutil
+    import subprocess
+
+    if any(k.startswith("ROCPROF") for k in os.environ) or not shutil.which("amd-smi"):
+        return None
+    loop = "while :; do date +%s.%N; amd-smi metric --clock; sleep 0.05; done"
+    return subprocess.Popen(["bash", "-c", loop], stdout=open(path, "w"), stderr=subprocess.DEVNULL,
+                            start_new_session=True)
+
+
+def stop_clock_sampler(proc, path: str, t0: float, t1: float):
+    """Stops the sampler and returns the mean GFX clock (MHz, over all XCDs and
+    the samples taken between t0 and t1 on the wall clock) and the sample count."""
+    import re
+    import signal
+
+    try:
+        os.killpg(proc.pid, signal.SIGTERM)
+    except ProcessLookupError:
+        pass
+    proc.wait(timeout=10)
+    text = open(path).read()
+    blocks = re.split(r"^(\d+\.\d+)\s*$", text, flags=re.M)
+    means = []
+    for i in range(1, len(blocks) - 1, 2):
+        ts = float(blocks[i])
+        vals = [float(v) for v in re.findall(r"GFX_\d+:\s*\n\s*CLK:\s*([\d.]+)\s*MHz", blocks[i + 1])]
+        if t0 <= ts <= t1 and vals:
+            means.append(sum(vals) / len(vals))
+    if not means:
+        return None, 0
+    return sum(means) / len(means), len(means)
+
+
+def clock_leg(inst, x, sampler, path: str, seconds: float = 3.0):
+    """Mean shader clock while the same forward runs back to back for `seconds`."""
+    import torch
+
+    end = time.time() + seconds
+    t0 = time.time() + 0.3          # skip the first samples while clocks ramp
+    n = 0
+    while time.time() < end:
+        inst.submit(x)
+        inst.wait()
+        n += 1
+    torch.cuda.synchronize()
+    t1 = time.time()
+    mhz, samples = stop_clock_sampler(sampler, path, t0, t1)
+    return {"method": "amd-smi metric --clock sampled while the forward runs back to back "
+                      f"({n} batches, {seconds:.0f} s), mean over XCDs and samples",
+            "sclk_mhz": round(mhz, 1) if mhz else None, "samples": samples}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -444,7 +562,13 @@ def main() -> int:
                     help="time only the decode phase (a profiling aid: prints {\"decode\": ...})")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="first run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--no-clock", action="store_true", help="skip the measured shader clock leg")
+    ap.add_argument("--oracle-timing", action="store_true",
+                    help="time only the fp64 oracle on every workload (CPU; prints {\"oracle_timing\": ...})")
     args = ap.parse_args()
+    if args.oracle_timing:
+        print(json.dumps({"oracle_timing": oracle_timing()}))
+        return 0
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (the instances of this workload share one MI355X); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
@@ -453,6 +577,12 @@ def main() -> int:
     if args.timer_every < 1:
         print("--timer-every must be >= 1", file=sys.stderr)
         return 2
+
+    clock_path = os.path.join(ROOT, "gpurun_out", "bench_sclk_samples.txt")
+    sampler = None
+    if not (args.no_clock or args.decode_only or args.train_only):
+        os.makedirs(os.path.dirname(clock_path), exist_ok=True)
+        sampler = start_clock_sampler(clock_path)   # before anything touches the GPU
 
     import torch
 
@@ -520,6 +650,7 @@ def main() -> int:
             "frac": round(achieved / peak, 4),
             "traffic": (round(FFN2_TRAFFIC["bytes"]) if gemm_source_hash() == FFN2_TRAFFIC["source_sha256_16"]
                         else None),
+            "traffic_level": "L2 <-> memory side (FETCH_SIZE + WRITE_SIZE): L2 misses, possibly MALL hits",
             "kernel": "FFN-down GEMM + bias + LayerNorm residual", "avg_us": round(k_avg_s * 1e6, 2), "launches": k_launches,
             "timed_batches": f"every {args.timer_every}th of the {args.steps} timed batches"}
 
@@ -541,6 +672,13 @@ def main() -> int:
         "mfma_util_pct": round(mfma_util, 2),
         "roofline": roof,
     }
+    if sampler is not None:
+        clk = clock_leg(inst, x, sampler, clock_path)
+        if clk["sclk_mhz"]:
+            # the same utilisation against the peak at the clock the chip actually ran
+            clk["mfma_util_pct_at_sclk"] = round(mfma_util * 2400.0 / clk["sclk_mhz"], 2)
+            clk["ffn_down_frac_at_sclk"] = round(roof["frac"] * 2400.0 / clk["sclk_mhz"], 4)
+        result["clock"] = clk
     if not args.no_remask:
         result["remask"] = remask_overhead(inst, x)
     if not args.no_quota_sweep:
