@@ -5,7 +5,7 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
 
   python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 static proportional shared paired]
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--granule 32] [--small]
-                                       [--mix inference|train|decode]
+                                       [--mix inference|train|decode] [--queue-probe]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
 batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
@@ -608,6 +608,87 @@ def run_decode_mix(policies, horizon, warmup, period, small=False):
     return out, summary
 
 
+def queue_probe(seconds: float = 3.0) -> list:
+    """What a quota switch costs co-located instances on this chip: four
+    BERT-base-shaped instances (batch 4, one host thread each, disjoint
+    64-CU placements) run back-to-back batches while one of these happens:
+      fixed    nothing (the reference);
+      switch   each instance alternates between two prepared masks every batch;
+      churn    a fifth instance creates (and its cache evicts) a masked queue
+               every 20 ms;
+      idle+N   N more masked queues exist (idle instances' prepared masks).
+    Reports each phase's per-batch device time."""
+    n_cu = ie.device_info(0)[0]
+    insts = [ie.Instance(device=0, max_batch=4, max_seq=128, seed=51 + i, **BERT) for i in range(4)]
+    spare = ie.Instance(device=0, max_batch=1, max_seq=128, seed=60, **BERT)
+    x = torch.from_numpy(np.random.default_rng(7).standard_normal((4, 128, 768), dtype=np.float32)).to("cuda:0")
+    for i, inst in enumerate(insts):
+        inst.prepare_quota(64, 64 * i)
+        inst.prepare_quota(32, 64 * i)
+        inst.set_quota(64, 64 * i)
+        inst.submit(x)
+        inst.wait()
+    torch.cuda.synchronize()
+    rows, extra = [], []
+
+    def phase(name, switch=False, churn=False):
+        stop = threading.Event()
+        times = [[] for _ in insts]
+
+        def drive(i):
+            k = 0
+            while not stop.is_set():
+                if switch:
+                    insts[i].set_quota(64 if k % 2 == 0 else 32, 64 * i)
+                insts[i].submit(x)
+                insts[i].wait()
+                times[i].append(insts[i].last_batch_ms())
+                k += 1
+
+        def churner():
+            j = 0
+            while not stop.is_set():
+                spare.prepare_quota(8 + 8 * (j % 24), (8 * j) % n_cu)   # a never-seen placement each time
+                j += 1
+                time.sleep(0.02)
+
+        ths = [threading.Thread(target=drive, args=(i,)) for i in range(len(insts))]
+        if churn:
+            ths.append(threading.Thread(target=churner))
+        for t in ths:
+            t.start()
+        time.sleep(seconds)
+        stop.set()
+        for t in ths:
+            t.join()
+        allt = np.concatenate([np.array(t[3:]) for t in times])
+        med = float(np.median(allt))
+        rows.append({"phase": name, "batches": int(len(allt)), "p50_ms": round(med, 3),
+                     "p99_ms": round(float(np.percentile(allt, 99)), 3), "max_ms": round(float(allt.max()), 3),
+                     "over_5x_median": int((allt > 5 * med).sum())})
+        print(json.dumps(rows[-1]), flush=True)
+
+    small = dict(n_layers=1, d_model=128, n_heads=2, d_ff=512, pre_ln=0, causal=0, n_out=0)
+    try:
+        phase("fixed")
+        phase("switch", switch=True)
+        for i, inst in enumerate(insts):
+            inst.set_quota(64, 64 * i)
+        phase("churn", churn=True)
+        for n in (8, 16, 24):
+            while 2 * len(extra) < n:
+                k = len(extra)
+                e = ie.Instance(device=0, max_batch=1, max_seq=32, seed=70 + k, **small)
+                e.prepare_quota(8 + 8 * (k % 8), (32 * k) % n_cu)
+                e.prepare_quota(16 + 8 * (k % 8), (32 * k + 8) % n_cu)
+                extra.append(e)
+            phase(f"idle+{n}")
+    finally:
+        for inst in insts + [spare] + extra:
+            inst.close()
+    return rows
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--policy", nargs="+", default=["shared", "static", "proportional", "alg2"])
@@ -619,7 +700,12 @@ def main() -> int:
     ap.add_argument("--mix", choices=["inference", "train", "decode"], default="inference",
                     help="inference: the four-instance serving mix; train: inference beside a training instance; "
                          "decode: inference beside a token-by-token decoder")
+    ap.add_argument("--queue-probe", action="store_true",
+                    help="measure what creating, switching and keeping masked queues costs co-located instances")
     args = ap.parse_args()
+    if args.queue_probe:
+        queue_probe()
+        return 0
     if args.mix == "train":
         run_train_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small)
         return 0
