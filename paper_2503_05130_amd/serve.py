@@ -609,27 +609,31 @@ def run_decode_mix(policies, horizon, warmup, period, small=False):
 
 
 def queue_probe(seconds: float = 3.0) -> list:
-    """What a quota switch costs co-located instances on this chip: four
-    BERT-base-shaped instances (batch 4, one host thread each, disjoint
-    64-CU placements) run back-to-back batches while one of these happens:
+    """What quota switches and masked queues cost co-located instances on this
+    chip: four BERT-base-shaped instances (batch 4, one host thread each, on
+    disjoint 32-CU placements, two prepared each) run back-to-back batches
+    while one of these happens:
       fixed    nothing (the reference);
-      switch   each instance alternates between two prepared masks every batch;
-      churn    a fifth instance creates (and its cache evicts) a masked queue
-               every 20 ms;
+      switch   each instance alternates between its two prepared placements
+               (same size, disjoint) every batch;
+      churn    a fifth instance creates a masked queue for a never-seen
+               placement every 20 ms (its cache of 2 evicts one each time);
       idle+N   N more masked queues exist (idle instances' prepared masks).
-    Reports each phase's per-batch device time."""
+    Reports each phase's per-batch device time and how many masked queues the
+    process holds."""
     n_cu = ie.device_info(0)[0]
     insts = [ie.Instance(device=0, max_batch=4, max_seq=128, seed=51 + i, **BERT) for i in range(4)]
     spare = ie.Instance(device=0, max_batch=1, max_seq=128, seed=60, **BERT)
     x = torch.from_numpy(np.random.default_rng(7).standard_normal((4, 128, 768), dtype=np.float32)).to("cuda:0")
-    for i, inst in enumerate(insts):
-        inst.prepare_quota(64, 64 * i)
-        inst.prepare_quota(32, 64 * i)
-        inst.set_quota(64, 64 * i)
+    places = [((32, 64 * i), (32, 64 * i + 32)) for i in range(len(insts))]
+    for inst, (p0, p1) in zip(insts, places):
+        inst.prepare_quota(*p1)
+        inst.set_quota(*p0)
         inst.submit(x)
         inst.wait()
     torch.cuda.synchronize()
     rows, extra = [], []
+    held = {"insts": 2 * len(insts), "spare": 0, "extra": 0}
 
     def phase(name, switch=False, churn=False):
         stop = threading.Event()
@@ -639,7 +643,7 @@ def queue_probe(seconds: float = 3.0) -> list:
             k = 0
             while not stop.is_set():
                 if switch:
-                    insts[i].set_quota(64 if k % 2 == 0 else 32, 64 * i)
+                    insts[i].set_quota(*places[i][k % 2])
                 insts[i].submit(x)
                 insts[i].wait()
                 times[i].append(insts[i].last_batch_ms())
@@ -661,27 +665,32 @@ def queue_probe(seconds: float = 3.0) -> list:
         stop.set()
         for t in ths:
             t.join()
+        if churn:
+            held["spare"] = 2
         allt = np.concatenate([np.array(t[3:]) for t in times])
         med = float(np.median(allt))
-        rows.append({"phase": name, "batches": int(len(allt)), "p50_ms": round(med, 3),
-                     "p99_ms": round(float(np.percentile(allt, 99)), 3), "max_ms": round(float(allt.max()), 3),
-                     "over_5x_median": int((allt > 5 * med).sum())})
+        rows.append({"phase": name, "masked_queues": sum(held.values()), "batches": int(len(allt)),
+                     "p50_ms": round(med, 3), "p99_ms": round(float(np.percentile(allt, 99)), 3),
+                     "max_ms": round(float(allt.max()), 3), "over_5x_median": int((allt > 5 * med).sum())})
         print(json.dumps(rows[-1]), flush=True)
 
     small = dict(n_layers=1, d_model=128, n_heads=2, d_ff=512, pre_ln=0, causal=0, n_out=0)
     try:
         phase("fixed")
         phase("switch", switch=True)
-        for i, inst in enumerate(insts):
-            inst.set_quota(64, 64 * i)
+        for inst, (p0, _) in zip(insts, places):
+            inst.set_quota(*p0)
         phase("churn", churn=True)
-        for n in (8, 16, 24):
+        spare.close()
+        held["spare"] = 0
+        for n in (4, 8, 12, 16, 24):
             while 2 * len(extra) < n:
                 k = len(extra)
                 e = ie.Instance(device=0, max_batch=1, max_seq=32, seed=70 + k, **small)
                 e.prepare_quota(8 + 8 * (k % 8), (32 * k) % n_cu)
                 e.prepare_quota(16 + 8 * (k % 8), (32 * k + 8) % n_cu)
                 extra.append(e)
+            held["extra"] = 2 * len(extra)
             phase(f"idle+{n}")
     finally:
         for inst in insts + [spare] + extra:
