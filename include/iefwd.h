@@ -438,6 +438,34 @@ int iefwd_test_gemm_skinny(uint32_t epilogue, const void *a, const void *w, cons
                            const float *ln_z, const float *ln_gamma, const float *ln_beta, float ln_eps,
                            void *stream);
 
+/* The packed weight layout of the decode-step product (Sec. 3.4.1 footnote:
+ * an inference iteration is one batch; a decode iteration reads every weight
+ * once).  dst (N * K bf16, caller-owned, device) = W [N, K] rearranged for
+ * `groups` K-groups (1, 2 or 4; N % (16 / groups) == 0, K % (32 * groups) ==
+ * 0): 16-byte piece i of dst holds W[f][k .. k + 7] with
+ *   i = (b * steps + s) * 64 + l,  steps = K / (32 groups),
+ *   r = l % 16, c = l / 16, f = b * (16 / groups) + r % (16 / groups),
+ *   k = (r / (16 / groups)) * (K / groups) + 32 s + 8 c,
+ * so that each wave load instruction of the product reads 1 KB of
+ * consecutive addresses.  Instances created with kv_cache = 1 keep such a copy
+ * of their four matrices per layer. */
+int iefwd_test_skinny_pack(const void *w, void *dst, uint32_t N, uint32_t K, uint32_t groups, void *stream);
+
+/* iefwd_test_gemm_skinny on the packed copy (iefwd_test_skinny_pack) of W
+ * instead of W itself; `groups` must be the K-group count the product uses
+ * for (M, N, K) with or without the LayerNorm prologue
+ * (iefwd_test_skinny_groups), else EINVAL.  Results equal
+ * iefwd_test_gemm_skinny's bit for bit. */
+int iefwd_test_gemm_skinny_packed(uint32_t epilogue, const void *a, const void *w_packed, uint32_t groups,
+                                  const void *bias, const float *resid, void *out, uint32_t M, uint32_t N, uint32_t K,
+                                  const float *ln_z, const float *ln_gamma, const float *ln_beta, float ln_eps,
+                                  void *stream);
+
+/* The K-group count (1, 2 or 4) of the decode-step product for M rows,
+ * N % 16 == 0 and K % 32 == 0, with (ln != 0) or without the LayerNorm
+ * prologue.  Host only. */
+int iefwd_test_skinny_groups(uint32_t M, uint32_t N, uint32_t K, int ln, uint32_t *groups);
+
 /* QKV projection with head scatter: A bf16 [batch*seq, d], W bf16 [3d, d],
  * bias bf16 [3d].  Writes Q and K as bf16 [batch, heads, seq, dh] and V
  * transposed as bf16 [batch, heads, dh, seq_pad], seq_pad = seq rounded up to

@@ -72,6 +72,10 @@ SIGNATURES = {
     "iefwd_test_gemm_plan": (_i32, [_u32, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32), ctypes.POINTER(_u32),
                                      ctypes.POINTER(_u32), ctypes.POINTER(_u32)]),
     "iefwd_test_gemm_skinny": (_i32, [_u32, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp, _vp, _vp, _f32, _vp]),
+    "iefwd_test_skinny_pack": (_i32, [_vp, _vp, _u32, _u32, _u32, _vp]),
+    "iefwd_test_gemm_skinny_packed": (_i32, [_u32, _vp, _vp, _u32, _vp, _vp, _vp, _u32, _u32, _u32, _vp, _vp, _vp,
+                                             _f32, _vp]),
+    "iefwd_test_skinny_groups": (_i32, [_u32, _u32, _u32, _i32, ctypes.POINTER(_u32)]),
     "iefwd_test_gemm_qkv": (_i32, [_vp, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _vp]),
     "iefwd_test_attention": (_i32, [_vp, _vp, _vp, _vp, _u32, _u32, _u32, _u32, _i32, _vp]),
     "iefwd_test_layernorm": (_i32, [_vp, _vp, _vp, _vp, _vp, _u32, _u32, _f32, _vp]),
@@ -324,6 +328,26 @@ def test_gemm_skinny(epilogue, a, w, bias, resid, out, M, N, K, ln=None, stream=
     z, g, b, eps = ln if ln is not None else (None, None, None, 0.0)
     _check(lib().iefwd_test_gemm_skinny(epilogue, _ptr(a), _ptr(w), _ptr(bias), _ptr(resid), _ptr(out), M, N, K,
                                         _ptr(z), _ptr(g), _ptr(b), eps, _stream(stream)), "iefwd_test_gemm_skinny")
+
+
+def test_skinny_pack(w, dst, N, K, groups, stream=None) -> None:
+    """dst (N * K bf16, device) = W [N, K] in the decode product's packed layout for `groups` K-groups."""
+    _check(lib().iefwd_test_skinny_pack(_ptr(w), _ptr(dst), N, K, groups, _stream(stream)), "iefwd_test_skinny_pack")
+
+
+def test_gemm_skinny_packed(epilogue, a, w_packed, groups, bias, resid, out, M, N, K, ln=None, stream=None) -> None:
+    """test_gemm_skinny reading the packed copy of W (test_skinny_pack)."""
+    z, g, b, eps = ln if ln is not None else (None, None, None, 0.0)
+    _check(lib().iefwd_test_gemm_skinny_packed(epilogue, _ptr(a), _ptr(w_packed), groups, _ptr(bias), _ptr(resid),
+                                               _ptr(out), M, N, K, _ptr(z), _ptr(g), _ptr(b), eps, _stream(stream)),
+           "iefwd_test_gemm_skinny_packed")
+
+
+def test_skinny_groups(M, N, K, ln) -> int:
+    """The K-group count the decode product uses for (M, N, K), with or without the LayerNorm prologue."""
+    g = _u32()
+    _check(lib().iefwd_test_skinny_groups(M, N, K, 1 if ln else 0, ctypes.byref(g)), "iefwd_test_skinny_groups")
+    return g.value
 
 
 def test_gemm_qkv(a, w, bias, q, k, vt, batch, seq, d_model, n_heads, stream=None) -> None:

@@ -104,13 +104,21 @@ __global__ __launch_bounds__(kThreads) void decode_attention_kernel(
         }
     }
 
-    // 1. scores: all loads first (rows past n_keys are clamped to the last key: read, never used)
+    // 1. scores: all loads first (rows past n_keys are clamped to the last key:
+    // read, never used), and with them the V^T rows of step 3, which depend on
+    // nothing computed here: one memory round trip for the whole chunk
     u32x4 kr[NLOAD];
 #pragma unroll
     for (int i = 0; i < NLOAD; ++i) {
         const int j = min(j0 + i * KPI + tid / LPK, n_keys - 1);
         kr[i] = *reinterpret_cast<const u32x4 *>(Kh + (size_t)j * DH + part * 8);
     }
+    const int r_in = tid / LPR, kk = (tid % LPR) * 8;
+    const int kread = min(j0 + kk, vt_stride - 8);    // 16-byte aligned, inside the row; masked below
+    u32x4 vr[DH / RPP];
+#pragma unroll
+    for (int i = 0; i < DH / RPP; ++i)
+        vr[i] = *reinterpret_cast<const u32x4 *>(Vh + (size_t)(i * RPP + r_in) * vt_stride + kread);
     float mx = -INFINITY;
 #pragma unroll
     for (int i = 0; i < NLOAD; ++i) {
@@ -145,15 +153,9 @@ __global__ __launch_bounds__(kThreads) void decode_attention_kernel(
     for (int w = 0; w < kWaves; ++w) l += red[kWaves + w];
 
     // 3. the chunk's context: RPP rows of V^T per pass, LPR lanes x 8 keys per row
-    const int r_in = tid / LPR, kk = (tid % LPR) * 8;
     float pk[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) pk[e] = kk + e < nk ? sc[kk + e] : 0.f;
-    const int kread = min(j0 + kk, vt_stride - 8);    // 16-byte aligned, inside the row; masked below
-    u32x4 vr[DH / RPP];
-#pragma unroll
-    for (int i = 0; i < DH / RPP; ++i)
-        vr[i] = *reinterpret_cast<const u32x4 *>(Vh + (size_t)(i * RPP + r_in) * vt_stride + kread);
     const bool single = n_chunks == 1;
     float *slot = partials + ((size_t)bh * n_chunks + chunk) * SLOT;
     const float inv_l = 1.0f / l;
@@ -182,7 +184,8 @@ __global__ __launch_bounds__(kThreads) void decode_attention_kernel(
 }
 
 // 4. one workgroup of DH threads per (batch, head): the chunks' weights from
-// their maxima, then every context element summed over the chunks in order
+// their maxima, then every context element summed over the chunks in order.
+// Every partial this thread needs is requested before the first is used.
 template <int DH>
 __global__ __launch_bounds__(DH) void decode_combine_kernel(const float *__restrict__ partials,
                                                             bf16_t *__restrict__ ctx, int n_chunks) {
@@ -191,6 +194,10 @@ __global__ __launch_bounds__(DH) void decode_combine_kernel(const float *__restr
     __shared__ float lsum;
     const int tid = threadIdx.x, bh = blockIdx.x;
     const float *slots = partials + (size_t)bh * n_chunks * SLOT;
+    float part[kDecodeMaxChunks];
+#pragma unroll
+    for (int c = 0; c < kDecodeMaxChunks; ++c)
+        part[c] = slots[min(c, n_chunks - 1) * SLOT + 2 + tid];   // clamped: past n_chunks never used
     if (tid < 64) {
         const bool has = tid < n_chunks;
         const float m = has ? slots[tid * SLOT] : -INFINITY;
@@ -202,7 +209,9 @@ __global__ __launch_bounds__(DH) void decode_combine_kernel(const float *__restr
     }
     __syncthreads();
     float acc = 0.f;
-    for (int c = 0; c < n_chunks; ++c) acc = fmaf(wc[c], slots[c * SLOT + 2 + tid], acc);
+#pragma unroll
+    for (int c = 0; c < kDecodeMaxChunks; ++c)
+        if (c < n_chunks) acc = fmaf(wc[c], part[c], acc);
     ctx[(size_t)bh * DH + tid] = to_bf16_bits(acc / lsum);
 }
 

@@ -78,11 +78,19 @@ struct LnIn {
 // N % 16 == 0, K % 32 == 0; every epilogue but BiasLnResidF32.  Its K
 // summation order differs from launch_gemm's (the two agree within rounding).
 // With ln_in the activations are LayerNorm(z), normalised in the kernel (then
-// `a` is unused); that needs skinny_ln_fits(M, K).
+// `a` is unused); that needs skinny_ln_fits(M, K).  w_packed: W's packed copy
+// for packed_groups K-groups (launch_skinny_pack), read instead of w when the
+// product uses that many groups for this M (bit-identical results, faster).
 hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias,
                               const float *resid, void *out, int M, int N, int K, const QkvDst *qkv,
-                              hipStream_t stream, const LnIn *ln_in = nullptr);
+                              hipStream_t stream, const LnIn *ln_in = nullptr, const bf16_t *w_packed = nullptr,
+                              int packed_groups = 0);
 bool skinny_ln_fits(int M, int K);
+// Writes dst (N * K bf16) = W [N, K] rearranged for the skinny product with
+// `groups` K-groups: each 1 KB block holds one workgroup's fragment of one
+// 32-wide K step in lane order.  Needs N % (16 / groups) == 0 and
+// K % (32 * groups) == 0.
+hipError_t launch_skinny_pack(const bf16_t *w, bf16_t *dst, int N, int K, int groups, hipStream_t stream);
 // K-groups per MFMA the skinny product uses for this shape (1, 2 or 4), with
 // or without the LayerNorm prologue; its summation order depends on K and
 // this number.

@@ -91,10 +91,28 @@ __device__ inline uint32_t pack2(float lo, float hi) {
     return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
 }
 
+template <int CTRL>
+__device__ inline float dpp_move(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xf, 0xf, false));
+}
+
+// Sum over the wave's 64 lanes, the same value in every lane, in a fixed
+// order: lane pairs and pairs of pairs within each quad (DPP quad permutes
+// [1,0,3,2] and [2,3,0,1]), quads within each half row (row_half_mirror),
+// halves within each row of 16 (row_mirror), then the four row sums as
+// (r0 + r1) + (r2 + r3).  Each partner exchange adds the same two values in
+// both lanes, so every lane of a group holds bitwise the same sum.
 __device__ inline float wave_sum(float v) {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-    return v;
+    v += dpp_move<0xB1>(v);
+    v += dpp_move<0x4E>(v);
+    v += dpp_move<0x141>(v);
+    v += dpp_move<0x140>(v);
+    const int b = __builtin_bit_cast(int, v);
+    const float r0 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 0));
+    const float r1 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 16));
+    const float r2 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 32));
+    const float r3 = __builtin_bit_cast(float, __builtin_amdgcn_readlane(b, 48));
+    return (r0 + r1) + (r2 + r3);
 }
 
 // 16-byte chunk position of logical chunk 0 in LDS row r of a BK-wide K tile
@@ -640,7 +658,7 @@ hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
 // fit the chip at once.  The waves split the K steps (wave w takes w, w + 8,
 // ...); each lane loads its weight and activation fragments straight into
 // registers (16 bytes each; token columns past M repeat the last row and are
-// never stored), 8 K steps deep.  The waves' partial sums are added in wave order through
+// never stored), as many K steps deep as the wave has, up to 8.  The waves' partial sums are added in wave order through
 // LDS, then the K-groups in group order through lane shuffles: the summation
 // order depends on K and G only.
 //
@@ -648,15 +666,28 @@ hipError_t launch_tile(Epi epi, GemmParams &p, hipStream_t s) {
 // (a pre-LN block's input), normalised by the workgroup itself into LDS as
 // bf16 while the first weight fragments are already in flight.  Needs
 // M * K <= kSkinnyLnElems and K <= 4096.
+//
+// Weights come either row-major ([N, K]: one load instruction covers 16 rows
+// x 64 bytes) or packed (FRAG): a copy of W in which the 64 lanes' 16-byte
+// pieces of one (workgroup, K step) fragment are one contiguous 1 KB block,
+// in lane order, blocks ordered by workgroup then K step.  A load instruction
+// then reads 1 KB of consecutive addresses, which streams from HBM at the
+// rate of a plain copy; the fragments, the MFMAs and the summation order are
+// the same in both forms, so the results are bit-identical.  The packed copy
+// is specific to one K-group count G (skinny_pack).  The epilogue's operands
+// (bias, residual rows) and, without the LayerNorm prologue, the activations
+// are requested before the weights, so that no load is left to start after
+// the weight stream has ended.
 constexpr int kSkinnyWaves = 8, kSkinnyUnroll = 8;
 constexpr int kSkinnyLnElems = 16384;
 constexpr int kSkinnyCus = 256;              // MI355X compute units
 
 // One wave per row (rows w and w + 8 for wave w), the row held in registers
-// (lane l owns the f32x4 vectors l + 64 c).  load() issues the first row and
-// this thread's share of gamma and beta -- before the weight fragments, so
-// that they are not queued behind them; finish() stages gamma and beta in LDS,
-// takes mean and rstd two-pass over the registers with a fixed butterfly and
+// (lane l owns the f32x4 vectors l + 64 c).  load() issues the wave's first
+// row (waves past the last row load none) and this thread's share of gamma
+// and beta -- before the weight fragments, so that they are not queued behind
+// them; finish() stages gamma and beta in LDS,
+// takes mean and rstd two-pass over the registers with a fixed reduction tree (wave_sum) and
 // writes y = fma(gamma, (z - mean) * rstd, beta), rounded to bf16, into the
 // activation tile.  NVL = K / 256 rounded up to 8 or 16 (K <= 4096).
 // finish() contains one barrier, reached by every wave.
@@ -666,8 +697,9 @@ struct SkinnyLn {
     f32x4 v[NVL];
     f32x4 g[GBV], b[GBV];
 
-    // Unconditional loads (indices clamped into the row; the extra vectors are
-    // never used), so that the wait for them does not wait for the weights.
+    // Every vector of the row is loaded (indices clamped into the row; the
+    // extra vectors are never used), so that the wait for them does not wait
+    // for the weights.
     __device__ void load_row(const GemmParams &p, int r, int lane) {
         const f32x4 *zr = reinterpret_cast<const f32x4 *>(p.lnin.z + (size_t)r * p.K);
 #pragma unroll
@@ -681,7 +713,7 @@ struct SkinnyLn {
             g[j] = reinterpret_cast<const f32x4 *>(p.lnin.gamma)[i];
             b[j] = reinterpret_cast<const f32x4 *>(p.lnin.beta)[i];
         }
-        load_row(p, min(wave, p.M - 1), lane);
+        if (wave < p.M) load_row(p, wave, lane);
     }
 
     __device__ void finish(const GemmParams &p, bf16_t *a_lds, float *gb_lds, int tid, int lane, int wave) {
@@ -714,17 +746,29 @@ struct SkinnyLn {
                     }
             rstd = 1.0f / sqrtf(wave_sum(ss) * inv_k + p.lnin.eps);
         };
+        // gamma and beta of two vectors read before either is used (indices
+        // clamped: unused past the row)
         auto emit = [&](int r) {
 #pragma unroll
-            for (int c = 0; c < NVL; ++c) {
-                const int i = c * 64 + lane;
-                if (i < nv) {
-                    const f32x4 gg = g_l[i], bb = b_l[i];
-                    float y[4];
+            for (int c = 0; c < NVL; c += 2) {
+                f32x4 gg[2], bb[2];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) y[e] = __builtin_fmaf(gg[e], (v[c][e] - mean) * rstd, bb[e]);
-                    *reinterpret_cast<u32x2 *>(a_lds + (size_t)r * p.K + 4 * i) =
-                        u32x2{pack2(y[0], y[1]), pack2(y[2], y[3])};
+                for (int h = 0; h < 2; ++h) {
+                    const int i = min((c + h) * 64 + lane, nv - 1);
+                    gg[h] = g_l[i];
+                    bb[h] = b_l[i];
+                }
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const int i = (c + h) * 64 + lane;
+                    if (i < nv) {
+                        float y[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            y[e] = __builtin_fmaf(gg[h][e], (v[c + h][e] - mean) * rstd, bb[h][e]);
+                        *reinterpret_cast<u32x2 *>(a_lds + (size_t)r * p.K + 4 * i) =
+                            u32x2{pack2(y[0], y[1]), pack2(y[2], y[3])};
+                    }
                 }
             }
         };
@@ -739,49 +783,65 @@ struct SkinnyLn {
     }
 };
 
-// NVL: 0 = activations from a; 8 or 16 = LayerNorm prologue for K <= 2048 / 4096
-template <Epi EPI, int G, int NVL>
+// NVL: 0 = activations from a; 8 or 16 = LayerNorm prologue for K <= 2048 / 4096.
+// FRAG: p.w is the packed copy of W (skinny_pack) for this G.  U: K steps a
+// wave requests at once (skinny_unroll: the wave's share of the steps, up to 8).
+template <Epi EPI, int G, int NVL, bool FRAG, int U>
 __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p) {
     constexpr bool LNA = NVL > 0;
     constexpr int NW = kSkinnyWaves;
     constexpr int FPW = 16 / G, TPW = 16 / G;      // features and token columns per K-group
     constexpr int kPartBytes = (NW - 1) * 64 * 16;
-    // LayerNorm: the bf16 activation tile, then gamma and beta (fp32, K each)
-    constexpr int kLnBytes = kSkinnyLnElems * 2 + 2 * NVL * 256 * 4;
-    constexpr int kLdsBytes = LNA && kLnBytes > kPartBytes ? kLnBytes : kPartBytes;
+    // the LayerNorm prologue's bf16 activation tile, later the waves' partial
+    // sums; the prologue's gamma and beta (fp32, K each) in an array of their own
+    constexpr int kLdsBytes = LNA && kSkinnyLnElems * 2 > kPartBytes ? kSkinnyLnElems * 2 : kPartBytes;
     __shared__ __attribute__((aligned(16))) char lds[kLdsBytes];
+    __shared__ __attribute__((aligned(16))) float gb_lds[LNA ? 2 * NVL * 256 : 4];
     f32x4 (*part)[64] = reinterpret_cast<f32x4 (*)[64]>(lds);
     bf16_t *a_lds = reinterpret_cast<bf16_t *>(lds);
-    float *gb_lds = reinterpret_cast<float *>(lds + kSkinnyLnElems * 2);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int n0 = blockIdx.x * FPW;
     const int row = lane & 15, chunk = lane >> 4;               // operand row / column, 8-element K chunk
     const int kg = p.K / G;                                     // K-group length
     const int grp = row / FPW;                                  // K-group of this lane's row and column
     const int wf_row = n0 + row % FPW, a_row = min(row % TPW, p.M - 1);
-    const bf16_t *wrow = p.w + (size_t)wf_row * p.K + grp * kg + chunk * 8;
+    const int steps = kg / 32;
+    // row-major: step s of this lane at wrow + 32 s; packed: at wrow + 512 s
+    constexpr int WSTEP = FRAG ? 512 : 32;
+    const bf16_t *wrow = FRAG ? p.w + (size_t)blockIdx.x * steps * 512 + lane * 8
+                              : p.w + (size_t)wf_row * p.K + grp * kg + chunk * 8;
     const bf16_t *arow = (LNA ? a_lds : p.a) + (size_t)a_row * p.K + grp * kg + chunk * 8;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    const int steps = kg / 32;
-    bf16x8 wf[kSkinnyUnroll], af[kSkinnyUnroll];
-    // Fragments past the wave's last K step are not loaded but zero-filled, and
-    // every MFMA runs: a skipped step adds exactly zero.  (A conditional MFMA
-    // may be issued with the wave's EXEC mask empty, which does not stop it
-    // from reading its operand registers.)
+    // The epilogue's operands are fetched first.  Lane (fq, t) of wave 0
+    // stores features n0 + 4 fq .. + 3 of token t (see below); every lane
+    // loads (indices clamped into the operands, no branch), so that no wait
+    // for these loads is placed ahead of the weights'.
+    const int fq = lane / TPW, t = lane % TPW;
+    const bool stores = wave == 0 && lane < (FPW / 4) * TPW && t < p.M;
+    const int f_out = n0 + 4 * fq;
+    const u32x2 braw = *reinterpret_cast<const u32x2 *>(p.bias + min(f_out, p.N - 4));
+    f32x4 rres = {0.f, 0.f, 0.f, 0.f};
+    if constexpr (EPI == Epi::BiasResidF32)
+        rres = *reinterpret_cast<const f32x4 *>(p.resid + (size_t)min(t, p.M - 1) * p.N + min(f_out, p.N - 4));
+    // Fragments past the wave's last K step are replaced by zeros where the
+    // MFMA takes them, and every MFMA runs: a skipped step adds exactly zero.
+    // (A conditional MFMA may be issued with the wave's EXEC mask empty, which
+    // does not stop it from reading its operand registers.)  The selection sits
+    // at the MFMA, not at the load, so that no MFMA waits for a later fragment.
     const bf16x8 zero = {};
+    bf16x8 wf[U], af[U];
+    // Every load is issued, steps past the wave's last one clamped to it
+    // (their fragments are zeroed at the MFMA): no branch around a load, so
+    // each MFMA waits for its own fragments alone
     auto load_w = [&](int s0) {
 #pragma unroll
-        for (int u = 0; u < kSkinnyUnroll; ++u)
-            wf[u] = s0 + u * NW < steps ? *reinterpret_cast<const bf16x8 *>(wrow + (s0 + u * NW) * 32) : zero;
+        for (int u = 0; u < U; ++u)
+            wf[u] = *reinterpret_cast<const bf16x8 *>(wrow + min(s0 + u * NW, steps - 1) * WSTEP);
     };
-    // the same with every load issued (clamped to the last step, then zeroed):
-    // lets the LayerNorm prologue wait for its own loads alone
-    auto load_w_all = [&](int s0) {
+    auto load_a = [&](int s0) {
 #pragma unroll
-        for (int u = 0; u < kSkinnyUnroll; ++u) {
-            const bf16x8 x = *reinterpret_cast<const bf16x8 *>(wrow + min(s0 + u * NW, steps - 1) * 32);
-            wf[u] = s0 + u * NW < steps ? x : zero;
-        }
+        for (int u = 0; u < U; ++u)
+            af[u] = *reinterpret_cast<const bf16x8 *>(arow + min(s0 + u * NW, steps - 1) * 32);
     };
     if constexpr (LNA) {
         // the LayerNorm inputs first, then the weights; the activations are
@@ -789,19 +849,21 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
         SkinnyLn<NVL> ln;
         ln.load(p, threadIdx.x, lane, wave);
         __builtin_amdgcn_sched_barrier(0);     // keep these loads ahead of the weights' (in-order returns)
-        load_w_all(wave);
+        load_w(wave);
         ln.finish(p, a_lds, gb_lds, threadIdx.x, lane, wave);
         __syncthreads();
     } else {
+        // the first round's activations (L2-resident) ahead of the weights
+        load_a(wave);
         load_w(wave);
     }
-    for (int s0 = wave; s0 < steps; s0 += NW * kSkinnyUnroll) {
+    for (int s0 = wave; s0 < steps; s0 += NW * U) {
+        if (LNA || s0 != wave) load_a(s0);
 #pragma unroll
-        for (int u = 0; u < kSkinnyUnroll; ++u)
-            af[u] = s0 + u * NW < steps ? *reinterpret_cast<const bf16x8 *>(arow + (s0 + u * NW) * 32) : zero;
-#pragma unroll
-        for (int u = 0; u < kSkinnyUnroll; ++u) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[u], af[u], acc, 0, 0, 0);
-        if (s0 + NW * kSkinnyUnroll < steps) load_w(s0 + NW * kSkinnyUnroll);
+        for (int u = 0; u < U; ++u)
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(s0 + u * NW < steps ? wf[u] : zero,
+                                                          s0 + u * NW < steps ? af[u] : zero, acc, 0, 0, 0);
+        if (s0 + NW * U < steps) load_w(s0 + NW * U);
     }
     if constexpr (LNA) __syncthreads();                        // the partials reuse the activations' LDS
     if (wave > 0) part[wave - 1][lane] = acc;
@@ -812,7 +874,6 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
     // lane l holds product rows 4 (l / 16) + e, column l % 16.  Output lane
     // (fq, t) gathers features 4 fq .. 4 fq + 3 of token t from the diagonal
     // block of every K-group: row g FPW + 4 fq + e, column g TPW + t.
-    const int fq = lane / TPW, t = lane % TPW;
     if constexpr (G > 1) {
         f32x4 sum = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -823,10 +884,9 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
         }
         acc = sum;
     }
-    if (lane >= (FPW / 4) * TPW || t >= p.M) return;
-    const int f = n0 + 4 * fq;
+    if (!stores) return;
+    const int f = f_out;
     // this lane: features f .. f + 3 of token t
-    const u32x2 braw = *reinterpret_cast<const u32x2 *>(p.bias + f);
     float v0 = acc[0] + __uint_as_float(braw[0] << 16), v1 = acc[1] + __uint_as_float(braw[0] & 0xffff0000u);
     float v2 = acc[2] + __uint_as_float(braw[1] << 16), v3 = acc[3] + __uint_as_float(braw[1] & 0xffff0000u);
     if constexpr (EPI == Epi::BiasBf16 || EPI == Epi::BiasGeluBf16) {
@@ -836,7 +896,7 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
         *reinterpret_cast<u32x2 *>(static_cast<bf16_t *>(p.out) + (size_t)t * p.N + f) =
             u32x2{pack2(v0, v1), pack2(v2, v3)};
     } else if constexpr (EPI == Epi::BiasResidF32) {
-        const f32x4 r = *reinterpret_cast<const f32x4 *>(p.resid + (size_t)t * p.N + f);
+        const f32x4 r = rres;
         *reinterpret_cast<f32x4 *>(static_cast<float *>(p.out) + (size_t)t * p.N + f) =
             f32x4{r[0] + v0, r[1] + v1, r[2] + v2, r[3] + v3};
     } else if constexpr (EPI == Epi::Qkv) {
@@ -896,14 +956,16 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
 
 namespace {
 
-template <int G, int NVL>
+template <int G, int NVL, bool FRAG, int U>
 hipError_t launch_skinny(Epi epi, const GemmParams &p, hipStream_t stream) {
     const dim3 grid(p.N / (16 / G)), block(64 * kSkinnyWaves);
     switch (epi) {
-    case Epi::BiasBf16: return launch_kernel(skinny_kernel<Epi::BiasBf16, G, NVL>, grid, block, stream, p);
-    case Epi::BiasGeluBf16: return launch_kernel(skinny_kernel<Epi::BiasGeluBf16, G, NVL>, grid, block, stream, p);
-    case Epi::BiasResidF32: return launch_kernel(skinny_kernel<Epi::BiasResidF32, G, NVL>, grid, block, stream, p);
-    case Epi::Qkv: return launch_kernel(skinny_kernel<Epi::Qkv, G, NVL>, grid, block, stream, p);
+    case Epi::BiasBf16: return launch_kernel(skinny_kernel<Epi::BiasBf16, G, NVL, FRAG, U>, grid, block, stream, p);
+    case Epi::BiasGeluBf16:
+        return launch_kernel(skinny_kernel<Epi::BiasGeluBf16, G, NVL, FRAG, U>, grid, block, stream, p);
+    case Epi::BiasResidF32:
+        return launch_kernel(skinny_kernel<Epi::BiasResidF32, G, NVL, FRAG, U>, grid, block, stream, p);
+    case Epi::Qkv: return launch_kernel(skinny_kernel<Epi::Qkv, G, NVL, FRAG, U>, grid, block, stream, p);
     case Epi::BiasLnResidF32:
     case Epi::F32:
     case Epi::GeluBwdBf16: break;
@@ -911,14 +973,51 @@ hipError_t launch_skinny(Epi epi, const GemmParams &p, hipStream_t stream) {
     return hipErrorInvalidValue;
 }
 
+// K steps a wave requests at once: its share of the product's steps, rounded
+// up to a power of two, at most kSkinnyUnroll (more steps take more rounds)
+int skinny_unroll(int K, int G) {
+    const int per_wave = (K / G / 32 + kSkinnyWaves - 1) / kSkinnyWaves;
+    int u = 1;
+    while (u < per_wave && u < kSkinnyUnroll) u *= 2;
+    return u;
+}
+
+template <int G, int NVL, bool FRAG>
+hipError_t launch_skinny_u(Epi epi, const GemmParams &p, hipStream_t stream) {
+    switch (skinny_unroll(p.K, G)) {
+    case 1: return launch_skinny<G, NVL, FRAG, 1>(epi, p, stream);
+    case 2: return launch_skinny<G, NVL, FRAG, 2>(epi, p, stream);
+    case 4: return launch_skinny<G, NVL, FRAG, 4>(epi, p, stream);
+    default: return launch_skinny<G, NVL, FRAG, 8>(epi, p, stream);
+    }
+}
+
 template <int NVL>
-hipError_t launch_skinny_g(Epi epi, const GemmParams &p, hipStream_t stream) {
-    switch (skinny_groups(p.M, p.N, p.K, NVL > 0)) {
-    case 1: return launch_skinny<1, NVL>(epi, p, stream);
-    case 2: return launch_skinny<2, NVL>(epi, p, stream);
-    case 4: return launch_skinny<4, NVL>(epi, p, stream);
+hipError_t launch_skinny_g(Epi epi, const GemmParams &p, int g, bool frag, hipStream_t stream) {
+    switch (g) {
+    case 1: return frag ? launch_skinny_u<1, NVL, true>(epi, p, stream) : launch_skinny_u<1, NVL, false>(epi, p, stream);
+    case 2: return frag ? launch_skinny_u<2, NVL, true>(epi, p, stream) : launch_skinny_u<2, NVL, false>(epi, p, stream);
+    case 4: return frag ? launch_skinny_u<4, NVL, true>(epi, p, stream) : launch_skinny_u<4, NVL, false>(epi, p, stream);
     }
     return hipErrorInvalidValue;
+}
+
+// Packed copy for the skinny product with G K-groups: 16-byte piece i of dst
+// is what lane l of workgroup b loads at K step s in the row-major form, with
+// i = (b * steps + s) * 64 + l; steps = K / (32 G).
+template <int G>
+__global__ __launch_bounds__(256) void skinny_pack_kernel(const bf16_t *w, bf16_t *dst, int N, int K) {
+    constexpr int FPW = 16 / G;
+    const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+    const int kg = K / G, steps = kg / 32;
+    if (i >= (size_t)N * K / 8) return;
+    const int l = (int)(i % 64);
+    const size_t bs = i / 64;
+    const int s = (int)(bs % steps), b = (int)(bs / steps);
+    const int row = l & 15, chunk = l >> 4;
+    const int f = b * FPW + row % FPW, grp = row / FPW;
+    const size_t k = (size_t)grp * kg + s * 32 + chunk * 8;
+    reinterpret_cast<bf16x8 *>(dst)[i] = *reinterpret_cast<const bf16x8 *>(w + (size_t)f * K + k);
 }
 
 }  // namespace
@@ -937,9 +1036,21 @@ bool skinny_ln_fits(int M, int K) {
     return M >= 1 && M <= 16 && K % 32 == 0 && K <= 4096 && M * K <= kSkinnyLnElems;
 }
 
+hipError_t launch_skinny_pack(const bf16_t *w, bf16_t *dst, int N, int K, int groups, hipStream_t stream) {
+    if (N <= 0 || K <= 0 || (groups != 1 && groups != 2 && groups != 4)) return hipErrorInvalidValue;
+    if (N % (16 / groups) || K % (32 * groups)) return hipErrorInvalidValue;
+    const size_t pieces = (size_t)N * K / 8;
+    const dim3 grid((unsigned)((pieces + 255) / 256)), block(256);
+    switch (groups) {
+    case 1: return launch_kernel(skinny_pack_kernel<1>, grid, block, stream, w, dst, N, K);
+    case 2: return launch_kernel(skinny_pack_kernel<2>, grid, block, stream, w, dst, N, K);
+    default: return launch_kernel(skinny_pack_kernel<4>, grid, block, stream, w, dst, N, K);
+    }
+}
+
 hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *bias, const float *resid,
                               void *out, int M, int N, int K, const QkvDst *qkv, hipStream_t stream,
-                              const LnIn *ln_in) {
+                              const LnIn *ln_in, const bf16_t *w_packed, int packed_groups) {
     if (M <= 0) return hipSuccess;
     if (M > 16 || N % 16 || K % 32 || epi == Epi::BiasLnResidF32 || epi == Epi::F32 || epi == Epi::GeluBwdBf16)
         return hipErrorInvalidValue;
@@ -949,8 +1060,11 @@ hipError_t launch_gemm_skinny(Epi epi, const bf16_t *a, const bf16_t *w, const b
     p.M = M; p.N = N; p.K = K;
     if (qkv) p.qkv = *qkv;
     if (ln_in) p.lnin = *ln_in;
-    if (!ln_in) return launch_skinny_g<0>(epi, p, stream);
-    return K <= 2048 ? launch_skinny_g<8>(epi, p, stream) : launch_skinny_g<16>(epi, p, stream);
+    const int g = skinny_groups(M, N, K, ln_in != nullptr);
+    const bool frag = w_packed && packed_groups == g;
+    if (frag) p.w = w_packed;
+    if (!ln_in) return launch_skinny_g<0>(epi, p, g, frag, stream);
+    return K <= 2048 ? launch_skinny_g<8>(epi, p, g, frag, stream) : launch_skinny_g<16>(epi, p, g, frag, stream);
 }
 
 }  // namespace iefwd

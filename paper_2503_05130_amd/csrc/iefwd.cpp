@@ -129,6 +129,10 @@ void validate_config(const iefwd_config &c) {
 struct LayerWeights {
     bf16_t *wqkv, *bqkv, *wo, *bo, *w1, *b1, *w2, *b2;   // matrices output-major [out, in]
     float *g1, *be1, *g2, *be2;
+    // decode instances: packed copies of wqkv, wo, w1, w2 for the skinny
+    // product, and the K-group count each copy is packed for
+    bf16_t *packed[4] = {nullptr, nullptr, nullptr, nullptr};
+    int packed_groups[4] = {0, 0, 0, 0};
 };
 
 // Training state of an instance created with iefwd_train_create: the flat
@@ -182,8 +186,9 @@ struct iefwd_instance {
     DeviceInfo dev{};
     uint32_t head_dim = 0;
 
-    // weights: one device allocation, carved
-    void *wblob = nullptr;
+    // weights: one device allocation, carved; decode instances hold a second
+    // one with the packed copies of the four matrices per layer
+    void *wblob = nullptr, *pblob = nullptr;
     std::vector<LayerWeights> layers;
     float *gf = nullptr, *bef = nullptr;
     bf16_t *wh = nullptr, *bh = nullptr;
@@ -324,16 +329,20 @@ void run_forward(iefwd_instance *I, const float *x, int decode_pos = -1) {
     const bool skinny = decode && T <= 16;
     const bool fuse_ln = skinny && c.pre_ln && skinny_ln_fits(T, d);
     const int n_cu = (int)mask_popcount(I->mask, I->dev.n_cu);   // the quota this batch runs on
-    auto gemm = [&](Epi epi, const bf16_t *a, const bf16_t *wt, const bf16_t *bias, const float *resid, void *out,
-                    int N, int K, const QkvDst *qkv, const LnResid *ln_resid, const LnIn *ln_in = nullptr) {
-        if (skinny && !ln_resid) return launch_gemm_skinny(epi, a, wt, bias, resid, out, T, N, K, qkv, s, ln_in);
+    // j: which of the layer's four matrices (its packed copy serves decode steps)
+    auto gemm = [&](Epi epi, const bf16_t *a, const LayerWeights &w, int j, const bf16_t *bias, const float *resid,
+                    void *out, int N, int K, const QkvDst *qkv, const LnResid *ln_resid, const LnIn *ln_in = nullptr) {
+        const bf16_t *wt = j == 0 ? w.wqkv : j == 1 ? w.wo : j == 2 ? w.w1 : w.w2;
+        if (skinny && !ln_resid)
+            return launch_gemm_skinny(epi, a, wt, bias, resid, out, T, N, K, qkv, s, ln_in, w.packed[j],
+                                      w.packed_groups[j]);
         return launch_gemm(epi, a, wt, bias, resid, out, T, N, K, qkv, s, ln_resid, nullptr, n_cu);
     };
     auto attention_block = [&](int l, const bf16_t *y_bf16, const LayerWeights &w, const float *resid,
                                const LnResid *ln_resid, float *dst, const LnIn *ln_in = nullptr) {
         const QkvDst qd = qkv_dst(l);
         launch(I, IEFWD_K_QKV, "qkv gemm", [&] {
-            return gemm(Epi::Qkv, y_bf16, w.wqkv, w.bqkv, nullptr, nullptr, 3 * d, d, &qd, nullptr, ln_in);
+            return gemm(Epi::Qkv, y_bf16, w, 0, w.bqkv, nullptr, nullptr, 3 * d, d, &qd, nullptr, ln_in);
         });
         launch(I, IEFWD_K_ATTN, "attention", [&] {
             if (decode)
@@ -343,17 +352,17 @@ void run_forward(iefwd_instance *I, const float *x, int decode_pos = -1) {
                                     qd.vt_stride);
         });
         launch(I, IEFWD_K_OUTPROJ, "out-proj gemm", [&] {
-            return gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->ctx, w.wo, w.bo, resid, dst, d, d,
+            return gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->ctx, w, 1, w.bo, resid, dst, d, d,
                         nullptr, ln_resid);
         });
     };
     auto ffn_block = [&](const bf16_t *y_bf16, const LayerWeights &w, const float *resid, const LnResid *ln_resid,
                          float *dst, const LnIn *ln_in = nullptr) {
         launch(I, IEFWD_K_FFN1, "ffn1 gemm", [&] {
-            return gemm(Epi::BiasGeluBf16, y_bf16, w.w1, w.b1, nullptr, I->u, F, d, nullptr, nullptr, ln_in);
+            return gemm(Epi::BiasGeluBf16, y_bf16, w, 2, w.b1, nullptr, I->u, F, d, nullptr, nullptr, ln_in);
         });
         launch(I, IEFWD_K_FFN2, "ffn2 gemm", [&] {
-            return gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->u, w.w2, w.b2, resid, dst, d, F,
+            return gemm(ln_resid ? Epi::BiasLnResidF32 : Epi::BiasResidF32, I->u, w, 3, w.b2, resid, dst, d, F,
                         nullptr, ln_resid);
         });
     };
@@ -506,6 +515,45 @@ void upload_weights(iefwd_instance *I) {
         generate_vector_bf16(tensor_key(seed, L, 15), c.n_out, bs, stage16.data());
         put16(bh_off, c.n_out);
     }
+}
+
+// Decode instances: the packed copy of each layer's four matrices, for the
+// K-group count a decode step of up to 4 sequences uses (with the pre-LN
+// LayerNorm fused into the QKV and FFN-up products).  Larger decode batches of
+// matrices whose group count differs read the row-major weights.
+void pack_decode_weights(iefwd_instance *I) {
+    const iefwd_config &c = I->cfg;
+    const int d = (int)c.d_model, F = (int)c.d_ff;
+    const bool ln = skinny_ln_fits(1, d);
+    const int shape[4][2] = {{3 * d, d}, {d, d}, {F, d}, {d, F}};
+    const bool fused[4] = {ln, false, ln, false};
+    size_t bytes = 0;
+    std::vector<size_t> offs;
+    for (uint32_t l = 0; l < c.n_layers; ++l)
+        for (int j = 0; j < 4; ++j) {
+            offs.push_back(bytes);
+            bytes = round_up(bytes + (size_t)shape[j][0] * shape[j][1] * 2, 256);
+        }
+    if (hipMalloc(&I->pblob, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        I->pblob = nullptr;
+        fail(IEFWD_ENOMEM, "device allocation of the packed decode weights failed");
+    }
+    char *base = static_cast<char *>(I->pblob);
+    size_t oi = 0;
+    for (uint32_t l = 0; l < c.n_layers; ++l) {
+        LayerWeights &w = I->layers[l];
+        const bf16_t *src[4] = {w.wqkv, w.wo, w.w1, w.w2};
+        for (int j = 0; j < 4; ++j) {
+            const int N = shape[j][0], K = shape[j][1];
+            const int g = skinny_groups(1, N, K, fused[j]);
+            bf16_t *dst = reinterpret_cast<bf16_t *>(base + offs[oi++]);
+            hip_check(launch_skinny_pack(src[j], dst, N, K, g, I->stream), "weight packing");
+            w.packed[j] = dst;
+            w.packed_groups[j] = g;
+        }
+    }
+    hip_check(hipStreamSynchronize(I->stream), "hipStreamSynchronize");
 }
 
 void alloc_workspace(iefwd_instance *I) {
@@ -948,6 +996,7 @@ iefwd_instance::~iefwd_instance() {
     train.reset();
     if (wsblob) (void)hipFree(wsblob);
     if (kvblob) (void)hipFree(kvblob);
+    if (pblob) (void)hipFree(pblob);
     if (wblob) (void)hipFree(wblob);
 }
 
@@ -1051,6 +1100,7 @@ int create_instance(const iefwd_config *cfg, const iefwd_train_params *tp, int d
             fail(IEFWD_ENODEV, "device CU count is not a multiple of its XCD count");
         hip_check(inst->streams.acquire(all, &inst->stream), "hipExtStreamCreateWithCUMask");
         inst->mask = all;
+        if (cfg->kv_cache) pack_decode_weights(inst);
         if (tp) train_alloc(inst, *tp);
     });
     if (st != IEFWD_OK) {
@@ -1593,6 +1643,53 @@ int iefwd_test_gemm_skinny(uint32_t epilogue, const void *a, const void *w, cons
                                      out, (int)M, (int)N, (int)K, nullptr, (hipStream_t)stream,
                                      ln_z ? &lnin : nullptr),
                   "skinny gemm launch");
+    });
+}
+
+int iefwd_test_skinny_pack(const void *w, void *dst, uint32_t N, uint32_t K, uint32_t groups, void *stream) {
+    return guarded([&] {
+        if (!w || !dst) fail(IEFWD_EINVAL, "NULL pointer");
+        if (groups != 1 && groups != 2 && groups != 4) fail(IEFWD_EINVAL, "groups must be 1, 2 or 4");
+        if (N == 0 || N % (16 / groups) || K == 0 || K % (32 * groups))
+            fail(IEFWD_EINVAL, "N must be a positive multiple of 16 / groups, K of 32 * groups");
+        if ((uint64_t)N * K >= (1ull << 31)) fail(IEFWD_EINVAL, "too large");
+        hip_check(launch_skinny_pack((const bf16_t *)w, (bf16_t *)dst, (int)N, (int)K, (int)groups, (hipStream_t)stream),
+                  "skinny pack launch");
+    });
+}
+
+int iefwd_test_gemm_skinny_packed(uint32_t epilogue, const void *a, const void *w_packed, uint32_t groups,
+                                  const void *bias, const float *resid, void *out, uint32_t M, uint32_t N, uint32_t K,
+                                  const float *ln_z, const float *ln_gamma, const float *ln_beta, float ln_eps,
+                                  void *stream) {
+    return guarded([&] {
+        if (epilogue > IEFWD_EPI_BIAS_RESID_F32) fail(IEFWD_EINVAL, "unknown epilogue");
+        if (!w_packed || !bias || !out) fail(IEFWD_EINVAL, "NULL pointer");
+        if (epilogue == IEFWD_EPI_BIAS_RESID_F32 && !resid) fail(IEFWD_EINVAL, "resid is NULL");
+        if (M == 0 || M > 16) fail(IEFWD_EINVAL, "M must be in [1, 16]");
+        if (N == 0 || N % 16 || K == 0 || K % 32) fail(IEFWD_EINVAL, "N must be a positive multiple of 16, K of 32");
+        if ((uint64_t)N * K >= (1ull << 31)) fail(IEFWD_EINVAL, "too large");
+        LnIn lnin{ln_z, ln_gamma, ln_beta, ln_eps};
+        if (ln_z) {
+            if (!ln_gamma || !ln_beta) fail(IEFWD_EINVAL, "NULL LayerNorm parameters");
+            if (!skinny_ln_fits((int)M, (int)K)) fail(IEFWD_EINVAL, "the LayerNorm prologue needs K <= 4096 and M * K <= 16384");
+        } else if (!a) {
+            fail(IEFWD_EINVAL, "a is NULL");
+        }
+        if ((int)groups != skinny_groups((int)M, (int)N, (int)K, ln_z != nullptr))
+            fail(IEFWD_EINVAL, "the product uses another K-group count for this M, N, K");
+        hip_check(launch_gemm_skinny((Epi)epilogue, (const bf16_t *)a, (const bf16_t *)w_packed, (const bf16_t *)bias,
+                                     resid, out, (int)M, (int)N, (int)K, nullptr, (hipStream_t)stream,
+                                     ln_z ? &lnin : nullptr, (const bf16_t *)w_packed, (int)groups),
+                  "skinny gemm launch");
+    });
+}
+
+int iefwd_test_skinny_groups(uint32_t M, uint32_t N, uint32_t K, int ln, uint32_t *groups) {
+    return guarded([&] {
+        if (!groups) fail(IEFWD_EINVAL, "groups is NULL");
+        if (M == 0 || M > 16 || N == 0 || N % 16 || K == 0 || K % 32) fail(IEFWD_EINVAL, "bad shape");
+        *groups = (uint32_t)skinny_groups((int)M, (int)N, (int)K, ln != 0);
     });
 }
 

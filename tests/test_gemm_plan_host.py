@@ -55,3 +55,21 @@ def test_plan_rejects_bad_arguments():
         with pytest.raises(ie.IefwdError) as e:
             _plan(*args)
         assert e.value.status == ie.EINVAL
+
+
+@pytest.mark.parametrize("M,N,K,ln,groups", [
+    (2, 6144, 2048, True, 1),     # d-2048 QKV with the LayerNorm prologue: 2 groups would need 768 workgroups
+    (2, 6144, 2048, False, 2),
+    (4, 8192, 2048, True, 1),     # FFN-up
+    (2, 2048, 2048, False, 4),    # out-projection
+    (4, 2048, 8192, False, 4),    # FFN-down: up to 4 rows take 4 groups
+    (8, 2048, 8192, False, 2),    # 5-8 rows: 2
+    (9, 2048, 8192, False, 1),    # 9-16 rows: 1
+    (3, 2304, 768, True, 2),      # 4 groups would need 576 workgroups, past 2 per CU
+    (2, 2048, 96, False, 1),      # K not a multiple of 64
+])
+def test_skinny_group_count(M, N, K, ln, groups):
+    """The decode product's K-group rule: the most groups (up to 4, at most 16 /
+    groups rows) whose N / (16 / groups) workgroups fit 3 per CU (2 with the
+    LayerNorm prologue) on 256 CUs; the packed weight copy is made for it."""
+    assert ie.test_skinny_groups(M, N, K, ln) == groups
