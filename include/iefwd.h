@@ -85,7 +85,9 @@ typedef struct iefwd_config {
     uint32_t pre_ln;        /* 0 = post-LN (BERT-style), 1 = pre-LN + final LN */
     uint32_t causal;        /* 0 = bidirectional, 1 = causal mask */
     uint32_t kv_cache;      /* 1 = keep every layer's K and V for iefwd_decode (needs pre_ln = causal
-                               = 1 and max_seq <= 8192); 0 = prefill only (default) */
+                               = 1 and max_seq <= 8192), and a packed copy of the four weight
+                               matrices per layer for the decode step (the weights' device memory
+                               roughly doubles); 0 = prefill only (default) */
     float    ln_eps;        /* LayerNorm epsilon (default 1e-5) */
     float    w_std;         /* std of weight matrices (default 0.02) */
     float    b_std;         /* std of biases (default 0: biases are zero) */
