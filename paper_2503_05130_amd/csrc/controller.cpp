@@ -31,46 +31,86 @@ uint64_t QuotaController::window_sum(const Inst &in) {
     return s;
 }
 
+// Sec. 3.4.1 as a transition table.  Each period an SLO-sensitive instance's
+// observations fall into one condition, checked in this order:
+//   Violation  its KLC rose by more than eta_violation over its best (dT);
+//   Idle       it launched no kernels in its window;
+//   Alone      every co-located instance launched none in theirs;
+//   Sharing    otherwise.
+// The condition decides the shared state and the instance's own token rule;
+// the shared state decides the other instances' rule.  Token rules:
+//   LimitShare    MaxTokens * limit
+//   RequestShare  MaxTokens * request
+//   GrowToMax     R_last * eta_increase, at most MaxTokens
+//   GrowToLimit   R_last * eta_increase, at most MaxTokens * limit
+//   Yield         min(MaxTokens * request, R_last) / (1 + dT of the raiser)
+//   Keep          R_last
+// Readings where the paper's text leaves it open: Yield divides by the KLC
+// ratio 1 + dT (a division by dT alone would scale up for dT < 1), GrowToMax is
+// capped at MaxTokens, and T_min is the smallest KLC over the whole history.
+namespace {
+
+enum class Condition { Violation, Idle, Alone, Sharing };
+enum class Rule { LimitShare, RequestShare, GrowToMax, GrowToLimit, Yield, Keep };
+
+struct Transition {
+    QuotaController::State state;
+    Rule rule;
+};
+
+// SLO-sensitive instance: condition -> (shared state, own rule)
+constexpr Transition kSloTransition[] = {
+    /* Violation */ {QuotaController::Emergency, Rule::LimitShare},
+    /* Idle      */ {QuotaController::Recovery, Rule::RequestShare},
+    /* Alone     */ {QuotaController::Recovery, Rule::GrowToMax},
+    /* Sharing   */ {QuotaController::Contention, Rule::RequestShare},
+};
+
+// other instances: shared state -> rule
+constexpr Rule kOtherRule[] = {
+    /* None       */ Rule::LimitShare,
+    /* Emergency  */ Rule::Yield,
+    /* Recovery   */ Rule::GrowToLimit,
+    /* Contention */ Rule::Keep,
+};
+
+}  // namespace
+
+double QuotaController::tokens_by_rule(int rule, const Inst &in) const {
+    const double maxt = p_.max_tokens;
+    switch (static_cast<Rule>(rule)) {
+    case Rule::LimitShare: return maxt * in.limit;
+    case Rule::RequestShare: return maxt * in.request;
+    case Rule::GrowToMax: return std::min(in.r_last * p_.eta_increase, maxt);
+    case Rule::GrowToLimit: return std::min(in.r_last * p_.eta_increase, maxt * in.limit);
+    case Rule::Yield: return std::min(maxt * in.request, in.r_last) / (1.0 + owner_dt_);
+    case Rule::Keep: break;
+    }
+    return in.r_last;
+}
+
 double QuotaController::issue_slo(uint32_t i) {
     Inst &in = insts_[i];
     in.dt = in.t_min > 0 ? (in.t_current - in.t_min) / in.t_min : 0.0;
     bool others_idle = true;
     for (uint32_t j = 0; j < insts_.size(); ++j)
         if (j != i && window_sum(insts_[j]) != 0) others_idle = false;
-    const double maxt = p_.max_tokens;
-    State st;
-    double r;
-    if (in.dt > p_.eta_violation) {            // protective scale-up
-        st = Emergency;
-        r = maxt * in.limit;
-    } else if (window_sum(in) == 0) {          // idle: back to the request
-        st = Recovery;
-        r = maxt * in.request;
-    } else if (others_idle) {                  // co-located idle: grow
-        st = Recovery;
-        r = std::min(in.r_last * p_.eta_increase, maxt);
-    } else {
-        st = Contention;
-        r = maxt * in.request;
+    const Condition c = in.dt > p_.eta_violation ? Condition::Violation
+                        : window_sum(in) == 0    ? Condition::Idle
+                        : others_idle            ? Condition::Alone
+                                                 : Condition::Sharing;
+    const Transition t = kSloTransition[static_cast<int>(c)];
+    // only the instance that raised EMERGENCY may move the state out of it
+    if (state_ != Emergency || owner_ == (int64_t)i) {
+        state_ = t.state;
+        owner_ = t.state == Emergency ? (int64_t)i : -1;
+        owner_dt_ = t.state == Emergency ? in.dt : 0.0;
     }
-    if (state_ != Emergency || owner_ == (int64_t)i) {   // only the raiser may leave EMERGENCY
-        state_ = st;
-        owner_ = st == Emergency ? (int64_t)i : -1;
-        owner_dt_ = st == Emergency ? in.dt : 0.0;
-    }
-    return r;
+    return tokens_by_rule(static_cast<int>(t.rule), in);
 }
 
 double QuotaController::issue_other(uint32_t i) const {
-    const Inst &in = insts_[i];
-    const double maxt = p_.max_tokens;
-    switch (state_) {
-    case None: return maxt * in.limit;
-    case Emergency: return std::min(maxt * in.request, in.r_last) / (1.0 + owner_dt_);
-    case Recovery: return std::min(in.r_last * p_.eta_increase, maxt * in.limit);
-    case Contention: break;
-    }
-    return in.r_last;
+    return tokens_by_rule(static_cast<int>(kOtherRule[state_]), insts_[i]);
 }
 
 void QuotaController::issue(std::vector<double> &tokens, std::vector<uint32_t> &quotas,

@@ -4,20 +4,13 @@
 // Every control period each co-located instance reports the kernels it
 // launched during the period and the duration of its last iteration (the
 // kernel launching cycle, KLC: one batch for an inference instance).  issue()
-// then computes each instance's token issue R_issue:
-//   SLO-sensitive instances, from the relative KLC change dT = (T - T_min) / T_min:
-//     dT > eta_violation          -> EMERGENCY,  MaxTokens * limit
-//     no kernels in its window    -> RECOVERY,   MaxTokens * request
-//     no kernels in other windows -> RECOVERY,   min(R_last * eta_increase, MaxTokens)
-//     otherwise                   -> CONTENTION, MaxTokens * request
-//   other instances, from the shared state:
-//     NONE (no SLO-sensitive instance) -> MaxTokens * limit
-//     EMERGENCY  -> min(MaxTokens * request, R_last) / (1 + dT of the instance that raised it)
-//     RECOVERY   -> min(R_last * eta_increase, MaxTokens * limit)
-//     CONTENTION -> R_last
-// Only the instance that raised EMERGENCY can change the state again.  SLO-
-// sensitive instances are evaluated first (they set the state), then the
-// others, each group in id order.
+// then computes each instance's token issue R_issue from a transition table
+// (controller.cpp): an SLO-sensitive instance's condition in the period
+// (violation, idle, alone, sharing) sets the shared state and its own token
+// rule, and the shared state sets the other instances' rule.  Only the
+// instance that raised EMERGENCY can change the state again.  SLO-sensitive
+// instances are evaluated first (they set the state), then the others, each
+// group in id order.
 //
 // Tokens become quotas: round(R / granule) * granule clamped to
 // [min_quota, MaxTokens], then fitted so that no two instances share a CU:
@@ -74,6 +67,7 @@ private:
     };
     double issue_slo(uint32_t i);
     double issue_other(uint32_t i) const;
+    double tokens_by_rule(int rule, const Inst &in) const;
     static uint64_t window_sum(const Inst &in);
 
     Params p_;
