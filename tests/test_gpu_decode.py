@@ -71,6 +71,11 @@ DECODERS = [
     (dict(W.STRESS_INIT, n_layers=2, d_model=256, n_heads=4, d_ff=1024, pre_ln=1, causal=1, n_out=2), 3, 37, 4),
     (dict(W.STRESS_INIT, n_layers=2, d_model=256, n_heads=2, d_ff=640, pre_ln=1, causal=1, n_out=0), 2, 64, 3),
     (dict(n_layers=3, d_model=128, n_heads=2, d_ff=512, pre_ln=1, causal=1, n_out=3), 1, 1, 5),
+    # batches past 4: the products use fewer K-groups than the packed weight copies were made
+    # for, so all four read the row-major weights (6: two K-groups; 12: one, and the fused
+    # LayerNorm's waves normalise a second row each)
+    (dict(W.STRESS_INIT, n_layers=2, d_model=256, n_heads=4, d_ff=1024, pre_ln=1, causal=1, n_out=2), 6, 20, 3),
+    (dict(n_layers=2, d_model=128, n_heads=2, d_ff=512, pre_ln=1, causal=1, n_out=2), 12, 9, 3),
     # decode steps across the 2048 -> 2049 key boundary where the key chunking changes
     (dict(n_layers=1, d_model=128, n_heads=1, d_ff=256, pre_ln=1, causal=1, n_out=2), 2, 2046, 4),
 ]
