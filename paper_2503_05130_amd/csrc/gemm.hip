@@ -580,6 +580,20 @@ long tiles_of(int M, int N, int bm, int bn) { return (long)((M + bm - 1) / bm) *
 // product is too small to give three quarters of the CUs a larger tile.  Tile widths
 // divide `align` (d_model for the QKV scatter, so that no tile straddles the
 // Q / K / V boundaries).
+// Work on the share's busiest CU with a bm x bn tile: tiles per CU, rounded
+// up, times the tile's area.
+long busiest_cu_work(int M, int N, int bm, int bn, int n_cu) {
+    return (tiles_of(M, N, bm, bn) + n_cu - 1) / n_cu * (long)bm * bn;
+}
+
+// A 128 x 128 tile of the same K order replaces the first choice when it
+// leaves the busiest CU with at most 90% of the work: on shares whose CU
+// count does not divide the first choice's tiles (192 CUs: 512 tiles of
+// 64 x 96 leave some CUs three, 192 tiles of 128 x 128 one each).
+bool rebalance_to_128(int M, int N, int align, int n_cu, int bm, int bn) {
+    return align % 128 == 0 && 10 * busiest_cu_work(M, N, 128, 128, n_cu) <= 9 * busiest_cu_work(M, N, bm, bn, n_cu);
+}
+
 Tile choose_tile(int M, int N, int K, int align, int n_cu) {
     if (split_k_order(N, K)) {
         // every split-order product takes a split-order tile: SplitG (64 wide)
@@ -587,7 +601,7 @@ Tile choose_tile(int M, int N, int K, int align, int n_cu) {
         if (align % 96 && align % 128) return Tile::SplitG;
         const bool small = (align % 96 == 0 ? tiles_of(M, N, 64, 96) : tiles_of(M, N, 64, 128)) < 3L * n_cu / 4;
         if (small) return Tile::SplitG;
-        if (align % 96 == 0) return Tile::SplitC;
+        if (align % 96 == 0) return rebalance_to_128(M, N, align, n_cu, 64, 96) ? Tile::SplitD : Tile::SplitC;
         if (tiles_of(M, N, 64, 128) < 512) return Tile::SplitE;
         return Tile::SplitD;
     }
@@ -595,14 +609,21 @@ Tile choose_tile(int M, int N, int K, int align, int n_cu) {
         {Tile::A, 128, 192}, {Tile::D, 128, 128}, {Tile::B, 128, 96},
         {Tile::C, 64, 96}, {Tile::E, 64, 128}, {Tile::F, 64, 64}};
     Tile best = Tile::F;
+    int best_bm = 64, best_bn = 64;
     long best_n = 0;
     const long enough = std::min(256, 2 * n_cu);   // two tiles per CU on a share of <= 128 CUs
     for (const Cand &c : cands) {
         if (align % c.bn) continue;
         const long n = tiles_of(M, N, c.bm, c.bn);
-        if (n >= enough) return c.t;
-        if (n > best_n) { best = c.t; best_n = n; }
+        if (n >= enough) {
+            best = c.t;
+            best_bm = c.bm;
+            best_bn = c.bn;
+            break;
+        }
+        if (n > best_n) { best = c.t; best_bm = c.bm; best_bn = c.bn; best_n = n; }
     }
+    if (best != Tile::D && rebalance_to_128(M, N, align, n_cu, best_bm, best_bn)) return Tile::D;
     return best;
 }
 

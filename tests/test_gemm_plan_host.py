@@ -73,3 +73,22 @@ def test_skinny_group_count(M, N, K, ln, groups):
     groups rows) whose N / (16 / groups) workgroups fit 3 per CU (2 with the
     LayerNorm prologue) on 256 CUs; the packed weight copy is made for it."""
     assert ie.test_skinny_groups(M, N, K, ln) == groups
+
+
+@pytest.mark.parametrize("M,N,K,n_cu,tile", [
+    # BERT-base batch 32 (4096 tokens): FFN-down (even/odd order), FFN-up, out-projection
+    (4096, 768, 3072, 256, (64, 96)),    # 512 tiles, two per CU
+    (4096, 768, 3072, 192, (128, 128)),  # 64 x 96 would leave some CUs three tiles
+    (4096, 768, 3072, 128, (64, 96)),    # four per CU either way: the first choice stays
+    (4096, 3072, 768, 256, (128, 192)),
+    (4096, 3072, 768, 192, (128, 128)),
+    (4096, 768, 768, 256, (128, 96)),
+    (4096, 768, 768, 192, (128, 128)),
+    (4096, 2304, 768, 192, (128, 192)),  # QKV: 384 tiles fill 192 CUs twice
+])
+def test_tile_balances_the_share(M, N, K, n_cu, tile):
+    """On shares whose CU count leaves the first-choice tiles unevenly spread, a
+    128 x 128 tile of the same K order is taken when it leaves the busiest CU
+    with at most 90% of the work."""
+    k_order, tile_order, bm, bn = ie.test_gemm_plan(M, N, K, N, n_cu)
+    assert (bm, bn) == tile and k_order == tile_order
