@@ -417,15 +417,17 @@ int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void 
                     void *stream);
 
 /* Pure host function: how iefwd_test_gemm and the forward pass run an
- * M x N x K product on a stream with n_cu CUs.  k_order: the K summation order
+ * M x N x K product on a stream with n_cu CUs; ln_residual != 0 for the
+ * post-LN residual epilogue (the out-projection and FFN-down of a post-LN
+ * model), whose tile choice skips the 128 x 192 tile.  k_order: the K summation order
  * of the weight shape (0 = sequential 64-wide K tiles, 1 = even and odd K
  * tiles summed separately, then added); tile_order: the order the chosen tile
  * sums in, always equal to k_order; tile_m x tile_n: the output tile (tokens x
  * features).  align: the width every tile must divide (d_model for the QKV
  * product, else N).  EINVAL unless 1 <= M <= 2^24, N and K are multiples of 64
  * in [64, 65536], align is a multiple of 64 dividing N and 1 <= n_cu <= 1024. */
-int iefwd_test_gemm_plan(uint32_t M, uint32_t N, uint32_t K, uint32_t align, uint32_t n_cu, uint32_t *k_order,
-                         uint32_t *tile_order, uint32_t *tile_m, uint32_t *tile_n);
+int iefwd_test_gemm_plan(uint32_t M, uint32_t N, uint32_t K, uint32_t align, uint32_t n_cu, uint32_t ln_residual,
+                         uint32_t *k_order, uint32_t *tile_order, uint32_t *tile_m, uint32_t *tile_n);
 
 /* The decode-step product for M <= 16 activation rows: the same operands and
  * epilogues as iefwd_test_gemm, N % 16 == 0, K % 32 == 0.  Its K summation

@@ -69,7 +69,7 @@ SIGNATURES = {
     "iefwd_last_error": (ctypes.c_char_p, []),
     "iefwd_status_string": (ctypes.c_char_p, [_i32]),
     "iefwd_test_gemm": (_i32, [_u32, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp]),
-    "iefwd_test_gemm_plan": (_i32, [_u32, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32), ctypes.POINTER(_u32),
+    "iefwd_test_gemm_plan": (_i32, [_u32, _u32, _u32, _u32, _u32, _u32, ctypes.POINTER(_u32), ctypes.POINTER(_u32),
                                      ctypes.POINTER(_u32), ctypes.POINTER(_u32)]),
     "iefwd_test_gemm_skinny": (_i32, [_u32, _vp, _vp, _vp, _vp, _vp, _u32, _u32, _u32, _vp, _vp, _vp, _f32, _vp]),
     "iefwd_test_skinny_pack": (_i32, [_vp, _vp, _u32, _u32, _u32, _vp]),
@@ -376,10 +376,12 @@ def test_decode_attention(q, k, vt, ctx, batch, n_heads, n_keys, head_dim, k_row
            "iefwd_test_decode_attention")
 
 
-def test_gemm_plan(M: int, N: int, K: int, align: int, n_cu: int) -> tuple[int, int, int, int]:
-    """(k_order, tile_order, tile_m, tile_n) of an M x N x K product on n_cu CUs."""
+def test_gemm_plan(M: int, N: int, K: int, align: int, n_cu: int, ln_residual: bool = False) -> tuple[int, int, int, int]:
+    """(k_order, tile_order, tile_m, tile_n) of an M x N x K product on n_cu CUs (ln_residual: the
+    post-LN residual epilogue)."""
     o = [_u32() for _ in range(4)]
-    _check(lib().iefwd_test_gemm_plan(M, N, K, align, n_cu, *[ctypes.byref(v) for v in o]), "iefwd_test_gemm_plan")
+    _check(lib().iefwd_test_gemm_plan(M, N, K, align, n_cu, 1 if ln_residual else 0, *[ctypes.byref(v) for v in o]),
+           "iefwd_test_gemm_plan")
     return tuple(v.value for v in o)
 
 

@@ -64,7 +64,7 @@ struct GemmPlan {
     bool tile_split;    // the chosen tile's order (must equal split_order)
     int bm, bn;         // output tile, tokens x features
 };
-GemmPlan gemm_plan(int M, int N, int K, int align, int n_cu);
+GemmPlan gemm_plan(int M, int N, int K, int align, int n_cu, bool ln_residual = false);
 
 // Activations given as LayerNorm(z): z fp32 [M, K] rows, gamma / beta fp32 [K].
 struct LnIn {

@@ -594,7 +594,11 @@ bool rebalance_to_128(int M, int N, int align, int n_cu, int bm, int bn) {
     return align % 128 == 0 && 10 * busiest_cu_work(M, N, 128, 128, n_cu) <= 9 * busiest_cu_work(M, N, bm, bn, n_cu);
 }
 
-Tile choose_tile(int M, int N, int K, int align, int n_cu) {
+// wide_ok = false skips the 128 x 192 tile: with the LayerNorm-residual
+// epilogue it needs more registers than its two workgroups per CU leave and
+// spills (at 64 CUs, where it is the first choice for a 768-wide product, the
+// 128 x 96 tile is 30% faster).
+Tile choose_tile(int M, int N, int K, int align, int n_cu, bool wide_ok = true) {
     if (split_k_order(N, K)) {
         // every split-order product takes a split-order tile: SplitG (64 wide)
         // serves any width the others do not divide, whatever M and n_cu are
@@ -613,7 +617,7 @@ Tile choose_tile(int M, int N, int K, int align, int n_cu) {
     long best_n = 0;
     const long enough = std::min(256, 2 * n_cu);   // two tiles per CU on a share of <= 128 CUs
     for (const Cand &c : cands) {
-        if (align % c.bn) continue;
+        if (align % c.bn || (!wide_ok && c.t == Tile::A)) continue;
         const long n = tiles_of(M, N, c.bm, c.bn);
         if (n >= enough) {
             best = c.t;
@@ -942,8 +946,8 @@ __global__ __launch_bounds__(64 * kSkinnyWaves) void skinny_kernel(GemmParams p)
 
 }  // namespace
 
-GemmPlan gemm_plan(int M, int N, int K, int align, int n_cu) {
-    const TileDims d = tile_dims(choose_tile(M, N, K, align, n_cu));
+GemmPlan gemm_plan(int M, int N, int K, int align, int n_cu, bool ln_residual) {
+    const TileDims d = tile_dims(choose_tile(M, N, K, align, n_cu, !ln_residual));
     return GemmPlan{split_k_order(N, K), d.split, d.bm, d.bn};
 }
 
@@ -960,7 +964,7 @@ hipError_t launch_gemm(Epi epi, const bf16_t *a, const bf16_t *w, const bf16_t *
     if (ln) p.ln = *ln;
     // N is a multiple of 64 (checked by the callers); d_model a multiple of 128
     const int align = epi == Epi::Qkv ? p.qkv.d_model : N;
-    switch (choose_tile(M, N, K, align, n_cu)) {
+    switch (choose_tile(M, N, K, align, n_cu, epi != Epi::BiasLnResidF32)) {
     case Tile::A: return launch_tile<CfgA>(epi, p, stream);
     case Tile::D: return launch_tile<CfgD>(epi, p, stream);
     case Tile::B: return launch_tile<CfgB>(epi, p, stream);

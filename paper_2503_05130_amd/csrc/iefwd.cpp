@@ -1606,7 +1606,8 @@ int iefwd_test_gemm(uint32_t epilogue, const void *a, const void *w, const void 
     });
 }
 
-int iefwd_test_gemm_plan(uint32_t M, uint32_t N, uint32_t K, uint32_t align, uint32_t n_cu, uint32_t *k_order,
+int iefwd_test_gemm_plan(uint32_t M, uint32_t N, uint32_t K, uint32_t align, uint32_t n_cu, uint32_t ln_residual,
+                         uint32_t *k_order,
                          uint32_t *tile_order, uint32_t *tile_m, uint32_t *tile_n) {
     return guarded([&] {
         if (!k_order || !tile_order || !tile_m || !tile_n) fail(IEFWD_EINVAL, "NULL pointer");
@@ -1614,7 +1615,7 @@ int iefwd_test_gemm_plan(uint32_t M, uint32_t N, uint32_t K, uint32_t align, uin
             fail(IEFWD_EINVAL, "need 1 <= M <= 2^24 and N, K multiples of 64 in [64, 65536]");
         if (align == 0 || align % 64 || N % align) fail(IEFWD_EINVAL, "align must be a multiple of 64 dividing N");
         if (n_cu == 0 || n_cu > 1024) fail(IEFWD_EINVAL, "n_cu must be in [1, 1024]");
-        const GemmPlan p = gemm_plan((int)M, (int)N, (int)K, (int)align, (int)n_cu);
+        const GemmPlan p = gemm_plan((int)M, (int)N, (int)K, (int)align, (int)n_cu, ln_residual != 0);
         *k_order = p.split_order ? 1u : 0u;
         *tile_order = p.tile_split ? 1u : 0u;
         *tile_m = (uint32_t)p.bm;

@@ -92,3 +92,14 @@ def test_tile_balances_the_share(M, N, K, n_cu, tile):
     with at most 90% of the work."""
     k_order, tile_order, bm, bn = ie.test_gemm_plan(M, N, K, N, n_cu)
     assert (bm, bn) == tile and k_order == tile_order
+
+
+@pytest.mark.parametrize("n_cu,plain,ln_residual", [
+    (64, (128, 192), (128, 128)),    # the 128 x 192 tile would spill with the LayerNorm residual
+    (128, (128, 96), (128, 96)),
+    (256, (128, 96), (128, 96)),
+])
+def test_ln_residual_epilogue_skips_the_widest_tile(n_cu, plain, ln_residual):
+    for flag, want in ((False, plain), (True, ln_residual)):
+        k_order, tile_order, bm, bn = ie.test_gemm_plan(4096, 768, 768, 768, n_cu, flag)
+        assert (bm, bn) == want and k_order == tile_order == 0
