@@ -6,6 +6,7 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
   python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 static proportional shared paired]
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--granule 32] [--small]
                                        [--mix inference|train|decode] [--queue-probe]
+                                       [--queue-order rounds|instance]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
 batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
@@ -31,7 +32,18 @@ Policies (each period):
                created or destroyed while the instances serve (creating or
                destroying one stalls every queue of the process for ~3 ms on
                MI355X, and more than ~20-24 live queues per process make the
-               hardware scheduler time-slice them)
+               hardware scheduler time-slice them).  The placements are
+               prepared in rounds, one queue per instance per round, in the
+               order the instances made their first queues (--queue-order
+               rounds); --queue-order instance prepares each instance's
+               placements in turn.  Measured on MI355X: in round order an
+               encoder's batches are unaffected by the decoders' long GEMM
+               launches; in instance order they run 5-8 x slower while any
+               decoder GEMM runs, whichever CUs it runs on.  This fits the
+               queues being dealt to the hardware's dispatch pipes in
+               creation order, with a queue waiting behind a neighbour's
+               launch whose workgroups are still being placed on the same
+               pipe.
 
 --granule sets the quota granularity (in CUs) of proportional and alg2.
 
@@ -451,26 +463,35 @@ def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRA
         time.sleep(period)
 
 
-def prepare_paired(served):
+def prepare_paired(served, queue_order="rounds"):
     """Prepares every placement the paired policy can issue, sizes each stream
     cache to hold exactly them (the full-device stream is dropped), and starts
-    every instance on the even split."""
+    every instance on the even split.  queue_order "rounds": one new queue per
+    instance per round, instances in the order their full-device queues were
+    made, so that the k-th queue of every instance sits at the same position
+    modulo the instance count; "instance": each instance's queues in turn."""
     n_cu = ie.device_info(0)[0]
-    for pi, (a, b) in enumerate(pairs_of(served)):
-        for idx, second in ((a, False), (b, True)):
-            inst = served[idx].inst
-            inst.set_stream_cache(len(PAIR_SPLITS) + 1)
-            for sp in PAIR_SPLITS:
-                inst.prepare_quota(*paired_placement(n_cu, pi, sp, second))
-            start = paired_placement(n_cu, pi, 64, second)
-            inst.set_quota(*start)
-            served[idx].applied = start
-            inst.submit(served[idx].pool[:1])   # moves the instance onto its placement
-            inst.wait()
-            inst.set_stream_cache(len(PAIR_SPLITS))
+    members = sorted((idx, pi, second) for pi, (a, b) in enumerate(pairs_of(served))
+                     for idx, second in ((a, False), (b, True)))
+    for idx, _, _ in members:
+        served[idx].inst.set_stream_cache(len(PAIR_SPLITS) + 1)
+    if queue_order == "rounds":
+        jobs = [(m, sp) for sp in PAIR_SPLITS for m in members]
+    else:
+        jobs = [(m, sp) for m in members for sp in PAIR_SPLITS]
+    for (idx, pi, second), sp in jobs:
+        served[idx].inst.prepare_quota(*paired_placement(n_cu, pi, sp, second))
+    for idx, pi, second in members:
+        inst = served[idx].inst
+        start = paired_placement(n_cu, pi, 64, second)
+        inst.set_quota(*start)
+        served[idx].applied = start
+        inst.submit(served[idx].pool[:1])   # moves the instance onto its placement
+        inst.wait()
+        inst.set_stream_cache(len(PAIR_SPLITS))
 
 
-def run_policy(policy, served, horizon, warmup, period, granule=GRANULE):
+def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_order="rounds"):
     for s in served:
         s.reset(horizon)
         if isinstance(s, (Trainee, Generator)):
@@ -479,7 +500,7 @@ def run_policy(policy, served, horizon, warmup, period, granule=GRANULE):
             s.inst.submit(s.pool[:1])          # warm the instance and its full-device stream
             s.inst.wait()
     if policy == "paired":
-        prepare_paired(served)
+        prepare_paired(served, queue_order)
     torch.cuda.synchronize()
     stop, history = threading.Event(), []
     t0 = time.perf_counter()
@@ -502,7 +523,8 @@ def run_policy(policy, served, horizon, warmup, period, granule=GRANULE):
     aggregate = {"requests_s": round(len(allat) / max(horizon - warmup, 1e-9), 1),
                  "p50_ms": round(float(np.percentile(allat, 50)), 3) if len(allat) else None,
                  "p99_ms": round(float(np.percentile(allat, 99)), 3) if len(allat) else None}
-    return {"policy": policy, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
+    extra = {"queue_order": queue_order} if policy == "paired" else {}
+    return {"policy": policy, **extra, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
             "granule": granule if policy in ("proportional", "alg2") else None, "aggregate": aggregate,
             "instances": [s.stats(warmup, horizon) if isinstance(s, (Trainee, Generator)) else s.stats(warmup)
                           for s in served],
@@ -711,6 +733,8 @@ def main() -> int:
                          "decode: inference beside a token-by-token decoder")
     ap.add_argument("--queue-probe", action="store_true",
                     help="measure what creating, switching and keeping masked queues costs co-located instances")
+    ap.add_argument("--queue-order", choices=["rounds", "instance"], default="rounds",
+                    help="order in which the paired policy prepares its placements' queues")
     args = ap.parse_args()
     if args.queue_probe:
         queue_probe()
@@ -730,7 +754,7 @@ def main() -> int:
         for pol in args.policy:
             name, _, per = pol.partition("@")          # "alg2@100": policy with its own period in ms
             period = float(per) if per else args.period_ms
-            res = run_policy(name, served, args.horizon, args.warmup, period / 1e3, args.granule)
+            res = run_policy(name, served, args.horizon, args.warmup, period / 1e3, args.granule, args.queue_order)
             print(json.dumps(res), flush=True)
     finally:
         for s in served:
