@@ -161,7 +161,13 @@ int iefwd_prepare_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first);
  * hardware scheduler time-slices them (12-33 ms stalls).  A serving loop that
  * moves quotas every control period should therefore prepare a fixed set of
  * placements once (iefwd_prepare_quota_at), size the cache to hold them, and
- * keep the whole process within that queue budget.  EINVAL outside 1 .. 16. */
+ * keep the whole process within that queue budget.  Also measured: the order
+ * the queues are created in matters.  Created in rounds (one per instance per
+ * round, the instances always in the same order), co-located instances keep
+ * their batch times; created instance by instance, a latency-sensitive
+ * instance's batches ran 5-8 times slower whenever another instance's long
+ * GEMM launches ran, on whatever CUs.  The queues appear to be dealt to the
+ * device's dispatch pipes in creation order.  EINVAL outside 1 .. 16. */
 int iefwd_set_stream_cache(iefwd_instance *inst, uint32_t capacity);
 
 /* Requests an explicit CU mask (n_words 32-bit words, bit order as above);
