@@ -136,7 +136,11 @@ int iefwd_destroy(iefwd_instance *inst);
 /* Requests a quota of n_cu CUs (1 .. device CUs) starting at mask bit `first`
  * (0 .. device CUs - 1), spread evenly over the XCDs as by iefwd_build_cu_mask.
  * Takes effect at the next iefwd_submit; a batch already in flight keeps its
- * CUs.  EINVAL if n_cu or first is out of range. */
+ * CUs.  EINVAL if n_cu or first is out of range.  Measured on MI355X: give
+ * quotas in multiples of 32 CUs.  Each XCD's CUs sit in 4 shader engines and
+ * workgroups are dealt to the engines in equal numbers, so a quota of 5-7 CUs
+ * per XCD runs at about the speed of 4 (the BERT-base batch-32 forward: 6.99 ms
+ * at 32 CUs, 6.42-6.50 ms at 40-56, 3.76 ms at 64). */
 int iefwd_set_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first);
 
 /* iefwd_set_quota_at(inst, n_cu, 0). */
