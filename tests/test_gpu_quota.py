@@ -13,11 +13,15 @@ from tests.gpu_util import DEV, instance_config, run_instance
 pytestmark = pytest.mark.gpu
 
 
-def observed_cus(stream_handle, n_groups=8192):
+def probe(stream_handle, n_groups=8192):
     out = torch.zeros(2 * n_groups, dtype=torch.int32, device=DEV)
     ie.test_cu_probe(n_groups, out, stream=stream_handle)
     torch.cuda.synchronize()
-    v = out.cpu().numpy().astype(np.uint32).reshape(-1, 2)
+    return out.cpu().numpy().astype(np.uint32).reshape(-1, 2)
+
+
+def observed_cus(stream_handle, n_groups=8192):
+    v = probe(stream_handle, n_groups)
     xcc = v[:, 0] & 0xF
     cu = (v[:, 1] >> 8) & 0xFF          # CU, shader-array and shader-engine fields of HW_ID
     return set(zip(xcc.tolist(), cu.tolist()))
@@ -120,3 +124,28 @@ def test_stream_cache_capacity():
         got = run_instance(inst, x)
         assert np.array_equal(got.view(np.uint32), ref.view(np.uint32))
         assert inst.get_cu_mask() == ie.build_cu_mask(256, 8, 96, 96)
+
+
+@pytest.mark.parametrize("q", [40, 56, 64, 96])
+def test_quota_spreads_over_shader_engines(q):
+    # each XCD's share of a quota is spread over its shader engines as evenly as
+    # it goes, and the workgroups of a launch are dealt to the engines in equal
+    # numbers (whatever their CU counts): printed, the CU spread asserted
+    shape = W.model_shape("encoder_l1_d128_s32_b2")
+    with ie.Instance(**instance_config(shape, 1, 32)) as inst:
+        inst.set_quota(q)
+        run_instance(inst, W.make_input(1, 1, 32, 128))
+        v = probe(inst.stream_handle(), 16384)
+    xcc, se, cu = v[:, 0] & 0xF, (v[:, 1] >> 13) & 0x7, (v[:, 1] >> 8) & 0xF
+    for x in range(8):
+        sel = xcc == x
+        cus = collections.defaultdict(set)
+        wgs = collections.Counter()
+        for s_, c_ in zip(se[sel].tolist(), cu[sel].tolist()):
+            cus[s_].add(c_)
+            wgs[s_] += 1
+        n = [len(cus[k]) for k in sorted(cus)]
+        if x == 0:
+            print(f"quota {q}, XCD 0: CUs per engine {n}, workgroups per engine {[wgs[k] for k in sorted(wgs)]}",
+                  flush=True)
+        assert sum(n) == q // 8 and max(n) - min(n) <= 1
