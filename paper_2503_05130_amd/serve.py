@@ -22,7 +22,10 @@ Policies (each period):
                CUs, at least 32), disjoint, all CUs handed out
   alg2         the fast scale-up/down controller (iefwd_ctl_*, 32-CU
                granule): kernels launched in the period and the per-batch
-               time go in, quotas and placements come out
+               time go in, quotas and placements come out.  A placement's
+               queue is made when the placement is first issued, in
+               whatever order the controller issues them, so the creation
+               order described under paired is not kept
   paired       quotas from a fixed vocabulary: instances are paired (each
                SLO-sensitive one with a best-effort one) and each pair owns
                a fixed 128-CU region whose split point moves in 32-CU steps
