@@ -3,7 +3,7 @@ instances, one dispatcher thread per instance, and a quota policy that
 re-masks the instances every control period (the paper's setting of
 Sec. 3.4 and its inference-inference experiments, Sec. 5).
 
-  python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 static proportional shared paired]
+  python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 alg2p static proportional shared paired]
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--granule 32] [--small]
                                        [--mix inference|train|decode] [--queue-probe]
                                        [--queue-order rounds|instance]
@@ -26,6 +26,10 @@ Policies (each period):
                queue is made when the placement is first issued, in
                whatever order the controller issues them, so the creation
                order described under paired is not kept
+  alg2p        Alg. 2 on the paired policy's placements: the controller
+               issues quotas as under alg2, and each pair's region is split
+               in the ratio of its two members' quotas, to the nearest of
+               the prepared splits (queues made as under paired)
   paired       quotas from a fixed vocabulary: instances are paired (each
                SLO-sensitive one with a best-effort one) and each pair owns
                a fixed 128-CU region whose split point moves in 32-CU steps
@@ -385,15 +389,35 @@ def paired_placement(n_cu, pair_idx, split, second):
     return (128 - split, base + split) if second else (split, base)
 
 
+def controller_quotas(ctl, served, last_k, firsts_out=None):
+    """One Alg. 2 period: reports each instance's kernels launched and KLC
+    (the median batch-time ratio of the period), returns the issued quotas
+    (and appends the issued first mask bits to firsts_out)."""
+    for i, s in enumerate(served):
+        with s.lock:
+            k, ratios = s.kernels, s.ratios
+            s.ratios = []
+        klc = float(np.median(ratios)) if ratios else 0.0
+        if klc > 0:
+            s.klc_log.append(klc)
+        ctl.report(i, k - last_k[i], klc)
+        last_k[i] = k
+    _, qs, firsts = ctl.issue()
+    if firsts_out is not None:
+        firsts_out.extend(firsts)
+    return list(qs)
+
+
 def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRANULE):
     n_cu = ie.device_info(0)[0]
     ctl = None
-    if policy == "alg2":
+    paired_like = policy in ("paired", "alg2p")
+    if policy in ("alg2", "alg2p"):
         ctl = ie.Controller(max_tokens=n_cu, granule=granule, min_quota=granule)
         for s in served:
             ctl.add(s.request, s.limit, s.slo)
     last_k = [s.kernels for s in served]
-    posted = [s.applied if policy == "paired" else None for s in served]
+    posted = [s.applied if paired_like else None for s in served]
     while not stop.is_set():
         now = time.perf_counter() - t0
         if now > horizon:
@@ -417,15 +441,22 @@ def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRA
             for q in qs:
                 plan.append((int(q), first))
                 first = (first + int(q)) % n_cu
-        elif policy == "paired":
+        elif paired_like:
             # Hand-over in order: a member may shrink at once, but it grows only
             # onto CUs its partner has already left (the partner's current or
             # last batch ran on `applied`; a quota change takes effect at a batch
             # boundary, and a decoder batch runs for tens of ms).
+            if policy == "alg2p":
+                # Alg. 2 decides the quotas; each pair's region is split in the
+                # ratio of its two members' quotas, to the nearest prepared split
+                cq = controller_quotas(ctl, served, last_k)
             plan = list(posted)
             for pi, (a, b) in enumerate(pairs_of(served)):
-                la, lb = max(served[a].queue_len(now), 0), max(served[b].queue_len(now), 0)
-                share = 0.5 if la + lb == 0 else la / (la + lb)
+                if policy == "alg2p":
+                    share = cq[a] / max(cq[a] + cq[b], 1)
+                else:
+                    la, lb = max(served[a].queue_len(now), 0), max(served[b].queue_len(now), 0)
+                    share = 0.5 if la + lb == 0 else la / (la + lb)
                 split = min(PAIR_SPLITS, key=lambda sp: abs(sp / 128.0 - share))
                 want = {a: paired_placement(n_cu, pi, split, False), b: paired_placement(n_cu, pi, split, True)}
                 grow = [i for i in (a, b) if want[i][0] > posted[i][0]]
@@ -441,23 +472,15 @@ def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRA
                     if not busy or placements_disjoint(want[i], held, n_cu):
                         plan[i] = want[i]
         else:
-            for i, s in enumerate(served):
-                with s.lock:
-                    k, ratios = s.kernels, s.ratios
-                    s.ratios = []
-                klc = float(np.median(ratios)) if ratios else 0.0
-                if klc > 0:
-                    s.klc_log.append(klc)
-                ctl.report(i, k - last_k[i], klc)
-                last_k[i] = k
-            _, qs, firsts = ctl.issue()
+            firsts = []
+            qs = controller_quotas(ctl, served, last_k, firsts)
             plan = list(zip(qs, firsts))
         # shrinking instances first, so that none starts a batch on CUs just handed to another
         order = sorted(range(len(served)), key=lambda i: plan[i][0] - (posted[i] or plan[i])[0])
         for i in order:
             s, p = served[i], plan[i]
             if p != posted[i]:
-                if policy != "paired":         # paired: every placement was prepared before the run
+                if not paired_like:            # paired: every placement was prepared before the run
                     s.inst.prepare_quota(*p)   # hardware queue created here, not on the batch path
                 posted[i] = p
             with s.lock:
@@ -502,7 +525,7 @@ def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_o
         else:
             s.inst.submit(s.pool[:1])          # warm the instance and its full-device stream
             s.inst.wait()
-    if policy == "paired":
+    if policy in ("paired", "alg2p"):
         prepare_paired(served, queue_order)
     torch.cuda.synchronize()
     stop, history = threading.Event(), []
@@ -517,7 +540,7 @@ def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_o
     ctl.join()
     qs = np.array([h[1] for h in history]) if history else np.zeros((0, len(served)))
     states = [h[2] for h in history]
-    if policy == "paired":
+    if policy in ("paired", "alg2p"):
         for s in served:
             s.inst.set_stream_cache(2)
     lat = [s.latency[(s.arrivals >= warmup) & np.isfinite(s.latency)] * 1e3 for s in served
@@ -526,9 +549,9 @@ def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_o
     aggregate = {"requests_s": round(len(allat) / max(horizon - warmup, 1e-9), 1),
                  "p50_ms": round(float(np.percentile(allat, 50)), 3) if len(allat) else None,
                  "p99_ms": round(float(np.percentile(allat, 99)), 3) if len(allat) else None}
-    extra = {"queue_order": queue_order} if policy == "paired" else {}
+    extra = {"queue_order": queue_order} if policy in ("paired", "alg2p") else {}
     return {"policy": policy, **extra, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
-            "granule": granule if policy in ("proportional", "alg2") else None, "aggregate": aggregate,
+            "granule": granule if policy in ("proportional", "alg2", "alg2p") else None, "aggregate": aggregate,
             "instances": [s.stats(warmup, horizon) if isinstance(s, (Trainee, Generator)) else s.stats(warmup)
                           for s in served],
             "mean_quota": [round(float(v), 1) for v in qs.mean(0)] if len(qs) else None,

@@ -17,7 +17,7 @@ def served():
         x.inst.close()
 
 
-@pytest.mark.parametrize("policy", ["shared", "static", "proportional", "alg2", "paired"])
+@pytest.mark.parametrize("policy", ["shared", "static", "proportional", "alg2", "paired", "alg2p"])
 def test_policy_serves_every_request(served, policy):
     print(f"serve policy={policy}", flush=True)
     res = serve.run_policy(policy, served, horizon=1.5, warmup=0.2, period=0.01)
@@ -28,9 +28,9 @@ def test_policy_serves_every_request(served, policy):
     assert res["periods"] > 10
     q = np.array(res["mean_quota"])
     assert np.all((q >= 8) & (q <= 256))
-    if policy == "alg2":
+    if policy in ("alg2", "alg2p"):
         assert sum(res["state_counts"].values()) == res["periods"]
-    if policy == "paired":
+    if policy in ("paired", "alg2p"):
         # quotas from the fixed vocabulary only: each instance uses at most the 3 placements of its pair
         for st in res["instances"]:
             assert st["distinct_placements"] <= 3, st
