@@ -345,7 +345,8 @@ const char *iefwd_status_string(int status);
  * Per period, for every instance: R_current = kernels launched during the
  * period (RW keeps the last `window` of them), KLC = duration of its last
  * completed batch (T_current; T_min = the smallest reported).  SLO-sensitive
- * instances (evaluated first, in id order), dT = (T_current - T_min) / T_min:
+ * instances (evaluated first, in id order), dT = (T_current - T_min) / T_min,
+ * or 0 in a period with no KLC reported:
  *   dT > eta_violation                 -> EMERGENCY,  MaxTokens * limit
  *   its RW sums to 0                   -> RECOVERY,   MaxTokens * request
  *   every other instance's RW is 0     -> RECOVERY,   min(R_last * eta_increase, MaxTokens)
@@ -366,7 +367,9 @@ const char *iefwd_status_string(int status);
  * only if the instances outnumber MaxTokens / min_quota.
  * Readings where the paper is silent: the eta defaults; dividing by the KLC
  * ratio 1 + dT rather than dT (dT < 1 would scale up); the SLO scale-up capped
- * at MaxTokens; T_min over the whole history. */
+ * at MaxTokens; T_min over the whole history; no KLC carried over from one
+ * period to the next (a held-over KLC would keep an instance that went idle
+ * after a violation in EMERGENCY, so it could never reach RECOVERY). */
 typedef struct iefwd_ctl iefwd_ctl;
 
 enum { IEFWD_CTL_NONE = 0, IEFWD_CTL_EMERGENCY = 1, IEFWD_CTL_RECOVERY = 2, IEFWD_CTL_CONTENTION = 3 };

@@ -32,8 +32,13 @@ design notes):
       so it is capped at MaxTokens.
   R4  SLO-sensitive instances are evaluated first in a period (they set the
       shared state), then the others, each group in id order.
-  R5  T_current is the most recent reported KLC, T_min the smallest ever
-      reported; before any KLC is reported dT = 0.  R_last starts at
+  R5  T_current is the KLC reported for the current period, T_min the
+      smallest ever reported.  A period in which the instance completed no
+      iteration has no T_current and its dT is 0: nothing was seen to slow
+      down.  (Holding the previous period's KLC instead would keep an instance
+      that went idle after a violation in EMERGENCY, so the text's rule that
+      an instance with no recent kernels scales down could never follow an
+      EMERGENCY.)  Before any KLC is reported dT = 0.  R_last starts at
       MaxTokens * request.  RW holds the last `window` kernel counts.
   R6  tokens become a CU quota: round(R / granule) * granule, clamped to
       [min_quota, MaxTokens].  A CU mask cannot be oversubscribed without the
@@ -67,7 +72,7 @@ class _Inst:
     rw: deque = field(default_factory=deque)
     r_last: float = 0.0
     r_current: int = 0
-    t_current: float = 0.0
+    t_current: float = 0.0          # 0: no KLC this period
     t_min: float = math.inf
     dt: float = 0.0
 
@@ -105,7 +110,7 @@ class Controller:
 
     def _issue_slo(self, i: int) -> float:
         inst = self.insts[i]
-        inst.dt = (inst.t_current - inst.t_min) / inst.t_min if inst.t_min < math.inf else 0.0
+        inst.dt = (inst.t_current - inst.t_min) / inst.t_min if inst.t_current > 0 else 0.0
         others_idle = all(sum(o.rw) == 0 for j, o in enumerate(self.insts) if j != i)
         if inst.dt > self.eta_violation:
             state, r = EMERGENCY, self.max_tokens * inst.limit
@@ -150,6 +155,7 @@ class Controller:
         for i, inst in enumerate(self.insts):
             inst.r_last = out[i]
             inst.r_current = 0
+            inst.t_current = 0.0           # the next period starts with no KLC
         return out
 
     def _fit(self, qs, idx, avail):

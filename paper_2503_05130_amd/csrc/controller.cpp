@@ -47,7 +47,10 @@ uint64_t QuotaController::window_sum(const Inst &in) {
 //   Keep          R_last
 // Readings where the paper's text leaves it open: Yield divides by the KLC
 // ratio 1 + dT (a division by dT alone would scale up for dT < 1), GrowToMax is
-// capped at MaxTokens, and T_min is the smallest KLC over the whole history.
+// capped at MaxTokens, T_min is the smallest KLC over the whole history, and a
+// period in which an instance completed no iteration has no T_current and dT 0
+// (carrying the last KLC over would hold an instance that went idle after a
+// violation in Violation, and the Idle condition could never follow it).
 namespace {
 
 enum class Condition { Violation, Idle, Alone, Sharing };
@@ -91,7 +94,7 @@ double QuotaController::tokens_by_rule(int rule, const Inst &in) const {
 
 double QuotaController::issue_slo(uint32_t i) {
     Inst &in = insts_[i];
-    in.dt = in.t_min > 0 ? (in.t_current - in.t_min) / in.t_min : 0.0;
+    in.dt = in.t_current > 0 ? (in.t_current - in.t_min) / in.t_min : 0.0;
     bool others_idle = true;
     for (uint32_t j = 0; j < insts_.size(); ++j)
         if (j != i && window_sum(insts_[j]) != 0) others_idle = false;
@@ -141,6 +144,7 @@ void QuotaController::issue(std::vector<double> &tokens, std::vector<uint32_t> &
     for (uint32_t i = 0; i < n; ++i) {
         insts_[i].r_last = tokens[i];
         insts_[i].r_current = 0;
+        insts_[i].t_current = 0;   // a period with no completed iteration has no KLC
         const double units = std::floor(tokens[i] / p_.granule + 0.5);
         quotas[i] = (uint32_t)std::max<double>(p_.min_quota, std::min<double>(p_.max_tokens, units * p_.granule));
     }

@@ -62,7 +62,8 @@ private:
         std::deque<uint64_t> rw;      // kernels per period, newest last
         uint64_t r_current = 0;
         double r_last = 0;
-        double t_current = 0, t_min = -1;   // t_min < 0: no KLC reported yet
+        double t_current = 0;   // KLC of this period; 0: none reported in it
+        double t_min = -1;      // < 0: no KLC reported yet
         double dt = 0;
     };
     double issue_slo(uint32_t i);

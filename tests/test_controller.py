@@ -97,6 +97,32 @@ def test_idle_slo_instance_scales_down_and_colocated_grows():
     assert grow[-1] == 128.0
 
 
+def test_idle_after_a_violation_leaves_emergency_and_scales_down():
+    # a burst raises EMERGENCY; when the SLO instance then goes quiet (no
+    # kernels, no completed iteration) nothing is seen to slow down: it falls
+    # back to its request at once and, after a whole idle window, the
+    # co-located instance grows again (Sec. 3.4.1: no recent kernels -> scale
+    # down).  A KLC held over from the burst would keep EMERGENCY and shrink
+    # the neighbour by the KLC ratio every period instead.
+    c = O.Controller(window=2, eta_violation=0.2, eta_increase=1.25)
+    c.add(0.25, 0.5, True)
+    c.add(0.75, 1.0, False)
+    periods(c, [[(50, 10.0), (50, 10.0)]])
+    r = periods(c, [[(50, 30.0), (50, 10.0)]])[-1]
+    assert c.state == EMERG and r == [128.0, 192.0 / 3.0]
+    rs, states = [], []
+    for _ in range(5):
+        rs.append(periods(c, [[(0, 0), (50, 10.0)]])[-1])
+        states.append(c.state)
+    assert states == [CONT, RECOV, RECOV, RECOV, RECOV]
+    assert all(r[0] == 64.0 for r in rs)
+    v, grow = 192.0 / 3.0, []
+    for st in states:
+        v = v if st == CONT else min(v * 1.25, 256.0)
+        grow.append(v)
+    assert [r[1] for r in rs] == grow
+
+
 def test_window_remembers_recent_kernels():
     # one burst keeps an instance active for exactly `window` periods
     c = O.Controller(window=3)
