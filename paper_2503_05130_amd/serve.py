@@ -1,4 +1,4 @@
-"""Co-located serving on one GPU: Poisson request streams into several
+"""Co-located serving on one GPU: Poisson or Gamma request streams into several
 instances, one dispatcher thread per instance, and a quota policy that
 re-masks the instances every control period (the paper's setting of
 Sec. 3.4 and its inference-inference experiments, Sec. 5).
@@ -6,7 +6,8 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
   python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 alg2p static proportional shared paired]
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--granule 32] [--small]
                                        [--mix inference|train|decode] [--queue-probe]
-                                       [--queue-order rounds|instance]
+                                       [--queue-order rounds|instance] [--cv 1] [--klc device|cycle]
+                                       [--eta-violation 0.2] [--window 4]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
 batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
@@ -54,6 +55,12 @@ Policies (each period):
 
 --granule sets the quota granularity (in CUs) of proportional and alg2.
 
+--cv sets the coefficient of variation of the inference instances'
+inter-arrival gaps: 1 is a Poisson stream; other values draw Gamma-distributed
+gaps of the same mean (shape 1/cv^2), the fluctuating workloads of the paper's
+fast-adaptivity experiment (Sec. 5).  In the train and decode mixes it applies
+to the inference instance.
+
 A new quota's masked stream is created by the control thread
 (iefwd_prepare_quota_at) before the quota is posted, so a dispatcher only
 switches streams at its next batch boundary.
@@ -64,8 +71,18 @@ batch of the same size it has run on the same quota (times 1 ms).  So the
 controller's KLC change measures the slowdown of an iteration of one shape on
 one CU share -- contention -- rather than a change of batch size or of its own
 quota (which the controller itself causes).  This per-<batch, quota> baseline
-is what the paper's profiler supplies (Sec. 3.2).  Inputs are seeded synthetic embeddings already
-in device memory; weights are the library's seeded random init.
+is what the paper's profiler supplies (Sec. 3.2).
+
+--klc cycle measures instead each batch's cycle from the arrival of its oldest
+request to its completion, relative to the same fastest device time.  The
+paper reads a KLC rise as contention or a burst of the instance's own requests
+(Sec. 3.4.1); there an instance's kernels wait for tokens, so a burst
+lengthens its launch cycle.  Under CU masks nothing holds a launch back and a
+batch's device time does not see a burst, which shows only as requests
+waiting for the instance's CUs: the cycle counts that wait.
+
+Inputs are seeded synthetic embeddings already in device memory; weights are
+the library's seeded random init.
 """
 from __future__ import annotations
 
@@ -97,8 +114,24 @@ def default_mix(small: bool = False):
             ("dec_b", DECODER, 1024, 2, 10.0, 0.25, 0.5, False, 54)]
 
 
+def arrival_gaps(rng, rate, cv, n):
+    """n inter-arrival gaps of mean 1/rate.  cv 1: exponential (a Poisson
+    stream); otherwise Gamma with shape 1/cv^2 and scale cv^2/rate, whose
+    coefficient of variation is cv -- the fluctuating workloads of the paper's
+    fast-adaptivity experiment (Sec. 5), where CV grows up to 6."""
+    if cv <= 0:
+        raise ValueError("cv must be positive")
+    if cv == 1.0:
+        return rng.exponential(1.0 / rate, size=n)
+    k = 1.0 / (cv * cv)
+    return rng.gamma(k, 1.0 / (rate * k), size=n)
+
+
 class Served:
     """One instance with its request stream, pool of inputs and statistics."""
+
+    cv = 1.0                                # coefficient of variation of the inter-arrival gaps
+    klc = "device"                          # what the KLC of a batch measures: "device" or "cycle"
 
     def __init__(self, idx, name, shape, seq, max_batch, rate, request, limit, slo, seed, pool=16):
         self.idx, self.name, self.seq, self.max_batch, self.rate = idx, name, seq, max_batch, rate
@@ -112,7 +145,7 @@ class Served:
     def reset(self, horizon):
         """Fresh request stream (the same for every policy) and statistics."""
         arr = np.random.default_rng(5100 + self.idx)
-        gaps = arr.exponential(1.0 / self.rate, size=int(self.rate * horizon * 2) + 16)
+        gaps = arrival_gaps(arr, self.rate, self.cv, int(self.rate * horizon * 2) + 16)
         t = np.cumsum(gaps)
         self.arrivals = t[t < horizon]
         self.latency = np.full(len(self.arrivals), np.nan)
@@ -143,6 +176,7 @@ class Served:
                 time.sleep(min(self.arrivals[self.next] - now, 0.002))
                 continue
             k = min(self.max_batch, self.queue_len(now))
+            oldest = self.arrivals[self.next]
             with self.lock:                 # taking the quota and marking the batch start together
                 pend, self.pending = self.pending, None
                 self.busy = True
@@ -169,9 +203,10 @@ class Served:
             key = (k, self.applied[0] if self.applied else 0)
             best = min(self.best_ms.get(key, ms), ms)
             self.best_ms[key] = best
+            cyc = (done - oldest) * 1e3 if self.klc == "cycle" else ms
             with self.lock:
                 self.kernels = self.inst.kernels_launched()
-                self.ratios.append(ms / best)
+                self.ratios.append(cyc / best)
 
     def batch_stats(self, warmup):
         """Device time per batch (ms): first batches after a quota switch and the others."""
@@ -189,6 +224,7 @@ class Served:
         return {"name": self.name, "requests": int(keep.sum()), "dropped": int(np.isnan(self.latency).sum()),
                 "batch_device_ms": self.batch_stats(warmup),
                 "p50_ms": round(float(np.percentile(lat, 50)), 3) if len(lat) else None,
+                "p95_ms": round(float(np.percentile(lat, 95)), 3) if len(lat) else None,
                 "p99_ms": round(float(np.percentile(lat, 99)), 3) if len(lat) else None,
                 "batches": self.batches, "quota_changes": self.changes, "distinct_placements": len(self.plans),
                 "klc_ratio_p50_p90": ([round(float(np.percentile(self.klc_log, p)), 3) for p in (50, 90)]
@@ -408,12 +444,12 @@ def controller_quotas(ctl, served, last_k, firsts_out=None):
     return list(qs)
 
 
-def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRANULE):
+def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRANULE, ctl_params=None):
     n_cu = ie.device_info(0)[0]
     ctl = None
     paired_like = policy in ("paired", "alg2p")
     if policy in ("alg2", "alg2p"):
-        ctl = ie.Controller(max_tokens=n_cu, granule=granule, min_quota=granule)
+        ctl = ie.Controller(max_tokens=n_cu, granule=granule, min_quota=granule, **(ctl_params or {}))
         for s in served:
             ctl.add(s.request, s.limit, s.slo)
     last_k = [s.kernels for s in served]
@@ -517,7 +553,7 @@ def prepare_paired(served, queue_order="rounds"):
         inst.set_stream_cache(len(PAIR_SPLITS))
 
 
-def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_order="rounds"):
+def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_order="rounds", ctl_params=None):
     for s in served:
         s.reset(horizon)
         if isinstance(s, (Trainee, Generator)):
@@ -531,7 +567,8 @@ def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_o
     stop, history = threading.Event(), []
     t0 = time.perf_counter()
     threads = [threading.Thread(target=s.run, args=(t0, horizon, stop)) for s in served]
-    ctl = threading.Thread(target=control_loop, args=(policy, served, t0, horizon, period, stop, history, granule))
+    ctl = threading.Thread(target=control_loop,
+                           args=(policy, served, t0, horizon, period, stop, history, granule, ctl_params))
     for t in threads + [ctl]:
         t.start()
     for t in threads:
@@ -548,8 +585,11 @@ def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_o
     allat = np.concatenate(lat) if lat else np.zeros(0)
     aggregate = {"requests_s": round(len(allat) / max(horizon - warmup, 1e-9), 1),
                  "p50_ms": round(float(np.percentile(allat, 50)), 3) if len(allat) else None,
+                 "p95_ms": round(float(np.percentile(allat, 95)), 3) if len(allat) else None,
                  "p99_ms": round(float(np.percentile(allat, 99)), 3) if len(allat) else None}
     extra = {"queue_order": queue_order} if policy in ("paired", "alg2p") else {}
+    if policy in ("alg2", "alg2p") and ctl_params:
+        extra["ctl_params"] = dict(ctl_params)
     return {"policy": policy, **extra, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
             "granule": granule if policy in ("proportional", "alg2", "alg2p") else None, "aggregate": aggregate,
             "instances": [s.stats(warmup, horizon) if isinstance(s, (Trainee, Generator)) else s.stats(warmup)
@@ -573,15 +613,18 @@ def train_mix(small: bool = False):
     return [inf, trn]
 
 
-def run_train_mix(policies, horizon, warmup, period, small=False):
+def run_train_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="device", ctl_params=None):
     """Each policy with both instances, then each instance alone on the whole
     GPU ("exclusive"); the paper compares co-location against exclusive."""
     served = train_mix(small)
+    served[0].cv, served[0].klc = cv, klc   # the inference instance's arrivals and KLC
     out = []
     try:
         for pol in policies:
             name, _, per = pol.partition("@")
-            res = run_policy(name, served, horizon, warmup, (float(per) if per else period) / 1e3)
+            res = run_policy(name, served, horizon, warmup, (float(per) if per else period) / 1e3,
+                             ctl_params=ctl_params)
+            res["label"] = pol
             out.append(res)
             print(json.dumps(res), flush=True)
         for one in served:
@@ -599,11 +642,12 @@ def run_train_mix(policies, horizon, warmup, period, small=False):
             continue
         inf, trn = r["instances"]
         e_inf, e_trn = excl["bert_inf"], excl["bert_train"]
-        summary[r["policy"]] = {
+        summary[r.get("label", r["policy"])] = {
             "inference_p50_vs_exclusive": round(inf["p50_ms"] / e_inf["p50_ms"], 3) if inf["p50_ms"] else None,
+            "inference_p95_vs_exclusive": round(inf["p95_ms"] / e_inf["p95_ms"], 3) if inf["p95_ms"] else None,
             "inference_p99_vs_exclusive": round(inf["p99_ms"] / e_inf["p99_ms"], 3) if inf["p99_ms"] else None,
             "training_throughput_vs_exclusive": round(trn["steps_s"] / e_trn["steps_s"], 3) if e_trn["steps_s"] else None}
-    print(json.dumps({"train_inf_summary": summary}), flush=True)
+    print(json.dumps({"train_inf_summary": summary, "cv": cv, "klc": klc}), flush=True)
     return out, summary
 
 
@@ -621,14 +665,17 @@ def decode_mix(small: bool = False):
     return [inf, gen]
 
 
-def run_decode_mix(policies, horizon, warmup, period, small=False):
+def run_decode_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="device", ctl_params=None):
     """Each policy with both instances, then each alone on the whole GPU."""
     served = decode_mix(small)
+    served[0].cv, served[0].klc = cv, klc   # the inference instance's arrivals and KLC
     out = []
     try:
         for pol in policies:
             name, _, per = pol.partition("@")
-            res = run_policy(name, served, horizon, warmup, (float(per) if per else period) / 1e3)
+            res = run_policy(name, served, horizon, warmup, (float(per) if per else period) / 1e3,
+                             ctl_params=ctl_params)
+            res["label"] = pol
             out.append(res)
             print(json.dumps(res), flush=True)
         for one in served:
@@ -646,13 +693,14 @@ def run_decode_mix(policies, horizon, warmup, period, small=False):
             continue
         inf, gen = r["instances"]
         e_inf, e_gen = excl["bert_inf"], excl["decoder_gen"]
-        summary[r["policy"]] = {
+        summary[r.get("label", r["policy"])] = {
             "inference_p50_vs_exclusive": round(inf["p50_ms"] / e_inf["p50_ms"], 3) if inf["p50_ms"] else None,
+            "inference_p95_vs_exclusive": round(inf["p95_ms"] / e_inf["p95_ms"], 3) if inf["p95_ms"] else None,
             "inference_p99_vs_exclusive": round(inf["p99_ms"] / e_inf["p99_ms"], 3) if inf["p99_ms"] else None,
             "tpot_p50_vs_exclusive": round(gen["tpot_p50_ms"] / e_gen["tpot_p50_ms"], 3) if gen["tpot_p50_ms"] else None,
             "tpot_p99_vs_exclusive": round(gen["tpot_p99_ms"] / e_gen["tpot_p99_ms"], 3) if gen["tpot_p99_ms"] else None,
             "decode_tokens_vs_exclusive": round(gen["tokens_s"] / e_gen["tokens_s"], 3) if e_gen["tokens_s"] else None}
-    print(json.dumps({"decode_inf_summary": summary}), flush=True)
+    print(json.dumps({"decode_inf_summary": summary, "cv": cv, "klc": klc}), flush=True)
     return out, summary
 
 
@@ -759,28 +807,45 @@ def main() -> int:
                          "decode: inference beside a token-by-token decoder")
     ap.add_argument("--queue-probe", action="store_true",
                     help="measure what creating, switching and keeping masked queues costs co-located instances")
+    ap.add_argument("--cv", type=float, default=1.0,
+                    help="coefficient of variation of the inference instances' inter-arrival gaps "
+                         "(1: Poisson; otherwise Gamma-distributed gaps of the same mean)")
+    ap.add_argument("--klc", choices=["device", "cycle"], default="device",
+                    help="KLC reported to alg2/alg2p: a batch's device time, or its cycle from the arrival of "
+                         "its oldest request, each relative to the fastest batch of its size and quota")
+    ap.add_argument("--eta-violation", type=float, default=None,
+                    help="alg2/alg2p: relative KLC rise that raises EMERGENCY (the library's default if omitted)")
+    ap.add_argument("--window", type=int, default=None,
+                    help="alg2/alg2p: kernel-rate window RW in control periods (the library's default if omitted)")
     ap.add_argument("--queue-order", choices=["rounds", "instance"], default="rounds",
                     help="order in which the paired policy prepares its placements' queues")
     args = ap.parse_args()
+    ctl_params = {k: v for k, v in (("eta_violation", args.eta_violation), ("window", args.window)) if v is not None}
     if args.queue_probe:
         queue_probe()
         return 0
     if args.mix == "train":
-        run_train_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small)
+        run_train_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, args.cv, args.klc,
+                      ctl_params)
         return 0
     if args.mix == "decode":
-        run_decode_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small)
+        run_decode_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, args.cv, args.klc,
+                      ctl_params)
         return 0
     t = time.perf_counter()
     served = build_mix(default_mix(args.small))
+    for s in served:
+        s.cv, s.klc = args.cv, args.klc
     print(json.dumps({"setup_s": round(time.perf_counter() - t, 1),
-                      "mix": [(s.name, s.seq, s.max_batch, s.rate, s.request, s.limit, s.slo) for s in served]}),
+                      "mix": [(s.name, s.seq, s.max_batch, s.rate, s.request, s.limit, s.slo) for s in served],
+                      "cv": args.cv, "klc": args.klc}),
           flush=True)
     try:
         for pol in args.policy:
             name, _, per = pol.partition("@")          # "alg2@100": policy with its own period in ms
             period = float(per) if per else args.period_ms
-            res = run_policy(name, served, args.horizon, args.warmup, period / 1e3, args.granule, args.queue_order)
+            res = run_policy(name, served, args.horizon, args.warmup, period / 1e3, args.granule, args.queue_order,
+                             ctl_params)
             print(json.dumps(res), flush=True)
     finally:
         for s in served:

@@ -71,3 +71,70 @@ def test_prepare_order(monkeypatch, order):
         assert [i for i, _, _ in log] == [i for i in range(n) for _ in range(k)]
     # the caches end holding exactly the prepared placements
     assert all(s.inst.cache == k for s in served)
+
+
+@pytest.mark.parametrize("cv", [1.0, 2.0, 4.0, 6.0])
+def test_arrival_gaps_mean_and_cv(cv):
+    # Gamma gaps with shape 1/cv^2 and scale cv^2/rate: mean 1/rate, std cv/rate
+    import numpy as np
+    g = serve.arrival_gaps(np.random.default_rng(7), 200.0, cv, 400_000)
+    assert (g >= 0).all()
+    assert abs(g.mean() * 200.0 - 1.0) < 0.03
+    assert abs(g.std() / g.mean() - cv) < 0.03 * cv
+
+
+def test_arrival_gaps_poisson_stream_unchanged():
+    # cv 1 is the exponential stream the harness drew before the option existed
+    import numpy as np
+    a = serve.arrival_gaps(np.random.default_rng(5100), 200.0, 1.0, 1000)
+    b = np.random.default_rng(5100).exponential(1.0 / 200.0, size=1000)
+    assert np.array_equal(a, b)
+    with pytest.raises(ValueError):
+        serve.arrival_gaps(np.random.default_rng(0), 200.0, 0.0, 4)
+
+
+class FakeDev:
+    """Stands in for an instance: every batch takes `ms` of device time."""
+
+    def __init__(self, ms):
+        self.ms, self.n = ms, 0
+
+    def set_quota(self, q, first):
+        pass
+
+    def submit(self, x):
+        self.n += 1
+
+    def wait(self):
+        import time
+        time.sleep(self.ms / 1e3)
+
+    def last_batch_ms(self):
+        return self.ms
+
+    def kernels_launched(self):
+        return 100 * self.n
+
+
+@pytest.mark.parametrize("klc", ["device", "cycle"])
+def test_dispatcher_klc_modes(monkeypatch, klc):
+    # a burst of 12 requests at t = 0 into batches of up to 4 taking 2 ms each:
+    # device-time ratios stay 1, cycle ratios grow with the wait in the queue
+    import threading
+    import time
+    import numpy as np
+    monkeypatch.setattr(serve.ie, "device_info", lambda dev: (256, 8))
+    s = object.__new__(serve.Served)
+    s.idx, s.name, s.max_batch, s.rate, s.slo = 0, "fake", 4, 1.0, True
+    s.inst, s.pool, s.lock, s.klc = FakeDev(2.0), [None] * 16, threading.Lock(), klc
+    s.reset(1.0)
+    s.arrivals = np.zeros(12)
+    s.latency = np.full(12, np.nan)
+    s.run(time.perf_counter(), 1.0, threading.Event())
+    assert s.next == 12 and s.batches == 3 and np.isfinite(s.latency).all()
+    if klc == "device":
+        assert s.ratios == [1.0, 1.0, 1.0]
+    else:
+        # the k-th batch's oldest request waited for the k-1 batches before it
+        assert all(r >= k + 1 for k, r in enumerate(s.ratios))
+        assert s.ratios == sorted(s.ratios)
