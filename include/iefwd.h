@@ -380,12 +380,21 @@ typedef struct {
     uint32_t window;         /* RW length in control periods; >= 1 */
     uint32_t granule;        /* quotas are multiples of this many CUs; >= 1 */
     uint32_t min_quota;      /* smallest quota issued; 1 .. max_tokens */
-    uint32_t reserved0;      /* must be 0 */
+    uint32_t flags;          /* 0 or IEFWD_CTL_TEMPORARY_YIELD (below) */
     double eta_violation;    /* relative KLC increase that raises EMERGENCY; >= 0 */
     double eta_increase;     /* multiplicative scale-up per period; >= 1 */
 } iefwd_ctl_params;
 
-/* Defaults: max_tokens 256, window 4, granule 8, min_quota 8,
+/* flags: the text calls the co-located instances' scale-down under EMERGENCY
+ * temporary, while the listing keeps R_last in CONTENTION, so that without
+ * this flag a yielded issue becomes R_last and is undone only through
+ * RECOVERY (the SLO-sensitive instances idle for a whole window).  With it a
+ * yielded issue leaves R_last, the plan held before the emergency, unchanged:
+ * consecutive EMERGENCY periods do not compound the yield, and CONTENTION
+ * afterwards restores the plan. */
+#define IEFWD_CTL_TEMPORARY_YIELD 1u
+
+/* Defaults: max_tokens 256, window 4, granule 8, min_quota 8, flags 0,
  * eta_violation 0.2, eta_increase 1.25. */
 int iefwd_ctl_params_init(iefwd_ctl_params *p);
 

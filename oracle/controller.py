@@ -51,6 +51,15 @@ design notes):
       instances take mask bits upward from 0 (id order), the others downward
       from the top (id order), so a change of one quota moves one boundary.
 
+  R8  the text calls the co-located instances' scale-down under EMERGENCY
+      temporary, while the listing keeps R_last in CONTENTION, so that a
+      scale-down is undone only through RECOVERY (the SLO instance idle for a
+      whole window).  Both are offered: by default (temporary_yield False) a
+      yielded issue becomes R_last, as the listing reads; with temporary_yield
+      True a yielded issue does not replace R_last, so the yield is computed
+      from the plan held before the emergency (consecutive EMERGENCY periods
+      do not compound it) and CONTENTION afterwards restores that plan.
+
 Parity unpinned against numbers printed in the paper (it prints no controller
 traces); pinned against the behaviour its text describes (tests).
 """
@@ -80,7 +89,8 @@ class _Inst:
 class Controller:
     """IssueToken (Alg. 2) for a set of co-located instances."""
 
-    def __init__(self, max_tokens=256, window=4, granule=8, min_quota=8, eta_violation=0.2, eta_increase=1.25):
+    def __init__(self, max_tokens=256, window=4, granule=8, min_quota=8, eta_violation=0.2, eta_increase=1.25,
+                 temporary_yield=False):
         self.max_tokens = float(max_tokens)
         self.n_cu = int(max_tokens)
         self.window = int(window)
@@ -88,6 +98,7 @@ class Controller:
         self.min_quota = int(min_quota)
         self.eta_violation = float(eta_violation)
         self.eta_increase = float(eta_increase)
+        self.temporary_yield = bool(temporary_yield)
         self.insts: list[_Inst] = []
         self.state = NONE
         self.owner = -1            # instance that raised EMERGENCY
@@ -152,8 +163,10 @@ class Controller:
         for i, inst in enumerate(self.insts):
             if not inst.slo:
                 out[i] = self._issue_other(i)
+        yielded = self.state == EMERGENCY and self.temporary_yield
         for i, inst in enumerate(self.insts):
-            inst.r_last = out[i]
+            if inst.slo or not yielded:        # a temporary yield leaves the plan R_last as it was
+                inst.r_last = out[i]
             inst.r_current = 0
             inst.t_current = 0.0           # the next period starts with no KLC
         return out

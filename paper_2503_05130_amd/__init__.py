@@ -467,22 +467,28 @@ class Trainer(Instance):
         return out
 
 
+CTL_TEMPORARY_YIELD = 1
+
+
 class CtlParams(ctypes.Structure):
     _fields_ = [("abi_version", _u32), ("max_tokens", _u32), ("window", _u32), ("granule", _u32),
-                ("min_quota", _u32), ("reserved0", _u32), ("eta_violation", ctypes.c_double),
+                ("min_quota", _u32), ("flags", _u32), ("eta_violation", ctypes.c_double),
                 ("eta_increase", ctypes.c_double)]
 
 
 class Controller:
     """The fast scale-up/down quota controller (iefwd_ctl_*): report each
     instance's kernels and last batch time once per control period, then
-    issue() returns (tokens, quotas, first mask bits) in id order."""
+    issue() returns (tokens, quotas, first mask bits) in id order.
+    temporary_yield=True sets IEFWD_CTL_TEMPORARY_YIELD."""
 
-    def __init__(self, **params):
+    def __init__(self, temporary_yield: bool = False, **params):
         p = CtlParams()
         _check(lib().iefwd_ctl_params_init(ctypes.byref(p)), "iefwd_ctl_params_init")
         for k, v in params.items():
             setattr(p, k, v)
+        if temporary_yield:
+            p.flags |= CTL_TEMPORARY_YIELD
         h = _vp()
         _check(lib().iefwd_ctl_create(ctypes.byref(p), ctypes.byref(h)), "iefwd_ctl_create")
         self._h = h.value

@@ -141,8 +141,13 @@ void QuotaController::issue(std::vector<double> &tokens, std::vector<uint32_t> &
     // the others downward from the top
     quotas.assign(n, 0);
     firsts.assign(n, 0);
+    // the text calls the co-located instances' EMERGENCY scale-down temporary:
+    // with temporary_yield their plan R_last survives it, so the yield does
+    // not compound over consecutive EMERGENCY periods and CONTENTION restores
+    // the plan; without it the yielded issue becomes R_last as in the listing
+    const bool yielded = state_ == Emergency && p_.temporary_yield;
     for (uint32_t i = 0; i < n; ++i) {
-        insts_[i].r_last = tokens[i];
+        if (insts_[i].slo || !yielded) insts_[i].r_last = tokens[i];
         insts_[i].r_current = 0;
         insts_[i].t_current = 0;   // a period with no completed iteration has no KLC
         const double units = std::floor(tokens[i] / p_.granule + 0.5);

@@ -37,6 +37,7 @@ public:
         uint32_t min_quota = 8;      // smallest quota issued
         double eta_violation = 0.2;  // relative KLC increase that raises EMERGENCY
         double eta_increase = 1.25;  // multiplicative scale-up per period
+        bool temporary_yield = false;  // an EMERGENCY yield leaves R_last (the plan) unchanged
     };
 
     explicit QuotaController(const Params &p) : p_(p) {}

@@ -1515,7 +1515,7 @@ int iefwd_ctl_create(const iefwd_ctl_params *p, iefwd_ctl **out) {
         if (!p) fail(IEFWD_EINVAL, "params is NULL");
         if (p->abi_version != IEFWD_ABI_VERSION) fail(IEFWD_EVERSION, "params.abi_version mismatch");
         if (p->max_tokens == 0 || p->window == 0 || p->granule == 0 || p->min_quota == 0 ||
-            p->min_quota > p->max_tokens || p->reserved0 != 0)
+            p->min_quota > p->max_tokens || (p->flags & ~IEFWD_CTL_TEMPORARY_YIELD) != 0)
             fail(IEFWD_EINVAL, "controller sizes out of range");
         if (!(p->eta_violation >= 0) || !(p->eta_increase >= 1) || !std::isfinite(p->eta_violation) ||
             !std::isfinite(p->eta_increase))
@@ -1527,6 +1527,7 @@ int iefwd_ctl_create(const iefwd_ctl_params *p, iefwd_ctl **out) {
         q.min_quota = p->min_quota;
         q.eta_violation = p->eta_violation;
         q.eta_increase = p->eta_increase;
+        q.temporary_yield = (p->flags & IEFWD_CTL_TEMPORARY_YIELD) != 0;
         *out = reinterpret_cast<iefwd_ctl *>(new QuotaController(q));
     });
 }

@@ -7,7 +7,7 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--granule 32] [--small]
                                        [--mix inference|train|decode] [--queue-probe]
                                        [--queue-order rounds|instance] [--cv 1] [--klc device|cycle]
-                                       [--eta-violation 0.2] [--window 4]
+                                       [--eta-violation 0.2] [--window 4] [--temporary-yield]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
 batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
@@ -817,10 +817,15 @@ def main() -> int:
                     help="alg2/alg2p: relative KLC rise that raises EMERGENCY (the library's default if omitted)")
     ap.add_argument("--window", type=int, default=None,
                     help="alg2/alg2p: kernel-rate window RW in control periods (the library's default if omitted)")
+    ap.add_argument("--temporary-yield", action="store_true",
+                    help="alg2/alg2p: an EMERGENCY scale-down of the co-located instances leaves their plan unchanged "
+                         "(IEFWD_CTL_TEMPORARY_YIELD)")
     ap.add_argument("--queue-order", choices=["rounds", "instance"], default="rounds",
                     help="order in which the paired policy prepares its placements' queues")
     args = ap.parse_args()
     ctl_params = {k: v for k, v in (("eta_violation", args.eta_violation), ("window", args.window)) if v is not None}
+    if args.temporary_yield:
+        ctl_params["temporary_yield"] = True
     if args.queue_probe:
         queue_probe()
         return 0

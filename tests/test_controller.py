@@ -123,6 +123,36 @@ def test_idle_after_a_violation_leaves_emergency_and_scales_down():
     assert [r[1] for r in rs] == grow
 
 
+def test_listing_yield_persists_under_contention():
+    # the listing: the yielded issue becomes R_last, and CONTENTION keeps it,
+    # so while the SLO instance stays busy the co-located one stays shrunk;
+    # two EMERGENCY periods in a row divide twice
+    c = O.Controller(eta_violation=0.2)
+    c.add(0.25, 0.5, True)
+    c.add(0.75, 1.0, False)
+    periods(c, [[(50, 10.0), (50, 10.0)]])
+    r = periods(c, [[(50, 20.0), (50, 10.0)]] * 2 + [[(50, 10.0), (50, 10.0)]] * 3)
+    assert [x[1] for x in r] == [96.0, 48.0, 48.0, 48.0, 48.0]
+    assert [x[0] for x in r] == [128.0, 128.0, 64.0, 64.0, 64.0]
+
+
+def test_temporary_yield_restores_the_plan():
+    # the text's "temporarily resized down": the yield is taken from the plan
+    # held before the emergency, does not compound, and CONTENTION restores it
+    c = O.Controller(eta_violation=0.2, temporary_yield=True)
+    c.add(0.25, 0.5, True)
+    c.add(0.75, 1.0, False)
+    periods(c, [[(50, 10.0), (50, 10.0)]])
+    r = periods(c, [[(50, 20.0), (50, 10.0)]] * 2 + [[(50, 10.0), (50, 10.0)]] * 3)
+    assert [x[1] for x in r] == [96.0, 96.0, 192.0, 192.0, 192.0]
+    assert [x[0] for x in r] == [128.0, 128.0, 64.0, 64.0, 64.0]
+    # once the SLO instance has been idle for a whole window (4 periods),
+    # RECOVERY grows the co-located one from the plan, not from the yield
+    r = periods(c, [[(0, 0), (50, 10.0)]] * 5)
+    assert [x[1] for x in r] == [192.0, 192.0, 192.0, 240.0, 256.0]
+    assert c.state == RECOV
+
+
 def test_window_remembers_recent_kernels():
     # one burst keeps an instance active for exactly `window` periods
     c = O.Controller(window=3)
@@ -222,7 +252,7 @@ def random_scenario(seed, n_periods=300):
 def test_library_matches_oracle(seed):
     insts, obs = random_scenario(seed)
     params = dict(window=int(1 + seed % 5), eta_violation=[0.1, 0.2, 0.5][seed % 3],
-                  eta_increase=[1.1, 1.25, 2.0][seed % 3])
+                  eta_increase=[1.1, 1.25, 2.0][seed % 3], temporary_yield=seed % 2 == 1)
     o = O.Controller(**params)
     lib = ie.Controller(**params)
     for req, lim, slo in insts:
@@ -250,7 +280,7 @@ def test_controller_abi_errors():
     h = ie.ctypes.c_void_p()
     for field, bad, status in [("abi_version", 99, ie.EVERSION), ("window", 0, ie.EINVAL),
                                ("min_quota", 300, ie.EINVAL), ("eta_increase", 0.5, ie.EINVAL),
-                               ("eta_violation", math.nan, ie.EINVAL), ("reserved0", 1, ie.EINVAL)]:
+                               ("eta_violation", math.nan, ie.EINVAL), ("flags", 2, ie.EINVAL)]:
         q = ie.CtlParams.from_buffer_copy(p)
         setattr(q, field, bad)
         assert ie.lib().iefwd_ctl_create(ie.ctypes.byref(q), ie.ctypes.byref(h)) == status, field
