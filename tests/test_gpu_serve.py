@@ -1,6 +1,6 @@
 """Co-located serving with a quota policy per control period (small models,
 short horizon): every request is served under each policy and the controller
-re-masks the instances."""
+re-masks the instances; also under bursty (Gamma) arrivals with the cycle KLC."""
 import numpy as np
 import pytest
 
@@ -73,3 +73,24 @@ def test_decode_beside_inference():
     for pol in ("static", "alg2"):
         v = summary[pol]
         assert v["inference_p50_vs_exclusive"] > 0 and v["tpot_p50_vs_exclusive"] > 0
+
+
+@pytest.mark.parametrize("temporary_yield", [False, True])
+def test_training_beside_bursty_inference(temporary_yield):
+    """Gamma arrivals at CV 4 into the inference instance, the cycle KLC, and
+    either yield reading of the controller (small models): every request is
+    served, training completes steps, and the controller's parameters are
+    recorded with the result."""
+    params = {"temporary_yield": True} if temporary_yield else None
+    print(f"train mix cv 4 klc cycle temporary_yield={temporary_yield}", flush=True)
+    out, summary = serve.run_train_mix(["alg2"], horizon=1.5, warmup=0.2, period=10.0, small=True, cv=4.0,
+                                       klc="cycle", ctl_params=params)
+    alg2 = out[0]
+    assert alg2["policy"] == "alg2" and alg2.get("ctl_params") == params
+    assert sum(alg2["state_counts"].values()) == alg2["periods"] > 10
+    inf, trn = alg2["instances"]
+    assert inf["dropped"] == 0 and inf["requests"] > 0
+    assert inf["p99_ms"] >= inf["p95_ms"] >= inf["p50_ms"] > 0
+    assert inf["klc_ratio_p50_p90"] is not None and inf["klc_ratio_p50_p90"][0] >= 0.99
+    assert trn["steps"] > 0
+    assert summary["alg2"]["inference_p95_vs_exclusive"] > 0
