@@ -506,7 +506,9 @@ def stop_clock_sampler(proc, path: str, t0: float, t1: float):
     except ProcessLookupError:
         pass
     proc.wait(timeout=10)
-    text = open(path).read()
+    with open(path) as f:
+        text = f.read()
+    os.remove(path)
     blocks = re.split(r"^(\d+\.\d+)\s*$", text, flags=re.M)
     means = []
     for i in range(1, len(blocks) - 1, 2):
@@ -578,11 +580,15 @@ def main() -> int:
         print("--timer-every must be >= 1", file=sys.stderr)
         return 2
 
-    clock_path = os.path.join(ROOT, "gpurun_out", "bench_sclk_samples.txt")
+    clock_path = None
     sampler = None
     if not (args.no_clock or args.decode_only or args.train_only):
-        os.makedirs(os.path.dirname(clock_path), exist_ok=True)
+        import tempfile
+        fd, clock_path = tempfile.mkstemp(prefix="bench_sclk_", suffix=".txt")
+        os.close(fd)
         sampler = start_clock_sampler(clock_path)   # before anything touches the GPU
+        if sampler is None:
+            os.remove(clock_path)
 
     import torch
 
