@@ -171,7 +171,10 @@ int iefwd_prepare_quota_at(iefwd_instance *inst, uint32_t n_cu, uint32_t first);
  * their batch times; created instance by instance, a latency-sensitive
  * instance's batches ran 5-8 times slower whenever another instance's long
  * GEMM launches ran, on whatever CUs.  The queues appear to be dealt to the
- * device's dispatch pipes in creation order.  EINVAL outside 1 .. 16. */
+ * device's dispatch pipes in creation order.  A placement still cached is not
+ * created again, which shifts every later queue of a round order: shrink the
+ * caches to 1 (the stream in use) before creating a set of placements in
+ * rounds.  EINVAL outside 1 .. 16. */
 int iefwd_set_stream_cache(iefwd_instance *inst, uint32_t capacity);
 
 /* Requests an explicit CU mask (n_words 32-bit words, bit order as above);

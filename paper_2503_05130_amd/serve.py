@@ -528,7 +528,9 @@ def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRA
 def prepare_paired(served, queue_order="rounds"):
     """Prepares every placement the paired policy can issue, sizes each stream
     cache to hold exactly them (the full-device stream is dropped), and starts
-    every instance on the even split.  queue_order "rounds": one new queue per
+    every instance on the even split.  Every cached masked stream but the
+    full-device one is destroyed first, so that each placement is created
+    here, in the chosen order.  queue_order "rounds": one new queue per
     instance per round, instances in the order their full-device queues were
     made, so that the k-th queue of every instance sits at the same position
     modulo the instance count; "instance": each instance's queues in turn."""
@@ -536,7 +538,15 @@ def prepare_paired(served, queue_order="rounds"):
     members = sorted((idx, pi, second) for pi, (a, b) in enumerate(pairs_of(served))
                      for idx, second in ((a, False), (b, True)))
     for idx, _, _ in members:
-        served[idx].inst.set_stream_cache(len(PAIR_SPLITS) + 1)
+        # Only the full-device stream survives: a placement still cached from
+        # an earlier policy would not be created below, and every later queue
+        # would land one step off the round order.
+        inst = served[idx].inst
+        inst.set_quota(n_cu, 0)
+        inst.submit(served[idx].pool[:1])
+        inst.wait()
+        inst.set_stream_cache(1)
+        inst.set_stream_cache(len(PAIR_SPLITS) + 1)
     if queue_order == "rounds":
         jobs = [(m, sp) for sp in PAIR_SPLITS for m in members]
     else:

@@ -7,20 +7,42 @@ from paper_2503_05130_amd import serve
 
 
 class FakeInst:
-    def __init__(self, log, idx):
-        self.log, self.idx, self.cache = log, idx, None
+    """A stream cache like the library's: an LRU of placements, the one in use
+    never evicted; prepare_quota creates a queue (logged) only for a placement
+    not already cached."""
+
+    def __init__(self, log, idx, n_cu=256):
+        self.log, self.idx, self.cache = log, idx, 2
+        self.current, self.pending = (n_cu, 0), None
+        self.lru = [self.current]               # least recently used first
+
+    def _touch(self, pl):
+        if pl in self.lru:
+            self.lru.remove(pl)
+        else:
+            self.log.append((self.idx,) + pl)
+        self.lru.append(pl)
+        self._trim()
+
+    def _trim(self):
+        while len(self.lru) > self.cache:
+            victim = next(p for p in self.lru if p != self.current)
+            self.lru.remove(victim)
 
     def set_stream_cache(self, n):
         self.cache = n
+        self._trim()
 
     def prepare_quota(self, q, first):
-        self.log.append((self.idx, q, first))
+        self._touch((q, first))
 
     def set_quota(self, q, first):
-        pass
+        self.pending = (q, first)
 
     def submit(self, x):
-        pass
+        if self.pending is not None:
+            self.current, self.pending = self.pending, None
+            self._touch(self.current)
 
     def wait(self):
         pass
@@ -70,7 +92,26 @@ def test_prepare_order(monkeypatch, order):
     else:
         assert [i for i, _, _ in log] == [i for i in range(n) for _ in range(k)]
     # the caches end holding exactly the prepared placements
-    assert all(s.inst.cache == k for s in served)
+    assert all(s.inst.cache == k and len(s.inst.lru) == k for s in served)
+
+
+def test_prepare_rounds_after_another_policy(monkeypatch):
+    # an earlier static policy left each instance's 64-CU placement cached; two
+    # of them coincide with paired placements.  The rounds must still create
+    # every placement, one queue per instance per round.
+    monkeypatch.setattr(serve.ie, "device_info", lambda dev: (256, 8))
+    log = []
+    served = mix(log)
+    for i, s in enumerate(served):
+        s.inst.set_quota(64, 64 * i)
+        s.inst.submit(None)
+        s.inst.set_quota(256, 0)
+        s.inst.submit(None)
+    log.clear()
+    assert {(64, 0), (64, 192)} & {serve.paired_placement(256, pi, 64, sec) for pi in (0, 1) for sec in (0, 1)}
+    serve.prepare_paired(served, "rounds")
+    k = len(serve.PAIR_SPLITS)
+    assert [i for i, _, _ in log] == list(range(len(served))) * k
 
 
 @pytest.mark.parametrize("cv", [1.0, 2.0, 4.0, 6.0])
