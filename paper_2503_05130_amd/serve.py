@@ -33,9 +33,11 @@ Policies (each period):
                the prepared splits (queues made as under paired)
   paired       quotas from a fixed vocabulary: instances are paired (each
                SLO-sensitive one with a best-effort one) and each pair owns
-               a fixed 128-CU region whose split point moves in 32-CU steps
-               (32 / 96, 64 / 64, 96 / 32) in proportion to the two queue
-               lengths.  Every placement is prepared before the run and the
+               a fixed region (the CUs split evenly among the pairs: 128 for
+               two pairs, all 256 for one) whose split point moves in
+               quarters of the region (32 / 96, 64 / 64, 96 / 32 of 128) in
+               proportion to the two queue lengths (a training instance
+               counts as one queued request).  Every placement is prepared before the run and the
                stream caches hold all of them, so no hardware queue is
                created or destroyed while the instances serve (creating or
                destroying one stalls every queue of the process for ~3 ms on
@@ -166,6 +168,11 @@ class Served:
     def queue_len(self, now):
         return int(np.searchsorted(self.arrivals, now, side="right")) - self.next
 
+    def touch(self):
+        """One small batch, so that a posted quota takes effect."""
+        self.inst.submit(self.pool[:1])
+        self.inst.wait()
+
     def run(self, t0, horizon, stop):
         slot = 0
         while not stop.is_set():
@@ -258,6 +265,7 @@ class Trainee:
         self.pending = None
         self.inst.set_quota(ie.device_info(0)[0], 0)
         self.applied = (ie.device_info(0)[0], 0)
+        self.busy = False                   # a step is in flight (on `applied`)
         self.batches = 0
         self.changes = 0
         self.klc_log = []
@@ -270,19 +278,25 @@ class Trainee:
         self.inst.step(self.x, self.labels)
         self.inst.wait()
 
+    touch = warm                            # one step applies a posted quota
+
     def run(self, t0, horizon, stop):
         while not stop.is_set():
             if time.perf_counter() - t0 > horizon:
                 return
             with self.lock:
                 pend, self.pending = self.pending, None
+                self.busy = True
             if pend is not None and pend != self.applied:
                 self.inst.set_quota(*pend)
-                self.applied = pend
+                with self.lock:
+                    self.applied = pend
                 self.changes += 1
                 self.plans.add(pend)
             self.inst.step(self.x, self.labels)
             self.inst.wait()
+            with self.lock:
+                self.busy = False
             self.done_at.append(time.perf_counter() - t0)
             ms = self.inst.last_batch_ms()
             self.step_ms.append(ms)
@@ -399,7 +413,12 @@ class Generator:
 
 
 GRANULE = 32   # default quota granularity of the dynamic policies: 4 CUs per XCD, few distinct masks
-PAIR_SPLITS = (32, 64, 96)   # CUs of the first instance of a pair in its 128-CU region
+PAIR_SPLITS = (32, 64, 96)   # first instance's share of its pair's region, in 128ths
+
+
+def pair_region(n_cu, n_pairs):
+    """CUs each pair owns: the device split evenly, in multiples of 32."""
+    return max(32, (n_cu // max(n_pairs, 1)) // 32 * 32)
 
 
 def pairs_of(served):
@@ -419,10 +438,12 @@ def placements_disjoint(p, q, n_cu):
     return not (bits(p) & bits(q))
 
 
-def paired_placement(n_cu, pair_idx, split, second):
-    """(quota, first bit) of one member of pair `pair_idx` at a given split."""
-    base = (128 * pair_idx) % n_cu
-    return (128 - split, base + split) if second else (split, base)
+def paired_placement(n_cu, pair_idx, split, second, region=128):
+    """(quota, first bit) of one member of pair `pair_idx` at a given split
+    (PAIR_SPLITS: 128ths of the pair's `region` CUs)."""
+    base = (region * pair_idx) % n_cu
+    cut = split * region // 128
+    return (region - cut, base + cut) if second else (cut, base)
 
 
 def controller_quotas(ctl, served, last_k, firsts_out=None):
@@ -487,14 +508,17 @@ def control_loop(policy, served, t0, horizon, period, stop, history, granule=GRA
                 # ratio of its two members' quotas, to the nearest prepared split
                 cq = controller_quotas(ctl, served, last_k)
             plan = list(posted)
-            for pi, (a, b) in enumerate(pairs_of(served)):
+            pairs = pairs_of(served)
+            region = pair_region(n_cu, len(pairs))
+            for pi, (a, b) in enumerate(pairs):
                 if policy == "alg2p":
                     share = cq[a] / max(cq[a] + cq[b], 1)
                 else:
                     la, lb = max(served[a].queue_len(now), 0), max(served[b].queue_len(now), 0)
                     share = 0.5 if la + lb == 0 else la / (la + lb)
                 split = min(PAIR_SPLITS, key=lambda sp: abs(sp / 128.0 - share))
-                want = {a: paired_placement(n_cu, pi, split, False), b: paired_placement(n_cu, pi, split, True)}
+                want = {a: paired_placement(n_cu, pi, split, False, region),
+                        b: paired_placement(n_cu, pi, split, True, region)}
                 grow = [i for i in (a, b) if want[i][0] > posted[i][0]]
                 for i in (a, b):                # the shrinking (or unchanged) member: posted at once
                     if i not in grow:
@@ -535,7 +559,9 @@ def prepare_paired(served, queue_order="rounds"):
     made, so that the k-th queue of every instance sits at the same position
     modulo the instance count; "instance": each instance's queues in turn."""
     n_cu = ie.device_info(0)[0]
-    members = sorted((idx, pi, second) for pi, (a, b) in enumerate(pairs_of(served))
+    pairs = pairs_of(served)
+    region = pair_region(n_cu, len(pairs))
+    members = sorted((idx, pi, second) for pi, (a, b) in enumerate(pairs)
                      for idx, second in ((a, False), (b, True)))
     for idx, _, _ in members:
         # Only the full-device stream survives: a placement still cached from
@@ -543,8 +569,7 @@ def prepare_paired(served, queue_order="rounds"):
         # would land one step off the round order.
         inst = served[idx].inst
         inst.set_quota(n_cu, 0)
-        inst.submit(served[idx].pool[:1])
-        inst.wait()
+        served[idx].touch()
         inst.set_stream_cache(1)
         inst.set_stream_cache(len(PAIR_SPLITS) + 1)
     if queue_order == "rounds":
@@ -552,14 +577,13 @@ def prepare_paired(served, queue_order="rounds"):
     else:
         jobs = [(m, sp) for m in members for sp in PAIR_SPLITS]
     for (idx, pi, second), sp in jobs:
-        served[idx].inst.prepare_quota(*paired_placement(n_cu, pi, sp, second))
+        served[idx].inst.prepare_quota(*paired_placement(n_cu, pi, sp, second, region))
     for idx, pi, second in members:
         inst = served[idx].inst
-        start = paired_placement(n_cu, pi, 64, second)
+        start = paired_placement(n_cu, pi, 64, second, region)
         inst.set_quota(*start)
         served[idx].applied = start
-        inst.submit(served[idx].pool[:1])   # moves the instance onto its placement
-        inst.wait()
+        served[idx].touch()                 # moves the instance onto its placement
         inst.set_stream_cache(len(PAIR_SPLITS))
 
 

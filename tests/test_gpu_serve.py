@@ -94,3 +94,21 @@ def test_training_beside_bursty_inference(temporary_yield):
     assert inf["klc_ratio_p50_p90"] is not None and inf["klc_ratio_p50_p90"][0] >= 0.99
     assert trn["steps"] > 0
     assert summary["alg2"]["inference_p95_vs_exclusive"] > 0
+
+
+def test_paired_policies_beside_training():
+    """One pair (inference beside training, small models) owns the whole
+    device: the paired and alg2p policies move its split among quarters of
+    the 256 CUs, every request is served and training completes steps."""
+    print("train mix paired alg2p", flush=True)
+    out, summary = serve.run_train_mix(["paired", "alg2p"], horizon=1.5, warmup=0.2, period=10.0, small=True)
+    assert [r["policy"] for r in out][:2] == ["paired", "alg2p"]
+    for r in out[:2]:
+        inf, trn = r["instances"]
+        assert inf["dropped"] == 0 and inf["requests"] > 0 and trn["steps"] > 0
+        for st in (inf, trn):
+            assert st["distinct_placements"] <= 3, st
+        q = np.array(r["mean_quota"])
+        # a grow is issued only once the partner has left the CUs, so the
+        # two quotas of a period sum to at most the device
+        assert np.all((q >= 64) & (q <= 192)) and q.sum() <= 256 + 1e-6, q

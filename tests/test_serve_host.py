@@ -52,6 +52,9 @@ class FakeServed:
     def __init__(self, log, idx, slo):
         self.inst, self.slo, self.pool, self.applied = FakeInst(log, idx), slo, [None], None
 
+    def touch(self):
+        self.inst.submit(None)
+
 
 def mix(log):
     # the default mix's order: two SLO-sensitive encoders, then two best-effort decoders
@@ -69,6 +72,18 @@ def test_pairs_and_placements():
             # the two pairs' regions never meet
             other = serve.paired_placement(256, 1 - pi, 64, False)
             assert serve.placements_disjoint(a, other, 256) and serve.placements_disjoint(b, other, 256)
+
+
+def test_one_pair_owns_the_device():
+    # one SLO-sensitive instance beside one best-effort one (inference beside
+    # training): the pair's region is every CU, split in quarters
+    assert serve.pair_region(256, 1) == 256 and serve.pair_region(256, 2) == 128
+    assert serve.pair_region(256, 3) == 64
+    got = [(serve.paired_placement(256, 0, sp, False, 256), serve.paired_placement(256, 0, sp, True, 256))
+           for sp in serve.PAIR_SPLITS]
+    assert got == [((64, 0), (192, 64)), ((128, 0), (128, 128)), ((192, 0), (64, 192))]
+    for a, b in got:
+        assert a[0] + b[0] == 256 and serve.placements_disjoint(a, b, 256)
 
 
 @pytest.mark.parametrize("order", ["rounds", "instance"])
