@@ -5,7 +5,7 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
 
   python -m paper_2503_05130_amd.serve [--policy alg2 alg2@100 alg2p static proportional shared paired]
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--granule 32] [--small]
-                                       [--mix inference|train|decode] [--queue-probe]
+                                       [--mix inference|train|train2|decode] [--queue-probe]
                                        [--queue-order rounds|instance] [--cv 1] [--klc device|cycle]
                                        [--eta-violation 0.2] [--window 4] [--temporary-yield]
 
@@ -637,21 +637,10 @@ def build_mix(mix):
     return [Served(i, *m) for i, m in enumerate(mix)]
 
 
-def train_mix(small: bool = False):
-    """The train-inf collocation mix: one BERT-base-shaped inference instance
-    (batches of up to 4, latency-sensitive) beside one training instance of the
-    same shape (batch 32 x 128, best effort)."""
-    shape, seq = (SMALL, 64) if small else (BERT, 128)
-    inf = Served(0, "bert_inf", shape, seq, 4, 200.0, 0.25, 0.5, True, 51)
-    trn = Trainee(1, "bert_train", shape, seq, 8 if small else 32, 0.75, 1.0, 55)
-    return [inf, trn]
-
-
-def run_train_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="device", ctl_params=None):
-    """Each policy with both instances, then each instance alone on the whole
-    GPU ("exclusive"); the paper compares co-location against exclusive."""
-    served = train_mix(small)
-    served[0].cv, served[0].klc = cv, klc   # the inference instance's arrivals and KLC
+def run_with_exclusive(served, policies, horizon, warmup, period, ctl_params=None):
+    """Each policy with every instance ("label" keeps a policy's @period),
+    then each instance alone on the whole GPU ("exclusive:<name>"); closes
+    the instances.  Returns the results and the exclusive statistics by name."""
     out = []
     try:
         for pol in policies:
@@ -670,6 +659,25 @@ def run_train_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="d
         for s in served:
             s.inst.close()
     excl = {r["instances"][0]["name"]: r["instances"][0] for r in out if r["policy"].startswith("exclusive")}
+    return out, excl
+
+
+def train_mix(small: bool = False):
+    """The train-inf collocation mix: one BERT-base-shaped inference instance
+    (batches of up to 4, latency-sensitive) beside one training instance of the
+    same shape (batch 32 x 128, best effort)."""
+    shape, seq = (SMALL, 64) if small else (BERT, 128)
+    inf = Served(0, "bert_inf", shape, seq, 4, 200.0, 0.25, 0.5, True, 51)
+    trn = Trainee(1, "bert_train", shape, seq, 8 if small else 32, 0.75, 1.0, 55)
+    return [inf, trn]
+
+
+def run_train_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="device", ctl_params=None):
+    """Each policy with both instances, then each instance alone on the whole
+    GPU ("exclusive"); the paper compares co-location against exclusive."""
+    served = train_mix(small)
+    served[0].cv, served[0].klc = cv, klc   # the inference instance's arrivals and KLC
+    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params)
     summary = {}
     for r in out:
         if r["policy"].startswith("exclusive"):
@@ -682,6 +690,33 @@ def run_train_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="d
             "inference_p99_vs_exclusive": round(inf["p99_ms"] / e_inf["p99_ms"], 3) if inf["p99_ms"] else None,
             "training_throughput_vs_exclusive": round(trn["steps_s"] / e_trn["steps_s"], 3) if e_trn["steps_s"] else None}
     print(json.dumps({"train_inf_summary": summary, "cv": cv, "klc": klc}), flush=True)
+    return out, summary
+
+
+def train2_mix(small: bool = False):
+    """The training-training collocation mix (Sec. 5): two BERT-base-shaped
+    training instances (batch 32 x 128 each, different seeds), both best
+    effort, request 50% / limit 100%."""
+    shape, seq, b = (SMALL, 64, 8) if small else (BERT, 128, 32)
+    return [Trainee(0, "train_a", shape, seq, b, 0.5, 1.0, 55), Trainee(1, "train_b", shape, seq, b, 0.5, 1.0, 57)]
+
+
+def run_train2_mix(policies, horizon, warmup, period, small=False, ctl_params=None):
+    """Each policy with both training instances, then each alone.  The
+    paper's figure of merit is the aggregate of the two throughputs, each
+    normalised by its exclusive throughput (2.0 would be two exclusive GPUs'
+    worth)."""
+    served = train2_mix(small)
+    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params)
+    summary = {}
+    for r in out:
+        if r["policy"].startswith("exclusive"):
+            continue
+        fr = [st["steps_s"] / excl[st["name"]]["steps_s"] if excl[st["name"]]["steps_s"] else 0.0
+              for st in r["instances"]]
+        summary[r.get("label", r["policy"])] = {"throughput_vs_exclusive": [round(f, 3) for f in fr],
+                                                "aggregate_vs_exclusive": round(sum(fr), 3)}
+    print(json.dumps({"train_train_summary": summary}), flush=True)
     return out, summary
 
 
@@ -703,24 +738,7 @@ def run_decode_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="
     """Each policy with both instances, then each alone on the whole GPU."""
     served = decode_mix(small)
     served[0].cv, served[0].klc = cv, klc   # the inference instance's arrivals and KLC
-    out = []
-    try:
-        for pol in policies:
-            name, _, per = pol.partition("@")
-            res = run_policy(name, served, horizon, warmup, (float(per) if per else period) / 1e3,
-                             ctl_params=ctl_params)
-            res["label"] = pol
-            out.append(res)
-            print(json.dumps(res), flush=True)
-        for one in served:
-            res = run_policy("shared", [one], horizon, warmup, period / 1e3)
-            res["policy"] = f"exclusive:{one.name}"
-            out.append(res)
-            print(json.dumps(res), flush=True)
-    finally:
-        for s in served:
-            s.inst.close()
-    excl = {r["instances"][0]["name"]: r["instances"][0] for r in out if r["policy"].startswith("exclusive")}
+    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params)
     summary = {}
     for r in out:
         if r["policy"].startswith("exclusive"):
@@ -836,9 +854,9 @@ def main() -> int:
     ap.add_argument("--period-ms", type=float, default=20.0)
     ap.add_argument("--granule", type=int, default=GRANULE, help="quota granularity (CUs) of proportional and alg2")
     ap.add_argument("--small", action="store_true", help="small models (quick functional run)")
-    ap.add_argument("--mix", choices=["inference", "train", "decode"], default="inference",
+    ap.add_argument("--mix", choices=["inference", "train", "train2", "decode"], default="inference",
                     help="inference: the four-instance serving mix; train: inference beside a training instance; "
-                         "decode: inference beside a token-by-token decoder")
+                         "train2: two training instances; decode: inference beside a token-by-token decoder")
     ap.add_argument("--queue-probe", action="store_true",
                     help="measure what creating, switching and keeping masked queues costs co-located instances")
     ap.add_argument("--cv", type=float, default=1.0,
@@ -866,6 +884,9 @@ def main() -> int:
     if args.mix == "train":
         run_train_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, args.cv, args.klc,
                       ctl_params)
+        return 0
+    if args.mix == "train2":
+        run_train2_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, ctl_params)
         return 0
     if args.mix == "decode":
         run_decode_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, args.cv, args.klc,

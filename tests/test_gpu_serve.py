@@ -112,3 +112,20 @@ def test_paired_policies_beside_training():
         # a grow is issued only once the partner has left the CUs, so the
         # two quotas of a period sum to at most the device
         assert np.all((q >= 64) & (q <= 192)) and q.sum() <= 256 + 1e-6, q
+
+
+def test_training_beside_training():
+    """The train-train mix (small models): both training instances complete
+    steps under each policy and alone, and the aggregate of their normalised
+    throughputs is reported."""
+    print("train2 mix", flush=True)
+    out, summary = serve.run_train2_mix(["static", "alg2"], horizon=1.5, warmup=0.2, period=10.0, small=True)
+    assert [r["policy"] for r in out] == ["static", "alg2", "exclusive:train_a", "exclusive:train_b"]
+    for r in out:
+        for st in r["instances"]:
+            assert st["training"] and st["steps"] > 0
+    for pol in ("static", "alg2"):
+        v = summary[pol]
+        assert len(v["throughput_vs_exclusive"]) == 2 and v["aggregate_vs_exclusive"] > 0
+    # no SLO-sensitive instance: the controller stays in NONE and splits the CUs
+    assert out[1]["state_counts"] == {"0": out[1]["periods"]}
