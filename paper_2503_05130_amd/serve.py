@@ -349,6 +349,7 @@ class Generator:
         self.pending = None
         self.inst.set_quota(ie.device_info(0)[0], 0)
         self.applied = (ie.device_info(0)[0], 0)
+        self.busy = False                   # an iteration is in flight (on `applied`)
         self.batches = 0
         self.changes = 0
         self.klc_log = []
@@ -363,17 +364,26 @@ class Generator:
         self.inst.decode(self.x_steps[0], self.prompt)
         self.inst.wait()
 
+    def touch(self):
+        """One prefill, so that a posted quota takes effect."""
+        self.inst.submit(self.x_prompt)
+        self.inst.wait()
+
     def _iteration(self, kind, launch):
         with self.lock:
             pend, self.pending = self.pending, None
+            self.busy = True
         if pend is not None and pend != self.applied:
             self.inst.set_quota(*pend)
-            self.applied = pend
+            with self.lock:
+                self.applied = pend
             self.changes += 1
             self.plans.add(pend)
         t = time.perf_counter()
         launch()
         self.inst.wait()
+        with self.lock:
+            self.busy = False
         wall = (time.perf_counter() - t) * 1e3
         ms = self.inst.last_batch_ms()
         self.batches += 1

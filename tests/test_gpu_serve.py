@@ -129,3 +129,18 @@ def test_training_beside_training():
         assert len(v["throughput_vs_exclusive"]) == 2 and v["aggregate_vs_exclusive"] > 0
     # no SLO-sensitive instance: the controller stays in NONE and splits the CUs
     assert out[1]["state_counts"] == {"0": out[1]["periods"]}
+
+
+def test_paired_policies_beside_decoding():
+    """The decode mix (small models) under the paired policies: its two
+    instances form one pair over the whole device; every request is served and
+    the decoder completes decode steps."""
+    print("decode mix paired alg2p", flush=True)
+    out, summary = serve.run_decode_mix(["paired", "alg2p"], horizon=1.5, warmup=0.2, period=10.0, small=True)
+    for r in out[:2]:
+        inf, gen = r["instances"]
+        assert inf["dropped"] == 0 and inf["requests"] > 0 and gen["steps"] > 0
+        for st in (inf, gen):
+            assert st["distinct_placements"] <= 3, st
+        q = np.array(r["mean_quota"])
+        assert np.all((q >= 64) & (q <= 192)) and q.sum() <= 256 + 1e-6, q
