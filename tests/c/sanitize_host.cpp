@@ -150,6 +150,9 @@ static void check_controller() {
     bad = p;
     bad.eta_increase = 0.5;
     CHECK(iefwd_ctl_create(&bad, &ctl) == IEFWD_EINVAL);
+    bad = p;
+    bad.flags = 2;   // an undefined flag bit
+    CHECK(iefwd_ctl_create(&bad, &ctl) == IEFWD_EINVAL);
     CHECK(iefwd_ctl_create(nullptr, &ctl) == IEFWD_EINVAL);
     CHECK(iefwd_ctl_destroy(nullptr) == IEFWD_OK);
     for (int stream = 0; stream < 40; ++stream) {
@@ -158,6 +161,7 @@ static void check_controller() {
         q.granule = 1u << (next_u64() % 4);
         q.min_quota = q.granule * (1 + (uint32_t)(next_u64() % 2));
         q.window = 1 + (uint32_t)(next_u64() % 6);
+        q.flags = (uint32_t)(next_u64() % 2) * IEFWD_CTL_TEMPORARY_YIELD;
         CHECK(iefwd_ctl_create(&q, &ctl) == IEFWD_OK);
         const uint32_t n = 1 + (uint32_t)(next_u64() % 6);
         for (uint32_t i = 0; i < n; ++i) {
