@@ -7,7 +7,7 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
                                        [--horizon 20] [--warmup 2] [--period-ms 20] [--granule 32] [--small]
                                        [--mix inference|train|train2|decode] [--queue-probe]
                                        [--queue-order rounds|instance] [--cv 1] [--klc device|cycle]
-                                       [--eta-violation 0.2] [--window 4] [--temporary-yield]
+                                       [--eta-violation 0.2] [--window 4] [--temporary-yield] [--timeline]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
 batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
@@ -597,7 +597,8 @@ def prepare_paired(served, queue_order="rounds"):
         inst.set_stream_cache(len(PAIR_SPLITS))
 
 
-def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_order="rounds", ctl_params=None):
+def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_order="rounds", ctl_params=None,
+               timeline=False):
     for s in served:
         s.reset(horizon)
         if isinstance(s, (Trainee, Generator)):
@@ -634,6 +635,14 @@ def run_policy(policy, served, horizon, warmup, period, granule=GRANULE, queue_o
     extra = {"queue_order": queue_order} if policy in ("paired", "alg2p") else {}
     if policy in ("alg2", "alg2p") and ctl_params:
         extra["ctl_params"] = dict(ctl_params)
+    if timeline:
+        # per control period: its end (s), the quotas posted, the controller state
+        # (-1 without one) and the requests that arrived at each instance in it
+        ends = [h[0] for h in history]
+        edges = np.array([0.0] + ends)
+        arrived = [np.histogram(s.arrivals, bins=edges)[0].tolist() if isinstance(s, Served) and len(ends)
+                   else [None] * len(ends) for s in served]
+        extra["timeline"] = [[h[0], h[1], h[2], [a[i] for a in arrived]] for i, h in enumerate(history)]
     return {"policy": policy, **extra, "horizon_s": horizon, "warmup_s": warmup, "period_ms": period * 1e3,
             "granule": granule if policy in ("proportional", "alg2", "alg2p") else None, "aggregate": aggregate,
             "instances": [s.stats(warmup, horizon) if isinstance(s, (Trainee, Generator)) else s.stats(warmup)
@@ -647,7 +656,7 @@ def build_mix(mix):
     return [Served(i, *m) for i, m in enumerate(mix)]
 
 
-def run_with_exclusive(served, policies, horizon, warmup, period, ctl_params=None):
+def run_with_exclusive(served, policies, horizon, warmup, period, ctl_params=None, timeline=False):
     """Each policy with every instance ("label" keeps a policy's @period),
     then each instance alone on the whole GPU ("exclusive:<name>"); closes
     the instances.  Returns the results and the exclusive statistics by name."""
@@ -656,7 +665,7 @@ def run_with_exclusive(served, policies, horizon, warmup, period, ctl_params=Non
         for pol in policies:
             name, _, per = pol.partition("@")
             res = run_policy(name, served, horizon, warmup, (float(per) if per else period) / 1e3,
-                             ctl_params=ctl_params)
+                             ctl_params=ctl_params, timeline=timeline)
             res["label"] = pol
             out.append(res)
             print(json.dumps(res), flush=True)
@@ -682,12 +691,13 @@ def train_mix(small: bool = False):
     return [inf, trn]
 
 
-def run_train_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="device", ctl_params=None):
+def run_train_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="device", ctl_params=None,
+                  timeline=False):
     """Each policy with both instances, then each instance alone on the whole
     GPU ("exclusive"); the paper compares co-location against exclusive."""
     served = train_mix(small)
     served[0].cv, served[0].klc = cv, klc   # the inference instance's arrivals and KLC
-    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params)
+    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params, timeline)
     summary = {}
     for r in out:
         if r["policy"].startswith("exclusive"):
@@ -711,13 +721,13 @@ def train2_mix(small: bool = False):
     return [Trainee(0, "train_a", shape, seq, b, 0.5, 1.0, 55), Trainee(1, "train_b", shape, seq, b, 0.5, 1.0, 57)]
 
 
-def run_train2_mix(policies, horizon, warmup, period, small=False, ctl_params=None):
+def run_train2_mix(policies, horizon, warmup, period, small=False, ctl_params=None, timeline=False):
     """Each policy with both training instances, then each alone.  The
     paper's figure of merit is the aggregate of the two throughputs, each
     normalised by its exclusive throughput (2.0 would be two exclusive GPUs'
     worth)."""
     served = train2_mix(small)
-    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params)
+    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params, timeline)
     summary = {}
     for r in out:
         if r["policy"].startswith("exclusive"):
@@ -744,11 +754,12 @@ def decode_mix(small: bool = False):
     return [inf, gen]
 
 
-def run_decode_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="device", ctl_params=None):
+def run_decode_mix(policies, horizon, warmup, period, small=False, cv=1.0, klc="device", ctl_params=None,
+                   timeline=False):
     """Each policy with both instances, then each alone on the whole GPU."""
     served = decode_mix(small)
     served[0].cv, served[0].klc = cv, klc   # the inference instance's arrivals and KLC
-    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params)
+    out, excl = run_with_exclusive(served, policies, horizon, warmup, period, ctl_params, timeline)
     summary = {}
     for r in out:
         if r["policy"].startswith("exclusive"):
@@ -882,6 +893,8 @@ def main() -> int:
     ap.add_argument("--temporary-yield", action="store_true",
                     help="alg2/alg2p: an EMERGENCY scale-down of the co-located instances leaves their plan unchanged "
                          "(IEFWD_CTL_TEMPORARY_YIELD)")
+    ap.add_argument("--timeline", action="store_true",
+                    help="add each period's quotas, controller state and arrivals to the results")
     ap.add_argument("--queue-order", choices=["rounds", "instance"], default="rounds",
                     help="order in which the paired policy prepares its placements' queues")
     args = ap.parse_args()
@@ -893,14 +906,14 @@ def main() -> int:
         return 0
     if args.mix == "train":
         run_train_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, args.cv, args.klc,
-                      ctl_params)
+                      ctl_params, args.timeline)
         return 0
     if args.mix == "train2":
-        run_train2_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, ctl_params)
+        run_train2_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, ctl_params, args.timeline)
         return 0
     if args.mix == "decode":
         run_decode_mix(args.policy, args.horizon, args.warmup, args.period_ms, args.small, args.cv, args.klc,
-                      ctl_params)
+                       ctl_params, args.timeline)
         return 0
     t = time.perf_counter()
     served = build_mix(default_mix(args.small))
@@ -915,7 +928,7 @@ def main() -> int:
             name, _, per = pol.partition("@")          # "alg2@100": policy with its own period in ms
             period = float(per) if per else args.period_ms
             res = run_policy(name, served, args.horizon, args.warmup, period / 1e3, args.granule, args.queue_order,
-                             ctl_params)
+                             ctl_params, args.timeline)
             print(json.dumps(res), flush=True)
     finally:
         for s in served:

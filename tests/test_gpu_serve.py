@@ -84,9 +84,18 @@ def test_training_beside_bursty_inference(temporary_yield):
     params = {"temporary_yield": True} if temporary_yield else None
     print(f"train mix cv 4 klc cycle temporary_yield={temporary_yield}", flush=True)
     out, summary = serve.run_train_mix(["alg2"], horizon=1.5, warmup=0.2, period=10.0, small=True, cv=4.0,
-                                       klc="cycle", ctl_params=params)
+                                       klc="cycle", ctl_params=params, timeline=True)
     alg2 = out[0]
     assert alg2["policy"] == "alg2" and alg2.get("ctl_params") == params
+    # the timeline: one entry per period, quotas within the device, the requests
+    # of the inference instance counted once each
+    tl = alg2["timeline"]
+    assert len(tl) == alg2["periods"]
+    assert all(len(q) == 2 and all(32 <= x <= 256 for x in q) and st in (1, 2, 3) for _, q, st, _ in tl)
+    assert [t for t, _, _, _ in tl] == sorted(t for t, _, _, _ in tl)
+    arrived = sum(a[0] for _, _, _, a in tl)
+    assert arrived > 0
+    assert all(a[1] is None for _, _, _, a in tl)      # the training instance has no arrivals
     assert sum(alg2["state_counts"].values()) == alg2["periods"] > 10
     inf, trn = alg2["instances"]
     assert inf["dropped"] == 0 and inf["requests"] > 0
