@@ -75,6 +75,10 @@ one CU share -- contention -- rather than a change of batch size or of its own
 quota (which the controller itself causes).  This per-<batch, quota> baseline
 is what the paper's profiler supplies (Sec. 3.2).
 
+--timeline adds to each policy's result, per control period, its end time,
+the quotas posted, the controller state and the requests that arrived at each
+inference instance.
+
 --klc cycle measures instead each batch's cycle from the arrival of its oldest
 request to its completion, relative to the same fastest device time.  The
 paper reads a KLC rise as contention or a burst of the instance's own requests
