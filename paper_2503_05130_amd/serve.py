@@ -8,6 +8,7 @@ Sec. 3.4 and its inference-inference experiments, Sec. 5).
                                        [--mix inference|train|train2|decode] [--queue-probe]
                                        [--queue-order rounds|instance] [--cv 1] [--klc device|cycle]
                                        [--eta-violation 0.2] [--window 4] [--temporary-yield] [--timeline]
+                                       [--exclusive]
 
 Default mix: two BERT-base-shaped encoders (post-LN, 12 x 768, S = 128,
 batches of up to 4, 200 requests/s each, latency-sensitive) and two causal
@@ -897,6 +898,8 @@ def main() -> int:
     ap.add_argument("--temporary-yield", action="store_true",
                     help="alg2/alg2p: an EMERGENCY scale-down of the co-located instances leaves their plan unchanged "
                          "(IEFWD_CTL_TEMPORARY_YIELD)")
+    ap.add_argument("--exclusive", action="store_true",
+                    help="inference mix: also run each instance alone on the whole GPU and report latency ratios")
     ap.add_argument("--timeline", action="store_true",
                     help="add each period's quotas, controller state and arrivals to the results")
     ap.add_argument("--queue-order", choices=["rounds", "instance"], default="rounds",
@@ -928,12 +931,29 @@ def main() -> int:
                       "cv": args.cv, "klc": args.klc}),
           flush=True)
     try:
+        out = []
         for pol in args.policy:
             name, _, per = pol.partition("@")          # "alg2@100": policy with its own period in ms
             period = float(per) if per else args.period_ms
             res = run_policy(name, served, args.horizon, args.warmup, period / 1e3, args.granule, args.queue_order,
                              ctl_params, args.timeline)
+            res["label"] = pol
+            out.append(res)
             print(json.dumps(res), flush=True)
+        if args.exclusive:
+            excl = {}
+            for one in served:
+                res = run_policy("shared", [one], args.horizon, args.warmup, args.period_ms / 1e3)
+                res["policy"] = f"exclusive:{one.name}"
+                excl[one.name] = res["instances"][0]
+                print(json.dumps(res), flush=True)
+            summary = {}
+            for r in out:
+                summary[r["label"]] = {st["name"]: {f"{k}_vs_exclusive": round(st[k] / excl[st["name"]][k], 3)
+                                                    for k in ("p50_ms", "p95_ms", "p99_ms")
+                                                    if st[k] and excl[st["name"]][k]}
+                                       for st in r["instances"]}
+            print(json.dumps({"inference_summary": summary, "cv": args.cv, "klc": args.klc}), flush=True)
     finally:
         for s in served:
             s.inst.close()
