@@ -153,3 +153,20 @@ def test_paired_policies_beside_decoding():
             assert st["distinct_placements"] <= 3, st
         q = np.array(r["mean_quota"])
         assert np.all((q >= 64) & (q <= 192)) and q.sum() <= 256 + 1e-6, q
+
+
+def test_inference_mix_cli_with_exclusive(monkeypatch, capsys):
+    """The command line on the four-instance mix (small models): a policy,
+    then every instance alone, and the latency ratios against exclusive."""
+    import json
+    import sys
+    print("cli inference mix --exclusive", flush=True)
+    monkeypatch.setattr(sys, "argv", ["serve", "--small", "--policy", "static", "--horizon", "1.5", "--warmup", "0.2",
+                                      "--cv", "2", "--klc", "cycle", "--exclusive"])
+    assert serve.main() == 0
+    lines = [json.loads(x) for x in capsys.readouterr().out.splitlines() if x.startswith("{")]
+    names = [x.get("policy") for x in lines if "policy" in x]
+    assert names == ["static", "exclusive:enc_a", "exclusive:enc_b", "exclusive:dec_a", "exclusive:dec_b"]
+    summary = lines[-1]["inference_summary"]["static"]
+    assert set(summary) == {"enc_a", "enc_b", "dec_a", "dec_b"}
+    assert all(v["p95_ms_vs_exclusive"] > 0 for v in summary.values())
