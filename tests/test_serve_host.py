@@ -194,3 +194,23 @@ def test_dispatcher_klc_modes(monkeypatch, klc):
         # the k-th batch's oldest request waited for the k-1 batches before it
         assert all(r >= k + 1 for k, r in enumerate(s.ratios))
         assert s.ratios == sorted(s.ratios)
+
+
+def test_serve_report_tables(capsys, tmp_path):
+    # the report reads the harness's JSON lines: one row per instance result,
+    # figures that do not apply shown as "-", the summary line echoed
+    import json
+    from paper_2503_05130_amd import serve_report
+    res = {"policy": "alg2", "label": "alg2@100", "mean_quota": [64.0, 192.0],
+           "state_counts": {"1": 2, "3": 8},
+           "instances": [{"name": "bert_inf", "p50_ms": 0.9, "p95_ms": 1.4, "p99_ms": 1.7, "quota_changes": 3},
+                         {"name": "bert_train", "training": True, "steps_s": 94.0, "quota_changes": 1}]}
+    f = tmp_path / "out.jsonl"
+    f.write_text(json.dumps({"setup_s": 1.0}) + "\n" + json.dumps(res) + "\n" +
+                 json.dumps({"train_inf_summary": {"alg2": {"x": 1}}}) + "\n")
+    assert serve_report.main([str(f)]) == 0
+    out = capsys.readouterr().out.splitlines()
+    assert out[0].startswith("| policy | instance |")
+    assert out[2] == "| alg2@100 | bert_inf | 64.0 | 0.9 | 1.4 | 1.7 | - | - | 3 | EMERGENCY 2, CONTENTION 8 |"
+    assert out[3] == "| alg2@100 | bert_train | 192.0 | - | - | - | 94.0 | - | 1 | EMERGENCY 2, CONTENTION 8 |"
+    assert out[-1].startswith("train_inf_summary: ")
