@@ -388,8 +388,8 @@ typedef struct {
     double eta_increase;     /* multiplicative scale-up per period; >= 1 */
 } iefwd_ctl_params;
 
-/* flags: the text calls the co-located instances' scale-down under EMERGENCY
- * temporary, while the listing keeps R_last in CONTENTION, so that without
+/* flags: Sec. 3.4.1 calls the co-located instances' scale-down under EMERGENCY
+ * temporary, while Alg. 2 keeps R_last in CONTENTION, so that without
  * this flag a yielded issue becomes R_last and is undone only through
  * RECOVERY (the SLO-sensitive instances idle for a whole window).  With it a
  * yielded issue leaves R_last, the plan held before the emergency, unchanged:

@@ -25,10 +25,10 @@ What the paper fixes (Sec. 3.4.1 and Alg. 2):
 Readings where the paper is silent or ambiguous (each also listed in the
 design notes):
   R1  eta_violation and eta_increase are not given: defaults 0.2 and 1.25.
-  R2  "scaled down by the KLC change": the listing divides by dT, which for
+  R2  "scaled down by the KLC change": Alg. 2 divides by dT, which for
       dT < 1 would scale the instance *up*; we divide by the KLC ratio
       1 + dT = T_current / T_min of the instance that raised EMERGENCY.
-  R3  the SLO scale-up branch is uncapped in the listing; tokens here are CUs,
+  R3  the SLO scale-up branch is uncapped in Alg. 2; tokens here are CUs,
       so it is capped at MaxTokens.
   R4  SLO-sensitive instances are evaluated first in a period (they set the
       shared state), then the others, each group in id order.
@@ -52,10 +52,10 @@ design notes):
       from the top (id order), so a change of one quota moves one boundary.
 
   R8  the text calls the co-located instances' scale-down under EMERGENCY
-      temporary, while the listing keeps R_last in CONTENTION, so that a
+      temporary, while Alg. 2 keeps R_last in CONTENTION, so that a
       scale-down is undone only through RECOVERY (the SLO instance idle for a
       whole window).  Both are offered: by default (temporary_yield False) a
-      yielded issue becomes R_last, as the listing reads; with temporary_yield
+      yielded issue becomes R_last, as Alg. 2 reads; with temporary_yield
       True a yielded issue does not replace R_last, so the yield is computed
       from the plan held before the emergency (consecutive EMERGENCY periods
       do not compound it) and CONTENTION afterwards restores that plan.

@@ -144,7 +144,7 @@ void QuotaController::issue(std::vector<double> &tokens, std::vector<uint32_t> &
     // the text calls the co-located instances' EMERGENCY scale-down temporary:
     // with temporary_yield their plan R_last survives it, so the yield does
     // not compound over consecutive EMERGENCY periods and CONTENTION restores
-    // the plan; without it the yielded issue becomes R_last as in the listing
+    // the plan; without it the yielded issue becomes R_last as in Alg. 2
     const bool yielded = state_ == Emergency && p_.temporary_yield;
     for (uint32_t i = 0; i < n; ++i) {
         if (insts_[i].slo || !yielded) insts_[i].r_last = tokens[i];
