@@ -16,6 +16,12 @@ pre-LN decoders (24 x 2048, 16 heads, FFN 8192, S = 1024, batches of up to
 2, 10 requests/s each, best effort).  Every request is one sequence; a
 dispatcher takes up to `max_batch` requests that have arrived, runs them as
 one batch and records each request's latency (completion - arrival).
+Other mixes (--mix): train, that BERT-base-shaped encoder beside a training
+instance of the same shape (Sec. 5 train-inf collocation); train2, two such
+training instances (training-training collocation); decode, the encoder
+beside a d = 2048 decoder generating token by token over its KV cache.  Each
+of these also runs every instance alone on the whole GPU (exclusive), as
+--exclusive does for the default mix.
 
 Policies (each period):
   shared       every instance on all CUs (no partitioning)
